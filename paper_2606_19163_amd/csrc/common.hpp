@@ -1,0 +1,115 @@
+// Shared device-side types and helpers of the stage kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pulse {
+
+enum DType : int { DT_F32 = 0, DT_BF16 = 1 };
+
+// One NHWC tensor: element type and channel stride (the tensor's C).
+struct Src {
+  const void* ptr;
+  int dtype;
+  int C;
+};
+
+// A virtual NHWC input of C channels read from up to two tensors without
+// materialising their concatenation: channel c < c0 comes from s0[c],
+// channel c >= c0 from s1[c - c0].  `add` (fp32, C channels, may be null)
+// is added element by element; it carries a buffered skip gradient into the
+// gradient that reaches a cached encoder output.
+struct VIn {
+  Src s0, s1;
+  int c0, C;
+  const float* add;
+};
+
+struct Geo {
+  int B, H, W;
+  __host__ __device__ long pixels() const { return (long)B * H * W; }
+  __host__ __device__ int hw() const { return H * W; }
+};
+
+// ---- bf16 helpers --------------------------------------------------------
+
+__device__ __forceinline__ float bf2f(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+// Load 8 consecutive channels [c, c+8) of one pixel of a tensor as fp32.
+__device__ __forceinline__ void ld8(const Src& s, long pix, int c, float v[8]) {
+  if (s.dtype == DT_BF16) {
+    const uint4 q = *reinterpret_cast<const uint4*>(
+        static_cast<const uint16_t*>(s.ptr) + pix * s.C + c);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+    const float4* p = reinterpret_cast<const float4*>(
+        static_cast<const float*>(s.ptr) + pix * s.C + c);
+    const float4 a = p[0], b = p[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
+// Load channels [c, c+8) of pixel `pix` of a virtual input (c multiple of 8,
+// the 8 channels never straddle the two sources because c0 % 8 == 0).
+__device__ __forceinline__ void ld8v(const VIn& v, long pix, int c, float out[8]) {
+  if (c < v.c0)
+    ld8(v.s0, pix, c, out);
+  else
+    ld8(v.s1, pix, c - v.c0, out);
+  if (v.add) {
+    const float4* p = reinterpret_cast<const float4*>(v.add + pix * v.C + c);
+    const float4 a = p[0], b = p[1];
+    out[0] += a.x; out[1] += a.y; out[2] += a.z; out[3] += a.w;
+    out[4] += b.x; out[5] += b.y; out[6] += b.z; out[7] += b.w;
+  }
+}
+
+// Store 8 fp32 values as channels [c, c+8) of pixel `pix` of a tensor.
+__device__ __forceinline__ void st8(void* ptr, int dtype, int C, long pix, int c,
+                                    const float v[8]) {
+  if (dtype == DT_BF16) {
+    uint4 q;
+    q.x = pack2(v[0], v[1]);
+    q.y = pack2(v[2], v[3]);
+    q.z = pack2(v[4], v[5]);
+    q.w = pack2(v[6], v[7]);
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(ptr) + pix * C + c) = q;
+  } else {
+    float4* p = reinterpret_cast<float4*>(static_cast<float*>(ptr) + pix * C + c);
+    p[0] = make_float4(v[0], v[1], v[2], v[3]);
+    p[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+__device__ __forceinline__ float silu_f(float z) {
+  return z / (1.0f + __expf(-z));
+}
+
+// d SiLU(z)/dz
+__device__ __forceinline__ float dsilu_f(float z) {
+  const float s = 1.0f / (1.0f + __expf(-z));
+  return s * (1.0f + z * (1.0f - s));
+}
+
+}  // namespace pulse

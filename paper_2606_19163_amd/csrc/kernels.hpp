@@ -1,0 +1,139 @@
+// Internal launcher interface between the host orchestration (stage.cpp) and
+// the HIP kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace pulse {
+
+constexpr int MAX_SEG = 3;
+
+// A contiguous range of the implicit operand: K in CONV mode, N in WGRAD
+// mode.  It is a 3x3 (taps = 9, zero padded) or 1x1 (taps = 1) conv over the
+// virtual input `in` of C channels, so it spans taps * C indices ordered
+// (tap, channel) -- the OHWI order of the weights.
+struct Seg {
+  int begin, end;
+  int taps;
+  int C;
+  VIn in;
+  float* grad;  // WGRAD: accumulation target, rows of length end - begin
+};
+
+struct GemmArgs {
+  Geo g;
+  int M, N, K;
+  int nseg;
+  Seg seg[MAX_SEG];
+  // CONV mode
+  const void* Bw;      // [N][ldb] weights in the compute dtype
+  int ldb;
+  const float* bias;   // [N] or null
+  const float* rowvec; // [B][N] or null, added to every pixel of image b
+  VIn resid;           // residual added in the epilogue (resid.s0.ptr null: none)
+  void* out;           // [P][ldo]
+  void* out2;          // optional second copy of out
+  int out_dtype;
+  int ldo;
+  // WGRAD mode
+  VIn gy;              // output gradient, M channels
+  int kchunk;          // pixels per split
+  float* part;         // [splits][M][N] fp32 partials
+};
+
+// implicit GEMM (igemm.hip); cfg: 0 = bf16 BK 64, 1 = bf16 BK 32, 2 = fp32
+int gemm_bk(int cfg);
+int gemm_bm(int cfg);
+int gemm_bn(int cfg);
+hipError_t launch_conv(const GemmArgs& a, int cfg, hipStream_t st);
+hipError_t launch_wgrad(const GemmArgs& a, int cfg, int splits, hipStream_t st);
+
+// ---- GroupNorm / reductions (norm.hip) -----------------------------------
+
+// Grid shape shared by the per-channel reduction kernels: image b, pixel
+// chunk of `cp` pixels, 64 channel vectors per block in x.
+struct RedGrid {
+  int chunks, cp;
+};
+RedGrid red_grid(const Geo& g, int C);
+
+// partial[b][chunk][2][C]: per-channel sum and sum of squares of x.
+hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
+                                   hipStream_t st);
+// mean/rstd [B][G] and the folded affine scale/shift [B][C].
+hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                    int G, float eps, const float* gamma, const float* beta,
+                                    float* mean, float* rstd, float* scale, float* shift,
+                                    hipStream_t st);
+// a = SiLU(x * scale + shift); channels < x.c0 go to dst0, the rest to dst1.
+hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale,
+                           const float* shift, void* dst0, void* dst1, int dtype,
+                           hipStream_t st);
+
+// GroupNorm+SiLU backward.  da: gradient w.r.t. SiLU(GN(x)) (fp32 [P][C]).
+// partial[b][chunk][0][c] = sum dz, [1][c] = sum dz * xhat with
+// dz = da * SiLU'(z), z = x * scale + shift, xhat = (x - mean) * rstd.
+hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+                                 const float* scale, const float* shift, const float* mean,
+                                 const float* rstd, int G, float* partial, hipStream_t st);
+// coef[b][g][2] = (sum_g gamma*dz, sum_g gamma*dz*xhat) / count, and
+// dgamma[c] += sum dz*xhat, dbeta[c] += sum dz.
+hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                  int G, const float* gamma, float* coef, float* dgamma,
+                                  float* dbeta, hipStream_t st);
+
+struct GnBwdOut {
+  void* dst0;      // channels [0, c_split): stride c_split
+  int dtype0;
+  void* dst1;      // channels [c_split, C): stride C - c_split (may be null if c_split == C)
+  int dtype1;
+  int c_split;
+  VIn add0;        // optional addend (add0.s0.ptr null: none), C channels
+  const float* add1;  // optional fp32 addend [P][C]
+  float* chan_partial;  // optional per-(b, chunk, c) sums of the output
+};
+// dx = rstd * (gamma*dz - coef0 - xhat*coef1) + addends, split-stored.
+hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+                               const float* scale, const float* shift, const float* mean,
+                               const float* rstd, const float* gamma, const float* coef,
+                               int G, const GnBwdOut& o, hipStream_t st);
+
+// partial[b][chunk][0][c] = sum over the chunk of v (v may carry an addend).
+hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
+                                   hipStream_t st);
+// acc0[c] += sum_{b,chunk} partial, acc1 likewise (may be null);
+// per_image[b][c] = sum_chunk partial (may be null).
+hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                    float* acc0, float* acc1, float* per_image,
+                                    hipStream_t st);
+
+// ---- timestep embedding, weights, copies (misc.hip) ----------------------
+
+// e[b][o] = bias_a[o] + bias_b[o] + sum_d Wl[o][d] * SiLU(temb[b][d])
+hipError_t launch_temb_fwd(const void* temb, int dtype, int B, int D, int O, const float* Wl,
+                           const float* bias_a, const float* bias_b, float* e,
+                           hipStream_t st);
+// dWl += de^T SiLU(temb); dbl += sum_b de; db1 += sum_b de;
+// dtemb += (de Wl) * SiLU'(temb) (dtemb may be null).
+hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, int D, int O,
+                           const float* Wl, float* dWl, float* dbl, float* db1, float* dtemb,
+                           hipStream_t st);
+
+// dst[r][col_off + c] = (dtype) src[r][c] for r < rows, c < cols.
+hipError_t launch_convert_rows(const float* src, int rows, int cols, void* dst, int ldd,
+                               int col_off, int dtype, hipStream_t st);
+// 3x3 data-gradient weights: dst[c][8 - tap][o] = src[o][tap][c].
+hipError_t launch_flip3x3(const float* src, int O, int C, void* dst, int dtype,
+                          hipStream_t st);
+// dst[c][o] = src[o][c]
+hipError_t launch_transpose(const float* src, int O, int C, void* dst, int dtype,
+                            hipStream_t st);
+// dst[i] = a[i] + (b ? b[i] : 0)
+hipError_t launch_vec_add(const float* a, const float* b, float* dst, int n, hipStream_t st);
+// dst = convert(src), n elements (dtypes as DType)
+hipError_t launch_cast(const void* src, int sdt, void* dst, int ddt, long n, hipStream_t st);
+
+}  // namespace pulse

@@ -1,0 +1,169 @@
+// Timestep-embedding projection, weight re-layouts and conversions (gfx950).
+// All small or streaming; none is on the MFMA path.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace pulse {
+
+namespace {
+
+__device__ __forceinline__ float ld_any(const void* p, int dtype, long i) {
+  return dtype == DT_BF16 ? bf2f(static_cast<const uint16_t*>(p)[i])
+                          : static_cast<const float*>(p)[i];
+}
+
+__device__ __forceinline__ void st_any(void* p, int dtype, long i, float v) {
+  if (dtype == DT_BF16)
+    static_cast<uint16_t*>(p)[i] = f2bf(v);
+  else
+    static_cast<float*>(p)[i] = v;
+}
+
+// one wave per (o, b): lanes stride over d, xor-shuffle tree reduction
+__global__ __launch_bounds__(64) void k_temb_fwd(const void* temb, int dtype, int D, int O,
+                                                 const float* Wl, const float* bias_a,
+                                                 const float* bias_b, float* e) {
+  const int o = blockIdx.x, b = blockIdx.y;
+  float s = 0.f;
+  for (int d = threadIdx.x; d < D; d += 64)
+    s += Wl[(long)o * D + d] * silu_f(ld_any(temb, dtype, (long)b * D + d));
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (threadIdx.x == 0) {
+    float v = s + bias_a[o];
+    if (bias_b) v += bias_b[o];
+    e[(long)b * O + o] = v;
+  }
+}
+
+// thread (o, d): dWl[o][d] += sum_b de[b][o] * SiLU(temb[b][d]); the extra
+// thread d == D of each row accumulates the bias gradients.
+__global__ void k_temb_bwd_w(const float* de, const void* temb, int dtype, int B, int D, int O,
+                             float* dWl, float* dbl, float* db1) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)O * (D + 1)) return;
+  const int o = (int)(i / (D + 1));
+  const int d = (int)(i - (long)o * (D + 1));
+  if (d < D) {
+    float s = 0.f;
+    for (int b = 0; b < B; ++b)
+      s += de[(long)b * O + o] * silu_f(ld_any(temb, dtype, (long)b * D + d));
+    dWl[(long)o * D + d] += s;
+  } else {
+    float s = 0.f;
+    for (int b = 0; b < B; ++b) s += de[(long)b * O + o];
+    dbl[o] += s;
+    if (db1) db1[o] += s;
+  }
+}
+
+// thread (b, d): dtemb[b][d] += SiLU'(temb[b][d]) * sum_o Wl[o][d] de[b][o]
+__global__ void k_temb_bwd_x(const float* de, const void* temb, int dtype, int B, int D, int O,
+                             const float* Wl, float* dtemb) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)B * D) return;
+  const int b = (int)(i / D);
+  const int d = (int)(i - (long)b * D);
+  float s = 0.f;
+  for (int o = 0; o < O; ++o) s += Wl[(long)o * D + d] * de[(long)b * O + o];
+  dtemb[i] += s * dsilu_f(ld_any(temb, dtype, i));
+}
+
+__global__ void k_convert_rows(const float* src, int rows, int cols, void* dst, int ldd,
+                               int col_off, int dtype) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)rows * cols) return;
+  const long r = i / cols;
+  const long c = i - r * cols;
+  st_any(dst, dtype, r * ldd + col_off + c, src[i]);
+}
+
+__global__ void k_flip3x3(const float* src, int O, int C, void* dst, int dtype) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)O * 9 * C) return;
+  // destination index (c, t, o)
+  const int o = (int)(i % O);
+  const long ct = i / O;
+  const int t = (int)(ct % 9);
+  const int c = (int)(ct / 9);
+  st_any(dst, dtype, i, src[((long)o * 9 + (8 - t)) * C + c]);
+}
+
+__global__ void k_transpose(const float* src, int O, int C, void* dst, int dtype) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)O * C) return;
+  const int o = (int)(i % O);
+  const int c = (int)(i / O);
+  st_any(dst, dtype, i, src[(long)o * C + c]);
+}
+
+__global__ void k_vec_add(const float* a, const float* b, float* dst, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = a[i] + (b ? b[i] : 0.f);
+}
+
+__global__ void k_cast(const void* src, int sdt, void* dst, int ddt, long n) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (long)gridDim.x * blockDim.x)
+    st_any(dst, ddt, i, ld_any(src, sdt, i));
+}
+
+unsigned nblk(long n, int t = 256) { return (unsigned)((n + t - 1) / t); }
+
+}  // namespace
+
+hipError_t launch_temb_fwd(const void* temb, int dtype, int B, int D, int O, const float* Wl,
+                           const float* bias_a, const float* bias_b, float* e,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(k_temb_fwd, dim3(O, B), dim3(64), 0, st, temb, dtype, D, O, Wl, bias_a,
+                     bias_b, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, int D, int O,
+                           const float* Wl, float* dWl, float* dbl, float* db1, float* dtemb,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(k_temb_bwd_w, dim3(nblk((long)O * (D + 1))), dim3(256), 0, st, de, temb,
+                     dtype, B, D, O, dWl, dbl, db1);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !dtemb) return e;
+  hipLaunchKernelGGL(k_temb_bwd_x, dim3(nblk((long)B * D)), dim3(256), 0, st, de, temb, dtype,
+                     B, D, O, Wl, dtemb);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_rows(const float* src, int rows, int cols, void* dst, int ldd,
+                               int col_off, int dtype, hipStream_t st) {
+  hipLaunchKernelGGL(k_convert_rows, dim3(nblk((long)rows * cols)), dim3(256), 0, st, src, rows,
+                     cols, dst, ldd, col_off, dtype);
+  return hipGetLastError();
+}
+
+hipError_t launch_flip3x3(const float* src, int O, int C, void* dst, int dtype,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(k_flip3x3, dim3(nblk((long)O * 9 * C)), dim3(256), 0, st, src, O, C, dst,
+                     dtype);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose(const float* src, int O, int C, void* dst, int dtype,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(k_transpose, dim3(nblk((long)O * C)), dim3(256), 0, st, src, O, C, dst,
+                     dtype);
+  return hipGetLastError();
+}
+
+hipError_t launch_vec_add(const float* a, const float* b, float* dst, int n, hipStream_t st) {
+  hipLaunchKernelGGL(k_vec_add, dim3(nblk(n)), dim3(256), 0, st, a, b, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast(const void* src, int sdt, void* dst, int ddt, long n, hipStream_t st) {
+  long b = (n + 255) / 256;
+  if (b > 8192) b = 8192;
+  if (b < 1) b = 1;
+  hipLaunchKernelGGL(k_cast, dim3((unsigned)b), dim3(256), 0, st, src, sdt, dst, ddt, n);
+  return hipGetLastError();
+}
+
+}  // namespace pulse

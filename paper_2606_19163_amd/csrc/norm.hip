@@ -1,0 +1,417 @@
+// GroupNorm + SiLU forward/backward and per-channel reductions over NHWC
+// activations (gfx950).  All of it is HBM-bound streaming: a block owns one
+// image, one chunk of pixels and 64 channel vectors of 8 channels; its 256
+// threads are 64 channel vectors x 4 pixel lanes, so each pixel row of a
+// block is one contiguous, coalesced read.  Reductions are deterministic:
+// fixed per-thread order, a fixed LDS tree, per-(image, chunk) partials and
+// a finalize that sums them in a fixed order (group sums in fp64).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace pulse {
+
+namespace {
+
+constexpr int VX = 64;  // channel vectors per block
+constexpr int PY = 4;   // pixel lanes per block
+
+struct Range {
+  int b, p0, p1, v, c;
+  bool active;
+};
+
+__device__ __forceinline__ Range block_range(const Geo& g, RedGrid rg, int C) {
+  Range r;
+  r.b = blockIdx.x;
+  r.p0 = blockIdx.y * rg.cp;
+  r.p1 = min(r.p0 + rg.cp, g.hw());
+  r.v = blockIdx.z * VX + threadIdx.x;
+  r.c = r.v * 8;
+  r.active = r.c < C;
+  return r;
+}
+
+// Sum the 4 pixel lanes of NV values per thread through LDS and let lane 0
+// write them to out[0..NV) (out already offset by channel).
+template <int NV>
+__device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, bool active,
+                                                  float* out0, float* out1) {
+  const int tx = threadIdx.x, ty = threadIdx.y;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) sm[(ty * VX + tx) * NV + i] = v[i];
+  __syncthreads();
+  if (ty == 0 && active) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      float s = sm[tx * NV + i];
+#pragma unroll
+      for (int y = 1; y < PY; ++y) s += sm[(y * VX + tx) * NV + i];
+      v[i] = s;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) out0[i] = v[i];
+    if (out1) {
+#pragma unroll
+      for (int i = 0; i < 8 && 8 + i < NV; ++i) out1[i] = v[8 + i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid rg,
+                                                          float* partial) {
+  __shared__ float sm[PY * VX * 16];
+  const Range r = block_range(g, rg, x.C);
+  float acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  if (r.active) {
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+      float f[8];
+      ld8v(x, (long)r.b * g.hw() + p, r.c, f);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        acc[i] += f[i];
+        acc[8 + i] += f[i] * f[i];
+      }
+    }
+  }
+  float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
+  lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
+}
+
+__global__ __launch_bounds__(256) void k_gn_stats_finalize(const float* partial, Geo g,
+                                                           RedGrid rg, int C, int G, float eps,
+                                                           const float* gamma, const float* beta,
+                                                           float* mean, float* rstd,
+                                                           float* scale, float* shift) {
+  __shared__ float sm_mean[256], sm_rstd[256];
+  const int b = blockIdx.x;
+  const int cg = C / G;
+  const double cnt = (double)g.hw() * cg;
+  for (int gi = threadIdx.x; gi < G; gi += blockDim.x) {
+    double S = 0.0, Q = 0.0;
+    for (int ch = 0; ch < rg.chunks; ++ch) {
+      const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+      for (int c = gi * cg; c < (gi + 1) * cg; ++c) {
+        S += base[c];
+        Q += base[C + c];
+      }
+    }
+    const double m = S / cnt;
+    double var = Q / cnt - m * m;
+    if (var < 0.0) var = 0.0;
+    const float rs = (float)(1.0 / sqrt(var + (double)eps));
+    sm_mean[gi] = (float)m;
+    sm_rstd[gi] = rs;
+    mean[b * G + gi] = (float)m;
+    rstd[b * G + gi] = rs;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    const int gi = c / cg;
+    const float sc = gamma[c] * sm_rstd[gi];
+    scale[(long)b * C + c] = sc;
+    shift[(long)b * C + c] = beta[c] - sm_mean[gi] * sc;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gn_apply(VIn x, Geo g, const float* scale,
+                                                  const float* shift, void* dst0, void* dst1,
+                                                  int dtype) {
+  const int NV = x.C / 8;
+  const long total = g.pixels() * NV;
+  const int HW = g.hw();
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long)gridDim.x * blockDim.x) {
+    const long pix = i / NV;
+    const int c = (int)(i - pix * NV) * 8;
+    const int b = (int)(pix / HW);
+    float f[8];
+    ld8v(x, pix, c, f);
+    const float4* sc = reinterpret_cast<const float4*>(scale + (long)b * x.C + c);
+    const float4* sh = reinterpret_cast<const float4*>(shift + (long)b * x.C + c);
+    const float4 s0 = sc[0], s1 = sc[1], h0 = sh[0], h1 = sh[1];
+    const float ss[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+    const float hh[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = silu_f(f[j] * ss[j] + hh[j]);
+    if (c < x.c0)
+      st8(dst0, dtype, x.c0, pix, c, f);
+    else
+      st8(dst1, dtype, x.C - x.c0, pix, c - x.c0, f);
+  }
+}
+
+// Per-thread constants of the GroupNorm backward for 8 channels of image b.
+struct GnConst {
+  float sc[8], sh[8], mu[8], rs[8];
+};
+
+__device__ __forceinline__ void load_gn_const(GnConst& k, int b, int c, int C, int G,
+                                              const float* scale, const float* shift,
+                                              const float* mean, const float* rstd) {
+  const int cg = C / G;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int gi = (c + j) / cg;
+    k.sc[j] = scale[(long)b * C + c + j];
+    k.sh[j] = shift[(long)b * C + c + j];
+    k.mu[j] = mean[b * G + gi];
+    k.rs[j] = rstd[b * G + gi];
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, Geo g,
+                                                        RedGrid rg, const float* scale,
+                                                        const float* shift, const float* mean,
+                                                        const float* rstd, int G,
+                                                        float* partial) {
+  __shared__ float sm[PY * VX * 16];
+  const Range r = block_range(g, rg, x.C);
+  float acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  if (r.active) {
+    GnConst k;
+    load_gn_const(k, r.b, r.c, x.C, G, scale, shift, mean, rstd);
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+      const long pix = (long)r.b * g.hw() + p;
+      float f[8], d[8];
+      ld8v(x, pix, r.c, f);
+      const float4* dp = reinterpret_cast<const float4*>(da + pix * x.C + r.c);
+      const float4 d0 = dp[0], d1 = dp[1];
+      d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
+      d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float z = f[j] * k.sc[j] + k.sh[j];
+        const float dz = d[j] * dsilu_f(z);
+        const float xh = (f[j] - k.mu[j]) * k.rs[j];
+        acc[j] += dz;
+        acc[8 + j] += dz * xh;
+      }
+    }
+  }
+  float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
+  lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
+}
+
+__global__ __launch_bounds__(256) void k_gn_bwd_coef(const float* partial, Geo g, RedGrid rg,
+                                                     int C, int G, const float* gamma,
+                                                     float* coef) {
+  const int b = blockIdx.x;
+  const int cg = C / G;
+  const double cnt = (double)g.hw() * cg;
+  for (int gi = threadIdx.x; gi < G; gi += blockDim.x) {
+    double S1 = 0.0, S2 = 0.0;
+    for (int ch = 0; ch < rg.chunks; ++ch) {
+      const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+      for (int c = gi * cg; c < (gi + 1) * cg; ++c) {
+        S1 += (double)gamma[c] * base[c];
+        S2 += (double)gamma[c] * base[C + c];
+      }
+    }
+    coef[(b * G + gi) * 2 + 0] = (float)(S1 / cnt);
+    coef[(b * G + gi) * 2 + 1] = (float)(S2 / cnt);
+  }
+}
+
+// out0[c] += sum_{b,chunk} partial[..][0][c]; out1[c] += ..[1][c] (nullable);
+// per_image[b][c] = sum_chunk partial[b][..][0][c] (nullable); acc1 gets the
+// same total as out0 when `dup` is set (a second bias sharing the gradient).
+__global__ void k_chan_finalize(const float* partial, int B, int chunks, int C, float* out0,
+                                float* out1, float* dup, float* per_image) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  float t0 = 0.f, t1 = 0.f;
+  for (int b = 0; b < B; ++b) {
+    float s0 = 0.f, s1 = 0.f;
+    for (int ch = 0; ch < chunks; ++ch) {
+      const float* base = partial + ((long)b * chunks + ch) * 2 * C;
+      s0 += base[c];
+      if (out1) s1 += base[C + c];
+    }
+    if (per_image) per_image[(long)b * C + c] = s0;
+    t0 += s0;
+    t1 += s1;
+  }
+  if (out0) out0[c] += t0;
+  if (dup) dup[c] += t0;
+  if (out1) out1[c] += t1;
+}
+
+__global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Geo g,
+                                                      RedGrid rg, const float* scale,
+                                                      const float* shift, const float* mean,
+                                                      const float* rstd, const float* gamma,
+                                                      const float* coef, int G, GnBwdOut o) {
+  __shared__ float sm[PY * VX * 8];
+  const Range r = block_range(g, rg, x.C);
+  const int C = x.C;
+  const int cg = C / G;
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  if (r.active) {
+    GnConst k;
+    load_gn_const(k, r.b, r.c, C, G, scale, shift, mean, rstd);
+    float ga[8], c0[8], c1[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int gi = (r.c + j) / cg;
+      ga[j] = gamma[r.c + j];
+      c0[j] = coef[(r.b * G + gi) * 2 + 0];
+      c1[j] = coef[(r.b * G + gi) * 2 + 1];
+    }
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+      const long pix = (long)r.b * g.hw() + p;
+      float f[8], d[8], out[8];
+      ld8v(x, pix, r.c, f);
+      const float4* dp = reinterpret_cast<const float4*>(da + pix * C + r.c);
+      const float4 d0 = dp[0], d1 = dp[1];
+      d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
+      d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float z = f[j] * k.sc[j] + k.sh[j];
+        const float dz = d[j] * dsilu_f(z);
+        const float xh = (f[j] - k.mu[j]) * k.rs[j];
+        out[j] = k.rs[j] * (ga[j] * dz - c0[j] - xh * c1[j]);
+      }
+      if (o.add0.s0.ptr) {
+        float e[8];
+        ld8v(o.add0, pix, r.c, e);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) out[j] += e[j];
+      }
+      if (o.add1) {
+        const float4* ap = reinterpret_cast<const float4*>(o.add1 + pix * C + r.c);
+        const float4 a0 = ap[0], a1 = ap[1];
+        out[0] += a0.x; out[1] += a0.y; out[2] += a0.z; out[3] += a0.w;
+        out[4] += a1.x; out[5] += a1.y; out[6] += a1.z; out[7] += a1.w;
+      }
+      if (r.c < o.c_split)
+        st8(o.dst0, o.dtype0, o.c_split, pix, r.c, out);
+      else
+        st8(o.dst1, o.dtype1, C - o.c_split, pix, r.c - o.c_split, out);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] += out[j];
+    }
+  }
+  if (o.chan_partial) {
+    float* base = o.chan_partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * C;
+    lane_reduce_store<8>(acc, sm, r.active, base + r.c, nullptr);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid rg,
+                                                          float* partial) {
+  __shared__ float sm[PY * VX * 8];
+  const Range r = block_range(g, rg, v.C);
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  if (r.active) {
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+      float f[8];
+      ld8v(v, (long)r.b * g.hw() + p, r.c, f);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] += f[j];
+    }
+  }
+  float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * v.C;
+  lane_reduce_store<8>(acc, sm, r.active, base + r.c, nullptr);
+}
+
+dim3 red_dims(const Geo& g, RedGrid rg, int C) {
+  const int nvb = (C / 8 + VX - 1) / VX;
+  return dim3(g.B, rg.chunks, nvb);
+}
+
+}  // namespace
+
+RedGrid red_grid(const Geo& g, int C) {
+  const int nvb = (C / 8 + VX - 1) / VX;
+  const int hw = g.hw();
+  int chunks = 2048 / (g.B * nvb);
+  const int max_chunks = (hw + 15) / 16;
+  if (chunks > max_chunks) chunks = max_chunks;
+  if (chunks < 1) chunks = 1;
+  RedGrid rg;
+  rg.cp = (hw + chunks - 1) / chunks;
+  rg.chunks = (hw + rg.cp - 1) / rg.cp;
+  return rg;
+}
+
+hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
+                                   hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_stats_partial, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, x, g, rg,
+                     partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                    int G, float eps, const float* gamma, const float* beta,
+                                    float* mean, float* rstd, float* scale, float* shift,
+                                    hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_stats_finalize, dim3(g.B), dim3(256), 0, st, partial, g, rg, C, G,
+                     eps, gamma, beta, mean, rstd, scale, shift);
+  return hipGetLastError();
+}
+
+hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale, const float* shift,
+                           void* dst0, void* dst1, int dtype, hipStream_t st) {
+  const long total = g.pixels() * (x.C / 8);
+  long blocks = (total + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_gn_apply, dim3((unsigned)blocks), dim3(256), 0, st, x, g, scale, shift,
+                     dst0, dst1, dtype);
+  return hipGetLastError();
+}
+
+hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+                                 const float* scale, const float* shift, const float* mean,
+                                 const float* rstd, int G, float* partial, hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_bwd_partial, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, da, x, g, rg,
+                     scale, shift, mean, rstd, G, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                  int G, const float* gamma, float* coef, float* dgamma,
+                                  float* dbeta, hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_bwd_coef, dim3(g.B), dim3(256), 0, st, partial, g, rg, C, G, gamma,
+                     coef);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // dbeta from slot 0 (sum dz), dgamma from slot 1 (sum dz * xhat)
+  hipLaunchKernelGGL(k_chan_finalize, dim3((C + 255) / 256), dim3(256), 0, st, partial, g.B,
+                     rg.chunks, C, dbeta, dgamma, (float*)nullptr, (float*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+                               const float* scale, const float* shift, const float* mean,
+                               const float* rstd, const float* gamma, const float* coef,
+                               int G, const GnBwdOut& o, hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_bwd_apply, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, da, x, g, rg,
+                     scale, shift, mean, rstd, gamma, coef, G, o);
+  return hipGetLastError();
+}
+
+hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
+                                   hipStream_t st) {
+  hipLaunchKernelGGL(k_chan_sum_partial, red_dims(g, rg, v.C), dim3(VX, PY), 0, st, v, g, rg,
+                     partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
+                                    float* acc0, float* acc1, float* per_image,
+                                    hipStream_t st) {
+  hipLaunchKernelGGL(k_chan_finalize, dim3((C + 255) / 256), dim3(256), 0, st, partial, g.B,
+                     rg.chunks, C, acc0, (float*)nullptr, acc1, per_image);
+  return hipGetLastError();
+}
+
+}  // namespace pulse

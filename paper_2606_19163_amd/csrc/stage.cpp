@@ -1,0 +1,1186 @@
+// Host side of the stage library: descriptor validation, parameter and
+// workspace layout, the skip cache and per-microbatch bookkeeping, and the
+// kernel sequence of every forward / backward half.  Implements
+// include/pulse_stage.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "pulse_stage.h"
+
+using namespace pulse;
+
+namespace {
+
+thread_local std::string g_err;
+
+pulse_status fail(pulse_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIPCHK(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(PULSE_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+constexpr int MAX_SLOTS = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+enum RowState { R_FRESH = 1, R_ENC_FWD = 2, R_DEC_FWD = 3, R_DEC_BWD = 4 };
+
+struct ParamInfo {
+  std::string name;
+  int64_t off;
+  int32_t shape[4];
+  int64_t numel;
+};
+
+// Offsets of one GroupNorm's saved statistics inside a row.
+struct GnSave {
+  size_t mean, rstd, scale, shift;
+};
+
+struct Block {
+  bool dec;
+  int cin, cout, c0;  // c0: channels of the first source (dec: c_up)
+  int slot;           // enc: skip_slot_out, dec: skip_slot_in
+  bool conv_sc;
+  // parameter offsets (elements)
+  int64_t W1, b1, Wl, bl, g1, be1, g2, be2, W2, b2, Ws, bs;
+  // compute copies of the weights (workspace byte offsets)
+  size_t wf1, wf2, wd1, wd2, wsd, bias2;
+  int ldb2;
+  // per-row saved tensors (byte offsets inside a row)
+  size_t a1_0, a1_1, h1, a2, out_saved;
+  GnSave gn1, gn2;
+};
+
+struct Row {
+  int mb = -1;
+  int state = 0;
+  bool enc_done = false;
+  uint8_t act[MAX_SLOTS] = {};
+  uint8_t grad[MAX_SLOTS] = {};
+};
+
+struct TimedLaunch {
+  hipEvent_t a, b;
+  double flops;
+};
+
+}  // namespace
+
+struct pulse_stage {
+  // descriptor
+  pulse_stage_desc d{};
+  std::vector<pulse_enc_block> enc;
+  std::vector<pulse_dec_block> dec;
+  bool dry = false;
+  int dtype = DT_F32;
+  size_t esz = 4;
+  int gcfg = 2;
+  Geo geo{};
+  long P = 0;
+  int G = 1;
+  float eps = 1e-5f;
+  int D = 0;
+  // parameters
+  std::vector<ParamInfo> params;
+  int64_t n_params = 0;
+  std::vector<Block> eb, db;
+  // slots
+  int n_slots = 0;
+  int slot_ch[MAX_SLOTS];
+  int slot_reader[MAX_SLOTS];   // decoder block index or -1
+  int slot_producer[MAX_SLOTS]; // encoder block index, -2 = stage input, -1 = none
+  // workspace layout
+  size_t ws_bytes = 0, off_rows = 0, row_size = 0, off_scratch = 0;
+  size_t row_act[MAX_SLOTS], row_grad[MAX_SLOTS];
+  size_t row_temb[2] = {0, 0}, row_xin = 0, row_u = 0;
+  size_t s_da = 0, s_dxs = 0, s_dh1 = 0, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
+         s_de = 0, s_e = 0;
+  size_t part_cap = 0;
+  // binding
+  const float* prm = nullptr;
+  float* grd = nullptr;
+  char* ws = nullptr;
+  bool bound = false;
+  bool synced = false;
+  std::vector<Row> rows;
+  // timing of the implicit-GEMM conv launches
+  bool timing = false;
+  std::vector<TimedLaunch> timed;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+
+  char* row_base(int r) const { return ws + off_rows + (size_t)r * row_size; }
+  void* scratch(size_t off) const { return ws + off_scratch + off; }
+  float* sf(size_t off) const { return reinterpret_cast<float*>(scratch(off)); }
+  const float* pp(int64_t off) const { return prm + off; }
+  float* gp(int64_t off) const { return off < 0 ? nullptr : grd + off; }
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// layout
+// ---------------------------------------------------------------------------
+
+int64_t add_param(pulse_stage* s, const std::string& name, std::initializer_list<int> shape) {
+  ParamInfo p;
+  p.name = name;
+  p.off = s->n_params;
+  int i = 0;
+  p.numel = 1;
+  for (int x : shape) {
+    p.shape[i++] = x;
+    p.numel *= x;
+  }
+  for (; i < 4; ++i) p.shape[i] = 0;
+  s->params.push_back(p);
+  s->n_params += (p.numel + 63) / 64 * 64;
+  return p.off;
+}
+
+void layout_params(pulse_stage* s, Block& b, const std::string& pre) {
+  b.W1 = add_param(s, pre + "W1", {b.cout, 3, 3, b.cin});
+  b.b1 = add_param(s, pre + "b1", {b.cout});
+  b.Wl = add_param(s, pre + "Wl", {b.cout, s->D});
+  b.bl = add_param(s, pre + "bl", {b.cout});
+  b.g1 = add_param(s, pre + "g1", {b.cin});
+  b.be1 = add_param(s, pre + "be1", {b.cin});
+  b.g2 = add_param(s, pre + "g2", {b.cout});
+  b.be2 = add_param(s, pre + "be2", {b.cout});
+  b.W2 = add_param(s, pre + "W2", {b.cout, 3, 3, b.cout});
+  b.b2 = add_param(s, pre + "b2", {b.cout});
+  if (b.conv_sc) {
+    b.Ws = add_param(s, pre + "Ws", {b.cout, b.cin});
+    b.bs = add_param(s, pre + "bs", {b.cout});
+  } else {
+    b.Ws = b.bs = -1;
+  }
+}
+
+size_t act_bytes(const pulse_stage* s, int C) { return (size_t)s->P * C * s->esz; }
+
+void layout_gn(const pulse_stage* s, GnSave& g, size_t& off, int C) {
+  g.mean = off;
+  off += align256((size_t)s->geo.B * s->G * 4);
+  g.rstd = off;
+  off += align256((size_t)s->geo.B * s->G * 4);
+  g.scale = off;
+  off += align256((size_t)s->geo.B * C * 4);
+  g.shift = off;
+  off += align256((size_t)s->geo.B * C * 4);
+}
+
+int pick_splits(const pulse_stage* s, int M, int N, int& kchunk) {
+  const int bm = gemm_bm(s->gcfg), bn = gemm_bn(s->gcfg), bk = gemm_bk(s->gcfg);
+  const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  long splits = (512 + tiles - 1) / tiles;
+  const long maxs = (s->P + 255) / 256;
+  if (splits > maxs) splits = maxs;
+  if (splits < 1) splits = 1;
+  long kc = (s->P + splits - 1) / splits;
+  kc = (kc + bk - 1) / bk * bk;
+  kchunk = (int)kc;
+  return (int)((s->P + kc - 1) / kc);
+}
+
+pulse_status build_layout(pulse_stage* s) {
+  const pulse_stage_desc& d = s->d;
+  s->dtype = d.dtype == PULSE_BF16 ? DT_BF16 : DT_F32;
+  s->esz = d.dtype == PULSE_BF16 ? 2 : 4;
+  s->geo = Geo{d.batch, d.height, d.width};
+  s->P = s->geo.pixels();
+  s->G = d.groups;
+  s->eps = d.eps;
+  s->D = d.temb_dim;
+
+  // blocks and parameters
+  int cmax = 0;
+  for (int k = 0; k < d.n_enc; ++k) {
+    Block b{};
+    b.dec = false;
+    b.cin = s->enc[k].c_in;
+    b.cout = s->enc[k].c_out;
+    b.c0 = b.cin;
+    b.slot = s->enc[k].skip_slot_out;
+    b.conv_sc = b.cin != b.cout;
+    layout_params(s, b, "enc" + std::to_string(k) + ".");
+    s->eb.push_back(b);
+    cmax = std::max(cmax, std::max(b.cin, b.cout));
+  }
+  for (int k = 0; k < d.n_dec; ++k) {
+    Block b{};
+    b.dec = true;
+    b.cin = s->dec[k].c_up + s->dec[k].c_skip;
+    b.cout = s->dec[k].c_out;
+    b.c0 = s->dec[k].c_up;
+    b.slot = s->dec[k].skip_slot_in;
+    b.conv_sc = b.cin != b.cout;
+    layout_params(s, b, "dec" + std::to_string(k) + ".");
+    s->db.push_back(b);
+    cmax = std::max(cmax, std::max(b.cin, b.cout));
+  }
+
+  // bf16 tiles take 64 channels per K-step when every channel count allows
+  if (s->dtype == DT_F32) {
+    s->gcfg = 2;
+  } else {
+    bool k64 = true;
+    auto chk = [&](int c) { if (c % 64) k64 = false; };
+    for (auto& b : s->eb) { chk(b.cin); chk(b.cout); chk(b.c0); }
+    for (auto& b : s->db) { chk(b.cin); chk(b.cout); chk(b.c0); }
+    s->gcfg = k64 ? 0 : 1;
+  }
+
+  // workspace: weight copies | rows | scratch
+  size_t off = 0;
+  for (auto* v : {&s->eb, &s->db})
+    for (auto& b : *v) {
+      b.wf1 = off; off += align256((size_t)b.cout * 9 * b.cin * s->esz);
+      b.ldb2 = 9 * b.cout + (b.conv_sc ? b.cin : 0);
+      b.wf2 = off; off += align256((size_t)b.cout * b.ldb2 * s->esz);
+      b.wd1 = off; off += align256((size_t)b.cin * 9 * b.cout * s->esz);
+      b.wd2 = off; off += align256((size_t)b.cout * 9 * b.cout * s->esz);
+      b.wsd = off; off += b.conv_sc ? align256((size_t)b.cin * b.cout * s->esz) : 0;
+      b.bias2 = off; off += align256((size_t)b.cout * 4);
+    }
+  s->off_rows = off;
+
+  // one row per in-flight microbatch
+  size_t r = 0;
+  for (int sl = 0; sl < s->n_slots; ++sl) {
+    s->row_act[sl] = r;
+    r += s->slot_ch[sl] ? align256(act_bytes(s, s->slot_ch[sl])) : 0;
+    s->row_grad[sl] = r;
+    r += s->slot_ch[sl] ? align256((size_t)s->P * s->slot_ch[sl] * 4) : 0;
+  }
+  for (int h = 0; h < 2; ++h) {
+    s->row_temb[h] = r;
+    r += align256((size_t)s->geo.B * s->D * s->esz);
+  }
+  s->row_xin = r; r += d.input_skip_slot >= 0 ? 0 : align256(act_bytes(s, s->eb[0].cin));
+  s->row_u = r; r += align256(act_bytes(s, s->db[0].c0));
+  for (auto* v : {&s->eb, &s->db})
+    for (auto& b : *v) {
+      b.a1_0 = r; r += align256(act_bytes(s, b.c0));
+      b.a1_1 = r; r += b.cin > b.c0 ? align256(act_bytes(s, b.cin - b.c0)) : 0;
+      b.h1 = r; r += align256(act_bytes(s, b.cout));
+      b.a2 = r; r += align256(act_bytes(s, b.cout));
+      b.out_saved = r; r += align256(act_bytes(s, b.cout));
+      layout_gn(s, b.gn1, r, b.cin);
+      layout_gn(s, b.gn2, r, b.cout);
+    }
+  s->row_size = align256(r);
+  off += s->row_size * d.max_inflight;
+  s->off_scratch = off;
+
+  // scratch shared by all calls
+  size_t sc = 0;
+  const size_t fbig = align256((size_t)s->P * cmax * 4);
+  s->s_da = sc; sc += fbig;
+  s->s_dxs = sc; sc += fbig;
+  s->s_dh1 = sc; sc += fbig;
+  s->s_g[0] = sc; sc += fbig;
+  s->s_g[1] = sc; sc += fbig;
+  size_t part = 0, red = 0;
+  for (auto* v : {&s->eb, &s->db})
+    for (auto& b : *v) {
+      int kc;
+      int sp = pick_splits(s, b.cout, b.ldb2, kc);
+      part = std::max(part, (size_t)sp * b.cout * b.ldb2);
+      sp = pick_splits(s, b.cout, 9 * b.cin, kc);
+      part = std::max(part, (size_t)sp * b.cout * 9 * b.cin);
+      for (int c : {b.cin, b.cout}) {
+        RedGrid rg = red_grid(s->geo, c);
+        red = std::max(red, (size_t)s->geo.B * rg.chunks * 2 * c);
+      }
+    }
+  s->part_cap = part;
+  s->s_part = sc; sc += align256(part * 4);
+  s->s_red = sc; sc += align256(red * 4);
+  s->s_coef = sc; sc += align256((size_t)s->geo.B * s->G * 2 * 4);
+  s->s_de = sc; sc += align256((size_t)s->geo.B * cmax * 4);
+  s->s_e = sc; sc += align256((size_t)s->geo.B * cmax * 4);
+  s->ws_bytes = s->off_scratch + sc;
+  return PULSE_OK;
+}
+
+pulse_status validate_desc(const pulse_stage_desc* d) {
+  if (!d) return fail(PULSE_E_INVALID_ARG, "desc is NULL");
+  if (d->dtype != PULSE_F32 && d->dtype != PULSE_BF16)
+    return fail(PULSE_E_INVALID_ARG, "dtype %d unknown", (int)d->dtype);
+  if (d->batch < 1 || d->height < 1 || d->width < 1)
+    return fail(PULSE_E_SHAPE, "batch/height/width must be >= 1");
+  if ((long)d->batch * d->height * d->width > (1L << 28))
+    return fail(PULSE_E_SHAPE, "too many pixels");
+  if (d->groups < 1 || d->groups > 256) return fail(PULSE_E_SHAPE, "groups must be in [1, 256]");
+  if (!(d->eps >= 0.0f)) return fail(PULSE_E_SHAPE, "eps must be >= 0");
+  if (d->temb_dim < 1) return fail(PULSE_E_SHAPE, "temb_dim must be >= 1");
+  if (d->n_enc < 1 || d->n_dec < 1 || !d->enc || !d->dec)
+    return fail(PULSE_E_SHAPE, "need at least one encoder and one decoder block");
+  if (d->max_inflight < 1 || d->max_inflight > 64)
+    return fail(PULSE_E_SHAPE, "max_inflight must be in [1, 64]");
+  auto okc = [&](int c) { return c >= 32 && c % 32 == 0 && c % d->groups == 0 && c <= 8192; };
+  for (int k = 0; k < d->n_enc; ++k) {
+    const auto& b = d->enc[k];
+    if (!okc(b.c_in) || !okc(b.c_out))
+      return fail(PULSE_E_SHAPE, "enc[%d]: channels must be multiples of 32 and of groups", k);
+    if (k > 0 && b.c_in != d->enc[k - 1].c_out)
+      return fail(PULSE_E_SHAPE, "enc[%d].c_in != enc[%d].c_out", k, k - 1);
+    if (b.skip_slot_out < -1 || b.skip_slot_out >= MAX_SLOTS)
+      return fail(PULSE_E_SHAPE, "enc[%d].skip_slot_out out of range", k);
+  }
+  for (int k = 0; k < d->n_dec; ++k) {
+    const auto& b = d->dec[k];
+    if (!okc(b.c_up) || !okc(b.c_skip) || !okc(b.c_out) || !okc(b.c_up + b.c_skip))
+      return fail(PULSE_E_SHAPE, "dec[%d]: channels must be multiples of 32 and of groups", k);
+    if (b.c_up + b.c_skip == b.c_out)
+      return fail(PULSE_E_SHAPE, "dec[%d]: c_up + c_skip must differ from c_out", k);
+    if (k > 0 && b.c_up != d->dec[k - 1].c_out)
+      return fail(PULSE_E_SHAPE, "dec[%d].c_up != dec[%d].c_out", k, k - 1);
+    if (b.skip_slot_in < 0 || b.skip_slot_in >= MAX_SLOTS)
+      return fail(PULSE_E_SHAPE, "dec[%d].skip_slot_in out of range", k);
+  }
+  if (d->input_skip_slot < -1 || d->input_skip_slot >= MAX_SLOTS)
+    return fail(PULSE_E_SHAPE, "input_skip_slot out of range");
+  return PULSE_OK;
+}
+
+pulse_status build_slots(pulse_stage* s) {
+  const pulse_stage_desc& d = s->d;
+  for (int i = 0; i < MAX_SLOTS; ++i) {
+    s->slot_ch[i] = 0;
+    s->slot_reader[i] = -1;
+    s->slot_producer[i] = -1;
+  }
+  int n = 0;
+  auto produce = [&](int slot, int ch, int who) -> pulse_status {
+    if (slot < 0) return PULSE_OK;
+    if (s->slot_producer[slot] != -1)
+      return fail(PULSE_E_SHAPE, "skip slot %d has two producers", slot);
+    s->slot_producer[slot] = who;
+    s->slot_ch[slot] = ch;
+    n = std::max(n, slot + 1);
+    return PULSE_OK;
+  };
+  pulse_status st;
+  if ((st = produce(d.input_skip_slot, d.enc[0].c_in, -2)) != PULSE_OK) return st;
+  for (int k = 0; k < d.n_enc; ++k)
+    if ((st = produce(d.enc[k].skip_slot_out, d.enc[k].c_out, k)) != PULSE_OK) return st;
+  for (int k = 0; k < d.n_dec; ++k) {
+    const int sl = d.dec[k].skip_slot_in;
+    if (s->slot_producer[sl] == -1)
+      return fail(PULSE_E_SHAPE, "dec[%d] reads skip slot %d that nothing fills", k, sl);
+    if (s->slot_reader[sl] != -1)
+      return fail(PULSE_E_SHAPE, "skip slot %d is read by two decoder blocks", sl);
+    if (s->slot_ch[sl] != d.dec[k].c_skip)
+      return fail(PULSE_E_SHAPE, "dec[%d].c_skip %d != slot %d channels %d", k,
+                  d.dec[k].c_skip, sl, s->slot_ch[sl]);
+    s->slot_reader[sl] = k;
+  }
+  s->n_slots = n;
+  return PULSE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// rows (skip cache + per-microbatch state)
+// ---------------------------------------------------------------------------
+
+int find_row(const pulse_stage* s, int mb) {
+  for (size_t i = 0; i < s->rows.size(); ++i)
+    if (s->rows[i].mb == mb) return (int)i;
+  return -1;
+}
+
+int free_row(const pulse_stage* s) {
+  for (size_t i = 0; i < s->rows.size(); ++i)
+    if (s->rows[i].mb < 0) return (int)i;
+  return -1;
+}
+
+void release_row(Row& r) { r = Row(); }
+
+bool row_empty(const pulse_stage* s, const Row& r) {
+  for (int i = 0; i < s->n_slots; ++i)
+    if (r.act[i] || r.grad[i]) return false;
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// kernel sequencing helpers
+// ---------------------------------------------------------------------------
+
+Src src_of(const void* p, int dtype, int C) { return Src{p, dtype, C}; }
+
+VIn vin1(const void* p, int dtype, int C, const float* add = nullptr) {
+  VIn v;
+  v.s0 = src_of(p, dtype, C);
+  v.s1 = src_of(nullptr, dtype, 0);
+  v.c0 = C;
+  v.C = C;
+  v.add = add;
+  return v;
+}
+
+VIn vin2(const void* p0, int dt0, int c0, const void* p1, int dt1, int c1) {
+  VIn v;
+  v.s0 = src_of(p0, dt0, c0);
+  v.s1 = src_of(p1, dt1, c1);
+  v.c0 = c0;
+  v.C = c0 + c1;
+  v.add = nullptr;
+  return v;
+}
+
+VIn vnone() {
+  VIn v{};
+  v.s0.ptr = nullptr;
+  return v;
+}
+
+hipEvent_t next_event(pulse_stage* s) {
+  if (s->ev_used == s->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    s->ev_pool.push_back(e);
+  }
+  return s->ev_pool[s->ev_used++];
+}
+
+pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (s->timing) {
+    e0 = next_event(s);
+    e1 = next_event(s);
+    if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
+  }
+  HIPCHK(launch_conv(a, s->gcfg, st));
+  if (s->timing && e0 && e1) {
+    HIPCHK(hipEventRecord(e1, st));
+    s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K});
+  }
+  return PULSE_OK;
+}
+
+GemmArgs gemm_base(const pulse_stage* s) {
+  GemmArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.g = s->geo;
+  a.resid = vnone();
+  a.gy = vnone();
+  return a;
+}
+
+Seg seg3(int begin, int C, const VIn& in, float* grad = nullptr) {
+  Seg g;
+  g.begin = begin;
+  g.end = begin + 9 * C;
+  g.taps = 9;
+  g.C = C;
+  g.in = in;
+  g.grad = grad;
+  return g;
+}
+
+Seg seg1(int begin, int C, const VIn& in, float* grad = nullptr) {
+  Seg g;
+  g.begin = begin;
+  g.end = begin + C;
+  g.taps = 1;
+  g.C = C;
+  g.in = in;
+  g.grad = grad;
+  return g;
+}
+
+// forward conv: out[P][N] = sum_seg conv(seg) (+bias, +rowvec, +resid)
+pulse_status conv_fwd(pulse_stage* s, int N, std::initializer_list<Seg> segs, const void* W,
+                      int ldb, const float* bias, const float* rowvec, const VIn& resid,
+                      void* out, void* out2, int out_dtype, hipStream_t st) {
+  GemmArgs a = gemm_base(s);
+  a.M = (int)s->P;
+  a.N = N;
+  int k = 0;
+  for (const Seg& g : segs) {
+    a.seg[a.nseg++] = g;
+    k = g.end;
+  }
+  a.K = k;
+  a.Bw = W;
+  a.ldb = ldb;
+  a.bias = bias;
+  a.rowvec = rowvec;
+  a.resid = resid;
+  a.out = out;
+  a.out2 = out2;
+  a.out_dtype = out_dtype;
+  a.ldo = N;
+  return run_conv(s, a, st);
+}
+
+pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const VIn& gy,
+                   hipStream_t st) {
+  GemmArgs a = gemm_base(s);
+  a.M = M;
+  int n = 0;
+  for (const Seg& g : segs) {
+    a.seg[a.nseg++] = g;
+    n = g.end;
+  }
+  a.N = n;
+  a.K = (int)s->P;
+  a.gy = gy;
+  int kchunk;
+  const int splits = pick_splits(s, M, n, kchunk);
+  if ((size_t)splits * M * n > s->part_cap)
+    return fail(PULSE_E_SHAPE, "internal: wgrad partial buffer too small");
+  a.kchunk = kchunk;
+  a.part = s->sf(s->s_part);
+  HIPCHK(launch_wgrad(a, s->gcfg, splits, st));
+  return PULSE_OK;
+}
+
+pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
+                        const float* gamma, const float* beta, void* dst0, void* dst1,
+                        hipStream_t st) {
+  const RedGrid rg = red_grid(s->geo, x.C);
+  float* red = s->sf(s->s_red);
+  HIPCHK(launch_gn_stats_partial(x, s->geo, rg, red, st));
+  float* mean = reinterpret_cast<float*>(row + g.mean);
+  float* rstd = reinterpret_cast<float*>(row + g.rstd);
+  float* scale = reinterpret_cast<float*>(row + g.scale);
+  float* shift = reinterpret_cast<float*>(row + g.shift);
+  HIPCHK(launch_gn_stats_finalize(red, s->geo, rg, x.C, s->G, s->eps, gamma, beta, mean, rstd,
+                                  scale, shift, st));
+  HIPCHK(launch_gn_apply(x, s->geo, scale, shift, dst0, dst1, s->dtype, st));
+  return PULSE_OK;
+}
+
+// GroupNorm+SiLU backward: da (fp32 [P][C]) -> o (split store + addends)
+pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
+                         const float* gamma, float* dgamma, float* dbeta, const float* da,
+                         const GnBwdOut& o, hipStream_t st) {
+  const RedGrid rg = red_grid(s->geo, x.C);
+  float* red = s->sf(s->s_red);
+  float* coef = s->sf(s->s_coef);
+  const float* mean = reinterpret_cast<const float*>(row + g.mean);
+  const float* rstd = reinterpret_cast<const float*>(row + g.rstd);
+  const float* scale = reinterpret_cast<const float*>(row + g.scale);
+  const float* shift = reinterpret_cast<const float*>(row + g.shift);
+  HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
+  HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta, st));
+  GnBwdOut oo = o;
+  if (oo.chan_partial) oo.chan_partial = red;  // reuse: the partials above are consumed
+  HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, oo,
+                             st));
+  return PULSE_OK;
+}
+
+// The virtual input (block input) of block b for row `row`.
+VIn block_input(pulse_stage* s, int r, const Block& b, int k, const void* dec_up) {
+  char* row = s->row_base(r);
+  const int dt = s->dtype;
+  if (!b.dec) {
+    const void* p;
+    if (k == 0) {
+      p = s->d.input_skip_slot >= 0 ? row + s->row_act[s->d.input_skip_slot] : row + s->row_xin;
+    } else {
+      const Block& prev = s->eb[k - 1];
+      p = prev.slot >= 0 ? row + s->row_act[prev.slot] : row + prev.out_saved;
+    }
+    return vin1(p, dt, b.cin);
+  }
+  const void* up = dec_up;
+  if (!up) up = (k == 0) ? row + s->row_u : row + s->db[k - 1].out_saved;
+  return vin2(up, dt, b.c0, row + s->row_act[b.slot], dt, b.cin - b.c0);
+}
+
+// One ResBlock forward.  `out` receives the block output, `out2` a copy.
+pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin, void* out,
+                           void* out2, hipStream_t st) {
+  char* row = s->row_base(r);
+  const int dt = s->dtype;
+  void* a1_0 = row + b.a1_0;
+  void* a1_1 = row + b.a1_1;
+  pulse_status ps;
+  // a1 = SiLU(GN1(x)), one tensor per source
+  if ((ps = gn_forward(s, row, b.gn1, xin, s->pp(b.g1), s->pp(b.be1), a1_0, a1_1, st)) != PULSE_OK)
+    return ps;
+  // e = b1 + bl + Wl SiLU(temb)
+  float* e = s->sf(s->s_e);
+  HIPCHK(launch_temb_fwd(row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
+                         s->pp(b.b1), s->pp(b.bl), e, st));
+  const VIn a1 = (b.cin > b.c0) ? vin2(a1_0, dt, b.c0, a1_1, dt, b.cin - b.c0)
+                                : vin1(a1_0, dt, b.cin);
+  void* h1 = row + b.h1;
+  if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cin, a1)}, s->ws + b.wf1, 9 * b.cin, nullptr, e,
+                     vnone(), h1, nullptr, dt, st)) != PULSE_OK)
+    return ps;
+  // a2 = SiLU(GN2(h1))
+  const VIn h1v = vin1(h1, dt, b.cout);
+  void* a2 = row + b.a2;
+  if ((ps = gn_forward(s, row, b.gn2, h1v, s->pp(b.g2), s->pp(b.be2), a2, nullptr, st)) !=
+      PULSE_OK)
+    return ps;
+  const VIn a2v = vin1(a2, dt, b.cout);
+  const float* bias2 = reinterpret_cast<const float*>(s->ws + b.bias2);
+  if (b.conv_sc)
+    return conv_fwd(s, b.cout, {seg3(0, b.cout, a2v), seg1(9 * b.cout, b.cin, xin)},
+                    s->ws + b.wf2, b.ldb2, bias2, nullptr, vnone(), out, out2, dt, st);
+  return conv_fwd(s, b.cout, {seg3(0, b.cout, a2v)}, s->ws + b.wf2, b.ldb2, bias2, nullptr, xin,
+                  out, out2, dt, st);
+}
+
+// One ResBlock backward.  dout: gradient w.r.t. the block output.  o: where
+// the gradient w.r.t. the block input goes (split/addends set by caller;
+// the residual / shortcut addend is filled in here).
+pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xin,
+                            const VIn& dout, GnBwdOut o, float* dtemb, hipStream_t st) {
+  char* row = s->row_base(r);
+  const int dt = s->dtype;
+  pulse_status ps;
+  // bias gradients of conv2 (and of the 1x1 shortcut, which sees the same dY)
+  {
+    const RedGrid rg = red_grid(s->geo, b.cout);
+    HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, s->sf(s->s_red), st));
+    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, s->gp(b.b2),
+                                    b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, st));
+  }
+  // weight gradients of conv2 and the shortcut, one GEMM
+  const VIn a2v = vin1(row + b.a2, dt, b.cout);
+  if (b.conv_sc) {
+    if ((ps = wgrad(s, b.cout,
+                    {seg3(0, b.cout, a2v, s->gp(b.W2)), seg1(9 * b.cout, b.cin, xin, s->gp(b.Ws))},
+                    dout, st)) != PULSE_OK)
+      return ps;
+  } else {
+    if ((ps = wgrad(s, b.cout, {seg3(0, b.cout, a2v, s->gp(b.W2))}, dout, st)) != PULSE_OK)
+      return ps;
+  }
+  // data gradients through conv2 and the shortcut
+  float* da = s->sf(s->s_da);
+  if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cout, dout)}, s->ws + b.wd2, 9 * b.cout, nullptr,
+                     nullptr, vnone(), da, nullptr, DT_F32, st)) != PULSE_OK)
+    return ps;
+  float* dxs = s->sf(s->s_dxs);
+  if (b.conv_sc) {
+    if ((ps = conv_fwd(s, b.cin, {seg1(0, b.cout, dout)}, s->ws + b.wsd, b.cout, nullptr, nullptr,
+                       vnone(), dxs, nullptr, DT_F32, st)) != PULSE_OK)
+      return ps;
+  }
+  // GN2 backward -> dh1, with per-image channel sums (the temb gradient)
+  float* dh1 = s->sf(s->s_dh1);
+  {
+    GnBwdOut o2{};
+    o2.dst0 = dh1;
+    o2.dtype0 = DT_F32;
+    o2.c_split = b.cout;
+    o2.add0 = vnone();
+    o2.chan_partial = s->sf(s->s_red);
+    const VIn h1v = vin1(row + b.h1, dt, b.cout);
+    if ((ps = gn_backward(s, row, b.gn2, h1v, s->pp(b.g2), s->gp(b.g2), s->gp(b.be2), da, o2,
+                          st)) != PULSE_OK)
+      return ps;
+    const RedGrid rg = red_grid(s->geo, b.cout);
+    float* de = s->sf(s->s_de);
+    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, nullptr, nullptr, de,
+                                    st));
+    HIPCHK(launch_temb_bwd(de, row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
+                           s->gp(b.Wl), s->gp(b.bl), s->gp(b.b1), dtemb, st));
+  }
+  // conv1 weight and data gradients
+  const VIn a1 = (b.cin > b.c0) ? vin2(row + b.a1_0, dt, b.c0, row + b.a1_1, dt, b.cin - b.c0)
+                                : vin1(row + b.a1_0, dt, b.cin);
+  const VIn dh1v = vin1(dh1, DT_F32, b.cout);
+  if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, st)) != PULSE_OK)
+    return ps;
+  if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
+                     nullptr, vnone(), da, nullptr, DT_F32, st)) != PULSE_OK)
+    return ps;
+  // GN1 backward + residual path -> gradient w.r.t. the block input
+  o.add0 = b.conv_sc ? vin1(dxs, DT_F32, b.cin) : dout;
+  o.chan_partial = nullptr;
+  return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
+}
+
+pulse_status check_ptr(const void* p, const char* what) {
+  if (!p) return fail(PULSE_E_INVALID_ARG, "%s is NULL", what);
+  if (reinterpret_cast<uintptr_t>(p) % 16)
+    return fail(PULSE_E_INVALID_ARG, "%s is not 16-byte aligned", what);
+  return PULSE_OK;
+}
+
+pulse_status need_bound(const pulse_stage* s) {
+  if (s->dry) return PULSE_OK;
+  if (!s->bound) return fail(PULSE_E_NOT_BOUND, "stage has no bound parameters/workspace");
+  if (!s->synced) return fail(PULSE_E_NOT_BOUND, "pulse_stage_sync_params has not run");
+  return PULSE_OK;
+}
+
+double block_flops(const pulse_stage* s, const Block& b) {
+  const double P = (double)s->P;
+  double f = 2.0 * P * b.cout * 9 * b.cin + 2.0 * P * b.cout * 9 * b.cout +
+             2.0 * s->geo.B * b.cout * s->D;
+  if (b.conv_sc) f += 2.0 * P * b.cout * b.cin;
+  return f;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+
+extern "C" {
+
+const char* pulse_last_error(void) { return g_err.c_str(); }
+
+pulse_status pulse_stage_create(const pulse_stage_desc* desc, pulse_stage** out) {
+  if (!out) return fail(PULSE_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pulse_status st = validate_desc(desc);
+  if (st != PULSE_OK) return st;
+  pulse_stage* s = new (std::nothrow) pulse_stage();
+  if (!s) return fail(PULSE_E_INVALID_ARG, "out of host memory");
+  s->d = *desc;
+  s->enc.assign(desc->enc, desc->enc + desc->n_enc);
+  s->dec.assign(desc->dec, desc->dec + desc->n_dec);
+  s->d.enc = s->enc.data();
+  s->d.dec = s->dec.data();
+  s->dry = (desc->flags & PULSE_FLAG_DRY_RUN) != 0;
+  if ((st = build_slots(s)) != PULSE_OK || (st = build_layout(s)) != PULSE_OK) {
+    delete s;
+    return st;
+  }
+  s->rows.resize(desc->max_inflight);
+  *out = s;
+  return PULSE_OK;
+}
+
+void pulse_stage_destroy(pulse_stage* s) {
+  if (!s) return;
+  for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+  delete s;
+}
+
+pulse_status pulse_stage_sizes(const pulse_stage* s, int64_t* n_params, size_t* ws_bytes) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (n_params) *n_params = s->n_params;
+  if (ws_bytes) *ws_bytes = s->dry ? 0 : s->ws_bytes;
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_param_layout(const pulse_stage* s, int32_t idx, char name[64],
+                                      int64_t* offset, int32_t shape[4]) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (idx == -1) {
+    if (!offset) return fail(PULSE_E_INVALID_ARG, "offset is NULL");
+    *offset = (int64_t)s->params.size();
+    return PULSE_OK;
+  }
+  if (idx < 0 || idx >= (int)s->params.size())
+    return fail(PULSE_E_INVALID_ARG, "parameter index %d out of range", idx);
+  const ParamInfo& p = s->params[idx];
+  if (name) {
+    std::strncpy(name, p.name.c_str(), 63);
+    name[63] = 0;
+  }
+  if (offset) *offset = p.off;
+  if (shape)
+    for (int i = 0; i < 4; ++i) shape[i] = p.shape[i];
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads, void* ws,
+                              size_t ws_bytes) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (s->dry) return fail(PULSE_E_STATE, "a dry-run stage binds no memory");
+  if (!params || !grads || !ws) return fail(PULSE_E_INVALID_ARG, "NULL pointer in bind");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 || reinterpret_cast<uintptr_t>(params) % 16 ||
+      reinterpret_cast<uintptr_t>(grads) % 16)
+    return fail(PULSE_E_INVALID_ARG, "workspace must be 256-byte, params/grads 16-byte aligned");
+  if (ws_bytes < s->ws_bytes)
+    return fail(PULSE_E_INVALID_ARG, "workspace %zu bytes < required %zu", ws_bytes,
+                s->ws_bytes);
+  if (pulse_stage_inflight(s) > 0)
+    return fail(PULSE_E_STATE, "cannot rebind with microbatches in flight");
+  s->prm = params;
+  s->grd = grads;
+  s->ws = static_cast<char*>(ws);
+  s->bound = true;
+  s->synced = false;
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_sync_params(pulse_stage* s, void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (s->dry) {
+    s->synced = true;
+    return PULSE_OK;
+  }
+  if (!s->bound) return fail(PULSE_E_NOT_BOUND, "stage is not bound");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int dt = s->dtype;
+  for (auto* v : {&s->eb, &s->db})
+    for (auto& b : *v) {
+      HIPCHK(launch_convert_rows(s->pp(b.W1), b.cout, 9 * b.cin, s->ws + b.wf1, 9 * b.cin, 0, dt,
+                                 st));
+      HIPCHK(launch_convert_rows(s->pp(b.W2), b.cout, 9 * b.cout, s->ws + b.wf2, b.ldb2, 0, dt,
+                                 st));
+      if (b.conv_sc)
+        HIPCHK(launch_convert_rows(s->pp(b.Ws), b.cout, b.cin, s->ws + b.wf2, b.ldb2,
+                                   9 * b.cout, dt, st));
+      HIPCHK(launch_flip3x3(s->pp(b.W1), b.cout, b.cin, s->ws + b.wd1, dt, st));
+      HIPCHK(launch_flip3x3(s->pp(b.W2), b.cout, b.cout, s->ws + b.wd2, dt, st));
+      if (b.conv_sc) HIPCHK(launch_transpose(s->pp(b.Ws), b.cout, b.cin, s->ws + b.wsd, dt, st));
+      HIPCHK(launch_vec_add(s->pp(b.b2), b.conv_sc ? s->pp(b.bs) : nullptr,
+                            reinterpret_cast<float*>(s->ws + b.bias2), b.cout, st));
+    }
+  s->synced = true;
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, const void* in,
+                                 const void* temb, void* out, void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (half != PULSE_ENC && half != PULSE_DEC) return fail(PULSE_E_INVALID_ARG, "bad half");
+  if (mb < 0) return fail(PULSE_E_INVALID_ARG, "mb must be >= 0");
+  pulse_status ps;
+  if (!s->dry) {
+    if ((ps = need_bound(s)) != PULSE_OK) return ps;
+    if ((ps = check_ptr(in, "in")) != PULSE_OK || (ps = check_ptr(temb, "temb")) != PULSE_OK ||
+        (ps = check_ptr(out, "out")) != PULSE_OK)
+      return ps;
+  }
+  int r = find_row(s, mb);
+  const pulse_stage_desc& d = s->d;
+  if (half == PULSE_ENC) {
+    if (r >= 0 && s->rows[r].state != R_FRESH)
+      return fail(PULSE_E_STATE, "mb %d: encoder forward already ran", mb);
+    if (r >= 0) {
+      const Row& row = s->rows[r];
+      if (d.input_skip_slot >= 0 && row.act[d.input_skip_slot])
+        return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb,
+                    d.input_skip_slot);
+      for (auto& b : s->eb)
+        if (b.slot >= 0 && row.act[b.slot])
+          return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb, b.slot);
+    } else {
+      r = free_row(s);
+      if (r < 0)
+        return fail(PULSE_E_CACHE_FULL, "mb %d: %d microbatches already in flight", mb,
+                    d.max_inflight);
+    }
+  } else {
+    if (r < 0) return fail(PULSE_E_STATE, "mb %d: decoder forward before encoder forward", mb);
+    const Row& row = s->rows[r];
+    if (row.state != R_ENC_FWD && row.state != R_FRESH)
+      return fail(PULSE_E_STATE, "mb %d: decoder forward out of order (state %d)", mb, row.state);
+    for (auto& b : s->db)
+      if (!row.act[b.slot])
+        return fail(PULSE_E_CACHE_MISS, "mb %d: skip slot %d absent", mb, b.slot);
+  }
+
+  if (!s->dry) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* row = s->row_base(r);
+    const int dt = s->dtype;
+    HIPCHK(hipMemcpyAsync(row + s->row_temb[half == PULSE_DEC ? 1 : 0], temb, (size_t)s->geo.B * s->D * s->esz,
+                          hipMemcpyDeviceToDevice, st));
+    if (half == PULSE_ENC) {
+      void* xin_store = d.input_skip_slot >= 0 ? row + s->row_act[d.input_skip_slot]
+                                               : row + s->row_xin;
+      HIPCHK(hipMemcpyAsync(xin_store, in, act_bytes(s, s->eb[0].cin), hipMemcpyDeviceToDevice,
+                            st));
+      const int n = (int)s->eb.size();
+      for (int k = 0; k < n; ++k) {
+        const Block& b = s->eb[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        void* o1;
+        void* o2 = nullptr;
+        if (b.slot >= 0) {
+          o1 = row + s->row_act[b.slot];
+          if (k == n - 1) o2 = out;
+        } else {
+          o1 = (k == n - 1) ? out : row + b.out_saved;
+        }
+        if ((ps = block_forward(s, r, b, xin, o1, o2, st)) != PULSE_OK) return ps;
+      }
+      (void)dt;
+    } else {
+      HIPCHK(hipMemcpyAsync(row + s->row_u, in, act_bytes(s, s->db[0].c0),
+                            hipMemcpyDeviceToDevice, st));
+      const int n = (int)s->db.size();
+      for (int k = 0; k < n; ++k) {
+        const Block& b = s->db[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        void* o1 = (k == n - 1) ? out : row + b.out_saved;
+        if ((ps = block_forward(s, r, b, xin, o1, nullptr, st)) != PULSE_OK) return ps;
+      }
+    }
+  }
+
+  Row& row = s->rows[r];
+  if (half == PULSE_ENC) {
+    row.mb = mb;
+    row.state = R_ENC_FWD;
+    row.enc_done = true;
+    if (d.input_skip_slot >= 0) row.act[d.input_skip_slot] = 1;
+    for (auto& b : s->eb)
+      if (b.slot >= 0) row.act[b.slot] = 1;
+  } else {
+    row.state = R_DEC_FWD;
+  }
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, const void* dout,
+                                  void* din, float* dtemb, void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (half != PULSE_ENC && half != PULSE_DEC) return fail(PULSE_E_INVALID_ARG, "bad half");
+  if (mb < 0) return fail(PULSE_E_INVALID_ARG, "mb must be >= 0");
+  pulse_status ps;
+  if (!s->dry) {
+    if ((ps = need_bound(s)) != PULSE_OK) return ps;
+    if ((ps = check_ptr(dout, "dout")) != PULSE_OK || (ps = check_ptr(din, "din")) != PULSE_OK)
+      return ps;
+    if (dtemb && reinterpret_cast<uintptr_t>(dtemb) % 4)
+      return fail(PULSE_E_INVALID_ARG, "dtemb_accum misaligned");
+  }
+  const int r = find_row(s, mb);
+  if (r < 0) return fail(PULSE_E_STATE, "mb %d is not in flight", mb);
+  const pulse_stage_desc& d = s->d;
+  {
+    const Row& row = s->rows[r];
+    if (half == PULSE_DEC && row.state != R_DEC_FWD)
+      return fail(PULSE_E_STATE, "mb %d: decoder backward needs the decoder forward", mb);
+    if (half == PULSE_ENC) {
+      if (row.state != R_DEC_BWD || !row.enc_done)
+        return fail(PULSE_E_STATE, "mb %d: encoder backward needs encoder forward and decoder "
+                    "backward", mb);
+      auto need = [&](int sl) { return sl >= 0 && s->slot_reader[sl] >= 0 && !row.grad[sl]; };
+      if (need(d.input_skip_slot))
+        return fail(PULSE_E_CACHE_MISS, "mb %d: skip gradient of slot %d absent", mb,
+                    d.input_skip_slot);
+      for (auto& b : s->eb)
+        if (need(b.slot))
+          return fail(PULSE_E_CACHE_MISS, "mb %d: skip gradient of slot %d absent", mb, b.slot);
+    }
+  }
+
+  if (!s->dry) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* row = s->row_base(r);
+    const int dt = s->dtype;
+    int cur = 0;
+    if (half == PULSE_DEC) {
+      const int n = (int)s->db.size();
+      for (int k = n - 1; k >= 0; --k) {
+        const Block& b = s->db[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        const VIn dy = (k == n - 1) ? vin1(dout, dt, b.cout)
+                                    : vin1(s->sf(s->s_g[cur]), DT_F32, b.cout);
+        GnBwdOut o{};
+        o.c_split = b.c0;
+        if (k == 0) {
+          o.dst0 = din;
+          o.dtype0 = dt;
+        } else {
+          o.dst0 = s->sf(s->s_g[cur ^ 1]);
+          o.dtype0 = DT_F32;
+        }
+        o.dst1 = row + s->row_grad[b.slot];
+        o.dtype1 = DT_F32;
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
+        cur ^= 1;
+      }
+    } else {
+      const int n = (int)s->eb.size();
+      for (int k = n - 1; k >= 0; --k) {
+        const Block& b = s->eb[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        const float* dskip = (b.slot >= 0 && s->slot_reader[b.slot] >= 0)
+                                 ? reinterpret_cast<const float*>(row + s->row_grad[b.slot])
+                                 : nullptr;
+        const VIn dy = (k == n - 1) ? vin1(dout, dt, b.cout, dskip)
+                                    : vin1(s->sf(s->s_g[cur]), DT_F32, b.cout, dskip);
+        GnBwdOut o{};
+        o.c_split = b.cin;
+        if (k == 0) {
+          o.dst0 = din;
+          o.dtype0 = dt;
+          if (d.input_skip_slot >= 0 && s->slot_reader[d.input_skip_slot] >= 0)
+            o.add1 = reinterpret_cast<const float*>(row + s->row_grad[d.input_skip_slot]);
+        } else {
+          o.dst0 = s->sf(s->s_g[cur ^ 1]);
+          o.dtype0 = DT_F32;
+        }
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
+        cur ^= 1;
+      }
+    }
+  }
+
+  Row& row = s->rows[r];
+  if (half == PULSE_DEC) {
+    row.state = R_DEC_BWD;
+    for (auto& b : s->db) row.grad[b.slot] = 1;
+  } else {
+    release_row(row);
+  }
+  return PULSE_OK;
+}
+
+pulse_status pulse_skip_cache_put(pulse_stage* s, int32_t mb, int32_t slot, const void* src,
+                                  void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (mb < 0) return fail(PULSE_E_INVALID_ARG, "mb must be >= 0");
+  if (slot < 0 || slot >= s->n_slots || !s->slot_ch[slot])
+    return fail(PULSE_E_INVALID_ARG, "slot %d does not exist", slot);
+  pulse_status ps;
+  if (!s->dry) {
+    if (!s->bound) return fail(PULSE_E_NOT_BOUND, "stage is not bound");
+    if ((ps = check_ptr(src, "src")) != PULSE_OK) return ps;
+  }
+  int r = find_row(s, mb);
+  if (r >= 0) {
+    if (s->rows[r].act[slot])
+      return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb, slot);
+  } else {
+    r = free_row(s);
+    if (r < 0)
+      return fail(PULSE_E_CACHE_FULL, "mb %d: %d microbatches already in flight", mb,
+                  s->d.max_inflight);
+  }
+  if (!s->dry)
+    HIPCHK(hipMemcpyAsync(s->row_base(r) + s->row_act[slot], src, act_bytes(s, s->slot_ch[slot]),
+                          hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
+  Row& row = s->rows[r];
+  if (row.mb < 0) {
+    row.mb = mb;
+    row.state = R_FRESH;
+  }
+  row.act[slot] = 1;
+  return PULSE_OK;
+}
+
+pulse_status pulse_skip_cache_take(pulse_stage* s, int32_t mb, int32_t slot,
+                                   pulse_skip_kind kind, void* dst, void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (kind != PULSE_SKIP_ACT && kind != PULSE_SKIP_GRAD)
+    return fail(PULSE_E_INVALID_ARG, "bad kind");
+  if (slot < 0 || slot >= s->n_slots || !s->slot_ch[slot])
+    return fail(PULSE_E_INVALID_ARG, "slot %d does not exist", slot);
+  pulse_status ps;
+  if (!s->dry) {
+    if (!s->bound) return fail(PULSE_E_NOT_BOUND, "stage is not bound");
+    if ((ps = check_ptr(dst, "dst")) != PULSE_OK) return ps;
+  }
+  const int r = find_row(s, mb);
+  if (r < 0) return fail(PULSE_E_CACHE_MISS, "mb %d is not in flight", mb);
+  Row& row = s->rows[r];
+  uint8_t& present = kind == PULSE_SKIP_ACT ? row.act[slot] : row.grad[slot];
+  if (!present)
+    return fail(PULSE_E_CACHE_MISS, "mb %d slot %d %s absent", mb, slot,
+                kind == PULSE_SKIP_ACT ? "activation" : "gradient");
+  if (!s->dry) {
+    const size_t off = kind == PULSE_SKIP_ACT ? s->row_act[slot] : s->row_grad[slot];
+    const size_t bytes = kind == PULSE_SKIP_ACT ? act_bytes(s, s->slot_ch[slot])
+                                                : (size_t)s->P * s->slot_ch[slot] * 4;
+    HIPCHK(hipMemcpyAsync(dst, s->row_base(r) + off, bytes, hipMemcpyDeviceToDevice,
+                          static_cast<hipStream_t>(stream)));
+  }
+  present = 0;
+  if (!row.enc_done && (row.state == R_FRESH || row.state == R_DEC_BWD) && row_empty(s, row))
+    release_row(row);
+  return PULSE_OK;
+}
+
+pulse_status pulse_skip_cache_state(const pulse_stage* s, int32_t mb, int32_t slot,
+                                    int32_t* state) {
+  if (!s || !state) return fail(PULSE_E_INVALID_ARG, "NULL argument");
+  if (slot < 0 || slot >= s->n_slots || !s->slot_ch[slot])
+    return fail(PULSE_E_INVALID_ARG, "slot %d does not exist", slot);
+  const int r = find_row(s, mb);
+  *state = 0;
+  if (r >= 0)
+    *state = (s->rows[r].act[slot] ? PULSE_SKIP_ACT_PRESENT : 0) |
+             (s->rows[r].grad[slot] ? PULSE_SKIP_GRAD_PRESENT : 0);
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_release(pulse_stage* s, int32_t mb) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  const int r = find_row(s, mb);
+  if (r < 0) return fail(PULSE_E_STATE, "mb %d is not in flight", mb);
+  release_row(s->rows[r]);
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_reset(pulse_stage* s) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  for (auto& r : s->rows) release_row(r);
+  return PULSE_OK;
+}
+
+int32_t pulse_stage_inflight(const pulse_stage* s) {
+  if (!s) return -1;
+  int n = 0;
+  for (auto& r : s->rows) n += r.mb >= 0;
+  return n;
+}
+
+pulse_status pulse_stage_timing(pulse_stage* s, int32_t enable) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  s->timing = enable != 0;
+  s->timed.clear();
+  s->ev_used = 0;
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_timing_read(pulse_stage* s, int64_t* launches, double* ms,
+                                     double* flops) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  double t = 0.0, f = 0.0;
+  for (const auto& tl : s->timed) {
+    HIPCHK(hipEventSynchronize(tl.b));
+    float x = 0.f;
+    HIPCHK(hipEventElapsedTime(&x, tl.a, tl.b));
+    t += x;
+    f += tl.flops;
+  }
+  if (launches) *launches = (int64_t)s->timed.size();
+  if (ms) *ms = t;
+  if (flops) *flops = f;
+  s->timed.clear();
+  s->ev_used = 0;
+  return PULSE_OK;
+}
+
+double pulse_stage_flops(const pulse_stage* s) {
+  if (!s) return 0.0;
+  double f = 0.0;
+  for (auto& b : s->eb) f += block_flops(s, b);
+  for (auto& b : s->db) f += block_flops(s, b);
+  return 3.0 * f;
+}
+
+}  // extern "C"
