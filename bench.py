@@ -1,0 +1,208 @@
+"""Throughput of one skip-collocated Pulse stage (forward + backward) on one
+MI355X, through the C ABI.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload l64]
+
+A step is one pass of the whole hot path over one microbatch of synthetic
+input already resident in HBM: encoder forward (skips cached in HBM),
+decoder forward (reading [upstream || skip] from the cache), decoder
+backward (skip gradient buffered), encoder backward (skip gradient added).
+The ``wave`` workload's step is one wave iteration of the four SD levels
+with 4 microbatches in flight (all forwards, then backwards in reverse).
+
+Prints ONE JSON line (rank 0): stage fwd+bwd TFLOP/s with the fraction of
+the bf16 MFMA peak, microbatches/s, the roofline of the implicit-GEMM conv
+kernel (its launches bracketed by HIP events on the stage stream during the
+timed steps) and the CPU oracle timed on a bounded sample of the same
+workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the fp32 stage)
+METRIC = "stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s, 64x64x320 stage"
+
+
+def workload_desc(name):
+    from paper_2606_19163_amd import configs
+    if name == "wave":
+        return configs.wave_levels()
+    return [configs.get(name)]
+
+
+def describe(name, descs):
+    d = descs[0]
+    if name == "wave":
+        return {"workload": "wave: 4 collocated stages (64x64x320, 32x32x640, 16x16x1280, "
+                            "8x8x1280) at batch 8, 4 microbatches in flight, all forwards "
+                            "then backwards in reverse",
+                "batch": 8, "microbatches": 4, "levels": 4}
+    chans = sorted({b["c_out"] for b in d["enc"]} | {b["c_in"] for b in d["enc"]})
+    return {"workload": f"{name}: one collocated stage, batch {d['batch']}, "
+                        f"{d['height']}x{d['width']}, channels {chans}, "
+                        f"{len(d['enc'])} encoder + {len(d['dec'])} decoder ResBlocks, "
+                        f"GroupNorm {d['groups']} groups, t-emb {d['temb_dim']}",
+            "batch": d["batch"], "height": d["height"], "width": d["width"],
+            "enc_blocks": [[b["c_in"], b["c_out"]] for b in d["enc"]],
+            "dec_blocks": [[b["c_up"], b["c_skip"], b["c_out"]] for b in d["dec"]]}
+
+
+def cpu_baseline(name, descs, seed, sample_batch):
+    """The oracle, as it stands, on `sample_batch` images of the workload's
+    first stage (forward + backward), scaled to TFLOP/s."""
+    import numpy as np
+    from oracle import pulse_oracle as O
+    from paper_2606_19163_amd import configs, synth
+    from paper_2606_19163_amd import stage as S
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    d = configs.shrink(descs[0], batch=sample_batch)
+    params, b = synth.make_all(d, seed)
+    f = lambda x: {k: np.asarray(v, np.float64) for k, v in x.items()}
+    p64, b64 = f(params), f(b)
+    flops = S.Stage(d, dry_run=True).flops()
+    t0 = time.perf_counter()
+    O.stage_run(d, p64, b64["x"], b64["u"], b64["temb"], b64["g_enc"], b64["g_dec"])
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{sample_batch} of {descs[0]['batch']} images of one microbatch of the "
+                      f"first stage ({d['height']}x{d['width']}), forward + backward, numpy "
+                      f"fp64; {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="l64",
+                    choices=["l64", "l32", "l16", "l8", "tiny", "wave"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-batch", type=int, default=2)
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="do not bracket the conv launches with HIP events")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the stage's multi-GPU sharding (pipeline "
+              "neighbours over xGMI, data-parallel all-reduce) is not built here; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2606_19163_amd import configs, synth
+    from paper_2606_19163_amd import stage as S
+
+    torch.cuda.set_device(0)
+    descs = workload_desc(args.workload)
+    n_mb = 4 if args.workload == "wave" else 1
+    seed = configs.SEEDS["wave" if args.workload == "wave" else args.workload]
+    if args.workload == "wave":
+        params, bounds = synth.make_wave(descs, seed, n_mb)
+    else:
+        p0, b0 = synth.make_all(descs[0], seed)
+        params, bounds = [p0], [[b0]]
+    stages, dev = [], []
+    for i, d in enumerate(descs):
+        st = S.Stage(d)
+        st.set_params(params[i])
+        stages.append(st)
+        dev.append([{k: st.to_dev(v) for k, v in bb.items()} for bb in bounds[i]])
+    dtembs = [torch.zeros((d["batch"], d["temb_dim"]), device="cuda") for d in descs]
+    outs = [[{} for _ in range(n_mb)] for _ in descs]
+    for i, d in enumerate(descs):
+        for m in range(n_mb):
+            outs[i][m]["y_enc"] = stages[i].act(d["enc"][-1]["c_out"])
+            outs[i][m]["y_dec"] = stages[i].act(d["dec"][-1]["c_out"])
+            outs[i][m]["dx"] = stages[i].act(d["enc"][0]["c_in"])
+            outs[i][m]["du"] = stages[i].act(d["dec"][0]["c_up"])
+    flops_step = sum(st.flops() for st in stages) * n_mb
+
+    def step():
+        for i, st in enumerate(stages):
+            for m in range(n_mb):
+                b = dev[i][m]
+                o = outs[i][m]
+                st.forward(S.ENC, m, b["x"], b["temb"], out=o["y_enc"])
+                st.forward(S.DEC, m, b["u"], b["temb"], out=o["y_dec"])
+            for m in reversed(range(n_mb)):
+                b = dev[i][m]
+                o = outs[i][m]
+                st.backward(S.DEC, m, b["g_dec"], din=o["du"], dtemb=dtembs[i])
+                st.backward(S.ENC, m, b["g_enc"], din=o["dx"], dtemb=dtembs[i])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = not args.no_kernel_events
+    for st in stages:
+        st.timing(events)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launches, kms, kflops = 0, 0.0, 0.0
+    for st in stages:
+        n, ms, fl = st.timing_read()
+        launches += n
+        kms += ms
+        kflops += fl
+        st.timing(False)
+
+    ms_step = elapsed * 1e3 / args.steps
+    tflops = flops_step * args.steps / elapsed / 1e12
+    bf16 = descs[0]["dtype"] == configs.BF16
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    line = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+        "config": describe(args.workload, descs),
+        "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
+        "microbatches_per_s": round(n_mb * args.steps / elapsed, 2),
+        "gflop_per_step": round(flops_step / 1e9, 2),
+    }
+    if events and launches:
+        achieved = kflops / (kms * 1e-3) / 1e12
+        line["roofline"] = {
+            "kernel": "igemm_conv (implicit-GEMM conv forward / data gradient)",
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+            "launches": launches, "avg_launch_us": round(kms * 1e3 / launches, 2),
+            "avg_gflop_per_launch": round(kflops / launches / 1e9, 3),
+        }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.workload, descs, seed,
+                                            min(args.cpu_sample_batch, descs[0]["batch"]))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
