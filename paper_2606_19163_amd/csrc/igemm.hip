@@ -6,24 +6,29 @@
 //  * CONV mode (forward and data gradient): C[m, n] = sum_k A[m, k] B[n, k]
 //    with m a pixel, n an output channel and k = (segment, tap, channel).
 //    A is never materialised: a K-step of BK columns lies inside one tap of
-//    one segment, so the block loads BK consecutive channels of the pixel
+//    one segment, so the block copies BK consecutive channels of the pixel
 //    shifted by that tap (zero outside the image) straight from the NHWC
 //    source(s).  A segment is a 3x3 or 1x1 conv over a virtual input that
 //    may read two tensors (the decoder's [upstream || skip]); several
 //    segments side by side along K fuse the 1x1 shortcut into the second
 //    3x3 conv of a block.  B is a row-major [N][K] weight matrix (for the
-//    data gradient: the flipped, transposed 3x3 weights).
+//    data gradient: the flipped, transposed 3x3 weights).  The epilogue adds
+//    bias / per-image row vector / residual and writes whole 16-byte vectors
+//    from an LDS-staged tile.
 //  * WGRAD mode (weight gradient): C[m, n] = sum_p dY[p, m] X[p + tap(n),
 //    c(n)] with m an output channel, n = (segment, tap, channel) and the
 //    contraction over pixels p, split across blockIdx.z into fixed pixel
 //    ranges whose fp32 partials a finalize kernel sums in a fixed order.
-//    Both operands are pixel-strided in NHWC, so each thread loads an 8x8
-//    (pixel x channel) micro-tile and writes it transposed to LDS.
+//    Both operands are pixel-strided in NHWC, so each thread copies an 8x8
+//    (pixel x channel) micro-tile and transposes it in registers (byte
+//    permutes) before the LDS store.
 //
-// bf16 operands use v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the
-// fp32 path uses v_mfma_f32_16x16x4_f32.  Operand tiles are staged in LDS
-// (K-contiguous rows padded against bank conflicts), double buffered, with
-// the next tile's global loads in flight while the current one is consumed.
+// Operands are copied raw in the compute dtype (every conversion happens in
+// the memory-bound kernels that produce them).  bf16 operands use
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the fp32 path uses
+// v_mfma_f32_16x16x4_f32.  Operand tiles are staged in LDS (K-contiguous rows
+// padded against bank conflicts), double buffered, with the next tile's
+// global loads in flight while the current one is consumed.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -39,13 +44,16 @@ struct Cfg {
   static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
   static constexpr int NT = WAVES_M * WAVES_N * 64;
   static constexpr int TM = WM / 16, TN = WN / 16;
-  static constexpr int ESZ = F32 ? 4 : 2;         // bytes per LDS element
+  static constexpr int ESZ = F32 ? 4 : 2;         // bytes per element
   static constexpr int LDK = BK + (F32 ? 4 : 8);  // padded LDS row (elements)
   static constexpr int KV = BK / 8;               // 8-element vectors per row
   static constexpr int VW = F32 ? 8 : 4;          // 32-bit words per vector
   static constexpr int LDS_A = BM * LDK * ESZ;
   static constexpr int LDS_B = BN * LDK * ESZ;
-  static constexpr int LDS_BYTES = 2 * (LDS_A + LDS_B);
+  static constexpr int LDS_OPS = 2 * (LDS_A + LDS_B);
+  static constexpr int LDC = BN + 4;              // fp32 epilogue tile row
+  static constexpr int LDS_EPI = BM * LDC * 4;
+  static constexpr int LDS_BYTES = LDS_OPS > LDS_EPI ? LDS_OPS : LDS_EPI;
   // CONV mode: vectors per thread for the A and B tiles
   static constexpr int NVA = (BM * KV) / NT;
   static constexpr int NVB = (BN * KV) / NT;
@@ -56,70 +64,78 @@ struct Cfg {
   static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
   static_assert(BK % 32 == 0, "BK");
   static_assert((BM * KV) % NT == 0 && (BN * KV) % NT == 0, "vector split");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
-// 8 operand elements in the LDS format: 8 fp32 words or 4 words of bf16 pairs
+// 8 operand elements: 8 fp32 words or 4 words of bf16 pairs
 template <bool F32>
 struct VecT {
   uint32_t w[F32 ? 8 : 4];
 };
 
 template <bool F32>
-__device__ __forceinline__ void to_vec(const float f[8], VecT<F32>& v) {
-  if constexpr (F32) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v.w[i] = __float_as_uint(f[i]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v.w[i] = pack2(f[2 * i], f[2 * i + 1]);
-  }
-}
-
-template <bool F32>
-__device__ __forceinline__ void zero_vec(VecT<F32>& v) {
+__device__ __forceinline__ void vzero(VecT<F32>& v) {
 #pragma unroll
   for (int i = 0; i < (F32 ? 8 : 4); ++i) v.w[i] = 0u;
+}
+
+// Raw copy of 8 elements of the compute dtype.
+template <bool F32>
+__device__ __forceinline__ void vload(const void* p, VecT<F32>& v) {
+  const uint4 q0 = reinterpret_cast<const uint4*>(p)[0];
+  v.w[0] = q0.x; v.w[1] = q0.y; v.w[2] = q0.z; v.w[3] = q0.w;
+  if constexpr (F32) {
+    const uint4 q1 = reinterpret_cast<const uint4*>(p)[1];
+    v.w[F32 ? 4 : 0] = q1.x; v.w[F32 ? 5 : 1] = q1.y;
+    v.w[F32 ? 6 : 2] = q1.z; v.w[F32 ? 7 : 3] = q1.w;
+  }
 }
 
 template <class C>
 __device__ __forceinline__ void lds_put(char* base, int row, int k, const VecT<C::F32>& v) {
   char* p = base + (row * C::LDK + k) * C::ESZ;
-  if constexpr (C::F32) {
-    reinterpret_cast<uint4*>(p)[0] = make_uint4(v.w[0], v.w[1], v.w[2], v.w[3]);
+  reinterpret_cast<uint4*>(p)[0] = make_uint4(v.w[0], v.w[1], v.w[2], v.w[3]);
+  if constexpr (C::F32)
     reinterpret_cast<uint4*>(p)[1] = make_uint4(v.w[C::F32 ? 4 : 0], v.w[C::F32 ? 5 : 1],
                                                 v.w[C::F32 ? 6 : 2], v.w[C::F32 ? 7 : 3]);
+}
+
+// Address of channel c of pixel pix of a raw two-source input.
+template <bool F32>
+__device__ __forceinline__ const char* vaddr(const VIn& v, long pix, int c) {
+  constexpr int esz = F32 ? 4 : 2;
+  if (c < v.c0) return static_cast<const char*>(v.s0.ptr) + (pix * v.s0.C + c) * esz;
+  return static_cast<const char*>(v.s1.ptr) + (pix * v.s1.C + (c - v.c0)) * esz;
+}
+
+// Transpose an 8x8 block: in[e] holds 8 channels of pixel e, out[q] gets 8
+// pixels of channel q.
+template <bool F32>
+__device__ __forceinline__ void transpose8(const VecT<F32> (&in)[8], VecT<F32> (&out)[8]) {
+  if constexpr (F32) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[q].w[e] = in[e].w[q];
   } else {
-    *reinterpret_cast<uint4*>(p) = make_uint4(v.w[0], v.w[1], v.w[2], v.w[3]);
+    // out[q].w[j] = (channel q of pixel 2j) | (channel q of pixel 2j+1) << 16
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = in[2 * j].w[q / 2], hi = in[2 * j + 1].w[q / 2];
+        out[q].w[j] = (q & 1) ? __builtin_amdgcn_perm(hi, lo, 0x07060302u)
+                              : __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+      }
   }
 }
 
 // Which segment holds index `i` (segments are sorted and contiguous).
-__device__ __forceinline__ int seg_of(const GemmArgs& a, int i) {
+__device__ __forceinline__ int seg_of(int nseg, int b1, int b2, int i) {
   int s = 0;
-#pragma unroll
-  for (int j = 1; j < MAX_SEG; ++j)
-    if (j < a.nseg && i >= a.seg[j].begin) s = j;
+  if (nseg > 1 && i >= b1) s = 1;
+  if (nseg > 2 && i >= b2) s = 2;
   return s;
-}
-
-// The segment `s` by value (selects instead of a dynamic index into the
-// kernel arguments).
-__device__ __forceinline__ Seg pick_seg(const GemmArgs& a, int s) {
-  Seg r = a.seg[0];
-#pragma unroll
-  for (int j = 1; j < MAX_SEG; ++j)
-    if (s == j) r = a.seg[j];
-  return r;
-}
-
-__device__ __forceinline__ void tap_offset(int taps, int tap, int& oy, int& ox) {
-  if (taps == 9) {
-    oy = tap / 3 - 1;
-    ox = tap % 3 - 1;
-  } else {
-    oy = 0;
-    ox = 0;
-  }
 }
 
 // Remap the linear block id so that consecutive tiles land on one XCD
@@ -185,6 +201,21 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, int wm,
   }
 }
 
+// Park the accumulators of every wave in an fp32 [BM][LDC] LDS tile.
+template <class C>
+__device__ __forceinline__ void acc_to_lds(float* ct, int wm, int wn, int lane,
+                                           const f32x4_t (&acc)[C::TM][C::TN]) {
+  const int r16 = lane & 15;
+  const int rq = (lane >> 4) * 4;
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        ct[(wm * C::WM + i * 16 + rq + r) * C::LDC + wn * C::WN + j * 16 + r16] = acc[i][j][r];
+}
+
 // ---------------------------------------------------------------------------
 // CONV mode
 // ---------------------------------------------------------------------------
@@ -209,19 +240,27 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
   const long P = a.g.pixels();
 
-  // pixel coordinates of this thread's A rows
+  // this thread's A rows: pixel index and the 9-bit mask of in-image taps
   const int kv = tid % C::KV;
-  int pimg[C::NVA], ph[C::NVA], pw[C::NVA];
-  bool pval[C::NVA];
+  long ppix[C::NVA];
+  uint32_t pmask[C::NVA];
 #pragma unroll
   for (int j = 0; j < C::NVA; ++j) {
     const long m = m0 + tid / C::KV + j * (C::NT / C::KV);
-    pval[j] = m < P;
-    const long mm = pval[j] ? m : 0;
-    pimg[j] = (int)(mm / HW);
-    const int rem = (int)(mm - (long)pimg[j] * HW);
-    ph[j] = rem / W;
-    pw[j] = rem - ph[j] * W;
+    ppix[j] = m;
+    uint32_t mask = 0;
+    if (m < P) {
+      const int img = (int)(m / HW);
+      const int rem = (int)(m - (long)img * HW);
+      const int h = rem / W;
+      const int w = rem - h * W;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int hh = h + t / 3 - 1, ww = w + t % 3 - 1;
+        if (hh >= 0 && hh < H && ww >= 0 && ww < W) mask |= 1u << t;
+      }
+    }
+    pmask[j] = mask;
   }
 
   VecT<C::F32> ra[C::NVA], rb[C::NVB];
@@ -232,51 +271,37 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
     const int r = k0 - sg.begin;
     const int tap = r / sg.C;
     const int cb = r - tap * sg.C + kv * 8;
-    int oy, ox;
-    tap_offset(sg.taps, tap, oy, ox);
+    // the centre tap of a 3x3 segment and every 1x1 tap read the pixel itself
+    const int t9 = sg.taps == 9 ? tap : 4;
+    const long shift = (long)(t9 / 3 - 1) * W + (t9 % 3 - 1);
 #pragma unroll
     for (int j = 0; j < C::NVA; ++j) {
-      const int hh = ph[j] + oy, ww = pw[j] + ox;
-      float f[8];
-      if (pval[j] && hh >= 0 && hh < H && ww >= 0 && ww < W) {
-        ld8v(sg.in, ((long)pimg[j] * H + hh) * W + ww, cb, f);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) f[q] = 0.f;
-      }
-      to_vec<C::F32>(f, ra[j]);
+      if ((pmask[j] >> t9) & 1u)
+        vload<C::F32>(vaddr<C::F32>(sg.in, ppix[j] + shift, cb), ra[j]);
+      else
+        vzero<C::F32>(ra[j]);
     }
   };
 
   auto load_tiles = [&](int kt) __attribute__((always_inline)) {
     const int k0 = kt * C::BK;
-    // the segment index is uniform across the block: branch on it so every
-    // access to the segment table uses a constant index
-    if (k0 < sg1.begin || nseg < 2)
+    // the segment is uniform across the block; branch so every access to the
+    // segment table uses a constant index
+    const int s = seg_of(nseg, sg1.begin, sg2.begin, k0);
+    if (s == 0)
       load_a(sg0, k0);
-    else if (k0 < sg2.begin || nseg < 3)
+    else if (s == 1)
       load_a(sg1, k0);
     else
       load_a(sg2, k0);
 #pragma unroll
     for (int j = 0; j < C::NVB; ++j) {
       const int n = n0 + tid / C::KV + j * (C::NT / C::KV);
-      // rows past N read row 0 and are zeroed (keeps the load unconditional)
-      const bool ok = n < a.N;
-      const char* p = static_cast<const char*>(a.Bw) +
-                      ((long)(ok ? n : 0) * a.ldb + k0 + kv * 8) * C::ESZ;
-      const uint4 q0 = reinterpret_cast<const uint4*>(p)[0];
-      rb[j].w[0] = ok ? q0.x : 0u;
-      rb[j].w[1] = ok ? q0.y : 0u;
-      rb[j].w[2] = ok ? q0.z : 0u;
-      rb[j].w[3] = ok ? q0.w : 0u;
-      if constexpr (C::F32) {
-        const uint4 q1 = reinterpret_cast<const uint4*>(p)[1];
-        rb[j].w[4] = ok ? q1.x : 0u;
-        rb[j].w[5] = ok ? q1.y : 0u;
-        rb[j].w[6] = ok ? q1.z : 0u;
-        rb[j].w[7] = ok ? q1.w : 0u;
-      }
+      if (n < a.N)
+        vload<C::F32>(static_cast<const char*>(a.Bw) + ((long)n * a.ldb + k0 + kv * 8) * C::ESZ,
+                      rb[j]);
+      else
+        vzero<C::F32>(rb[j]);
     }
   };
 
@@ -309,39 +334,38 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
     __syncthreads();
   }
 
-  // epilogue: + bias[n] + rowvec[img, n] + residual, store
-  const int r16 = lane & 15;
-  const int rq = (lane >> 4) * 4;
+  // epilogue: accumulators -> LDS -> rows of 8 channels (+bias, +rowvec,
+  // +residual) -> 16-byte stores
+  float* ct = reinterpret_cast<float*>(smem);
+  acc_to_lds<C>(ct, wm, wn, lane, acc);
+  __syncthreads();
+  constexpr int NV8 = C::BN / 8;
+  for (int i = tid; i < C::BM * NV8; i += C::NT) {
+    const int row = i / NV8;
+    const int n = n0 + (i - row * NV8) * 8;
+    const long m = m0 + row;
+    if (m >= P || n >= a.N) continue;
+    const float* src = ct + row * C::LDC + (n - n0);
+    float v[8];
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
+    for (int q = 0; q < 8; ++q) v[q] = src[q];
+    if (a.bias) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const long m = m0 + wm * C::WM + i * 16 + rq + r;
-      if (m >= P) continue;
-      const int img = (int)(m / HW);
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int n = n0 + wn * C::WN + j * 16 + r16;
-        if (n >= a.N) continue;
-        float v = acc[i][j][r];
-        if (a.bias) v += a.bias[n];
-        if (a.rowvec) v += a.rowvec[(long)img * a.N + n];
-        if (a.resid.s0.ptr) {
-          const Src& s = a.resid.s0;
-          v += (s.dtype == DT_BF16)
-                   ? bf2f(static_cast<const uint16_t*>(s.ptr)[m * s.C + n])
-                   : static_cast<const float*>(s.ptr)[m * s.C + n];
-        }
-        if (a.out_dtype == DT_BF16) {
-          const uint16_t b = f2bf(v);
-          static_cast<uint16_t*>(a.out)[m * a.ldo + n] = b;
-          if (a.out2) static_cast<uint16_t*>(a.out2)[m * a.ldo + n] = b;
-        } else {
-          static_cast<float*>(a.out)[m * a.ldo + n] = v;
-          if (a.out2) static_cast<float*>(a.out2)[m * a.ldo + n] = v;
-        }
-      }
+      for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
     }
+    if (a.rowvec) {
+      const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += rv[q];
+    }
+    if (a.resid.s0.ptr) {
+      float r[8];
+      ld8(a.resid.s0, m, n, r);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += r[q];
+    }
+    st8(a.out, a.out_dtype, a.ldo, m, n, v);
+    if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
   }
 }
 
@@ -369,8 +393,40 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
   const long P = a.g.pixels();
   const long pbeg = (long)z * a.kchunk;
   const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
+  const Seg sg0 = a.seg[0], sg1 = a.seg[1], sg2 = a.seg[2];
+  const int nseg = a.nseg;
+  const VIn gy = a.gy;
 
   VecT<C::F32> rt[C::NMT][8];
+
+  // B micro-tile: 8 columns (one segment, one tap, 8 channels) x 8 pixels
+  auto load_b = [&](const Seg& sg, int n, long p, VecT<C::F32> (&in)[8])
+      __attribute__((always_inline)) {
+    const int r = n - sg.begin;
+    const int tap = r / sg.C;
+    const int c = r - tap * sg.C;
+    const int t9 = sg.taps == 9 ? tap : 4;
+    const int oy = t9 / 3 - 1, ox = t9 % 3 - 1;
+    int img = (int)(p / HW);
+    int rem = (int)(p - (long)img * HW);
+    int h = rem / W;
+    int w = rem - h * W;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int hh = h + oy, ww = w + ox;
+      if (p + e < pend && hh >= 0 && hh < H && ww >= 0 && ww < W)
+        vload<C::F32>(vaddr<C::F32>(sg.in, p + e + (long)oy * W + ox, c), in[e]);
+      else
+        vzero<C::F32>(in[e]);
+      if (++w == W) {
+        w = 0;
+        if (++h == H) {
+          h = 0;
+          ++img;
+        }
+      }
+    }
+  };
 
   // micro-tile t: t < NMA -> A rows (output channels), else B rows (columns)
   auto load_tiles = [&](long p0) __attribute__((always_inline)) {
@@ -378,72 +434,37 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
     for (int u = 0; u < C::NMT; ++u) {
       const int t = tid + u * C::NT;
       if (t >= C::NMA + C::NMB) break;
+      VecT<C::F32> in[8];
       if (t < C::NMA) {
         const int oi = t / (C::BK / 8), pk = t % (C::BK / 8);
         const int o = m0 + oi * 8;
-        float f[8][8];
+        const long p = p0 + pk * 8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const long p = p0 + pk * 8 + e;
-          if (o < a.M && p < pend) {
-            ld8v(a.gy, p, o, f[e]);
-          } else {
-#pragma unroll
-            for (int q = 0; q < 8; ++q) f[e][q] = 0.f;
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          float col[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) col[e] = f[e][q];
-          to_vec<C::F32>(col, rt[u][q]);
+          if (o < a.M && p + e < pend)
+            vload<C::F32>(vaddr<C::F32>(gy, p + e, o), in[e]);
+          else
+            vzero<C::F32>(in[e]);
         }
       } else {
         const int tb = t - C::NMA;
         const int ni = tb / (C::BK / 8), pk = tb % (C::BK / 8);
         const int n = n0 + ni * 8;
-        float f[8][8];
-        const bool nval = n < a.N;
-        const int s = seg_of(a, nval ? n : 0);
-        const Seg sg = pick_seg(a, s);
-        const int r = (nval ? n : 0) - sg.begin;
-        const int tap = r / sg.C;
-        const int c = r - tap * sg.C;
-        int oy, ox;
-        tap_offset(sg.taps, tap, oy, ox);
-        // pixel coordinates of p0 + pk*8, then walk forward one pixel at a time
-        long p = p0 + pk * 8;
-        int img = (int)(p / HW);
-        int rem = (int)(p - (long)img * HW);
-        int h = rem / W;
-        int w = rem - h * W;
+        const long p = p0 + pk * 8;
+        if (n < a.N) {
+          const int s = seg_of(nseg, sg1.begin, sg2.begin, n);
+          if (s == 0)
+            load_b(sg0, n, p, in);
+          else if (s == 1)
+            load_b(sg1, n, p, in);
+          else
+            load_b(sg2, n, p, in);
+        } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int hh = h + oy, ww = w + ox;
-          if (nval && p < pend && hh >= 0 && hh < H && ww >= 0 && ww < W) {
-            ld8v(sg.in, ((long)img * H + hh) * W + ww, c, f[e]);
-          } else {
-#pragma unroll
-            for (int q = 0; q < 8; ++q) f[e][q] = 0.f;
-          }
-          ++p;
-          if (++w == W) {
-            w = 0;
-            if (++h == H) {
-              h = 0;
-              ++img;
-            }
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          float col[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) col[e] = f[e][q];
-          to_vec<C::F32>(col, rt[u][q]);
+          for (int e = 0; e < 8; ++e) vzero<C::F32>(in[e]);
         }
       }
+      transpose8<C::F32>(in, rt[u]);
     }
   };
 
@@ -487,21 +508,21 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
     }
   }
 
+  // partials through LDS so each row is written as whole 16-byte vectors
+  float* ct = reinterpret_cast<float*>(smem);
+  acc_to_lds<C>(ct, wm, wn, lane, acc);
+  __syncthreads();
   float* part = a.part + (long)z * a.M * a.N;
-  const int r16 = lane & 15;
-  const int rq = (lane >> 4) * 4;
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * C::WM + i * 16 + rq + r;
-      if (m >= a.M) continue;
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int n = n0 + wn * C::WN + j * 16 + r16;
-        if (n < a.N) part[(long)m * a.N + n] = acc[i][j][r];
-      }
-    }
+  constexpr int NV4 = C::BN / 4;
+  for (int i = tid; i < C::BM * NV4; i += C::NT) {
+    const int row = i / NV4;
+    const int n = n0 + (i - row * NV4) * 4;
+    const int m = m0 + row;
+    if (m >= a.M || n >= a.N) continue;
+    const float* src = ct + row * C::LDC + (n - n0);
+    *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
+        make_float4(src[0], src[1], src[2], src[3]);
+  }
 }
 
 // Sum the split partials in split order and accumulate into the gradients
@@ -513,8 +534,9 @@ __global__ void wgrad_finalize(GemmArgs a, int splits) {
   const int n = (int)(idx - (long)m * a.N);
   float s = 0.f;
   for (int z = 0; z < splits; ++z) s += a.part[(long)z * a.M * a.N + idx];
-  const int sgi = seg_of(a, n);
-  const Seg sg = pick_seg(a, sgi);
+  const Seg sg0 = a.seg[0], sg1 = a.seg[1], sg2 = a.seg[2];
+  const int si = seg_of(a.nseg, sg1.begin, sg2.begin, n);
+  const Seg& sg = si == 0 ? sg0 : (si == 1 ? sg1 : sg2);
   const int len = sg.end - sg.begin;
   sg.grad[(long)m * len + (n - sg.begin)] += s;
 }
@@ -531,8 +553,7 @@ template <class C>
 static hipError_t launch_conv_t(const GemmArgs& a, hipStream_t st) {
   const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL(igemm_conv<C>, dim3((unsigned)(tilesM * tilesN)), dim3(C::NT),
-                     0, st, a);
+  hipLaunchKernelGGL(igemm_conv<C>, dim3((unsigned)(tilesM * tilesN)), dim3(C::NT), 0, st, a);
   return hipGetLastError();
 }
 

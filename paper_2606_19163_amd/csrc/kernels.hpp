@@ -81,9 +81,10 @@ hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, Re
                                  const float* rstd, int G, float* partial, hipStream_t st);
 // coef[b][g][2] = (sum_g gamma*dz, sum_g gamma*dz*xhat) / count, and
 // dgamma[c] += sum dz*xhat, dbeta[c] += sum dz.
+// pi: scratch [2][B][C].
 hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                   int G, const float* gamma, float* coef, float* dgamma,
-                                  float* dbeta, hipStream_t st);
+                                  float* dbeta, float* pi, hipStream_t st);
 
 struct GnBwdOut {
   void* dst0;      // channels [0, c_split): stride c_split
@@ -104,10 +105,11 @@ hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedG
 // partial[b][chunk][0][c] = sum over the chunk of v (v may carry an addend).
 hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st);
-// acc0[c] += sum_{b,chunk} partial, acc1 likewise (may be null);
-// per_image[b][c] = sum_chunk partial (may be null).
+// pi[s][b][c] = sum_chunk partial[b][chunk][s][c] for s < nslot (pi: [nslot][B][C]);
+// then acc0[c] += sum_b pi[0][b][c], dup[c] += the same, acc1[c] += sum_b
+// pi[1][b][c] (each may be null).
 hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
-                                    float* acc0, float* acc1, float* per_image,
+                                    int nslot, float* pi, float* acc0, float* dup, float* acc1,
                                     hipStream_t st);
 
 // ---- timestep embedding, weights, copies (misc.hip) ----------------------
@@ -133,6 +135,9 @@ hipError_t launch_transpose(const float* src, int O, int C, void* dst, int dtype
                             hipStream_t st);
 // dst[i] = a[i] + (b ? b[i] : 0)
 hipError_t launch_vec_add(const float* a, const float* b, float* dst, int n, hipStream_t st);
+// dst = (ddt)(a + b) elementwise, a of dtype adt, b fp32
+hipError_t launch_add_cast(const void* a, int adt, const float* b, void* dst, int ddt, long n,
+                           hipStream_t st);
 // dst = convert(src), n elements (dtypes as DType)
 hipError_t launch_cast(const void* src, int sdt, void* dst, int ddt, long n, hipStream_t st);
 

@@ -108,6 +108,13 @@ __global__ void k_cast(const void* src, int sdt, void* dst, int ddt, long n) {
     st_any(dst, ddt, i, ld_any(src, sdt, i));
 }
 
+// dst = (ddt) (a + b), a of dtype adt, b fp32
+__global__ void k_add_cast(const void* a, int adt, const float* b, void* dst, int ddt, long n) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (long)gridDim.x * blockDim.x)
+    st_any(dst, ddt, i, ld_any(a, adt, i) + b[i]);
+}
+
 unsigned nblk(long n, int t = 256) { return (unsigned)((n + t - 1) / t); }
 
 }  // namespace
@@ -163,6 +170,16 @@ hipError_t launch_cast(const void* src, int sdt, void* dst, int ddt, long n, hip
   if (b > 8192) b = 8192;
   if (b < 1) b = 1;
   hipLaunchKernelGGL(k_cast, dim3((unsigned)b), dim3(256), 0, st, src, sdt, dst, ddt, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_add_cast(const void* a, int adt, const float* b, void* dst, int ddt, long n,
+                           hipStream_t st) {
+  long blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_add_cast, dim3((unsigned)blocks), dim3(256), 0, st, a, adt, b, dst, ddt,
+                     n);
   return hipGetLastError();
 }
 

@@ -79,39 +79,55 @@ __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid 
   lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
 }
 
+// Fixed-order block sum of two fp64 values (256 threads).
+__device__ __forceinline__ void block_sum2(double& a, double& b, double* sm) {
+  const int t = threadIdx.x;
+  sm[t] = a;
+  sm[256 + t] = b;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (t < off) {
+      sm[t] += sm[t + off];
+      sm[256 + t] += sm[256 + t + off];
+    }
+    __syncthreads();
+  }
+  a = sm[0];
+  b = sm[256];
+}
+
+// one block per (image, group): mean / rstd from the per-chunk channel sums,
+// then the folded affine of the group's channels
 __global__ __launch_bounds__(256) void k_gn_stats_finalize(const float* partial, Geo g,
                                                            RedGrid rg, int C, int G, float eps,
                                                            const float* gamma, const float* beta,
                                                            float* mean, float* rstd,
                                                            float* scale, float* shift) {
-  __shared__ float sm_mean[256], sm_rstd[256];
-  const int b = blockIdx.x;
+  __shared__ double sm[512];
+  const int b = blockIdx.x, gi = blockIdx.y;
   const int cg = C / G;
+  double S = 0.0, Q = 0.0;
+  for (int i = threadIdx.x; i < rg.chunks * cg; i += 256) {
+    const int ch = i / cg;
+    const int c = gi * cg + (i - ch * cg);
+    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+    S += base[c];
+    Q += base[C + c];
+  }
+  block_sum2(S, Q, sm);
   const double cnt = (double)g.hw() * cg;
-  for (int gi = threadIdx.x; gi < G; gi += blockDim.x) {
-    double S = 0.0, Q = 0.0;
-    for (int ch = 0; ch < rg.chunks; ++ch) {
-      const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
-      for (int c = gi * cg; c < (gi + 1) * cg; ++c) {
-        S += base[c];
-        Q += base[C + c];
-      }
-    }
-    const double m = S / cnt;
-    double var = Q / cnt - m * m;
-    if (var < 0.0) var = 0.0;
-    const float rs = (float)(1.0 / sqrt(var + (double)eps));
-    sm_mean[gi] = (float)m;
-    sm_rstd[gi] = rs;
+  const double m = S / cnt;
+  double var = Q / cnt - m * m;
+  if (var < 0.0) var = 0.0;
+  const float rs = (float)(1.0 / sqrt(var + (double)eps));
+  if (threadIdx.x == 0) {
     mean[b * G + gi] = (float)m;
     rstd[b * G + gi] = rs;
   }
-  __syncthreads();
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    const int gi = c / cg;
-    const float sc = gamma[c] * sm_rstd[gi];
+  for (int c = gi * cg + threadIdx.x; c < (gi + 1) * cg; c += 256) {
+    const float sc = gamma[c] * rs;
     scale[(long)b * C + c] = sc;
-    shift[(long)b * C + c] = beta[c] - sm_mean[gi] * sc;
+    shift[(long)b * C + c] = beta[c] - (float)m * sc;
   }
 }
 
@@ -196,48 +212,73 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, 
   lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
 }
 
+// one block per (image, group): coef = (sum gamma*dz, sum gamma*dz*xhat) / count
 __global__ __launch_bounds__(256) void k_gn_bwd_coef(const float* partial, Geo g, RedGrid rg,
                                                      int C, int G, const float* gamma,
                                                      float* coef) {
-  const int b = blockIdx.x;
+  __shared__ double sm[512];
+  const int b = blockIdx.x, gi = blockIdx.y;
   const int cg = C / G;
-  const double cnt = (double)g.hw() * cg;
-  for (int gi = threadIdx.x; gi < G; gi += blockDim.x) {
-    double S1 = 0.0, S2 = 0.0;
-    for (int ch = 0; ch < rg.chunks; ++ch) {
-      const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
-      for (int c = gi * cg; c < (gi + 1) * cg; ++c) {
-        S1 += (double)gamma[c] * base[c];
-        S2 += (double)gamma[c] * base[C + c];
-      }
-    }
+  double S1 = 0.0, S2 = 0.0;
+  for (int i = threadIdx.x; i < rg.chunks * cg; i += 256) {
+    const int ch = i / cg;
+    const int c = gi * cg + (i - ch * cg);
+    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+    S1 += (double)gamma[c] * base[c];
+    S2 += (double)gamma[c] * base[C + c];
+  }
+  block_sum2(S1, S2, sm);
+  if (threadIdx.x == 0) {
+    const double cnt = (double)g.hw() * cg;
     coef[(b * G + gi) * 2 + 0] = (float)(S1 / cnt);
     coef[(b * G + gi) * 2 + 1] = (float)(S2 / cnt);
   }
 }
 
-// out0[c] += sum_{b,chunk} partial[..][0][c]; out1[c] += ..[1][c] (nullable);
-// per_image[b][c] = sum_chunk partial[b][..][0][c] (nullable); acc1 gets the
-// same total as out0 when `dup` is set (a second bias sharing the gradient).
-__global__ void k_chan_finalize(const float* partial, int B, int chunks, int C, float* out0,
-                                float* out1, float* dup, float* per_image) {
+// Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
+// partial[b][chunk][s][c] for the first `nslot` slots.  Block (64 channels,
+// 4 chunk lanes) per (channel block, image).
+__global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, int chunks, int B,
+                                                        int C, int nslot, float* pi) {
+  __shared__ float sm[2][PY][VX];
+  const int c = blockIdx.x * VX + threadIdx.x;
+  const int b = blockIdx.y;
+  float s0 = 0.f, s1 = 0.f;
+  if (c < C) {
+    for (int ch = threadIdx.y; ch < chunks; ch += PY) {
+      const float* base = partial + ((long)b * chunks + ch) * 2 * C;
+      s0 += base[c];
+      if (nslot > 1) s1 += base[C + c];
+    }
+  }
+  sm[0][threadIdx.y][threadIdx.x] = s0;
+  sm[1][threadIdx.y][threadIdx.x] = s1;
+  __syncthreads();
+  if (threadIdx.y == 0 && c < C) {
+    float t0 = sm[0][0][threadIdx.x], t1 = sm[1][0][threadIdx.x];
+#pragma unroll
+    for (int y = 1; y < PY; ++y) {
+      t0 += sm[0][y][threadIdx.x];
+      t1 += sm[1][y][threadIdx.x];
+    }
+    pi[(long)b * C + c] = t0;
+    if (nslot > 1) pi[(long)(B + b) * C + c] = t1;
+  }
+}
+
+// acc0[c] += sum_b pi[0][b][c] (and dup[c]); acc1[c] += sum_b pi[1][b][c]
+__global__ void k_chan_total(const float* pi, int B, int C, float* acc0, float* dup,
+                             float* acc1) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= C) return;
   float t0 = 0.f, t1 = 0.f;
   for (int b = 0; b < B; ++b) {
-    float s0 = 0.f, s1 = 0.f;
-    for (int ch = 0; ch < chunks; ++ch) {
-      const float* base = partial + ((long)b * chunks + ch) * 2 * C;
-      s0 += base[c];
-      if (out1) s1 += base[C + c];
-    }
-    if (per_image) per_image[(long)b * C + c] = s0;
-    t0 += s0;
-    t1 += s1;
+    t0 += pi[(long)b * C + c];
+    if (acc1) t1 += pi[(long)(B + b) * C + c];
   }
-  if (out0) out0[c] += t0;
+  if (acc0) acc0[c] += t0;
   if (dup) dup[c] += t0;
-  if (out1) out1[c] += t1;
+  if (acc1) acc1[c] += t1;
 }
 
 __global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Geo g,
@@ -354,7 +395,7 @@ hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid 
                                     int G, float eps, const float* gamma, const float* beta,
                                     float* mean, float* rstd, float* scale, float* shift,
                                     hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_stats_finalize, dim3(g.B), dim3(256), 0, st, partial, g, rg, C, G,
+  hipLaunchKernelGGL(k_gn_stats_finalize, dim3(g.B, G), dim3(256), 0, st, partial, g, rg, C, G,
                      eps, gamma, beta, mean, rstd, scale, shift);
   return hipGetLastError();
 }
@@ -379,15 +420,13 @@ hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, Re
 
 hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                   int G, const float* gamma, float* coef, float* dgamma,
-                                  float* dbeta, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_coef, dim3(g.B), dim3(256), 0, st, partial, g, rg, C, G, gamma,
+                                  float* dbeta, float* pi, hipStream_t st) {
+  hipLaunchKernelGGL(k_gn_bwd_coef, dim3(g.B, G), dim3(256), 0, st, partial, g, rg, C, G, gamma,
                      coef);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // dbeta from slot 0 (sum dz), dgamma from slot 1 (sum dz * xhat)
-  hipLaunchKernelGGL(k_chan_finalize, dim3((C + 255) / 256), dim3(256), 0, st, partial, g.B,
-                     rg.chunks, C, dbeta, dgamma, (float*)nullptr, (float*)nullptr);
-  return hipGetLastError();
+  return launch_chan_sum_finalize(partial, g, rg, C, 2, pi, dbeta, nullptr, dgamma, st);
 }
 
 hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedGrid rg,
@@ -407,10 +446,14 @@ hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float
 }
 
 hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
-                                    float* acc0, float* acc1, float* per_image,
+                                    int nslot, float* pi, float* acc0, float* dup, float* acc1,
                                     hipStream_t st) {
-  hipLaunchKernelGGL(k_chan_finalize, dim3((C + 255) / 256), dim3(256), 0, st, partial, g.B,
-                     rg.chunks, C, acc0, (float*)nullptr, acc1, per_image);
+  hipLaunchKernelGGL(k_chan_per_image, dim3((C + VX - 1) / VX, g.B), dim3(VX, PY), 0, st,
+                     partial, rg.chunks, g.B, C, nslot, pi);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || (!acc0 && !dup && !acc1)) return e;
+  hipLaunchKernelGGL(k_chan_total, dim3((C + 255) / 256), dim3(256), 0, st, pi, g.B, C, acc0,
+                     dup, acc1);
   return hipGetLastError();
 }
 

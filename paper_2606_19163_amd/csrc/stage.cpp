@@ -113,7 +113,7 @@ struct pulse_stage {
   size_t row_act[MAX_SLOTS], row_grad[MAX_SLOTS];
   size_t row_temb[2] = {0, 0}, row_xin = 0, row_u = 0;
   size_t s_da = 0, s_dxs = 0, s_dh1 = 0, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
-         s_de = 0, s_e = 0;
+         s_pi = 0, s_e = 0;
   size_t part_cap = 0;
   // binding
   const float* prm = nullptr;
@@ -317,7 +317,7 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_part = sc; sc += align256(part * 4);
   s->s_red = sc; sc += align256(red * 4);
   s->s_coef = sc; sc += align256((size_t)s->geo.B * s->G * 2 * 4);
-  s->s_de = sc; sc += align256((size_t)s->geo.B * cmax * 4);
+  s->s_pi = sc; sc += align256((size_t)2 * s->geo.B * cmax * 4);
   s->s_e = sc; sc += align256((size_t)s->geo.B * cmax * 4);
   s->ws_bytes = s->off_scratch + sc;
   return PULSE_OK;
@@ -586,7 +586,8 @@ pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& 
   const float* scale = reinterpret_cast<const float*>(row + g.scale);
   const float* shift = reinterpret_cast<const float*>(row + g.shift);
   HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
-  HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta, st));
+  HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta,
+                                s->sf(s->s_pi), st));
   GnBwdOut oo = o;
   if (oo.chan_partial) oo.chan_partial = red;  // reuse: the partials above are consumed
   HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, oo,
@@ -661,8 +662,9 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   {
     const RedGrid rg = red_grid(s->geo, b.cout);
     HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, s->sf(s->s_red), st));
-    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, s->gp(b.b2),
-                                    b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, st));
+    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, 1, s->sf(s->s_pi),
+                                    s->gp(b.b2), b.conv_sc ? s->gp(b.bs) : nullptr, nullptr,
+                                    st));
   }
   // weight gradients of conv2 and the shortcut, one GEMM
   const VIn a2v = vin1(row + b.a2, dt, b.cout);
@@ -687,11 +689,11 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
       return ps;
   }
   // GN2 backward -> dh1, with per-image channel sums (the temb gradient)
-  float* dh1 = s->sf(s->s_dh1);
+  void* dh1 = s->scratch(s->s_dh1);
   {
     GnBwdOut o2{};
     o2.dst0 = dh1;
-    o2.dtype0 = DT_F32;
+    o2.dtype0 = dt;
     o2.c_split = b.cout;
     o2.add0 = vnone();
     o2.chan_partial = s->sf(s->s_red);
@@ -700,16 +702,16 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
                           st)) != PULSE_OK)
       return ps;
     const RedGrid rg = red_grid(s->geo, b.cout);
-    float* de = s->sf(s->s_de);
-    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, nullptr, nullptr, de,
-                                    st));
+    float* de = s->sf(s->s_pi);  // per-image sums of dh1: [B][cout]
+    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, 1, de, nullptr, nullptr,
+                                    nullptr, st));
     HIPCHK(launch_temb_bwd(de, row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
                            s->gp(b.Wl), s->gp(b.bl), s->gp(b.b1), dtemb, st));
   }
   // conv1 weight and data gradients
   const VIn a1 = (b.cin > b.c0) ? vin2(row + b.a1_0, dt, b.c0, row + b.a1_1, dt, b.cin - b.c0)
                                 : vin1(row + b.a1_0, dt, b.cin);
-  const VIn dh1v = vin1(dh1, DT_F32, b.cout);
+  const VIn dh1v = vin1(dh1, dt, b.cout);
   if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, st)) != PULSE_OK)
     return ps;
   if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
@@ -996,17 +998,11 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
       for (int k = n - 1; k >= 0; --k) {
         const Block& b = s->db[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
-        const VIn dy = (k == n - 1) ? vin1(dout, dt, b.cout)
-                                    : vin1(s->sf(s->s_g[cur]), DT_F32, b.cout);
+        const VIn dy = vin1((k == n - 1) ? dout : s->scratch(s->s_g[cur]), dt, b.cout);
         GnBwdOut o{};
         o.c_split = b.c0;
-        if (k == 0) {
-          o.dst0 = din;
-          o.dtype0 = dt;
-        } else {
-          o.dst0 = s->sf(s->s_g[cur ^ 1]);
-          o.dtype0 = DT_F32;
-        }
+        o.dst0 = (k == 0) ? din : s->scratch(s->s_g[cur ^ 1]);
+        o.dtype0 = dt;
         o.dst1 = row + s->row_grad[b.slot];
         o.dtype1 = DT_F32;
         if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
@@ -1014,25 +1010,30 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
       }
     } else {
       const int n = (int)s->eb.size();
+      // buffered skip gradient of a slot (null when nothing read the skip)
+      auto dskip_of = [&](int slot) -> const float* {
+        return (slot >= 0 && s->slot_reader[slot] >= 0)
+                   ? reinterpret_cast<const float*>(row + s->row_grad[slot])
+                   : nullptr;
+      };
+      // gradient reaching the last block's output: dout plus its skip gradient
+      const void* dlast = dout;
+      if (const float* ds = dskip_of(s->eb[n - 1].slot)) {
+        HIPCHK(launch_add_cast(dout, dt, ds, s->scratch(s->s_g[cur]), dt,
+                               (long)s->P * s->eb[n - 1].cout, st));
+        dlast = s->scratch(s->s_g[cur]);
+      }
       for (int k = n - 1; k >= 0; --k) {
         const Block& b = s->eb[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
-        const float* dskip = (b.slot >= 0 && s->slot_reader[b.slot] >= 0)
-                                 ? reinterpret_cast<const float*>(row + s->row_grad[b.slot])
-                                 : nullptr;
-        const VIn dy = (k == n - 1) ? vin1(dout, dt, b.cout, dskip)
-                                    : vin1(s->sf(s->s_g[cur]), DT_F32, b.cout, dskip);
+        const VIn dy = vin1((k == n - 1) ? dlast : s->scratch(s->s_g[cur]), dt, b.cout);
         GnBwdOut o{};
         o.c_split = b.cin;
-        if (k == 0) {
-          o.dst0 = din;
-          o.dtype0 = dt;
-          if (d.input_skip_slot >= 0 && s->slot_reader[d.input_skip_slot] >= 0)
-            o.add1 = reinterpret_cast<const float*>(row + s->row_grad[d.input_skip_slot]);
-        } else {
-          o.dst0 = s->sf(s->s_g[cur ^ 1]);
-          o.dtype0 = DT_F32;
-        }
+        o.dst0 = (k == 0) ? din : s->scratch(s->s_g[cur ^ 1]);
+        o.dtype0 = dt;
+        // the block input is the previous block's output (or the stage input):
+        // its buffered skip gradient joins here, once
+        o.add1 = dskip_of(k == 0 ? d.input_skip_slot : s->eb[k - 1].slot);
         if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
         cur ^= 1;
       }
