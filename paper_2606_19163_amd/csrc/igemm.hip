@@ -100,6 +100,56 @@ __device__ __forceinline__ void lds_put(char* base, int row, int k, const VecT<C
                                                 v.w[C::F32 ? 6 : 2], v.w[C::F32 ? 7 : 3]);
 }
 
+// Buffer resource over `bytes` bytes at p: loads at offsets past the end
+// return zero, which gives the zero padding without branches.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long bytes) {
+  const int n = bytes > 0x7fffffffL ? 0x7fffffff : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, p ? n : 0,
+                                           0x00020000);
+}
+
+constexpr uint32_t OOB = 0x80000000u;  // an offset past every buffer
+
+template <bool F32>
+__device__ __forceinline__ void bload(__amdgpu_buffer_rsrc_t r, uint32_t off, VecT<F32>& v) {
+  const auto q0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  v.w[0] = q0.x; v.w[1] = q0.y; v.w[2] = q0.z; v.w[3] = q0.w;
+  if constexpr (F32) {
+    const auto q1 =
+        __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16u, 0, 0));
+    v.w[F32 ? 4 : 0] = q1.x; v.w[F32 ? 5 : 1] = q1.y;
+    v.w[F32 ? 6 : 2] = q1.z; v.w[F32 ? 7 : 3] = q1.w;
+  }
+}
+
+// Per-segment constants of a kernel launch, kept in scalar registers: the
+// buffer resources of its one or two sources, their pixel pitch in bytes and
+// the channel split.
+struct SegRt {
+  __amdgpu_buffer_rsrc_t r0, r1;
+  uint32_t pitch0, pitch1;
+  int c0, C, taps, begin;
+};
+
+template <bool F32>
+__device__ __forceinline__ SegRt seg_rt(const Seg& g, long P) {
+  constexpr int esz = F32 ? 4 : 2;
+  SegRt s;
+  s.r0 = make_rsrc(g.in.s0.ptr, P * g.in.s0.C * esz);
+  s.r1 = make_rsrc(g.in.s1.ptr, P * g.in.s1.C * esz);
+  s.pitch0 = (uint32_t)(g.in.s0.C * esz);
+  s.pitch1 = (uint32_t)(g.in.s1.C * esz);
+  s.c0 = g.in.c0;
+  s.C = g.C;
+  s.taps = g.taps;
+  s.begin = g.begin;
+  return s;
+}
+
+__device__ __forceinline__ SegRt pick(int s, const SegRt& a, const SegRt& b, const SegRt& c) {
+  return s == 0 ? a : (s == 1 ? b : c);
+}
+
 // Address of channel c of pixel pix of a raw two-source input.
 template <bool F32>
 __device__ __forceinline__ const char* vaddr(const VIn& v, long pix, int c) {
@@ -242,12 +292,12 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
 
   // this thread's A rows: pixel index and the 9-bit mask of in-image taps
   const int kv = tid % C::KV;
-  long ppix[C::NVA];
+  uint32_t ppix[C::NVA];
   uint32_t pmask[C::NVA];
 #pragma unroll
   for (int j = 0; j < C::NVA; ++j) {
     const long m = m0 + tid / C::KV + j * (C::NT / C::KV);
-    ppix[j] = m;
+    ppix[j] = (uint32_t)m;
     uint32_t mask = 0;
     if (m < P) {
       const int img = (int)(m / HW);
@@ -262,47 +312,43 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
     }
     pmask[j] = mask;
   }
+  // weight rows of this thread (rows past N read as zeros)
+  uint32_t boff[C::NVB];
+#pragma unroll
+  for (int j = 0; j < C::NVB; ++j) {
+    const int n = n0 + tid / C::KV + j * (C::NT / C::KV);
+    boff[j] = n < a.N ? (uint32_t)((long)n * a.ldb * C::ESZ + kv * 8 * C::ESZ) : OOB;
+  }
 
   VecT<C::F32> ra[C::NVA], rb[C::NVB];
-  const Seg sg0 = a.seg[0], sg1 = a.seg[1], sg2 = a.seg[2];
   const int nseg = a.nseg;
-
-  auto load_a = [&](const Seg& sg, int k0) __attribute__((always_inline)) {
-    const int r = k0 - sg.begin;
-    const int tap = r / sg.C;
-    const int cb = r - tap * sg.C + kv * 8;
-    // the centre tap of a 3x3 segment and every 1x1 tap read the pixel itself
-    const int t9 = sg.taps == 9 ? tap : 4;
-    const long shift = (long)(t9 / 3 - 1) * W + (t9 % 3 - 1);
-#pragma unroll
-    for (int j = 0; j < C::NVA; ++j) {
-      if ((pmask[j] >> t9) & 1u)
-        vload<C::F32>(vaddr<C::F32>(sg.in, ppix[j] + shift, cb), ra[j]);
-      else
-        vzero<C::F32>(ra[j]);
-    }
-  };
+  const SegRt q0 = seg_rt<C::F32>(a.seg[0], P);
+  const SegRt q1 = seg_rt<C::F32>(a.seg[1], P);
+  const SegRt q2 = seg_rt<C::F32>(a.seg[2], P);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.Bw, (long)a.N * a.ldb * C::ESZ);
 
   auto load_tiles = [&](int kt) __attribute__((always_inline)) {
     const int k0 = kt * C::BK;
-    // the segment is uniform across the block; branch so every access to the
-    // segment table uses a constant index
-    const int s = seg_of(nseg, sg1.begin, sg2.begin, k0);
-    if (s == 0)
-      load_a(sg0, k0);
-    else if (s == 1)
-      load_a(sg1, k0);
-    else
-      load_a(sg2, k0);
+    // everything below up to the loads is uniform across the block
+    const SegRt q = pick(seg_of(nseg, q1.begin, q2.begin, k0), q0, q1, q2);
+    const int r = k0 - q.begin;
+    const int tap = r / q.C;
+    const int cb = r - tap * q.C;
+    const bool second = cb >= q.c0;
+    const __amdgpu_buffer_rsrc_t rs = second ? q.r1 : q.r0;
+    const uint32_t pitch = second ? q.pitch1 : q.pitch0;
+    const uint32_t coff = (uint32_t)(((second ? cb - q.c0 : cb) + kv * 8) * C::ESZ);
+    // the centre tap of a 3x3 segment and every 1x1 tap read the pixel itself
+    const int t9 = q.taps == 9 ? tap : 4;
+    const int shift = (t9 / 3 - 1) * W + (t9 % 3 - 1);
 #pragma unroll
-    for (int j = 0; j < C::NVB; ++j) {
-      const int n = n0 + tid / C::KV + j * (C::NT / C::KV);
-      if (n < a.N)
-        vload<C::F32>(static_cast<const char*>(a.Bw) + ((long)n * a.ldb + k0 + kv * 8) * C::ESZ,
-                      rb[j]);
-      else
-        vzero<C::F32>(rb[j]);
+    for (int j = 0; j < C::NVA; ++j) {
+      const uint32_t off = ((pmask[j] >> t9) & 1u) ? (ppix[j] + shift) * pitch + coff : OOB;
+      bload<C::F32>(rs, off, ra[j]);
     }
+    const uint32_t kb = (uint32_t)(k0 * C::ESZ);
+#pragma unroll
+    for (int j = 0; j < C::NVB; ++j) bload<C::F32>(rw, boff[j] + kb, rb[j]);
   };
 
   auto store_tiles = [&](int buf) __attribute__((always_inline)) {
@@ -393,36 +439,52 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
   const long P = a.g.pixels();
   const long pbeg = (long)z * a.kchunk;
   const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
-  const Seg sg0 = a.seg[0], sg1 = a.seg[1], sg2 = a.seg[2];
   const int nseg = a.nseg;
-  const VIn gy = a.gy;
+  const SegRt q0 = seg_rt<C::F32>(a.seg[0], P);
+  const SegRt q1 = seg_rt<C::F32>(a.seg[1], P);
+  const SegRt q2 = seg_rt<C::F32>(a.seg[2], P);
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gy.s0.ptr, P * a.gy.s0.C * C::ESZ);
+  const uint32_t gpitch = (uint32_t)(a.gy.s0.C * C::ESZ);
 
+  // this thread's micro-tiles, loaded raw (pixel-major) and transposed when
+  // they are written to LDS
   VecT<C::F32> rt[C::NMT][8];
 
   // B micro-tile: 8 columns (one segment, one tap, 8 channels) x 8 pixels
-  auto load_b = [&](const Seg& sg, int n, long p, VecT<C::F32> (&in)[8])
-      __attribute__((always_inline)) {
-    const int r = n - sg.begin;
-    const int tap = r / sg.C;
-    const int c = r - tap * sg.C;
-    const int t9 = sg.taps == 9 ? tap : 4;
+  auto load_b = [&](int n, long p, VecT<C::F32> (&in)[8]) __attribute__((always_inline)) {
+    const SegRt q = pick(seg_of(nseg, q1.begin, q2.begin, n), q0, q1, q2);
+    const int r = n - q.begin;
+    const int tap = r / q.C;
+    const int c = r - tap * q.C;
+    const bool second = c >= q.c0;
+    const __amdgpu_buffer_rsrc_t rs = second ? q.r1 : q.r0;
+    const uint32_t pitch = second ? q.pitch1 : q.pitch0;
+    const uint32_t coff = (uint32_t)((second ? c - q.c0 : c) * C::ESZ);
+    const int t9 = q.taps == 9 ? tap : 4;
     const int oy = t9 / 3 - 1, ox = t9 % 3 - 1;
-    int img = (int)(p / HW);
-    int rem = (int)(p - (long)img * HW);
-    int h = rem / W;
-    int w = rem - h * W;
+    const int img = (int)(p / HW);
+    const int rem = (int)(p - (long)img * HW);
+    const int h = rem / W;
+    const int w = rem - h * W;
+    if (W % 8 == 0) {
+      // the 8 pixels share one image row
+      const bool rowok = h + oy >= 0 && h + oy < H;
+      const uint32_t base = (uint32_t)(p + oy * W + ox);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int hh = h + oy, ww = w + ox;
-      if (p + e < pend && hh >= 0 && hh < H && ww >= 0 && ww < W)
-        vload<C::F32>(vaddr<C::F32>(sg.in, p + e + (long)oy * W + ox, c), in[e]);
-      else
-        vzero<C::F32>(in[e]);
-      if (++w == W) {
-        w = 0;
-        if (++h == H) {
-          h = 0;
-          ++img;
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = rowok && p + e < pend && w + e + ox >= 0 && w + e + ox < W;
+        bload<C::F32>(rs, ok ? (base + e) * pitch + coff : OOB, in[e]);
+      }
+    } else {
+      int hh = h, ww = w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = p + e < pend && hh + oy >= 0 && hh + oy < H && ww + ox >= 0 &&
+                        ww + ox < W;
+        bload<C::F32>(rs, ok ? (uint32_t)(p + e + oy * W + ox) * pitch + coff : OOB, in[e]);
+        if (++ww == W) {
+          ww = 0;
+          if (++hh == H) hh = 0;
         }
       }
     }
@@ -434,17 +496,14 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
     for (int u = 0; u < C::NMT; ++u) {
       const int t = tid + u * C::NT;
       if (t >= C::NMA + C::NMB) break;
-      VecT<C::F32> in[8];
       if (t < C::NMA) {
         const int oi = t / (C::BK / 8), pk = t % (C::BK / 8);
         const int o = m0 + oi * 8;
         const long p = p0 + pk * 8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          if (o < a.M && p + e < pend)
-            vload<C::F32>(vaddr<C::F32>(gy, p + e, o), in[e]);
-          else
-            vzero<C::F32>(in[e]);
+          const bool ok = o < a.M && p + e < pend;
+          bload<C::F32>(rg, ok ? (uint32_t)(p + e) * gpitch + o * C::ESZ : OOB, rt[u][e]);
         }
       } else {
         const int tb = t - C::NMA;
@@ -452,19 +511,12 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
         const int n = n0 + ni * 8;
         const long p = p0 + pk * 8;
         if (n < a.N) {
-          const int s = seg_of(nseg, sg1.begin, sg2.begin, n);
-          if (s == 0)
-            load_b(sg0, n, p, in);
-          else if (s == 1)
-            load_b(sg1, n, p, in);
-          else
-            load_b(sg2, n, p, in);
+          load_b(n, p, rt[u]);
         } else {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) vzero<C::F32>(in[e]);
+          for (int e = 0; e < 8; ++e) vzero<C::F32>(rt[u][e]);
         }
       }
-      transpose8<C::F32>(in, rt[u]);
     }
   };
 
@@ -475,15 +527,17 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
     for (int u = 0; u < C::NMT; ++u) {
       const int t = tid + u * C::NT;
       if (t >= C::NMA + C::NMB) break;
+      VecT<C::F32> tr[8];
+      transpose8<C::F32>(rt[u], tr);
       if (t < C::NMA) {
         const int oi = t / (C::BK / 8), pk = t % (C::BK / 8);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) lds_put<C>(As, oi * 8 + q, pk * 8, rt[u][q]);
+        for (int q = 0; q < 8; ++q) lds_put<C>(As, oi * 8 + q, pk * 8, tr[q]);
       } else {
         const int tb = t - C::NMA;
         const int ni = tb / (C::BK / 8), pk = tb % (C::BK / 8);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) lds_put<C>(Bs, ni * 8 + q, pk * 8, rt[u][q]);
+        for (int q = 0; q < 8; ++q) lds_put<C>(Bs, ni * 8 + q, pk * 8, tr[q]);
       }
     }
   };

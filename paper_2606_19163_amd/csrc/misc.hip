@@ -57,16 +57,26 @@ __global__ void k_temb_bwd_w(const float* de, const void* temb, int dtype, int B
   }
 }
 
-// thread (b, d): dtemb[b][d] += SiLU'(temb[b][d]) * sum_o Wl[o][d] de[b][o]
-__global__ void k_temb_bwd_x(const float* de, const void* temb, int dtype, int B, int D, int O,
-                             const float* Wl, float* dtemb) {
-  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (long)B * D) return;
-  const int b = (int)(i / D);
-  const int d = (int)(i - (long)b * D);
+// block (64 d x 8 o-lanes) per (d block, image b):
+// dtemb[b][d] += SiLU'(temb[b][d]) * sum_o Wl[o][d] de[b][o]
+__global__ __launch_bounds__(512) void k_temb_bwd_x(const float* de, const void* temb, int dtype,
+                                                    int B, int D, int O, const float* Wl,
+                                                    float* dtemb) {
+  __shared__ float sm[8][64];
+  const int d = blockIdx.x * 64 + threadIdx.x;
+  const int b = blockIdx.y;
   float s = 0.f;
-  for (int o = 0; o < O; ++o) s += Wl[(long)o * D + d] * de[(long)b * O + o];
-  dtemb[i] += s * dsilu_f(ld_any(temb, dtype, i));
+  if (d < D)
+    for (int o = threadIdx.y; o < O; o += 8) s += Wl[(long)o * D + d] * de[(long)b * O + o];
+  sm[threadIdx.y][threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.y == 0 && d < D) {
+    float t = sm[0][threadIdx.x];
+#pragma unroll
+    for (int y = 1; y < 8; ++y) t += sm[y][threadIdx.x];
+    const long i = (long)b * D + d;
+    dtemb[i] += t * dsilu_f(ld_any(temb, dtype, i));
+  }
 }
 
 __global__ void k_convert_rows(const float* src, int rows, int cols, void* dst, int ldd,
@@ -134,7 +144,7 @@ hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, 
                      dtype, B, D, O, dWl, dbl, db1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !dtemb) return e;
-  hipLaunchKernelGGL(k_temb_bwd_x, dim3(nblk((long)B * D)), dim3(256), 0, st, de, temb, dtype,
+  hipLaunchKernelGGL(k_temb_bwd_x, dim3((D + 63) / 64, B), dim3(64, 8), 0, st, de, temb, dtype,
                      B, D, O, Wl, dtemb);
   return hipGetLastError();
 }

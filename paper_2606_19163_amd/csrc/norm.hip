@@ -374,7 +374,8 @@ dim3 red_dims(const Geo& g, RedGrid rg, int C) {
 RedGrid red_grid(const Geo& g, int C) {
   const int nvb = (C / 8 + VX - 1) / VX;
   const int hw = g.hw();
-  int chunks = 2048 / (g.B * nvb);
+  int chunks = 1024 / (g.B * nvb);
+  if (chunks > 64) chunks = 64;
   const int max_chunks = (hw + 15) / 16;
   if (chunks > max_chunks) chunks = max_chunks;
   if (chunks < 1) chunks = 1;
