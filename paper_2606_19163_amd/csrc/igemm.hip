@@ -47,23 +47,21 @@ struct Cfg {
   static constexpr int ESZ = F32 ? 4 : 2;         // bytes per element
   static constexpr int LDK = BK + (F32 ? 4 : 8);  // padded LDS row (elements)
   static constexpr int KV = BK / 8;               // 8-element vectors per row
-  static constexpr int VW = F32 ? 8 : 4;          // 32-bit words per vector
   static constexpr int LDS_A = BM * LDK * ESZ;
   static constexpr int LDS_B = BN * LDK * ESZ;
   static constexpr int LDS_OPS = 2 * (LDS_A + LDS_B);
-  static constexpr int LDC = BN + 4;              // fp32 epilogue tile row
-  static constexpr int LDS_EPI = BM * LDC * 4;
+  static constexpr int LDC = BN + 4;              // fp32 epilogue rows
+  static constexpr int LDS_EPI = WM * LDC * 4;    // one wave row at a time
   static constexpr int LDS_BYTES = LDS_OPS > LDS_EPI ? LDS_OPS : LDS_EPI;
-  // CONV mode: vectors per thread for the A and B tiles
-  static constexpr int NVA = (BM * KV) / NT;
-  static constexpr int NVB = (BN * KV) / NT;
+  // CONV mode: 8-element vectors per thread for the A and B tiles
+  static constexpr int NVA = (BM * KV + NT - 1) / NT;
+  static constexpr int NVB = (BN * KV + NT - 1) / NT;
   // WGRAD mode: 8x8 micro-tiles per thread
   static constexpr int NMA = (BM / 8) * (BK / 8);
   static constexpr int NMB = (BN / 8) * (BK / 8);
   static constexpr int NMT = (NMA + NMB + NT - 1) / NT;
   static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
-  static_assert(BK % 32 == 0, "BK");
-  static_assert((BM * KV) % NT == 0 && (BN * KV) % NT == 0, "vector split");
+  static_assert(BK % 32 == 0 && NT % KV == 0, "BK");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
@@ -251,9 +249,10 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, int wm,
   }
 }
 
-// Park the accumulators of every wave in an fp32 [BM][LDC] LDS tile.
+// Park one wave's accumulators in an fp32 [WM][LDC] LDS tile (rows of the
+// wave's row group, columns of the whole block tile).
 template <class C>
-__device__ __forceinline__ void acc_to_lds(float* ct, int wm, int wn, int lane,
+__device__ __forceinline__ void acc_to_lds(float* ct, int wn, int lane,
                                            const f32x4_t (&acc)[C::TM][C::TN]) {
   const int r16 = lane & 15;
   const int rq = (lane >> 4) * 4;
@@ -263,7 +262,7 @@ __device__ __forceinline__ void acc_to_lds(float* ct, int wm, int wn, int lane,
     for (int j = 0; j < C::TN; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        ct[(wm * C::WM + i * 16 + rq + r) * C::LDC + wn * C::WN + j * 16 + r16] = acc[i][j][r];
+        ct[(i * 16 + rq + r) * C::LDC + wn * C::WN + j * 16 + r16] = acc[i][j][r];
 }
 
 // ---------------------------------------------------------------------------
@@ -291,12 +290,14 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
   const long P = a.g.pixels();
 
   // this thread's A rows: pixel index and the 9-bit mask of in-image taps
+  // (rows past the tile or past P get an empty mask and read zeros)
   const int kv = tid % C::KV;
   uint32_t ppix[C::NVA];
   uint32_t pmask[C::NVA];
 #pragma unroll
   for (int j = 0; j < C::NVA; ++j) {
-    const long m = m0 + tid / C::KV + j * (C::NT / C::KV);
+    const int rowt = tid / C::KV + j * (C::NT / C::KV);
+    const long m = rowt < C::BM ? m0 + rowt : P;
     ppix[j] = (uint32_t)m;
     uint32_t mask = 0;
     if (m < P) {
@@ -316,8 +317,10 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
   uint32_t boff[C::NVB];
 #pragma unroll
   for (int j = 0; j < C::NVB; ++j) {
-    const int n = n0 + tid / C::KV + j * (C::NT / C::KV);
-    boff[j] = n < a.N ? (uint32_t)((long)n * a.ldb * C::ESZ + kv * 8 * C::ESZ) : OOB;
+    const int rowt = tid / C::KV + j * (C::NT / C::KV);
+    const int n = n0 + rowt;
+    boff[j] = (rowt < C::BN && n < a.N) ? (uint32_t)((long)n * a.ldb * C::ESZ + kv * 8 * C::ESZ)
+                                        : OOB;
   }
 
   VecT<C::F32> ra[C::NVA], rb[C::NVB];
@@ -355,11 +358,15 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
     char* As = smem + buf * (C::LDS_A + C::LDS_B);
     char* Bs = As + C::LDS_A;
 #pragma unroll
-    for (int j = 0; j < C::NVA; ++j)
-      lds_put<C>(As, tid / C::KV + j * (C::NT / C::KV), kv * 8, ra[j]);
+    for (int j = 0; j < C::NVA; ++j) {
+      const int rowt = tid / C::KV + j * (C::NT / C::KV);
+      if ((C::BM * C::KV) % C::NT == 0 || rowt < C::BM) lds_put<C>(As, rowt, kv * 8, ra[j]);
+    }
 #pragma unroll
-    for (int j = 0; j < C::NVB; ++j)
-      lds_put<C>(Bs, tid / C::KV + j * (C::NT / C::KV), kv * 8, rb[j]);
+    for (int j = 0; j < C::NVB; ++j) {
+      const int rowt = tid / C::KV + j * (C::NT / C::KV);
+      if ((C::BN * C::KV) % C::NT == 0 || rowt < C::BN) lds_put<C>(Bs, rowt, kv * 8, rb[j]);
+    }
   };
 
   f32x4_t acc[C::TM][C::TN];
@@ -380,38 +387,42 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
     __syncthreads();
   }
 
-  // epilogue: accumulators -> LDS -> rows of 8 channels (+bias, +rowvec,
-  // +residual) -> 16-byte stores
+  // epilogue, one wave row group at a time: accumulators -> LDS -> rows of
+  // 8 channels (+bias, +rowvec, +residual) -> 16-byte stores
   float* ct = reinterpret_cast<float*>(smem);
-  acc_to_lds<C>(ct, wm, wn, lane, acc);
-  __syncthreads();
   constexpr int NV8 = C::BN / 8;
-  for (int i = tid; i < C::BM * NV8; i += C::NT) {
-    const int row = i / NV8;
-    const int n = n0 + (i - row * NV8) * 8;
-    const long m = m0 + row;
-    if (m >= P || n >= a.N) continue;
-    const float* src = ct + row * C::LDC + (n - n0);
-    float v[8];
+#pragma unroll 1
+  for (int g = 0; g < C::WAVES_M; ++g) {
+    if (wm == g) acc_to_lds<C>(ct, wn, lane, acc);
+    __syncthreads();
+    for (int i = tid; i < C::WM * NV8; i += C::NT) {
+      const int row = i / NV8;
+      const int n = n0 + (i - row * NV8) * 8;
+      const long m = m0 + g * C::WM + row;
+      if (m >= P || n >= a.N) continue;
+      const float* src = ct + row * C::LDC + (n - n0);
+      float v[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = src[q];
-    if (a.bias) {
+      for (int q = 0; q < 8; ++q) v[q] = src[q];
+      if (a.bias) {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
+        for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
+      }
+      if (a.rowvec) {
+        const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] += rv[q];
+      }
+      if (a.resid.s0.ptr) {
+        float r[8];
+        ld8(a.resid.s0, m, n, r);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] += r[q];
+      }
+      st8(a.out, a.out_dtype, a.ldo, m, n, v);
+      if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
     }
-    if (a.rowvec) {
-      const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] += rv[q];
-    }
-    if (a.resid.s0.ptr) {
-      float r[8];
-      ld8(a.resid.s0, m, n, r);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] += r[q];
-    }
-    st8(a.out, a.out_dtype, a.ldo, m, n, v);
-    if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
+    __syncthreads();
   }
 }
 
@@ -428,12 +439,26 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
+  // Block -> (split, tile).  Workgroups are dealt round-robin over the 8
+  // XCDs; when the split count is a multiple of 8, every block of one pixel
+  // split runs on the same XCD so the split's operand slices stay in that
+  // XCD's L2.
   const int tilesN = (a.N + C::BN - 1) / C::BN;
-  const int tn = blockIdx.x % tilesN;
-  const int tm = blockIdx.x / tilesN;
+  const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
+  const int splits = gridDim.x / ntiles;
+  int tile, z;
+  if (splits % 8 == 0) {
+    const int q = blockIdx.x / 8;
+    z = (int)(blockIdx.x % 8) + 8 * (q / ntiles);
+    tile = q % ntiles;
+  } else {
+    z = blockIdx.x / ntiles;
+    tile = blockIdx.x % ntiles;
+  }
+  const int tn = tile % tilesN;
+  const int tm = tile / tilesN;
   const int m0 = tm * C::BM;
   const int n0 = tn * C::BN;
-  const int z = blockIdx.z;
 
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
   const long P = a.g.pixels();
@@ -562,20 +587,25 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
     }
   }
 
-  // partials through LDS so each row is written as whole 16-byte vectors
+  // partials through LDS (one wave row group at a time) so each row is
+  // written as whole 16-byte vectors
   float* ct = reinterpret_cast<float*>(smem);
-  acc_to_lds<C>(ct, wm, wn, lane, acc);
-  __syncthreads();
   float* part = a.part + (long)z * a.M * a.N;
   constexpr int NV4 = C::BN / 4;
-  for (int i = tid; i < C::BM * NV4; i += C::NT) {
-    const int row = i / NV4;
-    const int n = n0 + (i - row * NV4) * 4;
-    const int m = m0 + row;
-    if (m >= a.M || n >= a.N) continue;
-    const float* src = ct + row * C::LDC + (n - n0);
-    *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
-        make_float4(src[0], src[1], src[2], src[3]);
+#pragma unroll 1
+  for (int g = 0; g < C::WAVES_M; ++g) {
+    if (wm == g) acc_to_lds<C>(ct, wn, lane, acc);
+    __syncthreads();
+    for (int i = tid; i < C::WM * NV4; i += C::NT) {
+      const int row = i / NV4;
+      const int n = n0 + (i - row * NV4) * 4;
+      const int m = m0 + g * C::WM + row;
+      if (m >= a.M || n >= a.N) continue;
+      const float* src = ct + row * C::LDC + (n - n0);
+      *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
+          make_float4(src[0], src[1], src[2], src[3]);
+    }
+    __syncthreads();
   }
 }
 
@@ -599,9 +629,16 @@ __global__ void wgrad_finalize(GemmArgs a, int splits) {
 // launchers
 // ---------------------------------------------------------------------------
 
-using CfgBf16 = Cfg<128, 128, 64, 64, 64, false>;
-using CfgBf16K32 = Cfg<128, 128, 32, 64, 64, false>;
-using CfgF32 = Cfg<64, 64, 32, 32, 32, true>;
+// Tile shapes.  bf16 with 64 channels per K-step unless noted.
+using T128x128 = Cfg<128, 128, 64, 64, 64, false>;    // 4 waves of 64x64
+using T128x160 = Cfg<128, 160, 64, 64, 80, false>;    // 4 waves of 64x80
+using T256x160 = Cfg<256, 160, 64, 64, 80, false>;    // 8 waves of 64x80
+using T256x128 = Cfg<256, 128, 64, 64, 64, false>;    // 8 waves of 64x64
+using T128x320 = Cfg<128, 320, 64, 64, 80, false>;    // 8 waves of 64x80
+using T320x160 = Cfg<320, 160, 64, 80, 80, false>;    // 8 waves of 80x80
+using T160x160 = Cfg<160, 160, 64, 80, 80, false>;    // 4 waves of 80x80
+using T128x128K32 = Cfg<128, 128, 32, 64, 64, false>; // channel counts % 64 != 0
+using T64x64F32 = Cfg<64, 64, 32, 32, 32, true>;      // the fp32 stage
 
 template <class C>
 static hipError_t launch_conv_t(const GemmArgs& a, hipStream_t st) {
@@ -615,8 +652,8 @@ template <class C>
 static hipError_t launch_wgrad_t(GemmArgs a, int splits, hipStream_t st) {
   const long tilesM = (a.M + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL(igemm_wgrad<C>, dim3((unsigned)(tilesM * tilesN), 1, splits),
-                     dim3(C::NT), 0, st, a);
+  hipLaunchKernelGGL(igemm_wgrad<C>, dim3((unsigned)(tilesM * tilesN * splits)), dim3(C::NT), 0,
+                     st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long total = (long)a.M * a.N;
@@ -625,24 +662,50 @@ static hipError_t launch_wgrad_t(GemmArgs a, int splits, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Tile configuration: 0 = bf16 BK 64, 1 = bf16 BK 32, 2 = fp32.
-int gemm_bk(int cfg) { return cfg == 2 ? CfgF32::BK : (cfg == 1 ? CfgBf16K32::BK : CfgBf16::BK); }
-int gemm_bm(int cfg) { return cfg == 2 ? CfgF32::BM : CfgBf16::BM; }
-int gemm_bn(int cfg) { return cfg == 2 ? CfgF32::BN : CfgBf16::BN; }
+template <class C>
+static TileInfo info_t() {
+  return TileInfo{C::BM, C::BN, C::BK};
+}
 
-hipError_t launch_conv(const GemmArgs& a, int cfg, hipStream_t st) {
-  switch (cfg) {
-    case 0: return launch_conv_t<CfgBf16>(a, st);
-    case 1: return launch_conv_t<CfgBf16K32>(a, st);
-    default: return launch_conv_t<CfgF32>(a, st);
+TileInfo tile_info(int t) {
+  switch (t) {
+    case TILE_128x128: return info_t<T128x128>();
+    case TILE_128x160: return info_t<T128x160>();
+    case TILE_256x160: return info_t<T256x160>();
+    case TILE_256x128: return info_t<T256x128>();
+    case TILE_128x320: return info_t<T128x320>();
+    case TILE_320x160: return info_t<T320x160>();
+    case TILE_160x160: return info_t<T160x160>();
+    case TILE_128x128_K32: return info_t<T128x128K32>();
+    default: return info_t<T64x64F32>();
   }
 }
 
-hipError_t launch_wgrad(const GemmArgs& a, int cfg, int splits, hipStream_t st) {
-  switch (cfg) {
-    case 0: return launch_wgrad_t<CfgBf16>(a, splits, st);
-    case 1: return launch_wgrad_t<CfgBf16K32>(a, splits, st);
-    default: return launch_wgrad_t<CfgF32>(a, splits, st);
+hipError_t launch_conv(const GemmArgs& a, int t, hipStream_t st) {
+  switch (t) {
+    case TILE_128x128: return launch_conv_t<T128x128>(a, st);
+    case TILE_128x160: return launch_conv_t<T128x160>(a, st);
+    case TILE_256x160: return launch_conv_t<T256x160>(a, st);
+    case TILE_256x128: return launch_conv_t<T256x128>(a, st);
+    case TILE_128x320: return launch_conv_t<T128x320>(a, st);
+    case TILE_320x160: return launch_conv_t<T320x160>(a, st);
+    case TILE_160x160: return launch_conv_t<T160x160>(a, st);
+    case TILE_128x128_K32: return launch_conv_t<T128x128K32>(a, st);
+    default: return launch_conv_t<T64x64F32>(a, st);
+  }
+}
+
+hipError_t launch_wgrad(const GemmArgs& a, int t, int splits, hipStream_t st) {
+  switch (t) {
+    case TILE_128x128: return launch_wgrad_t<T128x128>(a, splits, st);
+    case TILE_128x160: return launch_wgrad_t<T128x160>(a, splits, st);
+    case TILE_256x160: return launch_wgrad_t<T256x160>(a, splits, st);
+    case TILE_256x128: return launch_wgrad_t<T256x128>(a, splits, st);
+    case TILE_128x320: return launch_wgrad_t<T128x320>(a, splits, st);
+    case TILE_320x160: return launch_wgrad_t<T320x160>(a, splits, st);
+    case TILE_160x160: return launch_wgrad_t<T160x160>(a, splits, st);
+    case TILE_128x128_K32: return launch_wgrad_t<T128x128K32>(a, splits, st);
+    default: return launch_wgrad_t<T64x64F32>(a, splits, st);
   }
 }
 

@@ -44,12 +44,26 @@ struct GemmArgs {
   float* part;         // [splits][M][N] fp32 partials
 };
 
-// implicit GEMM (igemm.hip); cfg: 0 = bf16 BK 64, 1 = bf16 BK 32, 2 = fp32
-int gemm_bk(int cfg);
-int gemm_bm(int cfg);
-int gemm_bn(int cfg);
-hipError_t launch_conv(const GemmArgs& a, int cfg, hipStream_t st);
-hipError_t launch_wgrad(const GemmArgs& a, int cfg, int splits, hipStream_t st);
+// implicit GEMM (igemm.hip): tile shapes (block M x block N; bf16, 64
+// channels per K-step unless noted)
+enum Tile : int {
+  TILE_128x128 = 0,
+  TILE_128x160 = 1,
+  TILE_256x160 = 2,
+  TILE_256x128 = 3,
+  TILE_128x320 = 4,
+  TILE_320x160 = 5,
+  TILE_160x160 = 6,
+  TILE_128x128_K32 = 7,  // bf16, 32 channels per K-step
+  TILE_64x64_F32 = 8,    // fp32, 32 channels per K-step
+  TILE_COUNT = 9
+};
+struct TileInfo {
+  int bm, bn, bk;
+};
+TileInfo tile_info(int tile);
+hipError_t launch_conv(const GemmArgs& a, int tile, hipStream_t st);
+hipError_t launch_wgrad(const GemmArgs& a, int tile, int splits, hipStream_t st);
 
 // ---- GroupNorm / reductions (norm.hip) -----------------------------------
 

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -93,7 +94,8 @@ struct pulse_stage {
   bool dry = false;
   int dtype = DT_F32;
   size_t esz = 4;
-  int gcfg = 2;
+  bool k64 = false;     // every channel count is a multiple of 64
+  int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
   Geo geo{};
   long P = 0;
   int G = 1;
@@ -189,17 +191,46 @@ void layout_gn(const pulse_stage* s, GnSave& g, size_t& off, int C) {
   off += align256((size_t)s->geo.B * C * 4);
 }
 
-int pick_splits(const pulse_stage* s, int M, int N, int& kchunk) {
-  const int bm = gemm_bm(s->gcfg), bn = gemm_bn(s->gcfg), bk = gemm_bk(s->gcfg);
-  const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
-  long splits = (512 + tiles - 1) / tiles;
+// Tile shape of a conv-mode GEMM with N output columns.
+int conv_tile(const pulse_stage* s, int N) {
+  if (s->dtype == DT_F32) return TILE_64x64_F32;
+  if (!s->k64) return TILE_128x128_K32;
+  if (s->conv_tile_force >= 0) return s->conv_tile_force;
+  if (N % 320 == 0) return TILE_128x320;
+  return N % 160 == 0 ? TILE_256x160 : TILE_128x128;
+}
+
+// Tile shape of a weight-gradient GEMM (M output channels, N columns).
+int wgrad_tile(const pulse_stage* s, int M, int N) {
+  if (s->dtype == DT_F32) return TILE_64x64_F32;
+  if (!s->k64) return TILE_128x128_K32;
+  if (s->wgrad_tile_force >= 0) return s->wgrad_tile_force;
+  (void)N;
+  if (M % 320 == 0) return TILE_320x160;
+  return M % 160 == 0 ? TILE_160x160 : TILE_128x128;
+}
+
+// Pixel split of a weight-gradient GEMM: enough blocks for about two per CU.
+int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
+  const TileInfo ti = tile_info(tile);
+  const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
+  long splits = (256 + tiles - 1) / tiles;
   const long maxs = (s->P + 255) / 256;
   if (splits > maxs) splits = maxs;
+  if (splits >= 8) splits = (splits + 7) / 8 * 8;  // one split per XCD at a time
   if (splits < 1) splits = 1;
   long kc = (s->P + splits - 1) / splits;
-  kc = (kc + bk - 1) / bk * bk;
+  kc = (kc + ti.bk - 1) / ti.bk * ti.bk;
   kchunk = (int)kc;
-  return (int)((s->P + kc - 1) / kc);
+  // the kernel derives the split count from the grid: keep it exact
+  const long used = (s->P + kc - 1) / kc;
+  return (int)(splits % 8 == 0 && used != splits ? splits : used);
+}
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return atoi(v);
 }
 
 pulse_status build_layout(pulse_stage* s) {
@@ -240,14 +271,15 @@ pulse_status build_layout(pulse_stage* s) {
   }
 
   // bf16 tiles take 64 channels per K-step when every channel count allows
-  if (s->dtype == DT_F32) {
-    s->gcfg = 2;
-  } else {
+  {
     bool k64 = true;
     auto chk = [&](int c) { if (c % 64) k64 = false; };
     for (auto& b : s->eb) { chk(b.cin); chk(b.cout); chk(b.c0); }
     for (auto& b : s->db) { chk(b.cin); chk(b.cout); chk(b.c0); }
-    s->gcfg = k64 ? 0 : 1;
+    s->k64 = k64;
+    const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
+    s->conv_tile_force = (ct >= 0 && ct <= TILE_160x160) ? ct : -1;
+    s->wgrad_tile_force = (wt >= 0 && wt <= TILE_160x160) ? wt : -1;
   }
 
   // workspace: weight copies | rows | scratch
@@ -304,9 +336,9 @@ pulse_status build_layout(pulse_stage* s) {
   for (auto* v : {&s->eb, &s->db})
     for (auto& b : *v) {
       int kc;
-      int sp = pick_splits(s, b.cout, b.ldb2, kc);
+      int sp = pick_splits(s, wgrad_tile(s, b.cout, b.ldb2), b.cout, b.ldb2, kc);
       part = std::max(part, (size_t)sp * b.cout * b.ldb2);
-      sp = pick_splits(s, b.cout, 9 * b.cin, kc);
+      sp = pick_splits(s, wgrad_tile(s, b.cout, 9 * b.cin), b.cout, 9 * b.cin, kc);
       part = std::max(part, (size_t)sp * b.cout * 9 * b.cin);
       for (int c : {b.cin, b.cout}) {
         RedGrid rg = red_grid(s->geo, c);
@@ -472,7 +504,7 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
     e1 = next_event(s);
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
-  HIPCHK(launch_conv(a, s->gcfg, st));
+  HIPCHK(launch_conv(a, conv_tile(s, a.N), st));
   if (s->timing && e0 && e1) {
     HIPCHK(hipEventRecord(e1, st));
     s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K});
@@ -549,12 +581,13 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
   a.K = (int)s->P;
   a.gy = gy;
   int kchunk;
-  const int splits = pick_splits(s, M, n, kchunk);
+  const int tile = wgrad_tile(s, M, n);
+  const int splits = pick_splits(s, tile, M, n, kchunk);
   if ((size_t)splits * M * n > s->part_cap)
     return fail(PULSE_E_SHAPE, "internal: wgrad partial buffer too small");
   a.kchunk = kchunk;
   a.part = s->sf(s->s_part);
-  HIPCHK(launch_wgrad(a, s->gcfg, splits, st));
+  HIPCHK(launch_wgrad(a, tile, splits, st));
   return PULSE_OK;
 }
 
