@@ -611,18 +611,24 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
 
 // Sum the split partials in split order and accumulate into the gradients
 // of each segment (rows of length end - begin: OHWI for 3x3, [O][I] for 1x1).
+// Four consecutive columns per thread (N and the segment bounds are
+// multiples of 8).
 __global__ void wgrad_finalize(GemmArgs a, int splits) {
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long idx = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (idx >= (long)a.M * a.N) return;
   const int m = (int)(idx / a.N);
   const int n = (int)(idx - (long)m * a.N);
-  float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += a.part[(long)z * a.M * a.N + idx];
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int z = 0; z < splits; ++z) {
+    const float4 v = *reinterpret_cast<const float4*>(a.part + (long)z * a.M * a.N + idx);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
   const Seg sg0 = a.seg[0], sg1 = a.seg[1], sg2 = a.seg[2];
   const int si = seg_of(a.nseg, sg1.begin, sg2.begin, n);
   const Seg& sg = si == 0 ? sg0 : (si == 1 ? sg1 : sg2);
   const int len = sg.end - sg.begin;
-  sg.grad[(long)m * len + (n - sg.begin)] += s;
+  float* g = sg.grad + (long)m * len + (n - sg.begin);
+  g[0] += s.x; g[1] += s.y; g[2] += s.z; g[3] += s.w;
 }
 
 // ---------------------------------------------------------------------------
@@ -656,7 +662,7 @@ static hipError_t launch_wgrad_t(GemmArgs a, int splits, hipStream_t st) {
                      st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const long total = (long)a.M * a.N;
+  const long total = (long)a.M * a.N / 4;
   hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
                      a, splits);
   return hipGetLastError();

@@ -68,9 +68,11 @@ hipError_t launch_wgrad(const GemmArgs& a, int tile, int splits, hipStream_t st)
 // ---- GroupNorm / reductions (norm.hip) -----------------------------------
 
 // Grid shape shared by the per-channel reduction kernels: image b, pixel
-// chunk of `cp` pixels, 64 channel vectors per block in x.
+// chunk of `cp` pixels, a block of vx channel vectors x py pixel lanes, zb
+// blocks across the channel vectors.
 struct RedGrid {
   int chunks, cp;
+  int vx, py, zb;
 };
 RedGrid red_grid(const Geo& g, int C);
 

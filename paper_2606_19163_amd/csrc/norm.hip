@@ -12,9 +12,9 @@ namespace pulse {
 
 namespace {
 
-constexpr int VX = 64;  // channel vectors per block
-constexpr int PY = 4;   // pixel lanes per block
-
+// Block shape of the per-channel kernels: rg.vx channel vectors (8 channels
+// each) x rg.py pixel lanes, at most 256 threads; blockIdx.z picks the
+// channel-vector slice.
 struct Range {
   int b, p0, p1, v, c;
   bool active;
@@ -25,27 +25,26 @@ __device__ __forceinline__ Range block_range(const Geo& g, RedGrid rg, int C) {
   r.b = blockIdx.x;
   r.p0 = blockIdx.y * rg.cp;
   r.p1 = min(r.p0 + rg.cp, g.hw());
-  r.v = blockIdx.z * VX + threadIdx.x;
+  r.v = blockIdx.z * rg.vx + threadIdx.x;
   r.c = r.v * 8;
-  r.active = r.c < C;
+  r.active = threadIdx.x < rg.vx && r.c < C;
   return r;
 }
 
-// Sum the 4 pixel lanes of NV values per thread through LDS and let lane 0
-// write them to out[0..NV) (out already offset by channel).
+// Sum the pixel lanes of NV values per thread through LDS (fixed order) and
+// let lane 0 write 8 of them to out0 (and the next 8 to out1).
 template <int NV>
-__device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, bool active,
-                                                  float* out0, float* out1) {
+__device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, RedGrid rg,
+                                                  bool active, float* out0, float* out1) {
   const int tx = threadIdx.x, ty = threadIdx.y;
 #pragma unroll
-  for (int i = 0; i < NV; ++i) sm[(ty * VX + tx) * NV + i] = v[i];
+  for (int i = 0; i < NV; ++i) sm[(ty * rg.vx + tx) * NV + i] = v[i];
   __syncthreads();
   if (ty == 0 && active) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       float s = sm[tx * NV + i];
-#pragma unroll
-      for (int y = 1; y < PY; ++y) s += sm[(y * VX + tx) * NV + i];
+      for (int y = 1; y < rg.py; ++y) s += sm[(y * rg.vx + tx) * NV + i];
       v[i] = s;
     }
 #pragma unroll
@@ -59,24 +58,36 @@ __device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, boo
 
 __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid rg,
                                                           float* partial) {
-  __shared__ float sm[PY * VX * 16];
+  __shared__ float sm[256 * 16];
   const Range r = block_range(g, rg, x.C);
   float acc[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   if (r.active) {
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
-      float f[8];
-      ld8v(x, (long)r.b * g.hw() + p, r.c, f);
+    // four pixels per iteration keep four loads in flight per thread
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += 4 * rg.py) {
+      float f[4][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        acc[i] += f[i];
-        acc[8 + i] += f[i] * f[i];
+      for (int u = 0; u < 4; ++u) {
+        const int pu = p + u * rg.py;
+        if (pu < r.p1) {
+          ld8v(x, (long)r.b * g.hw() + pu, r.c, f[u]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) f[u][i] = 0.f;
+        }
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          acc[i] += f[u][i];
+          acc[8 + i] += f[u][i] * f[u][i];
+        }
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
-  lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
+  lane_reduce_store<16>(acc, sm, rg, r.active, base + r.c, base + x.C + r.c);
 }
 
 // Fixed-order block sum of two fp64 values (256 threads).
@@ -182,7 +193,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, 
                                                         const float* shift, const float* mean,
                                                         const float* rstd, int G,
                                                         float* partial) {
-  __shared__ float sm[PY * VX * 16];
+  __shared__ float sm[256 * 16];
   const Range r = block_range(g, rg, x.C);
   float acc[16];
 #pragma unroll
@@ -190,26 +201,37 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, 
   if (r.active) {
     GnConst k;
     load_gn_const(k, r.b, r.c, x.C, G, scale, shift, mean, rstd);
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
-      const long pix = (long)r.b * g.hw() + p;
-      float f[8], d[8];
-      ld8v(x, pix, r.c, f);
-      const float4* dp = reinterpret_cast<const float4*>(da + pix * x.C + r.c);
-      const float4 d0 = dp[0], d1 = dp[1];
-      d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
-      d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += 2 * rg.py) {
+      float f[2][8], d[2][8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float z = f[j] * k.sc[j] + k.sh[j];
-        const float dz = d[j] * dsilu_f(z);
-        const float xh = (f[j] - k.mu[j]) * k.rs[j];
-        acc[j] += dz;
-        acc[8 + j] += dz * xh;
+      for (int u = 0; u < 2; ++u) {
+        const int pu = p + u * rg.py;
+        if (pu < r.p1) {
+          const long pix = (long)r.b * g.hw() + pu;
+          ld8v(x, pix, r.c, f[u]);
+          const float4* dp = reinterpret_cast<const float4*>(da + pix * x.C + r.c);
+          const float4 d0 = dp[0], d1 = dp[1];
+          d[u][0] = d0.x; d[u][1] = d0.y; d[u][2] = d0.z; d[u][3] = d0.w;
+          d[u][4] = d1.x; d[u][5] = d1.y; d[u][6] = d1.z; d[u][7] = d1.w;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) f[u][j] = d[u][j] = 0.f;
+        }
       }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float z = f[u][j] * k.sc[j] + k.sh[j];
+          const float dz = d[u][j] * dsilu_f(z);
+          const float xh = (f[u][j] - k.mu[j]) * k.rs[j];
+          acc[j] += dz;
+          acc[8 + j] += dz * xh;
+        }
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
-  lane_reduce_store<16>(acc, sm, r.active, base + r.c, base + x.C + r.c);
+  lane_reduce_store<16>(acc, sm, rg, r.active, base + r.c, base + x.C + r.c);
 }
 
 // one block per (image, group): coef = (sum gamma*dz, sum gamma*dz*xhat) / count
@@ -238,6 +260,9 @@ __global__ __launch_bounds__(256) void k_gn_bwd_coef(const float* partial, Geo g
 // Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
 // partial[b][chunk][s][c] for the first `nslot` slots.  Block (64 channels,
 // 4 chunk lanes) per (channel block, image).
+constexpr int VX = 64;  // k_chan_per_image: 64 channels x 4 chunk lanes
+constexpr int PY = 4;
+
 __global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, int chunks, int B,
                                                         int C, int nslot, float* pi) {
   __shared__ float sm[2][PY][VX];
@@ -286,7 +311,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Ge
                                                       const float* shift, const float* mean,
                                                       const float* rstd, const float* gamma,
                                                       const float* coef, int G, GnBwdOut o) {
-  __shared__ float sm[PY * VX * 8];
+  __shared__ float sm[256 * 8];
   const Range r = block_range(g, rg, x.C);
   const int C = x.C;
   const int cg = C / G;
@@ -304,7 +329,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Ge
       c0[j] = coef[(r.b * G + gi) * 2 + 0];
       c1[j] = coef[(r.b * G + gi) * 2 + 1];
     }
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
       const long pix = (long)r.b * g.hw() + p;
       float f[8], d[8], out[8];
       ld8v(x, pix, r.c, f);
@@ -341,19 +366,19 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Ge
   }
   if (o.chan_partial) {
     float* base = o.chan_partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * C;
-    lane_reduce_store<8>(acc, sm, r.active, base + r.c, nullptr);
+    lane_reduce_store<8>(acc, sm, rg, r.active, base + r.c, nullptr);
   }
 }
 
 __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid rg,
                                                           float* partial) {
-  __shared__ float sm[PY * VX * 8];
+  __shared__ float sm[256 * 8];
   const Range r = block_range(g, rg, v.C);
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   if (r.active) {
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += PY) {
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
       float f[8];
       ld8v(v, (long)r.b * g.hw() + p, r.c, f);
 #pragma unroll
@@ -361,25 +386,30 @@ __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid 
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * v.C;
-  lane_reduce_store<8>(acc, sm, r.active, base + r.c, nullptr);
+  lane_reduce_store<8>(acc, sm, rg, r.active, base + r.c, nullptr);
 }
 
 dim3 red_dims(const Geo& g, RedGrid rg, int C) {
-  const int nvb = (C / 8 + VX - 1) / VX;
-  return dim3(g.B, rg.chunks, nvb);
+  (void)C;
+  return dim3(g.B, rg.chunks, rg.zb);
 }
+
+dim3 red_block(RedGrid rg) { return dim3(rg.vx, rg.py); }
 
 }  // namespace
 
 RedGrid red_grid(const Geo& g, int C) {
-  const int nvb = (C / 8 + VX - 1) / VX;
+  RedGrid rg;
+  const int nv = C / 8;
+  rg.zb = (nv + 127) / 128;
+  rg.vx = (nv + rg.zb - 1) / rg.zb;
+  rg.py = 256 / rg.vx;
   const int hw = g.hw();
-  int chunks = 1024 / (g.B * nvb);
-  if (chunks > 64) chunks = 64;
-  const int max_chunks = (hw + 15) / 16;
+  int chunks = 2048 / (g.B * rg.zb);
+  if (chunks > 128) chunks = 128;
+  const int max_chunks = (hw + 4 * rg.py - 1) / (4 * rg.py);
   if (chunks > max_chunks) chunks = max_chunks;
   if (chunks < 1) chunks = 1;
-  RedGrid rg;
   rg.cp = (hw + chunks - 1) / chunks;
   rg.chunks = (hw + rg.cp - 1) / rg.cp;
   return rg;
@@ -387,7 +417,7 @@ RedGrid red_grid(const Geo& g, int C) {
 
 hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_stats_partial, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, x, g, rg,
+  hipLaunchKernelGGL(k_gn_stats_partial, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg,
                      partial);
   return hipGetLastError();
 }
@@ -414,7 +444,7 @@ hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale, const
 hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, RedGrid rg,
                                  const float* scale, const float* shift, const float* mean,
                                  const float* rstd, int G, float* partial, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_partial, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, da, x, g, rg,
+  hipLaunchKernelGGL(k_gn_bwd_partial, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
                      scale, shift, mean, rstd, G, partial);
   return hipGetLastError();
 }
@@ -434,14 +464,14 @@ hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedG
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
                                int G, const GnBwdOut& o, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_apply, red_dims(g, rg, x.C), dim3(VX, PY), 0, st, da, x, g, rg,
+  hipLaunchKernelGGL(k_gn_bwd_apply, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
                      scale, shift, mean, rstd, gamma, coef, G, o);
   return hipGetLastError();
 }
 
 hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st) {
-  hipLaunchKernelGGL(k_chan_sum_partial, red_dims(g, rg, v.C), dim3(VX, PY), 0, st, v, g, rg,
+  hipLaunchKernelGGL(k_chan_sum_partial, red_dims(g, rg, v.C), red_block(rg), 0, st, v, g, rg,
                      partial);
   return hipGetLastError();
 }
