@@ -654,6 +654,13 @@ static hipError_t launch_conv_t(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+hipError_t launch_wgrad_finalize(const GemmArgs& a, int splits, hipStream_t st) {
+  const long total = (long)a.M * a.N / 4;
+  hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+                     a, splits);
+  return hipGetLastError();
+}
+
 template <class C>
 static hipError_t launch_wgrad_t(GemmArgs a, int splits, hipStream_t st) {
   const long tilesM = (a.M + C::BM - 1) / C::BM;

@@ -1,0 +1,639 @@
+// Implicit-GEMM convolution, second generation: operand tiles move from
+// HBM/L2 to LDS with the LDS-DMA loads of gfx950 (buffer_load ... lds /
+// global_load_lds_dwordx4), so no register staging and no VALU touch the
+// operands on their way to the matrix cores, and two LDS stages overlap the
+// next tile's loads with the current tile's MFMAs.
+//
+// A wave-wide DMA load writes 64 lanes x 16 bytes contiguously (lane i at
+// base + 16 i), so every tile is a dense array of 16-byte chunks and bank
+// conflicts are avoided by XOR-swizzling the chunk index instead of padding.
+//
+//  * CONV mode (forward, data gradient): tiles are K-contiguous rows of 64
+//    bf16 (128 bytes): A rows are pixels, B rows are output channels.
+//    Fragments are read with ds_read_b128.  Out-of-image taps and rows past
+//    the tile read as zero through out-of-range buffer offsets.
+//  * WGRAD mode: both tiles keep the NHWC order, rows of channels per pixel
+//    ([64 pixels][BM] and [64 pixels][BN]); the MFMA wants 8 consecutive
+//    pixels per lane, which ds_read_b64_tr_b16 delivers (two per fragment):
+//    within 16 lanes, lane j receives element j%4 of the rows addressed by
+//    lanes 4q + j/4, q = 0..3.  B columns may mix sources within one tile, so
+//    its DMA uses per-lane global addresses; invalid elements point at a
+//    zeroed 16-byte word.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace pulse {
+
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+constexpr uint32_t OOB = 0x80000000u;  // an offset past every buffer
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long bytes) {
+  const int n = bytes > 0x7fffffffL ? 0x7fffffff : (int)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, p ? n : 0,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ lds_ptr_t lds(char* p) { return (lds_ptr_t)p; }
+
+// s_waitcnt vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 128-byte rows of 8 chunks: chunk c of row r lives in slot c ^ swz(r).
+// Rows r and r+1 fall in opposite halves of a 256-byte bank period, so the
+// swizzle only has to separate rows of equal parity.
+__device__ __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
+
+}  // namespace
+
+template <int BM_, int BN_, int WM_, int WN_>
+struct CfgC {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64;
+  static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN, NW = WAVES_M * WAVES_N;
+  static constexpr int NT = NW * 64;
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int WLA = BM / 8, WLB = BN / 8, WL = WLA + WLB;  // 1 KB wave loads
+  static constexpr int NU = WL / NW;                                 // per wave
+  static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
+  static constexpr int LDC = BN + 4;
+  static_assert(16 * LDC * 4 <= STAGE, "epilogue slice must fit one stage");
+  static_assert(2 * STAGE <= 160 * 1024, "LDS");
+  static_assert(WL % NW == 0 && WLA % NW == 0, "wave loads must split evenly over the waves");
+  static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
+};
+
+template <int BM_, int BN_, int WM_, int WN_>
+struct CfgW {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64;
+  static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN, NW = WAVES_M * WAVES_N;
+  static constexpr int NT = NW * 64;
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int PA = BM * 2, PB = BN * 2;  // row pitch (bytes): one pixel
+  static constexpr int CA = BM / 8, CB = BN / 8;  // 16-byte chunks per row
+  static constexpr int A_BYTES = BK * PA, B_BYTES = BK * PB;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int WLA = A_BYTES / 1024, WLB = B_BYTES / 1024, WL = WLA + WLB;
+  static constexpr int NU = WL / NW;
+  static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
+  // transpose reads touch 4 consecutive rows: pitches that repeat every
+  // 256 or 128 bytes need the rows' chunk pairs moved apart
+  static constexpr bool SWA = (PA % 256 == 0 || PA % 256 == 128) && CA % 8 == 0;
+  static constexpr bool SWB = (PB % 256 == 0 || PB % 256 == 128) && CB % 8 == 0;
+  static constexpr int LDC = BN + 4;
+  static_assert(16 * LDC * 4 <= STAGE, "epilogue slice must fit one stage");
+  static_assert(2 * STAGE <= 160 * 1024, "LDS");
+  static_assert(WL % NW == 0 && WLA % NW == 0 && (BK * PA) % 1024 == 0 &&
+                    (BK * PB) % 1024 == 0,
+                "loads");
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "tile");
+};
+
+namespace {
+
+__device__ __forceinline__ int seg_of(int nseg, int b1, int b2, int i) {
+  int s = 0;
+  if (nseg > 1 && i >= b1) s = 1;
+  if (nseg > 2 && i >= b2) s = 2;
+  return s;
+}
+
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+  if (nb % 8 != 0) return bid;
+  return (bid % 8) * (nb / 8) + bid / 8;
+}
+
+struct SegRt {
+  __amdgpu_buffer_rsrc_t r0, r1;
+  uint32_t pitch0, pitch1;
+  int c0, C, taps, begin;
+};
+
+__device__ __forceinline__ SegRt seg_rt(const Seg& g, long P) {
+  SegRt s;
+  s.r0 = make_rsrc(g.in.s0.ptr, P * g.in.s0.C * 2);
+  s.r1 = make_rsrc(g.in.s1.ptr, P * g.in.s1.C * 2);
+  s.pitch0 = (uint32_t)(g.in.s0.C * 2);
+  s.pitch1 = (uint32_t)(g.in.s1.C * 2);
+  s.c0 = g.in.c0;
+  s.C = g.C;
+  s.taps = g.taps;
+  s.begin = g.begin;
+  return s;
+}
+
+__device__ __forceinline__ SegRt pick(int s, const SegRt& a, const SegRt& b, const SegRt& c) {
+  return s == 0 ? a : (s == 1 ? b : c);
+}
+
+// Stage the accumulator rows [i*16, i*16+16) of every wave of row group g
+// into an fp32 [16][LDC] LDS tile.
+template <int TM, int TN, int WN, int LDC>
+__device__ __forceinline__ void acc16_to_lds(float* ct, int wn, int lane, int i,
+                                             const f32x4_t (&acc)[TM][TN]) {
+  const int r16 = lane & 15;
+  const int rq = (lane >> 4) * 4;
+#pragma unroll
+  for (int ii = 0; ii < TM; ++ii) {
+    if (ii != i) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ct[(rq + r) * LDC + wn * WN + j * 16 + r16] = acc[ii][j][r];
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// CONV mode
+// ---------------------------------------------------------------------------
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
+  // the body exists for the device pass only (the host pass emits the launch stub)
+#if defined(__HIP_DEVICE_COMPILE__)
+  __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % C::WAVES_M;
+  const int wn = wave / C::WAVES_M;
+
+  const int tilesN = (a.N + C::BN - 1) / C::BN;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tn = bid % tilesN;
+  const int tm = bid / tilesN;
+  const long m0 = (long)tm * C::BM;
+  const int n0 = tn * C::BN;
+  const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
+  const long P = a.g.pixels();
+
+  // this lane's wave loads: wl = wave + u * NW; A rows first, then B rows.
+  // Lane (row rl = lane / 8 of the load, slot lane % 8) fetches logical chunk
+  // (lane % 8) ^ swz(row).
+  uint32_t ppix[C::NU], pmask[C::NU], coff[C::NU];
+#pragma unroll
+  for (int u = 0; u < C::NU; ++u) {
+    const int wl = wave + u * C::NW;
+    if (u < C::UA) {
+      const int r = wl * 8 + (lane >> 3);
+      const long m = m0 + r;
+      uint32_t mask = 0;
+      if (m < P) {
+        const int img = (int)(m / HW);
+        const int rem = (int)(m - (long)img * HW);
+        const int h = rem / W;
+        const int w = rem - h * W;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+          const int hh = h + t / 3 - 1, ww = w + t % 3 - 1;
+          if (hh >= 0 && hh < H && ww >= 0 && ww < W) mask |= 1u << t;
+        }
+      }
+      ppix[u] = (uint32_t)(m < P ? m : 0);
+      pmask[u] = mask;
+      coff[u] = (uint32_t)(((lane & 7) ^ swz128(r)) * 16);
+    } else {
+      const int r = (wl - C::WLA) * 8 + (lane >> 3);
+      const int n = n0 + r;
+      ppix[u] = 0;
+      pmask[u] = 0;
+      coff[u] = n < a.N ? (uint32_t)((long)n * a.ldb * 2 + ((lane & 7) ^ swz128(r)) * 16) : OOB;
+    }
+  }
+
+  const int nseg = a.nseg;
+  const SegRt q0 = seg_rt(a.seg[0], P);
+  const SegRt q1 = seg_rt(a.seg[1], P);
+  const SegRt q2 = seg_rt(a.seg[2], P);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.Bw, (long)a.N * a.ldb * 2);
+
+  auto issue = [&](int kt, char* base) __attribute__((always_inline)) {
+    const int k0 = kt * C::BK;
+    const SegRt q = pick(seg_of(nseg, q1.begin, q2.begin, k0), q0, q1, q2);
+    const int r = k0 - q.begin;
+    const int tap = r / q.C;
+    const int cb = r - tap * q.C;
+    const bool second = cb >= q.c0;
+    const __amdgpu_buffer_rsrc_t rs = second ? q.r1 : q.r0;
+    const uint32_t pitch = second ? q.pitch1 : q.pitch0;
+    const uint32_t cbyte = (uint32_t)((second ? cb - q.c0 : cb) * 2);
+    const int t9 = q.taps == 9 ? tap : 4;
+    const int shift = (t9 / 3 - 1) * W + (t9 % 3 - 1);
+#pragma unroll
+    for (int u = 0; u < C::NU; ++u) {
+      const int wl = wave + u * C::NW;
+      if (u < C::UA) {
+        const uint32_t off =
+            ((pmask[u] >> t9) & 1u) ? (ppix[u] + shift) * pitch + cbyte + coff[u] : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(base + wl * 1024), 16, off, 0, 0, 0);
+      } else {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds(base + wl * 1024), 16,
+                                                 coff[u] + (uint32_t)(k0 * 2), 0, 0, 0);
+      }
+    }
+  };
+
+  f32x4_t acc[C::TM][C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+  // Per K-step: wait for the stage, read every fragment of it into
+  // registers, then start the next stage's DMA and run the MFMAs while it
+  // lands.  All LDS reads of a stage precede the next DMA in program order,
+  // so the compiler's conservative wait for LDS-DMA before LDS reads is
+  // exactly the real dependency.
+  bf16x8_t af[2][C::TM], bfr[2][C::TN];
+  auto read = [&](const char* As) __attribute__((always_inline)) {
+    const char* Bs = As + C::A_BYTES;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int c = s * 4 + g4;
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        const int r = wm * C::WM + i * 16 + r16;
+        af[s][i] = *reinterpret_cast<const bf16x8_t*>(As + r * 128 + ((c ^ swz128(r)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        const int r = wn * C::WN + j * 16 + r16;
+        bfr[s][j] = *reinterpret_cast<const bf16x8_t*>(Bs + r * 128 + ((c ^ swz128(r)) << 4));
+      }
+    }
+  };
+  auto mma = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+  };
+
+  const int KT = a.K / C::BK;
+  issue(0, smem);
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    read(smem + (kt & 1) * C::STAGE);
+    if (kt + 1 < KT) issue(kt + 1, smem + ((kt + 1) & 1) * C::STAGE);
+    mma();
+  }
+  __syncthreads();
+
+  // epilogue in 16-row slices: accumulators -> LDS -> 8-channel rows
+  // (+bias, +rowvec, +residual) -> 16-byte stores
+  float* ct = reinterpret_cast<float*>(smem);
+  constexpr int NV8 = C::BN / 8;
+#pragma unroll 1
+  for (int g = 0; g < C::WAVES_M; ++g) {
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      if (wm == g) acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct, wn, lane, i, acc);
+      __syncthreads();
+      for (int e = tid; e < 16 * NV8; e += C::NT) {
+        const int row = e / NV8;
+        const int n = n0 + (e - row * NV8) * 8;
+        const long m = m0 + g * C::WM + i * 16 + row;
+        if (m >= P || n >= a.N) continue;
+        const float* src = ct + row * C::LDC + (n - n0);
+        const float4 s0 = reinterpret_cast<const float4*>(src)[0];
+        const float4 s1 = reinterpret_cast<const float4*>(src)[1];
+        float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        if (a.bias) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
+        }
+        if (a.rowvec) {
+          const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] += rv[q];
+        }
+        if (a.resid.s0.ptr) {
+          float rr[8];
+          ld8(a.resid.s0, m, n, rr);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] += rr[q];
+        }
+        st8(a.out, a.out_dtype, a.ldo, m, n, v);
+        if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
+      }
+      __syncthreads();
+    }
+  }
+#else
+  (void)a;
+#endif
+}
+
+// ---------------------------------------------------------------------------
+// WGRAD mode
+// ---------------------------------------------------------------------------
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* zero16) {
+  // the body exists for the device pass only (the host pass emits the launch stub)
+#if defined(__HIP_DEVICE_COMPILE__)
+  __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % C::WAVES_M;
+  const int wn = wave / C::WAVES_M;
+
+  // block -> (split, tile); all tiles of a split on one XCD when possible
+  const int tilesN = (a.N + C::BN - 1) / C::BN;
+  const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
+  const int splits = gridDim.x / ntiles;
+  int tile, z;
+  if (splits % 8 == 0) {
+    const int q = blockIdx.x / 8;
+    z = (int)(blockIdx.x % 8) + 8 * (q / ntiles);
+    tile = q % ntiles;
+  } else {
+    z = blockIdx.x / ntiles;
+    tile = blockIdx.x % ntiles;
+  }
+  const int m0 = (tile / tilesN) * C::BM;
+  const int n0 = (tile % tilesN) * C::BN;
+  const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
+  const long P = a.g.pixels();
+  const long pbeg = (long)z * a.kchunk;
+  const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
+
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gy.s0.ptr, P * a.gy.s0.C * 2);
+  const uint32_t gpitch = (uint32_t)(a.gy.s0.C * 2);
+
+  // Per wave load u: A loads (wl < WLA) fetch dY rows; B loads fetch the
+  // shifted activation columns through per-lane addresses.
+  // A: slot q -> pixel row q / CA, chunk (q % CA) ^ swz -> channel offset.
+  // B: slot q -> pixel row q / CB, column chunk -> (segment, tap, channel).
+  int rrow[C::NU];          // pixel row of the tile
+  uint32_t aoff[C::NU];     // A: channel byte offset in dY, or OOB
+  const char* bsrc[C::NU];  // B: source pointer at the column's channel
+  uint32_t bpitch[C::NU];
+  int bshift[C::NU], boy[C::NU], box[C::NU];
+  int bh[C::NU], bw[C::NU];  // B: image row / column of the current pixel
+#pragma unroll
+  for (int u = 0; u < C::NU; ++u) {
+    const int wl = wave + u * C::NW;
+    bsrc[u] = nullptr;
+    bpitch[u] = 0;
+    bshift[u] = boy[u] = box[u] = bh[u] = bw[u] = 0;
+    aoff[u] = OOB;
+    if (u < C::UA) {
+      const int q = wl * 64 + lane;
+      const int r = q / C::CA;
+      const int pc = q - r * C::CA;
+      const int lc = C::SWA ? (pc ^ (2 * (r & 3))) : pc;
+      rrow[u] = r;
+      const int o = m0 + lc * 8;
+      aoff[u] = o < a.M ? (uint32_t)(o * 2) : OOB;
+    } else {
+      const int q = (wl - C::WLA) * 64 + lane;
+      const int r = q / C::CB;
+      const int pc = q - r * C::CB;
+      const int lc = C::SWB ? (pc ^ (2 * (r & 3))) : pc;
+      rrow[u] = r;
+      const int n = n0 + lc * 8;
+      if (n < a.N) {
+        const int s = seg_of(a.nseg, a.seg[1].begin, a.seg[2].begin, n);
+        const Seg& sg = s == 0 ? a.seg[0] : (s == 1 ? a.seg[1] : a.seg[2]);
+        const int rr = n - sg.begin;
+        const int tap = rr / sg.C;
+        const int c = rr - tap * sg.C;
+        const int t9 = sg.taps == 9 ? tap : 4;
+        boy[u] = t9 / 3 - 1;
+        box[u] = t9 % 3 - 1;
+        bshift[u] = boy[u] * W + box[u];
+        const bool second = c >= sg.in.c0;
+        const Src& src = second ? sg.in.s1 : sg.in.s0;
+        bsrc[u] = static_cast<const char*>(src.ptr) + (second ? c - sg.in.c0 : c) * 2;
+        bpitch[u] = (uint32_t)(src.C * 2);
+      }
+      // image coordinates of pixel pbeg + r (advanced by 64 per K-step)
+      const long p = pbeg + r;
+      const long pp = p < P ? p : 0;
+      const int img = (int)(pp / HW);
+      const int rem = (int)(pp - (long)img * HW);
+      bh[u] = rem / W;
+      bw[u] = rem - bh[u] * W;
+    }
+  }
+
+  auto issue = [&](int kt, char* base) __attribute__((always_inline)) {
+    const long p0 = pbeg + (long)kt * C::BK;
+#pragma unroll
+    for (int u = 0; u < C::NU; ++u) {
+      const int wl = wave + u * C::NW;
+      const long p = p0 + rrow[u];
+      if (u < C::UA) {
+        const uint32_t off = p < pend ? (uint32_t)p * gpitch + aoff[u] : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, lds(base + wl * 1024), 16, off, 0, 0, 0);
+      } else {
+        const int hh = bh[u] + boy[u], ww = bw[u] + box[u];
+        const bool ok = bsrc[u] && p < pend && hh >= 0 && hh < H && ww >= 0 && ww < W;
+        const void* g = ok ? (const void*)(bsrc[u] + (long)(p + bshift[u]) * bpitch[u]) : zero16;
+        __builtin_amdgcn_global_load_lds(g, lds(base + C::A_BYTES + (wl - C::WLA) * 1024), 16, 0,
+                                         0);
+        // advance this lane's pixel by one K-step
+        int w = bw[u] + C::BK, h = bh[u];
+        while (w >= W) {
+          w -= W;
+          if (++h == H) h = 0;
+        }
+        bw[u] = w;
+        bh[u] = h;
+      }
+    }
+  };
+
+  f32x4_t acc[C::TM][C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int g16 = lane >> 4;
+  const int j16 = lane & 15;
+  // transpose-read address of lane (g16, j16): pixel row 8*g16 + 4*h + j16/4
+  // of the 32-pixel slice, channel 4*(j16%4) of the fragment's 16 columns
+  const int trow = 8 * g16 + (j16 >> 2);
+  const int tcol = 4 * (j16 & 3);
+
+  bf16x8_t af[2][C::TM], bfr[2][C::TN];
+  auto read = [&](const char* As) __attribute__((always_inline)) {
+    const char* Bs = As + C::A_BYTES;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        const int col = wm * C::WM + i * 16 + tcol;
+        v4s h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int r = s * 32 + trow + 4 * h;
+          const int lc = col >> 3;
+          const int pc = C::SWA ? (lc ^ (2 * (r & 3))) : lc;
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s*)(As + r * C::PA + pc * 16 + (col & 7) * 2));
+        }
+        af[s][i] = __builtin_bit_cast(bf16x8_t,
+                                      __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        const int col = wn * C::WN + j * 16 + tcol;
+        v4s h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int r = s * 32 + trow + 4 * h;
+          const int lc = col >> 3;
+          const int pc = C::SWB ? (lc ^ (2 * (r & 3))) : lc;
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s*)(Bs + r * C::PB + pc * 16 + (col & 7) * 2));
+        }
+        bfr[s][j] = __builtin_bit_cast(bf16x8_t,
+                                       __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    }
+  };
+  auto mma = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+  };
+
+  // same pipeline as the conv kernel: wait, read the stage, start the next
+  // stage's DMA, MFMAs
+  const int KT = (int)((pend - pbeg + C::BK - 1) / C::BK);
+  if (KT > 0) issue(0, smem);
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    read(smem + (kt & 1) * C::STAGE);
+    if (kt + 1 < KT) issue(kt + 1, smem + ((kt + 1) & 1) * C::STAGE);
+    mma();
+  }
+  __syncthreads();
+
+  // fp32 partials through LDS in 16-row slices, 16-byte stores
+  float* ct = reinterpret_cast<float*>(smem);
+  float* part = a.part + (long)z * a.M * a.N;
+  constexpr int NV4 = C::BN / 4;
+#pragma unroll 1
+  for (int g = 0; g < C::WAVES_M; ++g) {
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      if (wm == g) acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct, wn, lane, i, acc);
+      __syncthreads();
+      for (int e = tid; e < 16 * NV4; e += C::NT) {
+        const int row = e / NV4;
+        const int n = n0 + (e - row * NV4) * 4;
+        const int m = m0 + g * C::WM + i * 16 + row;
+        if (m >= a.M || n >= a.N) continue;
+        *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
+            *reinterpret_cast<const float4*>(ct + row * C::LDC + (n - n0));
+      }
+      __syncthreads();
+    }
+  }
+#else
+  (void)a;
+  (void)zero16;
+#endif
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+
+namespace launch2 {
+using C2_128x320 = CfgC<128, 320, 64, 80>;   // 8 waves
+using C2_128x160 = CfgC<128, 160, 64, 80>;   // 4 waves
+using C2_128x128 = CfgC<128, 128, 64, 64>;   // 4 waves
+using C2_256x128 = CfgC<256, 128, 64, 64>;   // 8 waves
+using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
+using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
+using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
+
+template <class C>
+static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
+  const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
+  const long tilesN = (a.N + C::BN - 1) / C::BN;
+  hipLaunchKernelGGL(igemm2_conv<C>, dim3((unsigned)(tilesM * tilesN)), dim3(C::NT), 0, st, a);
+  return hipGetLastError();
+}
+
+template <class C>
+static hipError_t wgrad2_t(const GemmArgs& a, int splits, const void* zero16, hipStream_t st) {
+  const long tilesM = (a.M + C::BM - 1) / C::BM;
+  const long tilesN = (a.N + C::BN - 1) / C::BN;
+  hipLaunchKernelGGL(igemm2_wgrad<C>, dim3((unsigned)(tilesM * tilesN * splits)), dim3(C::NT),
+                     0, st, a, zero16);
+  return hipGetLastError();
+}
+
+template <class C>
+static TileInfo info2() {
+  return TileInfo{C::BM, C::BN, C::BK};
+}
+}  // namespace launch2
+using namespace launch2;
+
+TileInfo tile2_info(int t) {
+  switch (t) {
+    case TILE2_C128x320: return info2<C2_128x320>();
+    case TILE2_C128x160: return info2<C2_128x160>();
+    case TILE2_C128x128: return info2<C2_128x128>();
+    case TILE2_C256x128: return info2<C2_256x128>();
+    case TILE2_W320x192: return info2<W2_320x192>();
+    case TILE2_W320x128: return info2<W2_320x128>();
+    default: return info2<W2_128x128>();
+  }
+}
+
+hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
+  switch (t) {
+    case TILE2_C128x320: return conv2_t<C2_128x320>(a, st);
+    case TILE2_C128x160: return conv2_t<C2_128x160>(a, st);
+    case TILE2_C256x128: return conv2_t<C2_256x128>(a, st);
+    default: return conv2_t<C2_128x128>(a, st);
+  }
+}
+
+hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero16,
+                         hipStream_t st) {
+  hipError_t e;
+  switch (t) {
+    case TILE2_W320x192: e = wgrad2_t<W2_320x192>(a, splits, zero16, st); break;
+    case TILE2_W320x128: e = wgrad2_t<W2_320x128>(a, splits, zero16, st); break;
+    default: e = wgrad2_t<W2_128x128>(a, splits, zero16, st); break;
+  }
+  if (e != hipSuccess) return e;
+  return launch_wgrad_finalize(a, splits, st);
+}
+
+}  // namespace pulse

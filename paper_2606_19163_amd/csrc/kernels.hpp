@@ -64,6 +64,24 @@ struct TileInfo {
 TileInfo tile_info(int tile);
 hipError_t launch_conv(const GemmArgs& a, int tile, hipStream_t st);
 hipError_t launch_wgrad(const GemmArgs& a, int tile, int splits, hipStream_t st);
+hipError_t launch_wgrad_finalize(const GemmArgs& a, int splits, hipStream_t st);
+
+// second generation (igemm2.hip): LDS-DMA operand loads, bf16 with 64
+// channels per K-step only.  zero16: 16 zero bytes of device memory.
+enum Tile2 : int {
+  TILE2_C128x320 = 0,
+  TILE2_C128x160 = 1,
+  TILE2_C128x128 = 2,
+  TILE2_C256x128 = 3,
+  TILE2_W320x192 = 4,
+  TILE2_W320x128 = 5,
+  TILE2_W128x128 = 6,
+  TILE2_COUNT = 7
+};
+TileInfo tile2_info(int tile);
+hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);
+hipError_t launch_wgrad2(const GemmArgs& a, int tile, int splits, const void* zero16,
+                         hipStream_t st);
 
 // ---- GroupNorm / reductions (norm.hip) -----------------------------------
 

@@ -96,6 +96,7 @@ struct pulse_stage {
   size_t esz = 4;
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
+  bool v2 = false;      // LDS-DMA GEMM kernels (bf16, 64-channel K-steps)
   Geo geo{};
   long P = 0;
   int G = 1;
@@ -115,7 +116,7 @@ struct pulse_stage {
   size_t row_act[MAX_SLOTS], row_grad[MAX_SLOTS];
   size_t row_temb[2] = {0, 0}, row_xin = 0, row_u = 0;
   size_t s_da = 0, s_dxs = 0, s_dh1 = 0, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
-         s_pi = 0, s_e = 0;
+         s_pi = 0, s_e = 0, s_zero = 0;
   size_t part_cap = 0;
   // binding
   const float* prm = nullptr;
@@ -191,11 +192,13 @@ void layout_gn(const pulse_stage* s, GnSave& g, size_t& off, int C) {
   off += align256((size_t)s->geo.B * C * 4);
 }
 
-// Tile shape of a conv-mode GEMM with N output columns.
+// Tile shape of a conv-mode GEMM with N output columns (a Tile2 value on
+// the LDS-DMA path, a Tile value otherwise).
 int conv_tile(const pulse_stage* s, int N) {
   if (s->dtype == DT_F32) return TILE_64x64_F32;
   if (!s->k64) return TILE_128x128_K32;
   if (s->conv_tile_force >= 0) return s->conv_tile_force;
+  if (s->v2) return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128;
   if (N % 320 == 0) return TILE_128x320;
   return N % 160 == 0 ? TILE_256x160 : TILE_128x128;
 }
@@ -206,13 +209,20 @@ int wgrad_tile(const pulse_stage* s, int M, int N) {
   if (!s->k64) return TILE_128x128_K32;
   if (s->wgrad_tile_force >= 0) return s->wgrad_tile_force;
   (void)N;
+  if (s->v2) return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128;
   if (M % 320 == 0) return TILE_320x160;
   return M % 160 == 0 ? TILE_160x160 : TILE_128x128;
 }
 
-// Pixel split of a weight-gradient GEMM: enough blocks for about two per CU.
+bool uses_v2(const pulse_stage* s) { return s->v2 && s->dtype == DT_BF16 && s->k64; }
+
+TileInfo info_of(const pulse_stage* s, int tile) {
+  return uses_v2(s) ? tile2_info(tile) : tile_info(tile);
+}
+
+// Pixel split of a weight-gradient GEMM: enough blocks for about one per CU.
 int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
-  const TileInfo ti = tile_info(tile);
+  const TileInfo ti = info_of(s, tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
   long splits = (256 + tiles - 1) / tiles;
   const long maxs = (s->P + 255) / 256;
@@ -277,9 +287,17 @@ pulse_status build_layout(pulse_stage* s) {
     for (auto& b : s->eb) { chk(b.cin); chk(b.cout); chk(b.c0); }
     for (auto& b : s->db) { chk(b.cin); chk(b.cout); chk(b.c0); }
     s->k64 = k64;
+    // PULSE_GEMM_V1=1 selects the register-staged GEMM kernels; the tile
+    // overrides (tuning) index Tile2 on the LDS-DMA path, Tile otherwise
+    s->v2 = env_int("PULSE_GEMM_V1", 0) == 0;
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
-    s->conv_tile_force = (ct >= 0 && ct <= TILE_160x160) ? ct : -1;
-    s->wgrad_tile_force = (wt >= 0 && wt <= TILE_160x160) ? wt : -1;
+    if (s->v2) {
+      s->conv_tile_force = (ct >= TILE2_C128x320 && ct <= TILE2_C256x128) ? ct : -1;
+      s->wgrad_tile_force = (wt >= TILE2_W320x192 && wt <= TILE2_W128x128) ? wt : -1;
+    } else {
+      s->conv_tile_force = (ct >= 0 && ct <= TILE_160x160) ? ct : -1;
+      s->wgrad_tile_force = (wt >= 0 && wt <= TILE_160x160) ? wt : -1;
+    }
   }
 
   // workspace: weight copies | rows | scratch
@@ -351,6 +369,7 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_coef = sc; sc += align256((size_t)s->geo.B * s->G * 2 * 4);
   s->s_pi = sc; sc += align256((size_t)2 * s->geo.B * cmax * 4);
   s->s_e = sc; sc += align256((size_t)s->geo.B * cmax * 4);
+  s->s_zero = sc; sc += 256;  // zero bytes read in place of out-of-image taps
   s->ws_bytes = s->off_scratch + sc;
   return PULSE_OK;
 }
@@ -504,7 +523,10 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
     e1 = next_event(s);
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
-  HIPCHK(launch_conv(a, conv_tile(s, a.N), st));
+  if (uses_v2(s))
+    HIPCHK(launch_conv2(a, conv_tile(s, a.N), st));
+  else
+    HIPCHK(launch_conv(a, conv_tile(s, a.N), st));
   if (s->timing && e0 && e1) {
     HIPCHK(hipEventRecord(e1, st));
     s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K});
@@ -587,7 +609,10 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
     return fail(PULSE_E_SHAPE, "internal: wgrad partial buffer too small");
   a.kchunk = kchunk;
   a.part = s->sf(s->s_part);
-  HIPCHK(launch_wgrad(a, tile, splits, st));
+  if (uses_v2(s))
+    HIPCHK(launch_wgrad2(a, tile, splits, s->scratch(s->s_zero), st));
+  else
+    HIPCHK(launch_wgrad(a, tile, splits, st));
   return PULSE_OK;
 }
 
@@ -889,6 +914,7 @@ pulse_status pulse_stage_sync_params(pulse_stage* s, void* stream) {
       HIPCHK(launch_vec_add(s->pp(b.b2), b.conv_sc ? s->pp(b.bs) : nullptr,
                             reinterpret_cast<float*>(s->ws + b.bias2), b.cout, st));
     }
+  HIPCHK(hipMemsetAsync(s->scratch(s->s_zero), 0, 256, st));
   s->synced = true;
   return PULSE_OK;
 }
