@@ -96,6 +96,9 @@ def main():
     ap.add_argument("--cpu-sample-batch", type=int, default=2)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket the conv launches with HIP events")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device-to-device copy of this many MiB before "
+                         "the warmup (the known-size kernel that scales HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -133,6 +136,13 @@ def main():
             outs[i][m]["dx"] = stages[i].act(d["enc"][0]["c_in"])
             outs[i][m]["du"] = stages[i].act(d["dec"][0]["c_up"])
     flops_step = sum(st.flops() for st in stages) * n_mb
+    if args.copy_calibration_mib > 0:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         for i, st in enumerate(stages):

@@ -107,10 +107,10 @@ hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale,
                            const float* shift, void* dst0, void* dst1, int dtype,
                            hipStream_t st);
 
-// GroupNorm+SiLU backward.  da: gradient w.r.t. SiLU(GN(x)) (fp32 [P][C]).
+// GroupNorm+SiLU backward.  da: gradient w.r.t. SiLU(GN(x)) ([P][C], any dtype).
 // partial[b][chunk][0][c] = sum dz, [1][c] = sum dz * xhat with
 // dz = da * SiLU'(z), z = x * scale + shift, xhat = (x - mean) * rstd.
-hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+hipError_t launch_gn_bwd_partial(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                  const float* scale, const float* shift, const float* mean,
                                  const float* rstd, int G, float* partial, hipStream_t st);
 // coef[b][g][2] = (sum_g gamma*dz, sum_g gamma*dz*xhat) / count, and
@@ -131,7 +131,7 @@ struct GnBwdOut {
   float* chan_partial;  // optional per-(b, chunk, c) sums of the output
 };
 // dx = rstd * (gamma*dz - coef0 - xhat*coef1) + addends, split-stored.
-hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
                                int G, const GnBwdOut& o, hipStream_t st);

@@ -19,20 +19,33 @@ __device__ __forceinline__ void st_any(void* p, int dtype, long i, float v) {
     static_cast<float*>(p)[i] = v;
 }
 
-// one wave per (o, b): lanes stride over d, xor-shuffle tree reduction
+// one wave per (o, b): lanes stride over d (four loads in flight per lane),
+// xor-shuffle tree reduction
 __global__ __launch_bounds__(64) void k_temb_fwd(const void* temb, int dtype, int D, int O,
                                                  const float* Wl, const float* bias_a,
                                                  const float* bias_b, float* e) {
   const int o = blockIdx.x, b = blockIdx.y;
-  float s = 0.f;
-  for (int d = threadIdx.x; d < D; d += 64)
-    s += Wl[(long)o * D + d] * silu_f(ld_any(temb, dtype, (long)b * D + d));
+  const float* w = Wl + (long)o * D;
+  const long t0 = (long)b * D;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  int d = threadIdx.x;
+  for (; d + 192 < D; d += 256) {
+    const float w0 = w[d], w1 = w[d + 64], w2 = w[d + 128], w3 = w[d + 192];
+    const float x0 = ld_any(temb, dtype, t0 + d), x1 = ld_any(temb, dtype, t0 + d + 64);
+    const float x2 = ld_any(temb, dtype, t0 + d + 128), x3 = ld_any(temb, dtype, t0 + d + 192);
+    s0 += w0 * silu_f(x0);
+    s1 += w1 * silu_f(x1);
+    s2 += w2 * silu_f(x2);
+    s3 += w3 * silu_f(x3);
+  }
+  for (; d < D; d += 64) s0 += w[d] * silu_f(ld_any(temb, dtype, t0 + d));
+  float s = (s0 + s1) + (s2 + s3);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
   if (threadIdx.x == 0) {
-    float v = s + bias_a[o];
-    if (bias_b) v += bias_b[o];
-    e[(long)b * O + o] = v;
+    float bias = bias_a[o];
+    if (bias_b) bias += bias_b[o];
+    e[(long)b * O + o] = s + bias;
   }
 }
 
@@ -57,23 +70,33 @@ __global__ void k_temb_bwd_w(const float* de, const void* temb, int dtype, int B
   }
 }
 
-// block (64 d x 8 o-lanes) per (d block, image b):
+// block (64 d x 16 o-lanes) per (d block, image b):
 // dtemb[b][d] += SiLU'(temb[b][d]) * sum_o Wl[o][d] de[b][o]
-__global__ __launch_bounds__(512) void k_temb_bwd_x(const float* de, const void* temb, int dtype,
-                                                    int B, int D, int O, const float* Wl,
-                                                    float* dtemb) {
-  __shared__ float sm[8][64];
+__global__ __launch_bounds__(1024) void k_temb_bwd_x(const float* de, const void* temb,
+                                                     int dtype, int B, int D, int O,
+                                                     const float* Wl, float* dtemb) {
+  __shared__ float sm[16][64];
   const int d = blockIdx.x * 64 + threadIdx.x;
   const int b = blockIdx.y;
   float s = 0.f;
-  if (d < D)
-    for (int o = threadIdx.y; o < O; o += 8) s += Wl[(long)o * D + d] * de[(long)b * O + o];
+  if (d < D) {
+    int o = threadIdx.y;
+    for (; o + 48 < O; o += 64) {
+      const float w0 = Wl[(long)o * D + d], w1 = Wl[(long)(o + 16) * D + d];
+      const float w2 = Wl[(long)(o + 32) * D + d], w3 = Wl[(long)(o + 48) * D + d];
+      s += w0 * de[(long)b * O + o];
+      s += w1 * de[(long)b * O + o + 16];
+      s += w2 * de[(long)b * O + o + 32];
+      s += w3 * de[(long)b * O + o + 48];
+    }
+    for (; o < O; o += 16) s += Wl[(long)o * D + d] * de[(long)b * O + o];
+  }
   sm[threadIdx.y][threadIdx.x] = s;
   __syncthreads();
   if (threadIdx.y == 0 && d < D) {
     float t = sm[0][threadIdx.x];
 #pragma unroll
-    for (int y = 1; y < 8; ++y) t += sm[y][threadIdx.x];
+    for (int y = 1; y < 16; ++y) t += sm[y][threadIdx.x];
     const long i = (long)b * D + d;
     dtemb[i] += t * dsilu_f(ld_any(temb, dtype, i));
   }
@@ -144,7 +167,7 @@ hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, 
                      dtype, B, D, O, dWl, dbl, db1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !dtemb) return e;
-  hipLaunchKernelGGL(k_temb_bwd_x, dim3((D + 63) / 64, B), dim3(64, 8), 0, st, de, temb, dtype,
+  hipLaunchKernelGGL(k_temb_bwd_x, dim3((D + 63) / 64, B), dim3(64, 16), 0, st, de, temb, dtype,
                      B, D, O, Wl, dtemb);
   return hipGetLastError();
 }

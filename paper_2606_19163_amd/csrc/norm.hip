@@ -174,21 +174,40 @@ struct GnConst {
   float sc[8], sh[8], mu[8], rs[8];
 };
 
+__device__ __forceinline__ void load8f(const float* p, float v[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+// Per-group value of each of the channels [c, c+8) (c a multiple of 8).
+// When a group has 4 or at least 8 channels those 8 channels touch at most
+// two groups, g0 = c / cg and g1 = (c + 7) / cg, and two loads suffice.
+__device__ __forceinline__ void load_group_pair(const float* v, int b, int G, int c, int cg,
+                                                float out[8]) {
+  if (cg == 4 || cg >= 8) {
+    const int g0 = c / cg, g1 = (c + 7) / cg;
+    const float a0 = v[b * G + g0], a1 = v[b * G + g1];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[j] = (c + j) / cg == g0 ? a0 : a1;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[j] = v[b * G + (c + j) / cg];
+  }
+}
+
 __device__ __forceinline__ void load_gn_const(GnConst& k, int b, int c, int C, int G,
                                               const float* scale, const float* shift,
                                               const float* mean, const float* rstd) {
   const int cg = C / G;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int gi = (c + j) / cg;
-    k.sc[j] = scale[(long)b * C + c + j];
-    k.sh[j] = shift[(long)b * C + c + j];
-    k.mu[j] = mean[b * G + gi];
-    k.rs[j] = rstd[b * G + gi];
-  }
+  load8f(scale + (long)b * C + c, k.sc);
+  load8f(shift + (long)b * C + c, k.sh);
+  load_group_pair(mean, b, G, c, cg, k.mu);
+  load_group_pair(rstd, b, G, c, cg, k.rs);
 }
 
-__global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, Geo g,
+__global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
                                                         RedGrid rg, const float* scale,
                                                         const float* shift, const float* mean,
                                                         const float* rstd, int G,
@@ -209,10 +228,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(const float* da, VIn x, 
         if (pu < r.p1) {
           const long pix = (long)r.b * g.hw() + pu;
           ld8v(x, pix, r.c, f[u]);
-          const float4* dp = reinterpret_cast<const float4*>(da + pix * x.C + r.c);
-          const float4 d0 = dp[0], d1 = dp[1];
-          d[u][0] = d0.x; d[u][1] = d0.y; d[u][2] = d0.z; d[u][3] = d0.w;
-          d[u][4] = d1.x; d[u][5] = d1.y; d[u][6] = d1.z; d[u][7] = d1.w;
+          ld8(da, pix, r.c, d[u]);
         } else {
 #pragma unroll
           for (int j = 0; j < 8; ++j) f[u][j] = d[u][j] = 0.f;
@@ -260,7 +276,11 @@ __global__ __launch_bounds__(256) void k_gn_bwd_coef(const float* partial, Geo g
 // Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
 // partial[b][chunk][s][c] for the first `nslot` slots.  Block (64 channels,
 // 4 chunk lanes) per (channel block, image).
-constexpr int VX = 64;  // k_chan_per_image: 64 channels x 4 chunk lanes
+// Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
+// partial[b][chunk][s][c] for the first `nslot` slots.  A block holds 64
+// channels x 4 chunk lanes of one image; each lane keeps four loads in
+// flight.
+constexpr int VX = 64;
 constexpr int PY = 4;
 
 __global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, int chunks, int B,
@@ -270,10 +290,28 @@ __global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, in
   const int b = blockIdx.y;
   float s0 = 0.f, s1 = 0.f;
   if (c < C) {
-    for (int ch = threadIdx.y; ch < chunks; ch += PY) {
-      const float* base = partial + ((long)b * chunks + ch) * 2 * C;
-      s0 += base[c];
-      if (nslot > 1) s1 += base[C + c];
+    const long stride = 2L * C;
+    const float* base = partial + (long)b * chunks * stride + c;
+    int ch = threadIdx.y;
+    for (; ch + 3 * PY < chunks; ch += 4 * PY) {
+      const float a0 = base[(ch + 0 * PY) * stride], a1 = base[(ch + 1 * PY) * stride];
+      const float a2 = base[(ch + 2 * PY) * stride], a3 = base[(ch + 3 * PY) * stride];
+      s0 += a0;
+      s0 += a1;
+      s0 += a2;
+      s0 += a3;
+      if (nslot > 1) {
+        const float e0 = base[(ch + 0 * PY) * stride + C], e1 = base[(ch + 1 * PY) * stride + C];
+        const float e2 = base[(ch + 2 * PY) * stride + C], e3 = base[(ch + 3 * PY) * stride + C];
+        s1 += e0;
+        s1 += e1;
+        s1 += e2;
+        s1 += e3;
+      }
+    }
+    for (; ch < chunks; ch += PY) {
+      s0 += base[ch * stride];
+      if (nslot > 1) s1 += base[ch * stride + C];
     }
   }
   sm[0][threadIdx.y][threadIdx.x] = s0;
@@ -306,7 +344,7 @@ __global__ void k_chan_total(const float* pi, int B, int C, float* acc0, float* 
   if (acc1) acc1[c] += t1;
 }
 
-__global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Geo g,
+__global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
                                                       RedGrid rg, const float* scale,
                                                       const float* shift, const float* mean,
                                                       const float* rstd, const float* gamma,
@@ -322,21 +360,30 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(const float* da, VIn x, Ge
     GnConst k;
     load_gn_const(k, r.b, r.c, C, G, scale, shift, mean, rstd);
     float ga[8], c0[8], c1[8];
+    load8f(gamma + r.c, ga);
+    if (cg == 4 || cg >= 8) {  // the 8 channels touch at most two groups
+      const int g0 = r.c / cg, g1 = (r.c + 7) / cg;
+      const float2 e0 = reinterpret_cast<const float2*>(coef)[r.b * G + g0];
+      const float2 e1 = reinterpret_cast<const float2*>(coef)[r.b * G + g1];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int gi = (r.c + j) / cg;
-      ga[j] = gamma[r.c + j];
-      c0[j] = coef[(r.b * G + gi) * 2 + 0];
-      c1[j] = coef[(r.b * G + gi) * 2 + 1];
+      for (int j = 0; j < 8; ++j) {
+        const bool first = (r.c + j) / cg == g0;
+        c0[j] = first ? e0.x : e1.x;
+        c1[j] = first ? e0.y : e1.y;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float2 e = reinterpret_cast<const float2*>(coef)[r.b * G + (r.c + j) / cg];
+        c0[j] = e.x;
+        c1[j] = e.y;
+      }
     }
     for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
       const long pix = (long)r.b * g.hw() + p;
       float f[8], d[8], out[8];
       ld8v(x, pix, r.c, f);
-      const float4* dp = reinterpret_cast<const float4*>(da + pix * C + r.c);
-      const float4 d0 = dp[0], d1 = dp[1];
-      d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
-      d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+      ld8(da, pix, r.c, d);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const float z = f[j] * k.sc[j] + k.sh[j];
@@ -441,7 +488,7 @@ hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale, const
   return hipGetLastError();
 }
 
-hipError_t launch_gn_bwd_partial(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+hipError_t launch_gn_bwd_partial(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                  const float* scale, const float* shift, const float* mean,
                                  const float* rstd, int G, float* partial, hipStream_t st) {
   hipLaunchKernelGGL(k_gn_bwd_partial, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
@@ -460,7 +507,7 @@ hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg
   return launch_chan_sum_finalize(partial, g, rg, C, 2, pi, dbeta, nullptr, dgamma, st);
 }
 
-hipError_t launch_gn_bwd_apply(const float* da, const VIn& x, const Geo& g, RedGrid rg,
+hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
                                int G, const GnBwdOut& o, hipStream_t st) {

@@ -634,11 +634,12 @@ pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x
 
 // GroupNorm+SiLU backward: da (fp32 [P][C]) -> o (split store + addends)
 pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
-                         const float* gamma, float* dgamma, float* dbeta, const float* da,
+                         const float* gamma, float* dgamma, float* dbeta, const void* da_ptr,
                          const GnBwdOut& o, hipStream_t st) {
   const RedGrid rg = red_grid(s->geo, x.C);
   float* red = s->sf(s->s_red);
   float* coef = s->sf(s->s_coef);
+  const Src da = src_of(da_ptr, s->dtype, x.C);
   const float* mean = reinterpret_cast<const float*>(row + g.mean);
   const float* rstd = reinterpret_cast<const float*>(row + g.rstd);
   const float* scale = reinterpret_cast<const float*>(row + g.scale);
@@ -736,14 +737,16 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
       return ps;
   }
   // data gradients through conv2 and the shortcut
-  float* da = s->sf(s->s_da);
+  // data gradients are stored in the stage dtype (the MFMA operands they feed
+  // are rounded to it anyway; the GroupNorm backward reads them once more)
+  void* da = s->scratch(s->s_da);
   if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cout, dout)}, s->ws + b.wd2, 9 * b.cout, nullptr,
-                     nullptr, vnone(), da, nullptr, DT_F32, st)) != PULSE_OK)
+                     nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
     return ps;
-  float* dxs = s->sf(s->s_dxs);
+  void* dxs = s->scratch(s->s_dxs);
   if (b.conv_sc) {
     if ((ps = conv_fwd(s, b.cin, {seg1(0, b.cout, dout)}, s->ws + b.wsd, b.cout, nullptr, nullptr,
-                       vnone(), dxs, nullptr, DT_F32, st)) != PULSE_OK)
+                       vnone(), dxs, nullptr, dt, st)) != PULSE_OK)
       return ps;
   }
   // GN2 backward -> dh1, with per-image channel sums (the temb gradient)
@@ -773,10 +776,10 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, st)) != PULSE_OK)
     return ps;
   if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
-                     nullptr, vnone(), da, nullptr, DT_F32, st)) != PULSE_OK)
+                     nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
     return ps;
   // GN1 backward + residual path -> gradient w.r.t. the block input
-  o.add0 = b.conv_sc ? vin1(dxs, DT_F32, b.cin) : dout;
+  o.add0 = b.conv_sc ? vin1(dxs, dt, b.cin) : dout;
   o.chan_partial = nullptr;
   return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
 }
