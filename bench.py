@@ -58,6 +58,39 @@ def describe(name, descs):
             "dec_blocks": [[b["c_up"], b["c_skip"], b["c_out"]] for b in d["dec"]]}
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "igemm2_conv_l64_traffic.md")
+KERNEL_SOURCES = ["igemm2.hip", "kernels.hpp", "common.hpp", "stage.cpp"]
+
+
+def kernel_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_19163_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name):
+    """HBM bytes per conv launch from the committed FETCH_SIZE/WRITE_SIZE
+    summary of the l64 stage; None when that summary was taken on other
+    kernel sources than the ones built here, or for another workload."""
+    if name != "l64" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_PROFILE) as fh:
+        for line in fh:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                vals[k.strip("`")] = v.strip().strip("`")
+    if vals.get("kernel_sources_sha256") != kernel_sources_sha256():
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(name, descs, seed, sample_batch):
     """The oracle, as it stands, on `sample_batch` images of the workload's
     first stage (forward + backward), scaled to TFLOP/s."""
@@ -169,12 +202,13 @@ def main():
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    launches, kms, kflops = 0, 0.0, 0.0
+    launches, kms, kflops, kbytes = 0, 0.0, 0.0, 0.0
     for st in stages:
-        n, ms, fl = st.timing_read()
+        n, ms, fl, by = st.timing_read()
         launches += n
         kms += ms
         kflops += fl
+        kbytes += by
         st.timing(False)
 
     ms_step = elapsed * 1e3 / args.steps
@@ -204,7 +238,11 @@ def main():
         line["roofline"] = {
             "kernel": "igemm_conv (implicit-GEMM conv forward / data gradient)",
             "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-            "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+            "traffic": measured_traffic(args.workload),
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                            "copy-calibrated)",
+            "algorithmic_bytes_per_launch": round(kbytes / launches),
             "launches": launches, "avg_launch_us": round(kms * 1e3 / launches, 2),
             "avg_gflop_per_launch": round(kflops / launches / 1e9, 3),
         }

@@ -190,10 +190,13 @@ int32_t pulse_stage_inflight(const pulse_stage* st);
 /* Per-kernel timing: when enabled, every launch of the implicit-GEMM conv
  * kernel is bracketed by HIP events on the call's stream.  _read
  * synchronises those events and returns the launch count, the summed
- * duration in ms and the summed algorithmic FLOPs since the last reset. */
+ * duration in ms, the summed algorithmic FLOPs (2*M*N*K) and the summed
+ * compulsory HBM bytes (each input element, weight and residual read once,
+ * each output written once) since the last reset; any output pointer may
+ * be NULL. */
 pulse_status pulse_stage_timing(pulse_stage* st, int32_t enable);
 pulse_status pulse_stage_timing_read(pulse_stage* st, int64_t* launches,
-                                     double* ms, double* flops);
+                                     double* ms, double* flops, double* bytes);
 
 /* FLOPs of one microbatch's ENC+DEC forward and backward as 2*M*N*K summed
  * over every conv (forward, data gradient, weight gradient) and the

@@ -32,8 +32,22 @@ The paper does not define the block arithmetic (Sec. II-A only says that the
 blocks hold attention and ResNet layers).  The ResBlock used here is the
 SD-style block: GroupNorm -> SiLU -> 3x3 conv (+ timestep-embedding add) ->
 GroupNorm -> SiLU -> 3x3 conv, plus a residual that is the identity when the
-channel count is unchanged and a 1x1 conv otherwise.  Every reading taken
-where the paper is silent is listed in the design doc.
+channel count is unchanged and a 1x1 conv otherwise.  Readings taken where
+the paper is silent:
+
+* every conv, the shortcut and the timestep linear carry a bias; GroupNorm
+  uses the biased variance with eps inside the square root, per sample, and
+  its groups follow the concatenated channel index (a group may straddle the
+  upstream/skip boundary);
+* zero padding is applied to the conv input after GroupNorm + SiLU;
+* the residual is an unscaled sum; no dropout;
+* the timestep path is SiLU, then Linear with bias, added after conv1 and
+  broadcast over the image -- parity unpinned: nothing in the paper fixes
+  this order, only torch (sharing the reading) checks it;
+* skips pair in mirror order (the last cached skip feeds the first decoder
+  block), following the symmetric placement rule; which tensors are cached
+  (e.g. the stage input of the 32x32 stage) is a descriptor choice -- parity
+  unpinned for the same reason.
 
 Every function is the plain definition written out; the only library
 primitives used as steps are matrix products (the channel sum of one

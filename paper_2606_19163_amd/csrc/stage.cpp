@@ -81,7 +81,7 @@ struct Row {
 
 struct TimedLaunch {
   hipEvent_t a, b;
-  double flops;
+  double flops, bytes;
 };
 
 }  // namespace
@@ -516,6 +516,30 @@ hipEvent_t next_event(pulse_stage* s) {
   return s->ev_pool[s->ev_used++];
 }
 
+double elt_bytes(int dtype) { return dtype == DT_BF16 ? 2.0 : 4.0; }
+
+double vin_bytes(const VIn& v, double pixels) {
+  if (!v.s0.ptr) return 0.0;
+  const double c0 = v.s1.ptr ? v.c0 : v.C;
+  double b = pixels * c0 * elt_bytes(v.s0.dtype);
+  if (v.s1.ptr) b += pixels * (v.C - v.c0) * elt_bytes(v.s1.dtype);
+  if (v.add) b += pixels * v.C * 4.0;
+  return b;
+}
+
+// Compulsory HBM bytes of one conv-mode launch: every input element once
+// (the 3x3 taps re-read the same pixels), the weights once, the residual,
+// and every output written.
+double conv_bytes(const pulse_stage* s, const GemmArgs& a) {
+  const double P = (double)a.M;
+  double b = 0.0;
+  for (int i = 0; i < a.nseg; ++i) b += vin_bytes(a.seg[i].in, P);
+  b += (double)a.N * a.K * elt_bytes(s->dtype);
+  b += vin_bytes(a.resid, P);
+  b += P * a.N * elt_bytes(a.out_dtype) * (a.out2 ? 2.0 : 1.0);
+  return b;
+}
+
 pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
@@ -529,7 +553,7 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
     HIPCHK(launch_conv(a, conv_tile(s, a.N), st));
   if (s->timing && e0 && e1) {
     HIPCHK(hipEventRecord(e1, st));
-    s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K});
+    s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K, conv_bytes(s, a)});
   }
   return PULSE_OK;
 }
@@ -1220,19 +1244,21 @@ pulse_status pulse_stage_timing(pulse_stage* s, int32_t enable) {
 }
 
 pulse_status pulse_stage_timing_read(pulse_stage* s, int64_t* launches, double* ms,
-                                     double* flops) {
+                                     double* flops, double* bytes) {
   if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
-  double t = 0.0, f = 0.0;
+  double t = 0.0, f = 0.0, by = 0.0;
   for (const auto& tl : s->timed) {
     HIPCHK(hipEventSynchronize(tl.b));
     float x = 0.f;
     HIPCHK(hipEventElapsedTime(&x, tl.a, tl.b));
     t += x;
     f += tl.flops;
+    by += tl.bytes;
   }
   if (launches) *launches = (int64_t)s->timed.size();
   if (ms) *ms = t;
   if (flops) *flops = f;
+  if (bytes) *bytes = by;
   s->timed.clear();
   s->ev_used = 0;
   return PULSE_OK;

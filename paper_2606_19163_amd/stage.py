@@ -111,6 +111,7 @@ def lib():
         L.pulse_stage_timing.restype = st
         L.pulse_stage_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_int64),
                                               ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_double)]
         L.pulse_stage_timing_read.restype = st
         L.pulse_stage_flops.argtypes = [_vp]
@@ -298,9 +299,10 @@ class Stage:
         n = ctypes.c_int64()
         ms = ctypes.c_double()
         fl = ctypes.c_double()
+        by = ctypes.c_double()
         _check(lib().pulse_stage_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms),
-                                             ctypes.byref(fl)))
-        return n.value, ms.value, fl.value
+                                             ctypes.byref(fl), ctypes.byref(by)))
+        return n.value, ms.value, fl.value, by.value
 
 
 def run_microbatch(stage, mb, b, dtemb=None):
