@@ -188,9 +188,12 @@ __device__ __forceinline__ int seg_of(int nseg, int b1, int b2, int i) {
 
 // Remap the linear block id so that consecutive tiles land on one XCD
 // (the hardware deals workgroups round-robin over the 8 XCDs).
+// Workgroups are dispatched round-robin over the 8 XCDs (block b on XCD
+// b % 8).  Map them so that XCD x runs one contiguous range of logical
+// blocks: XCD x holds q + (x < r) blocks for nb = 8 q + r.
 __device__ __forceinline__ int xcd_remap(int bid, int nb) {
-  if (nb % 8 != 0) return bid;
-  return (bid % 8) * (nb / 8) + bid / 8;
+  const int q = nb >> 3, r = nb & 7, x = bid & 7;
+  return x * q + (x < r ? x : r) + (bid >> 3);
 }
 
 template <class C>
@@ -439,22 +442,13 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
-  // Block -> (split, tile).  Workgroups are dealt round-robin over the 8
-  // XCDs; when the split count is a multiple of 8, every block of one pixel
-  // split runs on the same XCD so the split's operand slices stay in that
-  // XCD's L2.
+  // Block -> (split, tile), split-major over a contiguous range per XCD,
+  // so the blocks of one pixel split share that XCD's L2.
   const int tilesN = (a.N + C::BN - 1) / C::BN;
   const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
-  const int splits = gridDim.x / ntiles;
-  int tile, z;
-  if (splits % 8 == 0) {
-    const int q = blockIdx.x / 8;
-    z = (int)(blockIdx.x % 8) + 8 * (q / ntiles);
-    tile = q % ntiles;
-  } else {
-    z = blockIdx.x / ntiles;
-    tile = blockIdx.x % ntiles;
-  }
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int z = lb / ntiles;
+  const int tile = lb - z * ntiles;
   const int tn = tile % tilesN;
   const int tm = tile / tilesN;
   const int m0 = tm * C::BM;

@@ -55,21 +55,26 @@ __device__ __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
 
 }  // namespace
 
-template <int BM_, int BN_, int WM_, int WN_>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 2>
 struct CfgC {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64, STAGES = STAGES_;
   static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN, NW = WAVES_M * WAVES_N;
   static constexpr int NT = NW * 64;
   static constexpr int TM = WM / 16, TN = WN / 16;
   static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int WLA = BM / 8, WLB = BN / 8, WL = WLA + WLB;  // 1 KB wave loads
-  static constexpr int NU = WL / NW;                                 // per wave
+  static constexpr int NU = (WL + NW - 1) / NW;  // loads of waves < REM (all when REM == 0)
+  static constexpr int REM = WL % NW;
+  static constexpr int NU_LO = WL / NW;           // loads of waves >= REM
   static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
   static constexpr int LDC = BN + 4;
-  static_assert(16 * LDC * 4 <= STAGE, "epilogue slice must fit one stage");
-  static_assert(2 * STAGE <= 160 * 1024, "LDS");
-  static_assert(WL % NW == 0 && WLA % NW == 0, "wave loads must split evenly over the waves");
+  static_assert(STAGES == 2 || STAGES == 3, "stages");
+  static_assert(16 * LDC * 4 <= STAGES * STAGE, "epilogue slice must fit the stages");
+  static_assert(STAGES * STAGE <= 160 * 1024, "LDS");
+  static_assert(WLA % NW == 0, "A wave loads must split evenly over the waves");
+  static_assert(A_BYTES + (TN - 1) * 2048 < 65536, "fragment offsets are 16-bit immediates");
+  static_assert(TM + TN <= 15, "lgkmcnt");
   static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
 };
 
@@ -108,10 +113,47 @@ __device__ __forceinline__ int seg_of(int nseg, int b1, int b2, int i) {
   return s;
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs (block b on XCD
+// b % 8).  Map them so that XCD x runs one contiguous range of logical
+// blocks: XCD x holds q + (x < r) blocks for nb = 8 q + r.
 __device__ __forceinline__ int xcd_remap(int bid, int nb) {
-  if (nb % 8 != 0) return bid;
-  return (bid % 8) * (nb / 8) + bid / 8;
+  const int q = nb >> 3, r = nb & 7, x = bid & 7;
+  return x * q + (x < r ? x : r) + (bid >> 3);
 }
+
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// ds_read_b128 at addr + OFF.  Issued as inline asm so that the compiler's
+// waitcnt pass, which cannot tell LDS-DMA targets apart, does not insert a
+// vmcnt(0) before it: the kernel waits for its own DMA stages and for these
+// reads explicitly (lgkm_wait + tie).
+template <int OFF>
+__device__ __forceinline__ bf16x8_t ds_rd128(uint32_t addr) {
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+
+template <int N, int STRIDE, int BASE>
+__device__ __forceinline__ void ds_rd_n(bf16x8_t* dst, uint32_t addr) {
+  if constexpr (N > 0) {
+    ds_rd_n<N - 1, STRIDE, BASE>(dst, addr);
+    dst[N - 1] = ds_rd128<BASE + (N - 1) * STRIDE>(addr);
+  }
+}
+
+// s_waitcnt lgkmcnt(n) (vmcnt and expcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void lgkm_wait() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt");
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (N << 8) | (3 << 14));
+}
+
+// Order a value after the preceding waits: the MFMAs that consume it cannot
+// be scheduled above them.
+__device__ __forceinline__ void tie(bf16x8_t& v) { asm volatile("" : "+v"(v)); }
 
 struct SegRt {
   __amdgpu_buffer_rsrc_t r0, r1;
@@ -134,6 +176,18 @@ __device__ __forceinline__ SegRt seg_rt(const Seg& g, long P) {
 
 __device__ __forceinline__ SegRt pick(int s, const SegRt& a, const SegRt& b, const SegRt& c) {
   return s == 0 ? a : (s == 1 ? b : c);
+}
+
+// field-wise select (a select of whole structs can end up in scratch memory)
+__device__ __forceinline__ void select_into(SegRt& d, bool c, const SegRt& a, const SegRt& b) {
+  d.r0 = c ? a.r0 : b.r0;
+  d.r1 = c ? a.r1 : b.r1;
+  d.pitch0 = c ? a.pitch0 : b.pitch0;
+  d.pitch1 = c ? a.pitch1 : b.pitch1;
+  d.c0 = c ? a.c0 : b.c0;
+  d.C = c ? a.C : b.C;
+  d.taps = c ? a.taps : b.taps;
+  d.begin = c ? a.begin : b.begin;
 }
 
 // Stage the accumulator rows [i*16, i*16+16) of every wave of row group g
@@ -163,7 +217,7 @@ template <class C>
 __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // the body exists for the device pass only (the host pass emits the launch stub)
 #if defined(__HIP_DEVICE_COMPILE__)
-  __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[C::STAGES * C::STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -186,6 +240,9 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
 #pragma unroll
   for (int u = 0; u < C::NU; ++u) {
     const int wl = wave + u * C::NW;
+    ppix[u] = 0;
+    pmask[u] = 0;
+    coff[u] = OOB;
     if (u < C::UA) {
       const int r = wl * 8 + (lane >> 3);
       const long m = m0 + r;
@@ -204,45 +261,62 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
       ppix[u] = (uint32_t)(m < P ? m : 0);
       pmask[u] = mask;
       coff[u] = (uint32_t)(((lane & 7) ^ swz128(r)) * 16);
-    } else {
+    } else if (wl < C::WL) {
       const int r = (wl - C::WLA) * 8 + (lane >> 3);
       const int n = n0 + r;
-      ppix[u] = 0;
-      pmask[u] = 0;
       coff[u] = n < a.N ? (uint32_t)((long)n * a.ldb * 2 + ((lane & 7) ^ swz128(r)) * 16) : OOB;
     }
   }
 
-  const int nseg = a.nseg;
-  const SegRt q0 = seg_rt(a.seg[0], P);
   const SegRt q1 = seg_rt(a.seg[1], P);
   const SegRt q2 = seg_rt(a.seg[2], P);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.Bw, (long)a.N * a.ldb * 2);
+  const uint32_t sbase = lds_u32(smem);
 
-  auto issue = [&](int kt, char* base) __attribute__((always_inline)) {
-    const int k0 = kt * C::BK;
-    const SegRt q = pick(seg_of(nseg, q1.begin, q2.begin, k0), q0, q1, q2);
-    const int r = k0 - q.begin;
-    const int tap = r / q.C;
-    const int cb = r - tap * q.C;
-    const bool second = cb >= q.c0;
-    const __amdgpu_buffer_rsrc_t rs = second ? q.r1 : q.r0;
-    const uint32_t pitch = second ? q.pitch1 : q.pitch0;
-    const uint32_t cbyte = (uint32_t)((second ? cb - q.c0 : cb) * 2);
-    const int t9 = q.taps == 9 ? tap : 4;
-    const int shift = (t9 / 3 - 1) * W + (t9 % 3 - 1);
+  // K position of the next stage to issue: segment, tap (dy, dx) and
+  // channel, advanced by BK channels per stage without divisions
+  SegRt cur = seg_rt(a.seg[0], P);
+  int iseg = 0, itap = 0, icb = 0, idy = cur.taps == 9 ? -1 : 0, idx = idy;
+  uint32_t kbyte = 0;
+  auto advance = [&]() __attribute__((always_inline)) {
+    kbyte += C::BK * 2;
+    icb += C::BK;
+    if (icb >= cur.C) {
+      icb = 0;
+      ++itap;
+      if (++idx > 1) {
+        idx = -1;
+        ++idy;
+      }
+      if (itap >= cur.taps) {
+        ++iseg;
+        select_into(cur, iseg == 1, q1, q2);
+        itap = 0;
+        idy = idx = cur.taps == 9 ? -1 : 0;
+      }
+    }
+  };
+  auto issue = [&](uint32_t stage_off) __attribute__((always_inline)) {
+    const bool second = icb >= cur.c0;
+    const __amdgpu_buffer_rsrc_t rs = second ? cur.r1 : cur.r0;
+    const uint32_t pitch = second ? cur.pitch1 : cur.pitch0;
+    const uint32_t cbyte = (uint32_t)((second ? icb - cur.c0 : icb) * 2);
+    const int t9 = (idy + 1) * 3 + idx + 1;
+    const int shift = idy * W + idx;
 #pragma unroll
     for (int u = 0; u < C::NU; ++u) {
       const int wl = wave + u * C::NW;
+      char* dst = smem + stage_off + wl * 1024;
       if (u < C::UA) {
-        const uint32_t off =
-            ((pmask[u] >> t9) & 1u) ? (ppix[u] + shift) * pitch + cbyte + coff[u] : OOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(base + wl * 1024), 16, off, 0, 0, 0);
-      } else {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds(base + wl * 1024), 16,
-                                                 coff[u] + (uint32_t)(k0 * 2), 0, 0, 0);
+        const uint32_t off = ((pmask[u] >> t9) & 1u)
+                                 ? __umul24(ppix[u] + shift, pitch) + cbyte + coff[u]
+                                 : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst), 16, off, 0, 0, 0);
+      } else if (u < C::NU_LO || wl < C::WL) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds(dst), 16, coff[u] + kbyte, 0, 0, 0);
       }
     }
+    advance();
   };
 
   f32x4_t acc[C::TM][C::TN];
@@ -251,50 +325,67 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // fragment addresses: rows wm*WM + i*16 + r16 (A) and wn*WN + j*16 + r16
+  // (B) share one swizzle for every i / j, so each K-half needs one base
+  // address per operand and the row step is an immediate offset
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
-  // Per K-step: wait for the stage, read every fragment of it into
-  // registers, then start the next stage's DMA and run the MFMAs while it
-  // lands.  All LDS reads of a stage precede the next DMA in program order,
-  // so the compiler's conservative wait for LDS-DMA before LDS reads is
-  // exactly the real dependency.
+  uint32_t fa[2], fb[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int c = s * 4 + g4;
+    const int ra = wm * C::WM + r16, rb = wn * C::WN + r16;
+    fa[s] = (uint32_t)(ra * 128 + ((c ^ swz128(ra)) << 4));
+    fb[s] = (uint32_t)(rb * 128 + ((c ^ swz128(rb)) << 4));
+  }
+
+  // Per K-step: wait for this stage's DMA (the later stages stay in
+  // flight), barrier, issue every fragment read of the stage, start the DMA
+  // of the stage STAGES-1 ahead into the slot read one step ago, then the
+  // MFMAs of each K-half once its fragments have landed.
   bf16x8_t af[2][C::TM], bfr[2][C::TN];
-  auto read = [&](const char* As) __attribute__((always_inline)) {
-    const char* Bs = As + C::A_BYTES;
+  const int KT = a.K / C::BK;
+  issue(0);
+  if (C::STAGES == 3 && KT > 1) issue(C::STAGE);
+  int slot = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    if (C::STAGES == 3 && kt + 1 < KT) {
+      if (C::REM == 0 || wave < C::REM)
+        wait_vmcnt<C::NU>();
+      else
+        wait_vmcnt<C::NU_LO>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_s_barrier();
+    const uint32_t sb = sbase + (uint32_t)(slot * C::STAGE);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const int c = s * 4 + g4;
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i) {
-        const int r = wm * C::WM + i * 16 + r16;
-        af[s][i] = *reinterpret_cast<const bf16x8_t*>(As + r * 128 + ((c ^ swz128(r)) << 4));
-      }
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int r = wn * C::WN + j * 16 + r16;
-        bfr[s][j] = *reinterpret_cast<const bf16x8_t*>(Bs + r * 128 + ((c ^ swz128(r)) << 4));
-      }
+      ds_rd_n<C::TM, 2048, 0>(af[s], sb + fa[s]);
+      ds_rd_n<C::TN, 2048, C::A_BYTES>(bfr[s], sb + fb[s]);
     }
-  };
-  auto mma = [&]() __attribute__((always_inline)) {
+    if (kt + C::STAGES - 1 < KT) {
+      const int ns = slot + C::STAGES - 1;
+      issue((uint32_t)((ns >= C::STAGES ? ns - C::STAGES : ns) * C::STAGE));
+    }
+    slot = slot + 1 == C::STAGES ? 0 : slot + 1;
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int s = 0; s < 2; ++s) {
+      if (s == 0)
+        lgkm_wait<C::TM + C::TN>();
+      else
+        lgkm_wait<0>();
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) tie(af[s][i]);
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) tie(bfr[s][j]);
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
           acc[i][j] =
               __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
-  };
-
-  const int KT = a.K / C::BK;
-  issue(0, smem);
-  for (int kt = 0; kt < KT; ++kt) {
-    wait_vmcnt<0>();
-    __syncthreads();
-    read(smem + (kt & 1) * C::STAGE);
-    if (kt + 1 < KT) issue(kt + 1, smem + ((kt + 1) & 1) * C::STAGE);
-    mma();
+    }
   }
   __syncthreads();
 
@@ -358,19 +449,13 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
-  // block -> (split, tile); all tiles of a split on one XCD when possible
+  // block -> (split, tile), split-major over a contiguous range per XCD, so
+  // the blocks of one pixel split share that XCD's L2
   const int tilesN = (a.N + C::BN - 1) / C::BN;
   const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
-  const int splits = gridDim.x / ntiles;
-  int tile, z;
-  if (splits % 8 == 0) {
-    const int q = blockIdx.x / 8;
-    z = (int)(blockIdx.x % 8) + 8 * (q / ntiles);
-    tile = q % ntiles;
-  } else {
-    z = blockIdx.x / ntiles;
-    tile = blockIdx.x % ntiles;
-  }
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int z = lb / ntiles;
+  const int tile = lb - z * ntiles;
   const int m0 = (tile / tilesN) * C::BM;
   const int n0 = (tile % tilesN) * C::BN;
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
@@ -575,6 +660,8 @@ using C2_128x320 = CfgC<128, 320, 64, 80>;   // 8 waves
 using C2_128x160 = CfgC<128, 160, 64, 80>;   // 4 waves
 using C2_128x128 = CfgC<128, 128, 64, 64>;   // 4 waves
 using C2_256x128 = CfgC<256, 128, 64, 64>;   // 8 waves
+using C2_256x160S3 = CfgC<256, 160, 64, 80, 3>;  // 8 waves, 3 stages
+using C2_128x160S3 = CfgC<128, 160, 64, 80, 3>;  // 4 waves, 3 stages
 using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
 using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
@@ -609,6 +696,8 @@ TileInfo tile2_info(int t) {
     case TILE2_C128x160: return info2<C2_128x160>();
     case TILE2_C128x128: return info2<C2_128x128>();
     case TILE2_C256x128: return info2<C2_256x128>();
+    case TILE2_C256x160S3: return info2<C2_256x160S3>();
+    case TILE2_C128x160S3: return info2<C2_128x160S3>();
     case TILE2_W320x192: return info2<W2_320x192>();
     case TILE2_W320x128: return info2<W2_320x128>();
     default: return info2<W2_128x128>();
@@ -620,6 +709,8 @@ hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
     case TILE2_C128x320: return conv2_t<C2_128x320>(a, st);
     case TILE2_C128x160: return conv2_t<C2_128x160>(a, st);
     case TILE2_C256x128: return conv2_t<C2_256x128>(a, st);
+    case TILE2_C256x160S3: return conv2_t<C2_256x160S3>(a, st);
+    case TILE2_C128x160S3: return conv2_t<C2_128x160S3>(a, st);
     default: return conv2_t<C2_128x128>(a, st);
   }
 }

@@ -73,10 +73,14 @@ enum Tile2 : int {
   TILE2_C128x160 = 1,
   TILE2_C128x128 = 2,
   TILE2_C256x128 = 3,
-  TILE2_W320x192 = 4,
-  TILE2_W320x128 = 5,
-  TILE2_W128x128 = 6,
-  TILE2_COUNT = 7
+  TILE2_C256x160S3 = 4,  // three LDS stages, 8 waves, one block per CU
+  TILE2_C128x160S3 = 5,  // three LDS stages, 4 waves, one block per CU
+  TILE2_CONV_LAST = 5,
+  TILE2_W320x192 = 10,
+  TILE2_W320x128 = 11,
+  TILE2_W128x128 = 12,
+  TILE2_WGRAD_FIRST = 10,
+  TILE2_WGRAD_LAST = 12
 };
 TileInfo tile2_info(int tile);
 hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);

@@ -4,6 +4,7 @@
 // include/pulse_stage.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -198,7 +199,9 @@ int conv_tile(const pulse_stage* s, int N) {
   if (s->dtype == DT_F32) return TILE_64x64_F32;
   if (!s->k64) return TILE_128x128_K32;
   if (s->conv_tile_force >= 0) return s->conv_tile_force;
-  if (s->v2) return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128;
+  if (s->v2) {
+    return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128;
+  }
   if (N % 320 == 0) return TILE_128x320;
   return N % 160 == 0 ? TILE_256x160 : TILE_128x128;
 }
@@ -220,21 +223,34 @@ TileInfo info_of(const pulse_stage* s, int tile) {
   return uses_v2(s) ? tile2_info(tile) : tile_info(tile);
 }
 
-// Pixel split of a weight-gradient GEMM: enough blocks for about one per CU.
+// Pixel split of a weight-gradient GEMM.  With s splits the grid holds
+// tiles * s blocks of K / s pixels each; blocks run in ceil(tiles * s /
+// slots) rounds, and every split adds an fp32 partial of M x N that is
+// written once and read once by the finalize.  The split count minimises
+//   rounds(s) * T_tile / s + s * M * N * 8 / HBM
+// where T_tile is one tile's whole-K time at a nominal per-CU rate.
 int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
   const TileInfo ti = info_of(s, tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
-  long splits = (256 + tiles - 1) / tiles;
-  const long maxs = (s->P + 255) / 256;
-  if (splits > maxs) splits = maxs;
-  if (splits >= 8) splits = (splits + 7) / 8 * 8;  // one split per XCD at a time
-  if (splits < 1) splits = 1;
-  long kc = (s->P + splits - 1) / splits;
+  const long slots = 256L * (ti.bm * ti.bn <= 128 * 128 ? 2 : 1);  // resident blocks
+  const double t_tile = 2.0 * ti.bm * ti.bn * (double)s->P / 3.0e12;  // s, per CU
+  const double t_part = (double)M * N * 8.0 / 4.0e12;                  // s, per split
+  const long maxs = std::max(1L, (long)(s->P / (4 * ti.bk)));          // >= 4 K-steps each
+  long best = 1;
+  double best_t = 1e30;
+  for (long sp = 1; sp <= std::min(maxs, 256L); ++sp) {
+    const long rounds = (tiles * sp + slots - 1) / slots;
+    const double t = rounds * t_tile / sp + sp * t_part;
+    if (t < best_t * 0.999) {
+      best_t = t;
+      best = sp;
+    }
+  }
+  long kc = (s->P + best - 1) / best;
   kc = (kc + ti.bk - 1) / ti.bk * ti.bk;
   kchunk = (int)kc;
   // the kernel derives the split count from the grid: keep it exact
-  const long used = (s->P + kc - 1) / kc;
-  return (int)(splits % 8 == 0 && used != splits ? splits : used);
+  return (int)((s->P + kc - 1) / kc);
 }
 
 int env_int(const char* name, int dflt) {
@@ -292,8 +308,8 @@ pulse_status build_layout(pulse_stage* s) {
     s->v2 = env_int("PULSE_GEMM_V1", 0) == 0;
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
     if (s->v2) {
-      s->conv_tile_force = (ct >= TILE2_C128x320 && ct <= TILE2_C256x128) ? ct : -1;
-      s->wgrad_tile_force = (wt >= TILE2_W320x192 && wt <= TILE2_W128x128) ? wt : -1;
+      s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
+      s->wgrad_tile_force = (wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
     } else {
       s->conv_tile_force = (ct >= 0 && ct <= TILE_160x160) ? ct : -1;
       s->wgrad_tile_force = (wt >= 0 && wt <= TILE_160x160) ? wt : -1;
