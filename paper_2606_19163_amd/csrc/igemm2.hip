@@ -19,6 +19,8 @@
 //    lanes 4q + j/4, q = 0..3.  B columns may mix sources within one tile, so
 //    its DMA uses per-lane global addresses; invalid elements point at a
 //    zeroed 16-byte word.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -78,6 +80,44 @@ struct CfgC {
   static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
 };
 
+// Weight-gradient tiles are pixel-major rows of P bytes.  Row r is stored
+// rotated by rot(r) = a (r & 3) + b ((r >> 3) & 1) units of 32 bytes (16
+// channels), chosen so that each half-wave of a transpose read (rows
+// {0..3, 8..11} or {16..19, 24..27} of a 32-row slice, 32 bytes per row) hits
+// 8 distinct 32-byte bank groups of the 64-bank LDS.
+constexpr int rot_conflicts(int P, int a, int b) {
+  const int U = P / 32;
+  int bad = 0;
+  for (int s = 0; s < 2; ++s)
+    for (int h = 0; h < 2; ++h)
+      for (int hw = 0; hw < 2; ++hw)
+        for (int u = 0; u < U; ++u) {
+          int seen = 0;
+          for (int g = 2 * hw; g < 2 * hw + 2; ++g)
+            for (int q = 0; q < 4; ++q) {
+              const int r = 32 * s + 4 * h + 8 * g + q;
+              const int grp = (r * U + (u + a * (r & 3) + b * ((r >> 3) & 1)) % U) % 8;
+              if ((seen >> grp) & 1) ++bad;
+              seen |= 1 << grp;
+            }
+        }
+  return bad;
+}
+constexpr int best_rot(int P) {  // a + 256 * b of the first conflict-free pair
+  const int U = P / 32;
+  int best = 0, best_bad = 1 << 30;
+  for (int a = 0; a < U; ++a)
+    for (int b = 0; b < U; ++b) {
+      const int bad = rot_conflicts(P, a, b);
+      if (bad < best_bad) {
+        best_bad = bad;
+        best = a + 256 * b;
+      }
+      if (bad == 0) return best;
+    }
+  return best;
+}
+
 template <int BM_, int BN_, int WM_, int WN_>
 struct CfgW {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64;
@@ -91,16 +131,16 @@ struct CfgW {
   static constexpr int WLA = A_BYTES / 1024, WLB = B_BYTES / 1024, WL = WLA + WLB;
   static constexpr int NU = WL / NW;
   static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
-  // transpose reads touch 4 consecutive rows: pitches that repeat every
-  // 256 or 128 bytes need the rows' chunk pairs moved apart
-  static constexpr bool SWA = (PA % 256 == 0 || PA % 256 == 128) && CA % 8 == 0;
-  static constexpr bool SWB = (PB % 256 == 0 || PB % 256 == 128) && CB % 8 == 0;
+  static constexpr int RA = best_rot(PA), RB = best_rot(PB);
+  static constexpr int RA_A = RA % 256, RA_B = RA / 256, RB_A = RB % 256, RB_B = RB / 256;
   static constexpr int LDC = BN + 4;
   static_assert(16 * LDC * 4 <= STAGE, "epilogue slice must fit one stage");
   static_assert(2 * STAGE <= 160 * 1024, "LDS");
   static_assert(WL % NW == 0 && WLA % NW == 0 && (BK * PA) % 1024 == 0 &&
                     (BK * PB) % 1024 == 0,
                 "loads");
+  static_assert(BM % 16 == 0 && BN % 16 == 0, "rows of whole 32-byte units");
+  static_assert(36 * PA < 65536 && A_BYTES + 36 * PB < 65536, "read offsets are immediates");
   static_assert(WM % 16 == 0 && WN % 16 == 0, "tile");
 };
 
@@ -154,6 +194,28 @@ __device__ __forceinline__ void lgkm_wait() {
 // Order a value after the preceding waits: the MFMAs that consume it cannot
 // be scheduled above them.
 __device__ __forceinline__ void tie(bf16x8_t& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void tie(v4s& v) { asm volatile("" : "+v"(v)); }
+
+// ds_read_b64_tr_b16 at addr + OFF (see ds_rd128 for why it is inline asm)
+template <int OFF>
+__device__ __forceinline__ v4s ds_rdtr(uint32_t addr) {
+  v4s v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+
+// 16-byte chunk slot of logical chunk lc in row r of a rotated tile (C
+// chunks per row, rotation a (r & 3) + b ((r >> 3) & 1) units of 2 chunks)
+__device__ __forceinline__ int rot_slot(int lc, int r, int C, int a, int b) {
+  int p = lc + 2 * (a * (r & 3) + b * ((r >> 3) & 1));
+  while (p >= C) p -= C;
+  return p;
+}
+__device__ __forceinline__ int rot_logical(int pc, int r, int C, int a, int b) {
+  int p = pc - 2 * (a * (r & 3) + b * ((r >> 3) & 1));
+  while (p < 0) p += C;
+  return p;
+}
 
 struct SegRt {
   __amdgpu_buffer_rsrc_t r0, r1;
@@ -467,9 +529,9 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   const uint32_t gpitch = (uint32_t)(a.gy.s0.C * 2);
 
   // Per wave load u: A loads (wl < WLA) fetch dY rows; B loads fetch the
-  // shifted activation columns through per-lane addresses.
-  // A: slot q -> pixel row q / CA, chunk (q % CA) ^ swz -> channel offset.
-  // B: slot q -> pixel row q / CB, column chunk -> (segment, tap, channel).
+  // shifted activation columns through per-lane addresses.  Lane slot q of
+  // a load is physical chunk q % C of pixel row q / C; it fetches the
+  // logical chunk the row's rotation puts there.
   int rrow[C::NU];          // pixel row of the tile
   uint32_t aoff[C::NU];     // A: channel byte offset in dY, or OOB
   const char* bsrc[C::NU];  // B: source pointer at the column's channel
@@ -486,16 +548,14 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
     if (u < C::UA) {
       const int q = wl * 64 + lane;
       const int r = q / C::CA;
-      const int pc = q - r * C::CA;
-      const int lc = C::SWA ? (pc ^ (2 * (r & 3))) : pc;
+      const int lc = rot_logical(q - r * C::CA, r, C::CA, C::RA_A, C::RA_B);
       rrow[u] = r;
       const int o = m0 + lc * 8;
       aoff[u] = o < a.M ? (uint32_t)(o * 2) : OOB;
     } else {
       const int q = (wl - C::WLA) * 64 + lane;
       const int r = q / C::CB;
-      const int pc = q - r * C::CB;
-      const int lc = C::SWB ? (pc ^ (2 * (r & 3))) : pc;
+      const int lc = rot_logical(q - r * C::CB, r, C::CB, C::RB_A, C::RB_B);
       rrow[u] = r;
       const int n = n0 + lc * 8;
       if (n < a.N) {
@@ -556,71 +616,75 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Transpose reads: lane (g16, j16) addresses pixel row
+  // trow = 8 g16 + j16 / 4 (+ 32 s + 4 h) and channel 4 (j16 % 4) of a
+  // fragment's 16 columns.  Row bits 0-1 and 3 are fixed per lane, so the
+  // rotation and hence each fragment's column byte offset is too; the row
+  // step (s, h) is an immediate.
   const int g16 = lane >> 4;
   const int j16 = lane & 15;
-  // transpose-read address of lane (g16, j16): pixel row 8*g16 + 4*h + j16/4
-  // of the 32-pixel slice, channel 4*(j16%4) of the fragment's 16 columns
   const int trow = 8 * g16 + (j16 >> 2);
   const int tcol = 4 * (j16 & 3);
+  uint32_t ra[C::TM], rb[C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i) {
+    const int col = wm * C::WM + i * 16 + tcol;
+    ra[i] = (uint32_t)(trow * C::PA + rot_slot(col >> 3, trow, C::CA, C::RA_A, C::RA_B) * 16 +
+                       (col & 7) * 2);
+  }
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int col = wn * C::WN + j * 16 + tcol;
+    rb[j] = (uint32_t)(trow * C::PB + rot_slot(col >> 3, trow, C::CB, C::RB_A, C::RB_B) * 16 +
+                       (col & 7) * 2);
+  }
+  const uint32_t sbase = lds_u32(smem);
 
   bf16x8_t af[2][C::TM], bfr[2][C::TN];
-  auto read = [&](const char* As) __attribute__((always_inline)) {
-    const char* Bs = As + C::A_BYTES;
+  auto read = [&](uint32_t sb, bf16x8_t (&fa)[C::TM], bf16x8_t (&fb)[C::TN], auto s_tag)
+      __attribute__((always_inline)) {
+    constexpr int S = decltype(s_tag)::value;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int i = 0; i < C::TM; ++i) {
+      const v4s lo = ds_rdtr<(S * 32 + 0) * C::PA>(sb + ra[i]);
+      const v4s hi = ds_rdtr<(S * 32 + 4) * C::PA>(sb + ra[i]);
+      fa[i] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
 #pragma unroll
-      for (int i = 0; i < C::TM; ++i) {
-        const int col = wm * C::WM + i * 16 + tcol;
-        v4s h2[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int r = s * 32 + trow + 4 * h;
-          const int lc = col >> 3;
-          const int pc = C::SWA ? (lc ^ (2 * (r & 3))) : lc;
-          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s*)(As + r * C::PA + pc * 16 + (col & 7) * 2));
-        }
-        af[s][i] = __builtin_bit_cast(bf16x8_t,
-                                      __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-      }
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int col = wn * C::WN + j * 16 + tcol;
-        v4s h2[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int r = s * 32 + trow + 4 * h;
-          const int lc = col >> 3;
-          const int pc = C::SWB ? (lc ^ (2 * (r & 3))) : lc;
-          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s*)(Bs + r * C::PB + pc * 16 + (col & 7) * 2));
-        }
-        bfr[s][j] = __builtin_bit_cast(bf16x8_t,
-                                       __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-      }
+    for (int j = 0; j < C::TN; ++j) {
+      const v4s lo = ds_rdtr<C::A_BYTES + (S * 32 + 0) * C::PB>(sb + rb[j]);
+      const v4s hi = ds_rdtr<C::A_BYTES + (S * 32 + 4) * C::PB>(sb + rb[j]);
+      fb[j] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     }
   };
-  auto mma = [&]() __attribute__((always_inline)) {
+  auto mma = [&](bf16x8_t (&fa)[C::TM], bf16x8_t (&fb)[C::TN]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int i = 0; i < C::TM; ++i) tie(fa[i]);
 #pragma unroll
-      for (int i = 0; i < C::TM; ++i)
+    for (int j = 0; j < C::TN; ++j) tie(fb[j]);
 #pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] =
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
 
-  // same pipeline as the conv kernel: wait, read the stage, start the next
-  // stage's DMA, MFMAs
+  // Per K-step: wait for the stage, barrier, read the first 32 pixels'
+  // fragments, start the next stage's DMA, then the second half's reads
+  // overlap the first half's MFMAs.
   const int KT = (int)((pend - pbeg + C::BK - 1) / C::BK);
   if (KT > 0) issue(0, smem);
   for (int kt = 0; kt < KT; ++kt) {
     wait_vmcnt<0>();
-    __syncthreads();
-    read(smem + (kt & 1) * C::STAGE);
+    __builtin_amdgcn_s_barrier();
+    const uint32_t sb = sbase + (uint32_t)((kt & 1) * C::STAGE);
+    read(sb, af[0], bfr[0], std::integral_constant<int, 0>());
     if (kt + 1 < KT) issue(kt + 1, smem + ((kt + 1) & 1) * C::STAGE);
-    mma();
+    lgkm_wait<0>();
+    read(sb, af[1], bfr[1], std::integral_constant<int, 1>());
+    mma(af[0], bfr[0]);
+    lgkm_wait<0>();
+    mma(af[1], bfr[1]);
   }
   __syncthreads();
 
