@@ -19,6 +19,7 @@
 //    lanes 4q + j/4, q = 0..3.  B columns may mix sources within one tile, so
 //    its DMA uses per-lane global addresses; invalid elements point at a
 //    zeroed 16-byte word.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -286,14 +287,21 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
+  // block -> (K split, tile), split-major over a contiguous range per XCD
+  const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
+  const long P = a.g.pixels();
   const int tilesN = (a.N + C::BN - 1) / C::BN;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int ntiles = (int)((P + C::BM - 1) / C::BM) * tilesN;
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int z = lb / ntiles;
+  const int bid = lb - z * ntiles;
   const int tn = bid % tilesN;
   const int tm = bid / tilesN;
   const long m0 = (long)tm * C::BM;
   const int n0 = tn * C::BN;
-  const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
-  const long P = a.g.pixels();
+  const int KT_ALL = a.K / C::BK;
+  const int kt0 = z * a.ksteps;
+  const int KT = min(KT_ALL, kt0 + a.ksteps) - kt0;  // K-steps of this block
 
   // this lane's wave loads: wl = wave + u * NW; A rows first, then B rows.
   // Lane (row rl = lane / 8 of the load, slot lane % 8) fetches logical chunk
@@ -338,8 +346,20 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // K position of the next stage to issue: segment, tap (dy, dx) and
   // channel, advanced by BK channels per stage without divisions
   SegRt cur = seg_rt(a.seg[0], P);
-  int iseg = 0, itap = 0, icb = 0, idy = cur.taps == 9 ? -1 : 0, idx = idy;
-  uint32_t kbyte = 0;
+  int iseg = 0, itap = 0, icb = 0, idy, idx;
+  uint32_t kbyte = (uint32_t)(kt0 * C::BK * 2);
+  {
+    int kk = kt0 * C::BK;  // first K index of this split
+    while (iseg < 2 && kk >= cur.taps * cur.C) {
+      kk -= cur.taps * cur.C;
+      ++iseg;
+      select_into(cur, iseg == 1, q1, q2);
+    }
+    itap = kk / cur.C;
+    icb = kk - itap * cur.C;
+    idy = cur.taps == 9 ? itap / 3 - 1 : 0;
+    idx = cur.taps == 9 ? itap % 3 - 1 : 0;
+  }
   auto advance = [&]() __attribute__((always_inline)) {
     kbyte += C::BK * 2;
     icb += C::BK;
@@ -406,7 +426,6 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // of the stage STAGES-1 ahead into the slot read one step ago, then the
   // MFMAs of each K-half once its fragments have landed.
   bf16x8_t af[2][C::TM], bfr[2][C::TN];
-  const int KT = a.K / C::BK;
   issue(0);
   if (C::STAGES == 3 && KT > 1) issue(C::STAGE);
   int slot = 0;
@@ -469,6 +488,12 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         const float* src = ct + row * C::LDC + (n - n0);
         const float4 s0 = reinterpret_cast<const float4*>(src)[0];
         const float4 s1 = reinterpret_cast<const float4*>(src)[1];
+        if (a.ksplit > 1) {  // raw partial; the finalize adds the epilogue terms
+          float4* dp = reinterpret_cast<float4*>(a.part + ((long)z * P + m) * a.N + n);
+          dp[0] = s0;
+          dp[1] = s1;
+          continue;
+        }
         float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
         if (a.bias) {
 #pragma unroll
@@ -716,6 +741,55 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
 }
 
 // ---------------------------------------------------------------------------
+// K-split conv finalize: out = sum_z part[z] (fixed order) + bias + rowvec +
+// residual, one 8-channel vector per thread
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void conv_splitk_finalize(GemmArgs a) {
+  const long P = a.g.pixels();
+  const int NV = a.N / 8;
+  const int HW = a.g.H * a.g.W;
+  const long total = P * NV;
+  const long zs = P * a.N;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long)gridDim.x * blockDim.x) {
+    const long m = i / NV;
+    const int n = (int)(i - m * NV) * 8;
+    const float* src = a.part + m * a.N + n;
+    float v[8];
+    {
+      const float4 s0 = reinterpret_cast<const float4*>(src)[0];
+      const float4 s1 = reinterpret_cast<const float4*>(src)[1];
+      v[0] = s0.x; v[1] = s0.y; v[2] = s0.z; v[3] = s0.w;
+      v[4] = s1.x; v[5] = s1.y; v[6] = s1.z; v[7] = s1.w;
+    }
+    for (int zz = 1; zz < a.ksplit; ++zz) {
+      const float4 s0 = reinterpret_cast<const float4*>(src + zz * zs)[0];
+      const float4 s1 = reinterpret_cast<const float4*>(src + zz * zs)[1];
+      v[0] += s0.x; v[1] += s0.y; v[2] += s0.z; v[3] += s0.w;
+      v[4] += s1.x; v[5] += s1.y; v[6] += s1.z; v[7] += s1.w;
+    }
+    if (a.bias) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
+    }
+    if (a.rowvec) {
+      const float* rv = a.rowvec + (m / HW) * a.N + n;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += rv[q];
+    }
+    if (a.resid.s0.ptr) {
+      float rr[8];
+      ld8(a.resid.s0, m, n, rr);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += rr[q];
+    }
+    st8(a.out, a.out_dtype, a.ldo, m, n, v);
+    if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 
@@ -734,7 +808,14 @@ template <class C>
 static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
   const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL(igemm2_conv<C>, dim3((unsigned)(tilesM * tilesN)), dim3(C::NT), 0, st, a);
+  const int ks = a.ksplit > 1 ? a.ksplit : 1;
+  hipLaunchKernelGGL(igemm2_conv<C>, dim3((unsigned)(tilesM * tilesN * ks)), dim3(C::NT), 0, st,
+                     a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ks == 1) return e;
+  const long vec = a.g.pixels() * (a.N / 8);
+  const long blocks = std::min<long>((vec + 255) / 256, 2048);
+  hipLaunchKernelGGL(conv_splitk_finalize, dim3((unsigned)blocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -38,10 +38,13 @@ struct GemmArgs {
   void* out2;          // optional second copy of out
   int out_dtype;
   int ldo;
+  int ksplit;          // K splits (conv mode, LDS-DMA path): > 1 writes fp32
+  int ksteps;          // partials to part and a finalize applies the epilogue;
+                       // ksteps = K-steps per split
   // WGRAD mode
   VIn gy;              // output gradient, M channels
   int kchunk;          // pixels per split
-  float* part;         // [splits][M][N] fp32 partials
+  float* part;         // [splits][M][N] fp32 partials (both modes)
 };
 
 // implicit GEMM (igemm.hip): tile shapes (block M x block N; bf16, 64

@@ -223,6 +223,19 @@ TileInfo info_of(const pulse_stage* s, int tile) {
   return uses_v2(s) ? tile2_info(tile) : tile_info(tile);
 }
 
+// K splits of a conv-mode GEMM on the LDS-DMA path: enough blocks for two
+// per CU (the tile's occupancy), each split keeping at least 4 K-steps.
+int conv_ksplit(const pulse_stage* s, int tile, int N, int K) {
+  if (!uses_v2(s)) return 1;
+  const TileInfo ti = info_of(s, tile);
+  const long tiles = ((s->P + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
+  const long want = 512;
+  if (tiles >= want) return 1;
+  long ks = (want + tiles - 1) / tiles;
+  ks = std::min(ks, std::max(1L, (long)(K / ti.bk) / 4));
+  return (int)std::min(ks, 16L);
+}
+
 // Pixel split of a weight-gradient GEMM.  With s splits the grid holds
 // tiles * s blocks of K / s pixels each; blocks run in ceil(tiles * s /
 // slots) rounds, and every split adds an fp32 partial of M x N that is
@@ -377,6 +390,9 @@ pulse_status build_layout(pulse_stage* s) {
       for (int c : {b.cin, b.cout}) {
         RedGrid rg = red_grid(s->geo, c);
         red = std::max(red, (size_t)s->geo.B * rg.chunks * 2 * c);
+        // conv-mode K-split partials (an upper bound over the K of each launch)
+        const int ks = conv_ksplit(s, conv_tile(s, c), c, 1 << 30);
+        if (ks > 1) part = std::max(part, (size_t)ks * s->P * c);
       }
     }
   s->part_cap = part;
@@ -557,6 +573,17 @@ double conv_bytes(const pulse_stage* s, const GemmArgs& a) {
 }
 
 pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
+  const int tile = conv_tile(s, a.N);
+  const int ks = conv_ksplit(s, tile, a.N, a.K);
+  const int kt = a.K / info_of(s, tile).bk;
+  a.ksplit = ks;
+  a.ksteps = (kt + ks - 1) / ks;
+  if (ks > 1) {
+    a.ksplit = (kt + a.ksteps - 1) / a.ksteps;  // no empty split
+    if ((size_t)a.ksplit * a.M * a.N > s->part_cap)
+      return fail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
+    a.part = s->sf(s->s_part);
+  }
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
     e0 = next_event(s);
@@ -564,9 +591,9 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
   if (uses_v2(s))
-    HIPCHK(launch_conv2(a, conv_tile(s, a.N), st));
+    HIPCHK(launch_conv2(a, tile, st));
   else
-    HIPCHK(launch_conv(a, conv_tile(s, a.N), st));
+    HIPCHK(launch_conv(a, tile, st));
   if (s->timing && e0 && e1) {
     HIPCHK(hipEventRecord(e1, st));
     s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K, conv_bytes(s, a)});
