@@ -343,37 +343,38 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.Bw, (long)a.N * a.ldb * 2);
   const uint32_t sbase = lds_u32(smem);
 
-  // K position of the next stage to issue: segment, tap (dy, dx) and
-  // channel, advanced by BK channels per stage without divisions
+  // K position of the next stage to issue: segment, channel chunk and tap
+  // (dy, dx), walked chunk-major (the taps of one 64-channel chunk run back
+  // to back, so the shifted reads of one input slice stay in L2), without
+  // divisions.  The weight column of (tap, channel c) is begin + tap*C + c.
   SegRt cur = seg_rt(a.seg[0], P);
   int iseg = 0, itap = 0, icb = 0, idy, idx;
-  uint32_t kbyte = (uint32_t)(kt0 * C::BK * 2);
   {
-    int kk = kt0 * C::BK;  // first K index of this split
-    while (iseg < 2 && kk >= cur.taps * cur.C) {
-      kk -= cur.taps * cur.C;
+    int q = kt0;  // first K-step of this split
+    while (iseg < 2 && q >= cur.taps * (cur.C / C::BK)) {
+      q -= cur.taps * (cur.C / C::BK);
       ++iseg;
       select_into(cur, iseg == 1, q1, q2);
     }
-    itap = kk / cur.C;
-    icb = kk - itap * cur.C;
+    icb = (q / cur.taps) * C::BK;
+    itap = q - (q / cur.taps) * cur.taps;
     idy = cur.taps == 9 ? itap / 3 - 1 : 0;
     idx = cur.taps == 9 ? itap % 3 - 1 : 0;
   }
   auto advance = [&]() __attribute__((always_inline)) {
-    kbyte += C::BK * 2;
-    icb += C::BK;
-    if (icb >= cur.C) {
-      icb = 0;
-      ++itap;
-      if (++idx > 1) {
-        idx = -1;
-        ++idy;
-      }
-      if (itap >= cur.taps) {
+    ++itap;
+    if (++idx > 1) {
+      idx = -1;
+      ++idy;
+    }
+    if (itap >= cur.taps) {
+      itap = 0;
+      idy = idx = cur.taps == 9 ? -1 : 0;
+      icb += C::BK;
+      if (icb >= cur.C) {
+        icb = 0;
         ++iseg;
         select_into(cur, iseg == 1, q1, q2);
-        itap = 0;
         idy = idx = cur.taps == 9 ? -1 : 0;
       }
     }
@@ -385,6 +386,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     const uint32_t cbyte = (uint32_t)((second ? icb - cur.c0 : icb) * 2);
     const int t9 = (idy + 1) * 3 + idx + 1;
     const int shift = idy * W + idx;
+    const uint32_t kbyte = (uint32_t)((cur.begin + itap * cur.C + icb) * 2);
 #pragma unroll
     for (int u = 0; u < C::NU; ++u) {
       const int wl = wave + u * C::NW;
