@@ -101,13 +101,18 @@ __device__ __forceinline__ void st8(void* ptr, int dtype, int C, long pix, int c
   }
 }
 
-__device__ __forceinline__ float silu_f(float z) {
-  return z / (1.0f + __expf(-z));
+// sigmoid(z) = 1 / (1 + e^-z) with the hardware reciprocal (v_rcp_f32,
+// 1 ulp) in place of a correctly rounded division; e^-z overflowing to
+// +inf gives exactly 0
+__device__ __forceinline__ float sigmoid_f(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
 }
+
+__device__ __forceinline__ float silu_f(float z) { return z * sigmoid_f(z); }
 
 // d SiLU(z)/dz
 __device__ __forceinline__ float dsilu_f(float z) {
-  const float s = 1.0f / (1.0f + __expf(-z));
+  const float s = sigmoid_f(z);
   return s * (1.0f + z * (1.0f - s));
 }
 
