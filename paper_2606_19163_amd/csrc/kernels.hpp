@@ -122,10 +122,9 @@ hipError_t launch_gn_bwd_partial(const Src& da, const VIn& x, const Geo& g, RedG
                                  const float* rstd, int G, float* partial, hipStream_t st);
 // coef[b][g][2] = (sum_g gamma*dz, sum_g gamma*dz*xhat) / count, and
 // dgamma[c] += sum dz*xhat, dbeta[c] += sum dz.
-// pi: scratch [2][B][C].
 hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                   int G, const float* gamma, float* coef, float* dgamma,
-                                  float* dbeta, float* pi, hipStream_t st);
+                                  float* dbeta, hipStream_t st);
 
 struct GnBwdOut {
   void* dst0;      // channels [0, c_split): stride c_split
@@ -146,12 +145,13 @@ hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGri
 // partial[b][chunk][0][c] = sum over the chunk of v (v may carry an addend).
 hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st);
-// pi[s][b][c] = sum_chunk partial[b][chunk][s][c] for s < nslot (pi: [nslot][B][C]);
-// then acc0[c] += sum_b pi[0][b][c], dup[c] += the same, acc1[c] += sum_b
-// pi[1][b][c] (each may be null).
-hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
-                                    int nslot, float* pi, float* acc0, float* dup, float* acc1,
-                                    hipStream_t st);
+// pi[s][b][c] = sum_chunk partial[b][chunk][s][c] for s < nslot (pi: [nslot][B][C]).
+hipError_t launch_chan_per_image(const float* partial, const Geo& g, RedGrid rg, int C,
+                                 int nslot, float* pi, hipStream_t st);
+// acc0 (and dup) += sum of slot 0, acc1 += sum of slot 1 over every image and
+// chunk, in one pass (no per-image sums)
+hipError_t launch_chan_totals(const float* partial, const Geo& g, RedGrid rg, int C, int nslot,
+                              float* acc0, float* dup, float* acc1, hipStream_t st);
 
 // ---- timestep embedding, weights, copies (misc.hip) ----------------------
 

@@ -250,32 +250,6 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
   lane_reduce_store<16>(acc, sm, rg, r.active, base + r.c, base + x.C + r.c);
 }
 
-// one block per (image, group): coef = (sum gamma*dz, sum gamma*dz*xhat) / count
-__global__ __launch_bounds__(256) void k_gn_bwd_coef(const float* partial, Geo g, RedGrid rg,
-                                                     int C, int G, const float* gamma,
-                                                     float* coef) {
-  __shared__ double sm[512];
-  const int b = blockIdx.x, gi = blockIdx.y;
-  const int cg = C / G;
-  double S1 = 0.0, S2 = 0.0;
-  for (int i = threadIdx.x; i < rg.chunks * cg; i += 256) {
-    const int ch = i / cg;
-    const int c = gi * cg + (i - ch * cg);
-    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
-    S1 += (double)gamma[c] * base[c];
-    S2 += (double)gamma[c] * base[C + c];
-  }
-  block_sum2(S1, S2, sm);
-  if (threadIdx.x == 0) {
-    const double cnt = (double)g.hw() * cg;
-    coef[(b * G + gi) * 2 + 0] = (float)(S1 / cnt);
-    coef[(b * G + gi) * 2 + 1] = (float)(S2 / cnt);
-  }
-}
-
-// Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
-// partial[b][chunk][s][c] for the first `nslot` slots.  Block (64 channels,
-// 4 chunk lanes) per (channel block, image).
 // Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
 // partial[b][chunk][s][c] for the first `nslot` slots.  A block holds 64
 // channels x 4 chunk lanes of one image; each lane keeps four loads in
@@ -329,19 +303,110 @@ __global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, in
   }
 }
 
-// acc0[c] += sum_b pi[0][b][c] (and dup[c]); acc1[c] += sum_b pi[1][b][c]
-__global__ void k_chan_total(const float* pi, int B, int C, float* acc0, float* dup,
-                             float* acc1) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  float t0 = 0.f, t1 = 0.f;
-  for (int b = 0; b < B; ++b) {
-    t0 += pi[(long)b * C + c];
-    if (acc1) t1 += pi[(long)(B + b) * C + c];
+// Channel totals over every image and chunk in one pass: slot 0 is added to
+// acc0 (and dup), slot 1 to acc1.  A 1024-thread block holds 16 channels x
+// 64 row lanes; lane y sums the (image, chunk) rows y, y+64, ... and the
+// lanes meet in a fixed LDS tree.
+constexpr int TX = 16, TY = 64;
+
+__device__ __forceinline__ void chan_totals_block(const float* partial, int rows, int C,
+                                                  int nslot, int cblock, float* acc0,
+                                                  float* dup, float* acc1,
+                                                  float (&sm)[2][TY][TX]) {
+  const int tx = threadIdx.x % TX, ty = threadIdx.x / TX;
+  const int c = cblock * TX + tx;
+  float s0 = 0.f, s1 = 0.f;
+  if (c < C) {
+    const long stride = 2L * C;
+    const float* base = partial + c;
+    int i = ty;
+    for (; i + TY < rows; i += 2 * TY) {
+      const float a0 = base[i * stride], a1 = base[(i + TY) * stride];
+      const float e0 = nslot > 1 ? base[i * stride + C] : 0.f;
+      const float e1 = nslot > 1 ? base[(i + TY) * stride + C] : 0.f;
+      s0 += a0;
+      s0 += a1;
+      s1 += e0;
+      s1 += e1;
+    }
+    for (; i < rows; i += TY) {
+      s0 += base[i * stride];
+      if (nslot > 1) s1 += base[i * stride + C];
+    }
   }
-  if (acc0) acc0[c] += t0;
-  if (dup) dup[c] += t0;
-  if (acc1) acc1[c] += t1;
+  sm[0][ty][tx] = s0;
+  sm[1][ty][tx] = s1;
+  __syncthreads();
+  for (int off = TY / 2; off > 0; off >>= 1) {
+    if (ty < off) {
+      sm[0][ty][tx] += sm[0][ty + off][tx];
+      sm[1][ty][tx] += sm[1][ty + off][tx];
+    }
+    __syncthreads();
+  }
+  if (ty == 0 && c < C) {
+    if (acc0) acc0[c] += sm[0][0][tx];
+    if (dup) dup[c] += sm[0][0][tx];
+    if (acc1) acc1[c] += sm[1][0][tx];
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_chan_totals(const float* partial, int rows, int C,
+                                                      int nslot, float* acc0, float* dup,
+                                                      float* acc1) {
+  __shared__ float sm[2][TY][TX];
+  chan_totals_block(partial, rows, C, nslot, blockIdx.x, acc0, dup, acc1, sm);
+}
+
+// Fixed-order sum of two fp64 values over a 1024-thread block.
+__device__ __forceinline__ void block_sum2_1k(double& a, double& b, double* sm) {
+  const int t = threadIdx.x;
+  sm[t] = a;
+  sm[1024 + t] = b;
+  __syncthreads();
+  for (int off = 512; off > 0; off >>= 1) {
+    if (t < off) {
+      sm[t] += sm[t + off];
+      sm[1024 + t] += sm[1024 + t + off];
+    }
+    __syncthreads();
+  }
+  a = sm[0];
+  b = sm[1024];
+}
+
+// GroupNorm backward finalize in one launch of 1024-thread blocks: blocks
+// [0, ceil(C/16)) add dbeta (sum dz) and dgamma (sum dz * xhat) over every
+// image and chunk; the remaining B*G blocks each reduce one (image, group)
+// to coef = (sum gamma*dz, sum gamma*dz*xhat) / count.
+__global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, Geo g,
+                                                          RedGrid rg, int C, int G,
+                                                          const float* gamma, float* coef,
+                                                          float* dgamma, float* dbeta) {
+  __shared__ float smc[2][TY][TX];
+  __shared__ double sm[2048];
+  const int nchb = (C + TX - 1) / TX;
+  if ((int)blockIdx.x < nchb) {
+    chan_totals_block(partial, g.B * rg.chunks, C, 2, blockIdx.x, dbeta, nullptr, dgamma, smc);
+    return;
+  }
+  const int q = blockIdx.x - nchb;
+  const int b = q / G, gi = q - b * G;
+  const int cg = C / G;
+  double S1 = 0.0, S2 = 0.0;
+  for (int i = threadIdx.x; i < rg.chunks * cg; i += 1024) {
+    const int ch = i / cg;
+    const int c = gi * cg + (i - ch * cg);
+    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+    S1 += (double)gamma[c] * base[c];
+    S2 += (double)gamma[c] * base[C + c];
+  }
+  block_sum2_1k(S1, S2, sm);
+  if (threadIdx.x == 0) {
+    const double cnt = (double)g.hw() * cg;
+    coef[(b * G + gi) * 2 + 0] = (float)(S1 / cnt);
+    coef[(b * G + gi) * 2 + 1] = (float)(S2 / cnt);
+  }
 }
 
 __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
@@ -498,13 +563,18 @@ hipError_t launch_gn_bwd_partial(const Src& da, const VIn& x, const Geo& g, RedG
 
 hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                   int G, const float* gamma, float* coef, float* dgamma,
-                                  float* dbeta, float* pi, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_coef, dim3(g.B, G), dim3(256), 0, st, partial, g, rg, C, G, gamma,
-                     coef);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // dbeta from slot 0 (sum dz), dgamma from slot 1 (sum dz * xhat)
-  return launch_chan_sum_finalize(partial, g, rg, C, 2, pi, dbeta, nullptr, dgamma, st);
+                                  float* dbeta, hipStream_t st) {
+  const int nchb = (C + TX - 1) / TX;
+  hipLaunchKernelGGL(k_gn_bwd_finalize, dim3(nchb + g.B * G), dim3(1024), 0, st, partial, g, rg,
+                     C, G, gamma, coef, dgamma, dbeta);
+  return hipGetLastError();
+}
+
+hipError_t launch_chan_totals(const float* partial, const Geo& g, RedGrid rg, int C, int nslot,
+                              float* acc0, float* dup, float* acc1, hipStream_t st) {
+  hipLaunchKernelGGL(k_chan_totals, dim3((C + TX - 1) / TX), dim3(1024), 0, st, partial,
+                     g.B * rg.chunks, C, nslot, acc0, dup, acc1);
+  return hipGetLastError();
 }
 
 hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
@@ -523,15 +593,10 @@ hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float
   return hipGetLastError();
 }
 
-hipError_t launch_chan_sum_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
-                                    int nslot, float* pi, float* acc0, float* dup, float* acc1,
-                                    hipStream_t st) {
+hipError_t launch_chan_per_image(const float* partial, const Geo& g, RedGrid rg, int C,
+                                 int nslot, float* pi, hipStream_t st) {
   hipLaunchKernelGGL(k_chan_per_image, dim3((C + VX - 1) / VX, g.B), dim3(VX, PY), 0, st,
                      partial, rg.chunks, g.B, C, nslot, pi);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || (!acc0 && !dup && !acc1)) return e;
-  hipLaunchKernelGGL(k_chan_total, dim3((C + 255) / 256), dim3(256), 0, st, pi, g.B, C, acc0,
-                     dup, acc1);
   return hipGetLastError();
 }
 

@@ -712,8 +712,7 @@ pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& 
   const float* scale = reinterpret_cast<const float*>(row + g.scale);
   const float* shift = reinterpret_cast<const float*>(row + g.shift);
   HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
-  HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta,
-                                s->sf(s->s_pi), st));
+  HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta, st));
   GnBwdOut oo = o;
   if (oo.chan_partial) oo.chan_partial = red;  // reuse: the partials above are consumed
   HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, oo,
@@ -788,9 +787,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   {
     const RedGrid rg = red_grid(s->geo, b.cout);
     HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, s->sf(s->s_red), st));
-    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, 1, s->sf(s->s_pi),
-                                    s->gp(b.b2), b.conv_sc ? s->gp(b.bs) : nullptr, nullptr,
-                                    st));
+    HIPCHK(launch_chan_totals(s->sf(s->s_red), s->geo, rg, b.cout, 1, s->gp(b.b2),
+                              b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, st));
   }
   // weight gradients of conv2 and the shortcut, one GEMM
   const VIn a2v = vin1(row + b.a2, dt, b.cout);
@@ -831,8 +829,7 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
       return ps;
     const RedGrid rg = red_grid(s->geo, b.cout);
     float* de = s->sf(s->s_pi);  // per-image sums of dh1: [B][cout]
-    HIPCHK(launch_chan_sum_finalize(s->sf(s->s_red), s->geo, rg, b.cout, 1, de, nullptr, nullptr,
-                                    nullptr, st));
+    HIPCHK(launch_chan_per_image(s->sf(s->s_red), s->geo, rg, b.cout, 1, de, st));
     HIPCHK(launch_temb_bwd(de, row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
                            s->gp(b.Wl), s->gp(b.bl), s->gp(b.b1), dtemb, st));
   }
