@@ -220,10 +220,10 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
   if (r.active) {
     GnConst k;
     load_gn_const(k, r.b, r.c, x.C, G, scale, shift, mean, rstd);
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += 2 * rg.py) {
-      float f[2][8], d[2][8];
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
+      float f[1][8], d[1][8];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < 1; ++u) {
         const int pu = p + u * rg.py;
         if (pu < r.p1) {
           const long pix = (long)r.b * g.hw() + pu;
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
         }
       }
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
+      for (int u = 0; u < 1; ++u)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float z = f[u][j] * k.sc[j] + k.sh[j];
@@ -409,12 +409,16 @@ __global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, 
   }
 }
 
+// CHAN: the output's per-chunk channel sums are written (the timestep-
+// embedding gradient); ADD: the addends add0/add1 exist.  Each instance keeps
+// only the registers it needs.
+template <bool CHAN, bool ADD>
 __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
                                                       RedGrid rg, const float* scale,
                                                       const float* shift, const float* mean,
                                                       const float* rstd, const float* gamma,
                                                       const float* coef, int G, GnBwdOut o) {
-  __shared__ float sm[256 * 8];
+  __shared__ float sm[CHAN ? 256 * 8 : 1];
   const Range r = block_range(g, rg, x.C);
   const int C = x.C;
   const int cg = C / G;
@@ -422,26 +426,39 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   if (r.active) {
-    GnConst k;
-    load_gn_const(k, r.b, r.c, C, G, scale, shift, mean, rstd);
-    float ga[8], c0[8], c1[8];
-    load8f(gamma + r.c, ga);
-    if (cg == 4 || cg >= 8) {  // the 8 channels touch at most two groups
-      const int g0 = r.c / cg, g1 = (r.c + 7) / cg;
-      const float2 e0 = reinterpret_cast<const float2*>(coef)[r.b * G + g0];
-      const float2 e1 = reinterpret_cast<const float2*>(coef)[r.b * G + g1];
+    // out = rstd * (gamma * dz - c0 - xhat * c1) with xhat = (x - mean) * rstd,
+    // folded per channel into out = A dz + Bq x + Cq (fewer live registers)
+    float sc[8], sh[8], A[8], Bq[8], Cq[8];
+    {
+      GnConst k;
+      load_gn_const(k, r.b, r.c, C, G, scale, shift, mean, rstd);
+      float ga[8], c0[8], c1[8];
+      load8f(gamma + r.c, ga);
+      if (cg == 4 || cg >= 8) {  // the 8 channels touch at most two groups
+        const int g0 = r.c / cg, g1 = (r.c + 7) / cg;
+        const float2 e0 = reinterpret_cast<const float2*>(coef)[r.b * G + g0];
+        const float2 e1 = reinterpret_cast<const float2*>(coef)[r.b * G + g1];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const bool first = (r.c + j) / cg == g0;
-        c0[j] = first ? e0.x : e1.x;
-        c1[j] = first ? e0.y : e1.y;
+        for (int j = 0; j < 8; ++j) {
+          const bool first = (r.c + j) / cg == g0;
+          c0[j] = first ? e0.x : e1.x;
+          c1[j] = first ? e0.y : e1.y;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float2 e = reinterpret_cast<const float2*>(coef)[r.b * G + (r.c + j) / cg];
+          c0[j] = e.x;
+          c1[j] = e.y;
+        }
       }
-    } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float2 e = reinterpret_cast<const float2*>(coef)[r.b * G + (r.c + j) / cg];
-        c0[j] = e.x;
-        c1[j] = e.y;
+        sc[j] = k.sc[j];
+        sh[j] = k.sh[j];
+        A[j] = k.rs[j] * ga[j];
+        Bq[j] = -k.rs[j] * k.rs[j] * c1[j];
+        Cq[j] = -k.rs[j] * c0[j] - Bq[j] * k.mu[j];
       }
     }
     for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
@@ -451,18 +468,16 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
       ld8(da, pix, r.c, d);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float z = f[j] * k.sc[j] + k.sh[j];
-        const float dz = d[j] * dsilu_f(z);
-        const float xh = (f[j] - k.mu[j]) * k.rs[j];
-        out[j] = k.rs[j] * (ga[j] * dz - c0[j] - xh * c1[j]);
+        const float dz = d[j] * dsilu_f(f[j] * sc[j] + sh[j]);
+        out[j] = A[j] * dz + (Bq[j] * f[j] + Cq[j]);
       }
-      if (o.add0.s0.ptr) {
+      if (ADD && o.add0.s0.ptr) {
         float e[8];
         ld8v(o.add0, pix, r.c, e);
 #pragma unroll
         for (int j = 0; j < 8; ++j) out[j] += e[j];
       }
-      if (o.add1) {
+      if (ADD && o.add1) {
         const float4* ap = reinterpret_cast<const float4*>(o.add1 + pix * C + r.c);
         const float4 a0 = ap[0], a1 = ap[1];
         out[0] += a0.x; out[1] += a0.y; out[2] += a0.z; out[3] += a0.w;
@@ -472,11 +487,13 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
         st8(o.dst0, o.dtype0, o.c_split, pix, r.c, out);
       else
         st8(o.dst1, o.dtype1, C - o.c_split, pix, r.c - o.c_split, out);
+      if (CHAN) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] += out[j];
+        for (int j = 0; j < 8; ++j) acc[j] += out[j];
+      }
     }
   }
-  if (o.chan_partial) {
+  if (CHAN) {
     float* base = o.chan_partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * C;
     lane_reduce_store<8>(acc, sm, rg, r.active, base + r.c, nullptr);
   }
@@ -581,7 +598,10 @@ hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGri
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
                                int G, const GnBwdOut& o, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_apply, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
+  const bool chan = o.chan_partial != nullptr, add = o.add0.s0.ptr || o.add1;
+  auto kern = chan ? (add ? k_gn_bwd_apply<true, true> : k_gn_bwd_apply<true, false>)
+                   : (add ? k_gn_bwd_apply<false, true> : k_gn_bwd_apply<false, false>);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
                      scale, shift, mean, rstd, gamma, coef, G, o);
   return hipGetLastError();
 }
