@@ -58,28 +58,43 @@ __device__ __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
 
 }  // namespace
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 2>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 2, int BK_ = 64>
 struct CfgC {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = 64, STAGES = STAGES_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = BK_, STAGES = STAGES_;
   static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN, NW = WAVES_M * WAVES_N;
   static constexpr int NT = NW * 64;
   static constexpr int TM = WM / 16, TN = WN / 16;
-  static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+  static constexpr int RB = BK * 2;           // row bytes
+  static constexpr int CPR = RB / 16;         // 16-byte chunks per row
+  static constexpr int RPL = 1024 / RB;       // rows per 1 KB wave load
+  static constexpr int KH = BK / 32;          // MFMA K-steps (32) per stage
+  static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
   static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int WLA = BM / 8, WLB = BN / 8, WL = WLA + WLB;  // 1 KB wave loads
+  static constexpr int WLA = A_BYTES / 1024, WLB = B_BYTES / 1024, WL = WLA + WLB;
   static constexpr int NU = (WL + NW - 1) / NW;  // loads of waves < REM (all when REM == 0)
   static constexpr int REM = WL % NW;
   static constexpr int NU_LO = WL / NW;           // loads of waves >= REM
   static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
   static constexpr int LDC = BN + 4;
-  static_assert(STAGES == 2 || STAGES == 3, "stages");
+  static_assert(BK == 32 || BK == 64, "K-step");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert(16 * LDC * 4 <= STAGES * STAGE, "epilogue slice must fit the stages");
   static_assert(STAGES * STAGE <= 160 * 1024, "LDS");
+  static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "whole wave loads");
   static_assert(WLA % NW == 0, "A wave loads must split evenly over the waves");
-  static_assert(A_BYTES + (TN - 1) * 2048 < 65536, "fragment offsets are 16-bit immediates");
-  static_assert(TM + TN <= 15, "lgkmcnt");
-  static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
+  static_assert(A_BYTES + (TN - 1) * 16 * RB < 65536, "fragment offsets are 16-bit immediates");
+  static_assert(KH * (TM + TN) <= 15 || KH == 2, "lgkmcnt");
+  static_assert(BM % 16 == 0 && BN % 16 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile");
 };
+
+// Row swizzle of conv tiles: chunk c of row r lives in slot c ^ swz(r).  With
+// 128-byte rows, rows r and r+1 fall in opposite halves of the 256-byte bank
+// period and the swizzle separates rows of equal parity; with 64-byte rows,
+// four rows share a period and the swizzle separates rows r and r+4k.
+template <int RB>
+__device__ __forceinline__ int swz_row(int r) {
+  return RB == 128 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+}
 
 // Weight-gradient tiles are pixel-major rows of P bytes.  Row r is stored
 // rotated by rot(r) = a (r & 3) + b ((r >> 3) & 1) units of 32 bytes (16
@@ -314,7 +329,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     pmask[u] = 0;
     coff[u] = OOB;
     if (u < C::UA) {
-      const int r = wl * 8 + (lane >> 3);
+      const int r = wl * C::RPL + lane / C::CPR;
       const long m = m0 + r;
       uint32_t mask = 0;
       if (m < P) {
@@ -330,11 +345,12 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
       }
       ppix[u] = (uint32_t)(m < P ? m : 0);
       pmask[u] = mask;
-      coff[u] = (uint32_t)(((lane & 7) ^ swz128(r)) * 16);
+      coff[u] = (uint32_t)(((lane % C::CPR) ^ swz_row<C::RB>(r)) * 16);
     } else if (wl < C::WL) {
-      const int r = (wl - C::WLA) * 8 + (lane >> 3);
+      const int r = (wl - C::WLA) * C::RPL + lane / C::CPR;
       const int n = n0 + r;
-      coff[u] = n < a.N ? (uint32_t)((long)n * a.ldb * 2 + ((lane & 7) ^ swz128(r)) * 16) : OOB;
+      coff[u] = n < a.N ? (uint32_t)((long)n * a.ldb * 2 + ((lane % C::CPR) ^ swz_row<C::RB>(r)) * 16)
+                        : OOB;
     }
   }
 
@@ -390,7 +406,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
 #pragma unroll
     for (int u = 0; u < C::NU; ++u) {
       const int wl = wave + u * C::NW;
-      char* dst = smem + stage_off + wl * 1024;
+      char* dst = smem + stage_off + wl * 1024;  // 1 KB per wave load
       if (u < C::UA) {
         const uint32_t off = ((pmask[u] >> t9) & 1u)
                                  ? __umul24(ppix[u] + shift, pitch) + cbyte + coff[u]
@@ -414,38 +430,42 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // address per operand and the row step is an immediate offset
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
-  uint32_t fa[2], fb[2];
+  uint32_t fa[C::KH], fb[C::KH];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < C::KH; ++s) {
     const int c = s * 4 + g4;
     const int ra = wm * C::WM + r16, rb = wn * C::WN + r16;
-    fa[s] = (uint32_t)(ra * 128 + ((c ^ swz128(ra)) << 4));
-    fb[s] = (uint32_t)(rb * 128 + ((c ^ swz128(rb)) << 4));
+    fa[s] = (uint32_t)(ra * C::RB + ((c ^ swz_row<C::RB>(ra)) << 4));
+    fb[s] = (uint32_t)(rb * C::RB + ((c ^ swz_row<C::RB>(rb)) << 4));
   }
 
   // Per K-step: wait for this stage's DMA (the later stages stay in
   // flight), barrier, issue every fragment read of the stage, start the DMA
   // of the stage STAGES-1 ahead into the slot read one step ago, then the
   // MFMAs of each K-half once its fragments have landed.
-  bf16x8_t af[2][C::TM], bfr[2][C::TN];
+  bf16x8_t af[C::KH][C::TM], bfr[C::KH][C::TN];
   issue(0);
-  if (C::STAGES == 3 && KT > 1) issue(C::STAGE);
+#pragma unroll
+  for (int q = 1; q < C::STAGES - 1; ++q)
+    if (q < KT) issue((uint32_t)(q * C::STAGE));
   int slot = 0;
   for (int kt = 0; kt < KT; ++kt) {
-    if (C::STAGES == 3 && kt + 1 < KT) {
-      if (C::REM == 0 || wave < C::REM)
-        wait_vmcnt<C::NU>();
-      else
-        wait_vmcnt<C::NU_LO>();
-    } else {
+    // stages issued after this one: min(STAGES - 2, KT - 1 - kt), each NU
+    // (or NU_LO) loads of this wave
+    const int after = min(C::STAGES - 2, KT - 1 - kt);
+    const bool hi = C::REM == 0 || wave < C::REM;
+    if (after <= 0)
       wait_vmcnt<0>();
-    }
+    else if (after == 1)
+      hi ? wait_vmcnt<C::NU>() : wait_vmcnt<C::NU_LO>();
+    else
+      hi ? wait_vmcnt<2 * C::NU>() : wait_vmcnt<2 * C::NU_LO>();
     __builtin_amdgcn_s_barrier();
     const uint32_t sb = sbase + (uint32_t)(slot * C::STAGE);
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      ds_rd_n<C::TM, 2048, 0>(af[s], sb + fa[s]);
-      ds_rd_n<C::TN, 2048, C::A_BYTES>(bfr[s], sb + fb[s]);
+    for (int s = 0; s < C::KH; ++s) {
+      ds_rd_n<C::TM, 16 * C::RB, 0>(af[s], sb + fa[s]);
+      ds_rd_n<C::TN, 16 * C::RB, C::A_BYTES>(bfr[s], sb + fb[s]);
     }
     if (kt + C::STAGES - 1 < KT) {
       const int ns = slot + C::STAGES - 1;
@@ -453,8 +473,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     }
     slot = slot + 1 == C::STAGES ? 0 : slot + 1;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      if (s == 0)
+    for (int s = 0; s < C::KH; ++s) {
+      if (s + 1 < C::KH)
         lgkm_wait<C::TM + C::TN>();
       else
         lgkm_wait<0>();
@@ -802,6 +822,7 @@ using C2_128x128 = CfgC<128, 128, 64, 64>;   // 4 waves
 using C2_256x128 = CfgC<256, 128, 64, 64>;   // 8 waves
 using C2_256x160S3 = CfgC<256, 160, 64, 80, 3>;  // 8 waves, 3 stages
 using C2_128x160S3 = CfgC<128, 160, 64, 80, 3>;  // 4 waves, 3 stages
+using C2_128x160K32 = CfgC<128, 160, 64, 80, 4, 32>;  // 4 waves, 4 stages of 32 channels
 using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
 using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
@@ -845,6 +866,7 @@ TileInfo tile2_info(int t) {
     case TILE2_C256x128: return info2<C2_256x128>();
     case TILE2_C256x160S3: return info2<C2_256x160S3>();
     case TILE2_C128x160S3: return info2<C2_128x160S3>();
+    case TILE2_C128x160K32S4: return info2<C2_128x160K32>();
     case TILE2_W320x192: return info2<W2_320x192>();
     case TILE2_W320x128: return info2<W2_320x128>();
     default: return info2<W2_128x128>();
@@ -858,6 +880,7 @@ hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
     case TILE2_C256x128: return conv2_t<C2_256x128>(a, st);
     case TILE2_C256x160S3: return conv2_t<C2_256x160S3>(a, st);
     case TILE2_C128x160S3: return conv2_t<C2_128x160S3>(a, st);
+    case TILE2_C128x160K32S4: return conv2_t<C2_128x160K32>(a, st);
     default: return conv2_t<C2_128x128>(a, st);
   }
 }

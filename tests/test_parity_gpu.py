@@ -72,3 +72,19 @@ def test_l64_full_size_sampled():
         b1 = {k: v[n:n + 1] for k, v in b.items()}
         ref = _oracle(d1, params, b1)
         compare(desc, gpu, ref, grads=False, skip_rows=slice(n, n + 1), label=f"l64 n={n}")
+
+
+@pytest.mark.parametrize("tile", range(7))
+def test_every_conv_tile(tile, monkeypatch):
+    """Every implicit-GEMM conv tile shape of the LDS-DMA path (1-, 2- and
+    3/4-stage rings, 64- and 32-channel K-steps, with and without K splits)
+    against the oracle on the 64x64x320 stage's channels at a small image."""
+    monkeypatch.setenv("PULSE_CONV_TILE", str(tile))
+    _case(configs.shrink(configs.l64(), batch=2, hw=12, width=10), 2, f"l64s conv tile {tile}")
+
+
+@pytest.mark.parametrize("tile", [10, 11, 12])
+def test_every_wgrad_tile(tile, monkeypatch):
+    """Every weight-gradient tile shape of the LDS-DMA path."""
+    monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
+    _case(configs.shrink(configs.l32(), batch=2, hw=6, width=7), 3, f"l32s wgrad tile {tile}")
