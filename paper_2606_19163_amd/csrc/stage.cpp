@@ -118,7 +118,13 @@ struct pulse_stage {
   size_t row_temb[2] = {0, 0}, row_xin = 0, row_u = 0;
   size_t s_da = 0, s_dxs = 0, s_dh1 = 0, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
          s_pi = 0, s_e = 0, s_zero = 0;
-  size_t part_cap = 0;
+  size_t part_cap = 0;   // weight-gradient split partials (elements)
+  size_t kpart_cap = 0;  // conv K-split partials (elements)
+  size_t s_kpart = 0, s_red2 = 0;
+  // side stream: the weight-gradient GEMMs of the backward pass run on it,
+  // concurrently with the data-gradient chain on the caller's stream
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   // binding
   const float* prm = nullptr;
   float* grd = nullptr;
@@ -379,7 +385,7 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_dh1 = sc; sc += fbig;
   s->s_g[0] = sc; sc += fbig;
   s->s_g[1] = sc; sc += fbig;
-  size_t part = 0, red = 0;
+  size_t part = 0, kpart = 0, red = 0;
   for (auto* v : {&s->eb, &s->db})
     for (auto& b : *v) {
       int kc;
@@ -392,12 +398,15 @@ pulse_status build_layout(pulse_stage* s) {
         red = std::max(red, (size_t)s->geo.B * rg.chunks * 2 * c);
         // conv-mode K-split partials (an upper bound over the K of each launch)
         const int ks = conv_ksplit(s, conv_tile(s, c), c, 1 << 30);
-        if (ks > 1) part = std::max(part, (size_t)ks * s->P * c);
+        if (ks > 1) kpart = std::max(kpart, (size_t)ks * s->P * c);
       }
     }
   s->part_cap = part;
   s->s_part = sc; sc += align256(part * 4);
+  s->kpart_cap = kpart;
+  s->s_kpart = sc; sc += align256(kpart * 4);
   s->s_red = sc; sc += align256(red * 4);
+  s->s_red2 = sc; sc += align256(red * 4);  // reductions on the side stream
   s->s_coef = sc; sc += align256((size_t)s->geo.B * s->G * 2 * 4);
   s->s_pi = sc; sc += align256((size_t)2 * s->geo.B * cmax * 4);
   s->s_e = sc; sc += align256((size_t)s->geo.B * cmax * 4);
@@ -580,9 +589,9 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
   a.ksteps = (kt + ks - 1) / ks;
   if (ks > 1) {
     a.ksplit = (kt + a.ksteps - 1) / a.ksteps;  // no empty split
-    if ((size_t)a.ksplit * a.M * a.N > s->part_cap)
+    if ((size_t)a.ksplit * a.M * a.N > s->kpart_cap)
       return fail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
-    a.part = s->sf(s->s_part);
+    a.part = s->sf(s->s_kpart);
   }
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
@@ -776,6 +785,24 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
 }
 
 // One ResBlock backward.  dout: gradient w.r.t. the block output.  o: where
+// Fork: work enqueued on the side stream after this starts once everything
+// enqueued on `st` so far has finished.  Join: `st` continues once the side
+// stream's work so far has finished.  Without a side stream both are no-ops
+// and the side work runs on `st`.
+pulse_status fork_side(pulse_stage* s, hipStream_t st) {
+  if (!s->side) return PULSE_OK;
+  HIPCHK(hipEventRecord(s->ev_fork, st));
+  HIPCHK(hipStreamWaitEvent(s->side, s->ev_fork, 0));
+  return PULSE_OK;
+}
+
+pulse_status join_side(pulse_stage* s, hipStream_t st) {
+  if (!s->side) return PULSE_OK;
+  HIPCHK(hipEventRecord(s->ev_join, s->side));
+  HIPCHK(hipStreamWaitEvent(st, s->ev_join, 0));
+  return PULSE_OK;
+}
+
 // the gradient w.r.t. the block input goes (split/addends set by caller;
 // the residual / shortcut addend is filled in here).
 pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xin,
@@ -783,22 +810,27 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   char* row = s->row_base(r);
   const int dt = s->dtype;
   pulse_status ps;
-  // bias gradients of conv2 (and of the 1x1 shortcut, which sees the same dY)
+  // Parameter gradients of conv2 / the shortcut (bias sums and the weight
+  // GEMM) only read dout and saved activations: they run on the side stream
+  // while the data-gradient chain continues here.  The side stream has its
+  // own reduction buffer and weight-gradient partials.
+  hipStream_t sd = s->side ? s->side : st;
+  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;
   {
     const RedGrid rg = red_grid(s->geo, b.cout);
-    HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, s->sf(s->s_red), st));
-    HIPCHK(launch_chan_totals(s->sf(s->s_red), s->geo, rg, b.cout, 1, s->gp(b.b2),
-                              b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, st));
+    float* red = s->sf(s->side ? s->s_red2 : s->s_red);
+    HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, red, sd));
+    HIPCHK(launch_chan_totals(red, s->geo, rg, b.cout, 1, s->gp(b.b2),
+                              b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, sd));
   }
-  // weight gradients of conv2 and the shortcut, one GEMM
   const VIn a2v = vin1(row + b.a2, dt, b.cout);
   if (b.conv_sc) {
     if ((ps = wgrad(s, b.cout,
                     {seg3(0, b.cout, a2v, s->gp(b.W2)), seg1(9 * b.cout, b.cin, xin, s->gp(b.Ws))},
-                    dout, st)) != PULSE_OK)
+                    dout, sd)) != PULSE_OK)
       return ps;
   } else {
-    if ((ps = wgrad(s, b.cout, {seg3(0, b.cout, a2v, s->gp(b.W2))}, dout, st)) != PULSE_OK)
+    if ((ps = wgrad(s, b.cout, {seg3(0, b.cout, a2v, s->gp(b.W2))}, dout, sd)) != PULSE_OK)
       return ps;
   }
   // data gradients through conv2 and the shortcut
@@ -837,7 +869,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   const VIn a1 = (b.cin > b.c0) ? vin2(row + b.a1_0, dt, b.c0, row + b.a1_1, dt, b.cin - b.c0)
                                 : vin1(row + b.a1_0, dt, b.cin);
   const VIn dh1v = vin1(dh1, dt, b.cout);
-  if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, st)) != PULSE_OK)
+  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;  // dh1 is complete
+  if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, sd)) != PULSE_OK)
     return ps;
   if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
                      nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
@@ -845,7 +878,11 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // GN1 backward + residual path -> gradient w.r.t. the block input
   o.add0 = b.conv_sc ? vin1(dxs, dt, b.cin) : dout;
   o.chan_partial = nullptr;
-  return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
+  if ((ps = gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o,
+                        st)) != PULSE_OK)
+    return ps;
+  // the next block overwrites buffers the side work reads (dout, dh1)
+  return join_side(s, st);
 }
 
 pulse_status check_ptr(const void* p, const char* what) {
@@ -905,6 +942,9 @@ pulse_status pulse_stage_create(const pulse_stage_desc* desc, pulse_stage** out)
 void pulse_stage_destroy(pulse_stage* s) {
   if (!s) return;
   for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+  if (s->ev_fork) (void)hipEventDestroy(s->ev_fork);
+  if (s->ev_join) (void)hipEventDestroy(s->ev_join);
+  if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
 }
 
@@ -949,6 +989,12 @@ pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads,
                 s->ws_bytes);
   if (pulse_stage_inflight(s) > 0)
     return fail(PULSE_E_STATE, "cannot rebind with microbatches in flight");
+  if (!s->side && env_int("PULSE_SERIAL", 0) == 0) {
+    // default priority, no implicit synchronisation with the null stream
+    HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
+    HIPCHK(hipEventCreateWithFlags(&s->ev_fork, hipEventDisableTiming));
+    HIPCHK(hipEventCreateWithFlags(&s->ev_join, hipEventDisableTiming));
+  }
   s->prm = params;
   s->grd = grads;
   s->ws = static_cast<char*>(ws);
