@@ -116,7 +116,7 @@ struct pulse_stage {
   size_t ws_bytes = 0, off_rows = 0, row_size = 0, off_scratch = 0;
   size_t row_act[MAX_SLOTS], row_grad[MAX_SLOTS];
   size_t row_temb[2] = {0, 0}, row_xin = 0, row_u = 0;
-  size_t s_da = 0, s_dxs = 0, s_dh1 = 0, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
+  size_t s_da = 0, s_dxs = 0, s_dh1[2] = {0, 0}, s_g[2] = {0, 0}, s_part = 0, s_red = 0, s_coef = 0,
          s_pi = 0, s_e = 0, s_zero = 0;
   size_t part_cap = 0;   // weight-gradient split partials (elements)
   size_t kpart_cap = 0;  // conv K-split partials (elements)
@@ -125,6 +125,7 @@ struct pulse_stage {
   // concurrently with the data-gradient chain on the caller's stream
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_w2[2] = {nullptr, nullptr}, ev_w1[2] = {nullptr, nullptr};
   // binding
   const float* prm = nullptr;
   float* grd = nullptr;
@@ -382,7 +383,8 @@ pulse_status build_layout(pulse_stage* s) {
   const size_t fbig = align256((size_t)s->P * cmax * 4);
   s->s_da = sc; sc += fbig;
   s->s_dxs = sc; sc += fbig;
-  s->s_dh1 = sc; sc += fbig;
+  s->s_dh1[0] = sc; sc += fbig;
+  s->s_dh1[1] = sc; sc += fbig;
   s->s_g[0] = sc; sc += fbig;
   s->s_g[1] = sc; sc += fbig;
   size_t part = 0, kpart = 0, red = 0;
@@ -796,6 +798,27 @@ pulse_status fork_side(pulse_stage* s, hipStream_t st) {
   return PULSE_OK;
 }
 
+// Side-stream progress markers of one backward call: block k records w2
+// after its conv2 / shortcut parameter work (the last read of its dout) and
+// w1 after its conv1 weight gradient (the last read of its dh1); buffers
+// alternate between consecutive blocks, so block k waits for the marker of
+// the block that used the same buffer before it.
+struct BwdSync {
+  bool w2[2] = {false, false}, w1[2] = {false, false};
+};
+
+pulse_status mark_side(pulse_stage* s, hipEvent_t ev) {
+  if (!s->side) return PULSE_OK;
+  HIPCHK(hipEventRecord(ev, s->side));
+  return PULSE_OK;
+}
+
+pulse_status wait_mark(pulse_stage* s, hipEvent_t ev, bool recorded, hipStream_t st) {
+  if (!s->side || !recorded) return PULSE_OK;
+  HIPCHK(hipStreamWaitEvent(st, ev, 0));
+  return PULSE_OK;
+}
+
 pulse_status join_side(pulse_stage* s, hipStream_t st) {
   if (!s->side) return PULSE_OK;
   HIPCHK(hipEventRecord(s->ev_join, s->side));
@@ -806,7 +829,9 @@ pulse_status join_side(pulse_stage* s, hipStream_t st) {
 // the gradient w.r.t. the block input goes (split/addends set by caller;
 // the residual / shortcut addend is filled in here).
 pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xin,
-                            const VIn& dout, GnBwdOut o, float* dtemb, hipStream_t st) {
+                            const VIn& dout, GnBwdOut o, float* dtemb, hipStream_t st, int k,
+                            BwdSync& sy) {
+  const int par = k & 1;
   char* row = s->row_base(r);
   const int dt = s->dtype;
   pulse_status ps;
@@ -833,6 +858,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     if ((ps = wgrad(s, b.cout, {seg3(0, b.cout, a2v, s->gp(b.W2))}, dout, sd)) != PULSE_OK)
       return ps;
   }
+  if ((ps = mark_side(s, s->ev_w2[par])) != PULSE_OK) return ps;
+  sy.w2[par] = true;
   // data gradients through conv2 and the shortcut
   // data gradients are stored in the stage dtype (the MFMA operands they feed
   // are rounded to it anyway; the GroupNorm backward reads them once more)
@@ -846,8 +873,11 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
                        vnone(), dxs, nullptr, dt, st)) != PULSE_OK)
       return ps;
   }
-  // GN2 backward -> dh1, with per-image channel sums (the temb gradient)
-  void* dh1 = s->scratch(s->s_dh1);
+  // GN2 backward -> dh1, with per-image channel sums (the temb gradient);
+  // dh1 alternates between two buffers: the one written here was last read
+  // by the conv1 weight gradient of the block before the previous one
+  void* dh1 = s->scratch(s->s_dh1[par]);
+  if ((ps = wait_mark(s, s->ev_w1[par], sy.w1[par], st)) != PULSE_OK) return ps;
   {
     GnBwdOut o2{};
     o2.dst0 = dh1;
@@ -872,17 +902,18 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   if ((ps = fork_side(s, st)) != PULSE_OK) return ps;  // dh1 is complete
   if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, sd)) != PULSE_OK)
     return ps;
+  if ((ps = mark_side(s, s->ev_w1[par])) != PULSE_OK) return ps;
+  sy.w1[par] = true;
   if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
                      nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
     return ps;
   // GN1 backward + residual path -> gradient w.r.t. the block input
   o.add0 = b.conv_sc ? vin1(dxs, dt, b.cin) : dout;
   o.chan_partial = nullptr;
-  if ((ps = gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o,
-                        st)) != PULSE_OK)
-    return ps;
-  // the next block overwrites buffers the side work reads (dout, dh1)
-  return join_side(s, st);
+  // the GN1 backward writes the gradient buffer that was the previous block's
+  // dout: wait until the side stream has read it
+  if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
+  return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
 }
 
 pulse_status check_ptr(const void* p, const char* what) {
@@ -944,6 +975,10 @@ void pulse_stage_destroy(pulse_stage* s) {
   for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
   if (s->ev_fork) (void)hipEventDestroy(s->ev_fork);
   if (s->ev_join) (void)hipEventDestroy(s->ev_join);
+  for (int i = 0; i < 2; ++i) {
+    if (s->ev_w2[i]) (void)hipEventDestroy(s->ev_w2[i]);
+    if (s->ev_w1[i]) (void)hipEventDestroy(s->ev_w1[i]);
+  }
   if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
 }
@@ -994,6 +1029,10 @@ pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads,
     HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
     HIPCHK(hipEventCreateWithFlags(&s->ev_fork, hipEventDisableTiming));
     HIPCHK(hipEventCreateWithFlags(&s->ev_join, hipEventDisableTiming));
+    for (int i = 0; i < 2; ++i) {
+      HIPCHK(hipEventCreateWithFlags(&s->ev_w2[i], hipEventDisableTiming));
+      HIPCHK(hipEventCreateWithFlags(&s->ev_w1[i], hipEventDisableTiming));
+    }
   }
   s->prm = params;
   s->grd = grads;
@@ -1165,6 +1204,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     char* row = s->row_base(r);
     const int dt = s->dtype;
     int cur = 0;
+    BwdSync sy;
     if (half == PULSE_DEC) {
       const int n = (int)s->db.size();
       for (int k = n - 1; k >= 0; --k) {
@@ -1177,7 +1217,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
         o.dtype0 = dt;
         o.dst1 = row + s->row_grad[b.slot];
         o.dtype1 = DT_F32;
-        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy)) != PULSE_OK) return ps;
         cur ^= 1;
       }
     } else {
@@ -1206,10 +1246,12 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
         // the block input is the previous block's output (or the stage input):
         // its buffered skip gradient joins here, once
         o.add1 = dskip_of(k == 0 ? d.input_skip_slot : s->eb[k - 1].slot);
-        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st)) != PULSE_OK) return ps;
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy)) != PULSE_OK) return ps;
         cur ^= 1;
       }
     }
+    // the caller's stream sees every side-stream result
+    if ((ps = join_side(s, st)) != PULSE_OK) return ps;
   }
 
   Row& row = s->rows[r];
