@@ -440,8 +440,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   }
 
   // Per K-step: wait for this stage's DMA (the later stages stay in
-  // flight), barrier, issue every fragment read of the stage, start the DMA
-  // of the stage STAGES-1 ahead into the slot read one step ago, then the
+  // flight), barrier, start the DMA of the stage STAGES-1 ahead into the slot
+  // read one step ago, issue every fragment read of this stage, then the
   // MFMAs of each K-half once its fragments have landed.
   bf16x8_t af[C::KH][C::TM], bfr[C::KH][C::TN];
   issue(0);
@@ -462,14 +462,15 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
       hi ? wait_vmcnt<2 * C::NU>() : wait_vmcnt<2 * C::NU_LO>();
     __builtin_amdgcn_s_barrier();
     const uint32_t sb = sbase + (uint32_t)(slot * C::STAGE);
+    // the slot refilled here was read one step ago: every wave is past that
+    if (kt + C::STAGES - 1 < KT) {
+      const int ns = slot + C::STAGES - 1;
+      issue((uint32_t)((ns >= C::STAGES ? ns - C::STAGES : ns) * C::STAGE));
+    }
 #pragma unroll
     for (int s = 0; s < C::KH; ++s) {
       ds_rd_n<C::TM, 16 * C::RB, 0>(af[s], sb + fa[s]);
       ds_rd_n<C::TN, 16 * C::RB, C::A_BYTES>(bfr[s], sb + fb[s]);
-    }
-    if (kt + C::STAGES - 1 < KT) {
-      const int ns = slot + C::STAGES - 1;
-      issue((uint32_t)((ns >= C::STAGES ? ns - C::STAGES : ns) * C::STAGE));
     }
     slot = slot + 1 == C::STAGES ? 0 : slot + 1;
 #pragma unroll
