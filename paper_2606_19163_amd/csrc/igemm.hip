@@ -671,7 +671,7 @@ static hipError_t launch_wgrad_t(GemmArgs a, int splits, hipStream_t st) {
 
 template <class C>
 static TileInfo info_t() {
-  return TileInfo{C::BM, C::BN, C::BK};
+  return TileInfo{C::BM, C::BN, C::BK, 0};
 }
 
 TileInfo tile_info(int t) {

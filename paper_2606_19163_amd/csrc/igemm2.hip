@@ -76,6 +76,7 @@ struct CfgC {
   static constexpr int NU_LO = WL / NW;           // loads of waves >= REM
   static constexpr int UA = WLA / NW;  // loads u < UA fill A, the rest fill B
   static constexpr int LDC = BN + 4;
+  static constexpr int LDS_BYTES = STAGES * STAGE;
   static_assert(BK == 32 || BK == 64, "K-step");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert(16 * LDC * 4 <= STAGES * STAGE, "epilogue slice must fit the stages");
@@ -150,6 +151,7 @@ struct CfgW {
   static constexpr int RA = best_rot(PA), RB = best_rot(PB);
   static constexpr int RA_A = RA % 256, RA_B = RA / 256, RB_A = RB % 256, RB_B = RB / 256;
   static constexpr int LDC = BN + 4;
+  static constexpr int LDS_BYTES = 2 * STAGE;
   static_assert(16 * LDC * 4 <= STAGE, "epilogue slice must fit one stage");
   static_assert(2 * STAGE <= 160 * 1024, "LDS");
   static_assert(WL % NW == 0 && WLA % NW == 0 && (BK * PA) % 1024 == 0 &&
@@ -827,6 +829,7 @@ using C2_128x160K32 = CfgC<128, 160, 64, 80, 4, 32>;  // 4 waves, 4 stages of 32
 using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
 using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
+using W2_160x128 = CfgW<160, 128, 80, 64>;   // 4 waves
 
 template <class C>
 static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
@@ -854,7 +857,8 @@ static hipError_t wgrad2_t(const GemmArgs& a, int splits, const void* zero16, hi
 
 template <class C>
 static TileInfo info2() {
-  return TileInfo{C::BM, C::BN, C::BK};
+  constexpr int lds = C::LDS_BYTES;
+  return TileInfo{C::BM, C::BN, C::BK, (160 * 1024) / lds};
 }
 }  // namespace launch2
 using namespace launch2;
@@ -870,6 +874,7 @@ TileInfo tile2_info(int t) {
     case TILE2_C128x160K32S4: return info2<C2_128x160K32>();
     case TILE2_W320x192: return info2<W2_320x192>();
     case TILE2_W320x128: return info2<W2_320x128>();
+    case TILE2_W160x128: return info2<W2_160x128>();
     default: return info2<W2_128x128>();
   }
 }
@@ -892,6 +897,7 @@ hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero1
   switch (t) {
     case TILE2_W320x192: e = wgrad2_t<W2_320x192>(a, splits, zero16, st); break;
     case TILE2_W320x128: e = wgrad2_t<W2_320x128>(a, splits, zero16, st); break;
+    case TILE2_W160x128: e = wgrad2_t<W2_160x128>(a, splits, zero16, st); break;
     default: e = wgrad2_t<W2_128x128>(a, splits, zero16, st); break;
   }
   if (e != hipSuccess) return e;

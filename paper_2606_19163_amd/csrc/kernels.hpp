@@ -63,6 +63,7 @@ enum Tile : int {
 };
 struct TileInfo {
   int bm, bn, bk;
+  int per_cu;  // blocks resident per CU (LDS-limited), 0 when not known
 };
 TileInfo tile_info(int tile);
 hipError_t launch_conv(const GemmArgs& a, int tile, hipStream_t st);
@@ -83,8 +84,9 @@ enum Tile2 : int {
   TILE2_W320x192 = 10,
   TILE2_W320x128 = 11,
   TILE2_W128x128 = 12,
+  TILE2_W160x128 = 13,  // 4 waves, two blocks per CU
   TILE2_WGRAD_FIRST = 10,
-  TILE2_WGRAD_LAST = 12
+  TILE2_WGRAD_LAST = 13
 };
 TileInfo tile2_info(int tile);
 hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);

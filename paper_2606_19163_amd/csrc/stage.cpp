@@ -252,7 +252,8 @@ int conv_ksplit(const pulse_stage* s, int tile, int N, int K) {
 int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
   const TileInfo ti = info_of(s, tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
-  const long slots = 256L * (ti.bm * ti.bn <= 128 * 128 ? 2 : 1);  // resident blocks
+  const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : (ti.bm * ti.bn <= 128 * 128 ? 2 : 1);
+  const long slots = 256L * per_cu;  // resident blocks
   const double t_tile = 2.0 * ti.bm * ti.bn * (double)s->P / 3.0e12;  // s, per CU
   const double t_part = (double)M * N * 8.0 / 4.0e12;                  // s, per split
   const long maxs = std::max(1L, (long)(s->P / (4 * ti.bk)));          // >= 4 K-steps each

@@ -83,7 +83,7 @@ def test_every_conv_tile(tile, monkeypatch):
     _case(configs.shrink(configs.l64(), batch=2, hw=12, width=10), 2, f"l64s conv tile {tile}")
 
 
-@pytest.mark.parametrize("tile", [10, 11, 12])
+@pytest.mark.parametrize("tile", [10, 11, 12, 13])
 def test_every_wgrad_tile(tile, monkeypatch):
     """Every weight-gradient tile shape of the LDS-DMA path."""
     monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
