@@ -91,9 +91,33 @@ def measured_traffic(name):
         return None
 
 
-def cpu_baseline(name, descs, seed, sample_batch):
+def mfma_probe_tflops():
+    """Sustained bf16 MFMA rate of the GPU: register-operand MFMA chains with
+    no memory traffic (2048 workgroups of 4 waves, 400 iterations), timed with
+    HIP events; the median of 5 launches per shape."""
+    import torch
+    from paper_2606_19163_amd import stage as S
+    out = torch.empty(2048 * 256, dtype=torch.float32, device="cuda")
+    res = {}
+    for shape, name in ((32, "32x32x16"), (16, "16x16x32")):
+        S.mfma_probe(shape, 2048, 50, out)  # warm up
+        times = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fl = S.mfma_probe(shape, 2048, 400, out)
+            b.record()
+            b.synchronize()
+            times.append(a.elapsed_time(b))
+        times.sort()
+        res[name] = round(fl / (times[2] * 1e-3) / 1e12, 1)
+    return res
+
+
+def cpu_baseline(name, descs, seed, sample_batch, min_seconds=10.0):
     """The oracle, as it stands, on `sample_batch` images of the workload's
-    first stage (forward + backward), scaled to TFLOP/s."""
+    first stage (forward + backward), repeated until at least `min_seconds`
+    have passed, scaled to TFLOP/s."""
     import numpy as np
     from oracle import pulse_oracle as O
     from paper_2606_19163_amd import configs, synth
@@ -108,13 +132,15 @@ def cpu_baseline(name, descs, seed, sample_batch):
     f = lambda x: {k: np.asarray(v, np.float64) for k, v in x.items()}
     p64, b64 = f(params), f(b)
     flops = S.Stage(d, dry_run=True).flops()
-    t0 = time.perf_counter()
-    O.stage_run(d, p64, b64["x"], b64["u"], b64["temb"], b64["g_enc"], b64["g_dec"])
+    runs, t0 = 0, time.perf_counter()
+    while runs == 0 or time.perf_counter() - t0 < min_seconds:
+        O.stage_run(d, p64, b64["x"], b64["u"], b64["temb"], b64["g_enc"], b64["g_dec"])
+        runs += 1
     dt = time.perf_counter() - t0
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+    return {"value": runs * flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{sample_batch} of {descs[0]['batch']} images of one microbatch of the "
-                      f"first stage ({d['height']}x{d['width']}), forward + backward, numpy "
+            "sample": f"{runs} x {sample_batch} of {descs[0]['batch']} images of one microbatch of "
+                      f"the first stage ({d['height']}x{d['width']}), forward + backward, numpy "
                       f"fp64; {dt:.2f} s"}
 
 
@@ -126,7 +152,9 @@ def main():
     ap.add_argument("--workload", default="l64",
                     choices=["l64", "l32", "l16", "l8", "tiny", "wave"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-batch", type=int, default=2)
+    ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    ap.add_argument("--serial", action="store_true",
+                    help="keep the whole backward on the stage stream (no side stream)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket the conv launches with HIP events")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -140,6 +168,8 @@ def main():
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.serial:
+        os.environ["PULSE_SERIAL"] = "1"
     import numpy as np
     import torch
     from paper_2606_19163_amd import configs, synth
@@ -193,23 +223,32 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = not args.no_kernel_events
-    for st in stages:
-        st.timing(events)
-    torch.cuda.synchronize()
+    # the timed steps: the stage as it runs in production
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    # the conv kernel's roofline: the same steps again with every conv launch
+    # bracketed by HIP events on the stage stream (the backward then keeps
+    # its weight-gradient GEMMs on that stream, so each event pair times the
+    # kernel alone)
+    events = not args.no_kernel_events
     launches, kms, kflops, kbytes = 0, 0.0, 0.0, 0.0
-    for st in stages:
-        n, ms, fl, by = st.timing_read()
-        launches += n
-        kms += ms
-        kflops += fl
-        kbytes += by
-        st.timing(False)
+    if events:
+        for st in stages:
+            st.timing(True)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        for st in stages:
+            n, ms, fl, by = st.timing_read()
+            launches += n
+            kms += ms
+            kflops += fl
+            kbytes += by
+            st.timing(False)
 
     ms_step = elapsed * 1e3 / args.steps
     tflops = flops_step * args.steps / elapsed / 1e12
@@ -246,6 +285,8 @@ def main():
             "launches": launches, "avg_launch_us": round(kms * 1e3 / launches, 2),
             "avg_gflop_per_launch": round(kflops / launches / 1e9, 3),
         }
+    if bf16:
+        line["mfma_probe_tflops"] = mfma_probe_tflops()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, descs, seed,
                                             min(args.cpu_sample_batch, descs[0]["batch"]))

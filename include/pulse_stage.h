@@ -188,7 +188,10 @@ pulse_status pulse_stage_reset(pulse_stage* st);
 int32_t pulse_stage_inflight(const pulse_stage* st);
 
 /* Per-kernel timing: when enabled, every launch of the implicit-GEMM conv
- * kernel is bracketed by HIP events on the call's stream.  _read
+ * kernel is bracketed by HIP events on the call's stream, and the backward
+ * pass keeps all its work on that stream (no overlap with the
+ * weight-gradient GEMMs, which otherwise run on an internal stream), so
+ * the events time the kernel alone.  _read
  * synchronises those events and returns the launch count, the summed
  * duration in ms, the summed algorithmic FLOPs (2*M*N*K) and the summed
  * compulsory HBM bytes (each input element, weight and residual read once,
@@ -202,6 +205,17 @@ pulse_status pulse_stage_timing_read(pulse_stage* st, int64_t* launches,
  * over every conv (forward, data gradient, weight gradient) and the
  * timestep linear. */
 double pulse_stage_flops(const pulse_stage* st);
+
+/* Measurement helper, not part of the method: `blocks` workgroups of 256
+ * threads each run `iters` iterations of independent bf16 MFMAs of the given
+ * shape (32: 32x32x16, 16: 16x16x32) on register operands, with no memory
+ * traffic in the loop.  `out` is caller-owned device memory of
+ * blocks * 256 floats (one value per thread, kept so the chain is not
+ * removed); *flops receives the FLOPs of the launch.  The caller times the
+ * launch on `stream`.  PULSE_E_INVALID_ARG for a bad shape, count or NULL out;
+ * PULSE_E_HIP if the launch fails. */
+pulse_status pulse_mfma_probe(int32_t shape, int32_t blocks, int32_t iters, float* out,
+                              double* flops, void* stream);
 
 /* Thread-local description of the last error; valid until the next call. */
 const char* pulse_last_error(void);

@@ -37,7 +37,7 @@ CFLAGS = [
     "-I", CSRC,
 ]
 
-SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "stage.cpp"]
+SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "stage.cpp"]
 
 
 def _compile(src: str) -> str:

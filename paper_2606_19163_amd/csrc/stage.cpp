@@ -788,12 +788,17 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
 }
 
 // One ResBlock backward.  dout: gradient w.r.t. the block output.  o: where
+// The side stream is used unless per-kernel timing is on: timed conv
+// launches then run alone on the caller's stream, so their events measure
+// the kernel and not its overlap with the weight-gradient GEMMs.
+bool use_side(const pulse_stage* s) { return s->side && !s->timing; }
+
 // Fork: work enqueued on the side stream after this starts once everything
 // enqueued on `st` so far has finished.  Join: `st` continues once the side
 // stream's work so far has finished.  Without a side stream both are no-ops
 // and the side work runs on `st`.
 pulse_status fork_side(pulse_stage* s, hipStream_t st) {
-  if (!s->side) return PULSE_OK;
+  if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(s->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(s->side, s->ev_fork, 0));
   return PULSE_OK;
@@ -809,19 +814,19 @@ struct BwdSync {
 };
 
 pulse_status mark_side(pulse_stage* s, hipEvent_t ev) {
-  if (!s->side) return PULSE_OK;
+  if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(ev, s->side));
   return PULSE_OK;
 }
 
 pulse_status wait_mark(pulse_stage* s, hipEvent_t ev, bool recorded, hipStream_t st) {
-  if (!s->side || !recorded) return PULSE_OK;
+  if (!use_side(s) || !recorded) return PULSE_OK;
   HIPCHK(hipStreamWaitEvent(st, ev, 0));
   return PULSE_OK;
 }
 
 pulse_status join_side(pulse_stage* s, hipStream_t st) {
-  if (!s->side) return PULSE_OK;
+  if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(s->ev_join, s->side));
   HIPCHK(hipStreamWaitEvent(st, s->ev_join, 0));
   return PULSE_OK;
@@ -840,11 +845,11 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // GEMM) only read dout and saved activations: they run on the side stream
   // while the data-gradient chain continues here.  The side stream has its
   // own reduction buffer and weight-gradient partials.
-  hipStream_t sd = s->side ? s->side : st;
+  hipStream_t sd = use_side(s) ? s->side : st;
   if ((ps = fork_side(s, st)) != PULSE_OK) return ps;
   {
     const RedGrid rg = red_grid(s->geo, b.cout);
-    float* red = s->sf(s->side ? s->s_red2 : s->s_red);
+    float* red = s->sf(use_side(s) ? s->s_red2 : s->s_red);
     HIPCHK(launch_chan_sum_partial(dout, s->geo, rg, red, sd));
     HIPCHK(launch_chan_totals(red, s->geo, rg, b.cout, 1, s->gp(b.b2),
                               b.conv_sc ? s->gp(b.bs) : nullptr, nullptr, sd));

@@ -116,6 +116,9 @@ def lib():
         L.pulse_stage_timing_read.restype = st
         L.pulse_stage_flops.argtypes = [_vp]
         L.pulse_stage_flops.restype = ctypes.c_double
+        L.pulse_mfma_probe.argtypes = [_i32, _i32, _i32, _vp, ctypes.POINTER(ctypes.c_double),
+                                       _vp]
+        L.pulse_mfma_probe.restype = st
         L.pulse_last_error.argtypes = []
         L.pulse_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -303,6 +306,16 @@ class Stage:
         _check(lib().pulse_stage_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms),
                                              ctypes.byref(fl), ctypes.byref(by)))
         return n.value, ms.value, fl.value, by.value
+
+
+def mfma_probe(shape, blocks, iters, out, stream=None):
+    """Launch the matrix-core throughput probe (see pulse_mfma_probe) on the
+    current torch stream; returns the launch's FLOPs."""
+    import torch
+    fl = ctypes.c_double()
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    _check(lib().pulse_mfma_probe(shape, blocks, iters, out.data_ptr(), ctypes.byref(fl), s))
+    return fl.value
 
 
 def run_microbatch(stage, mb, b, dtemb=None):
