@@ -90,6 +90,12 @@ enum Tile2 : int {
 };
 TileInfo tile2_info(int tile);
 hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);
+// conv mode with halo reuse (igemm2.hip): 256-pixel tiles of whole image rows
+// x 160 output channels; every 64-channel input chunk's halo is loaded once
+// for all taps.  Applies when N % 160 == 0, W % 16 == 0, 256 % W == 0,
+// H*W % 256 == 0 and the halo fits 52 KB; no K split.
+bool halo_conv_fits(const Geo& g, int N);
+hipError_t launch_conv_halo(const GemmArgs& a, hipStream_t st);
 hipError_t launch_wgrad2(const GemmArgs& a, int tile, int splits, const void* zero16,
                          hipStream_t st);
 

@@ -97,6 +97,10 @@ struct pulse_stage {
   size_t esz = 4;
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
+  // halo-reuse conv: 0 never (default: it measured slower in the full step,
+  // where its 147 KB of LDS keeps the side stream's GEMMs off its CUs), 1
+  // when its grid fills the GPU, 2 whenever it fits
+  int halo = 0;
   bool v2 = false;      // LDS-DMA GEMM kernels (bf16, 64-channel K-steps)
   Geo geo{};
   long P = 0;
@@ -328,6 +332,7 @@ pulse_status build_layout(pulse_stage* s) {
     // overrides (tuning) index Tile2 on the LDS-DMA path, Tile otherwise
     s->v2 = env_int("PULSE_GEMM_V1", 0) == 0;
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
+    s->halo = env_int("PULSE_HALO", 0);
     if (s->v2) {
       s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
       s->wgrad_tile_force = (wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
@@ -602,7 +607,14 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
     e1 = next_event(s);
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
-  if (uses_v2(s))
+  // the halo-reuse kernel when it applies (one block per CU: only when the
+  // grid fills the GPU, unless forced) and no tile override is set
+  const bool halo = uses_v2(s) && s->conv_tile_force < 0 && ks == 1 && s->halo > 0 &&
+                    halo_conv_fits(s->geo, a.N) &&
+                    (s->halo == 2 || (s->P / 256) * (a.N / 160) >= 256);
+  if (halo)
+    HIPCHK(launch_conv_halo(a, st));
+  else if (uses_v2(s))
     HIPCHK(launch_conv2(a, tile, st));
   else
     HIPCHK(launch_conv(a, tile, st));

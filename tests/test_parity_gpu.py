@@ -88,3 +88,15 @@ def test_every_wgrad_tile(tile, monkeypatch):
     """Every weight-gradient tile shape of the LDS-DMA path."""
     monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
     _case(configs.shrink(configs.l32(), batch=2, hw=6, width=7), 3, f"l32s wgrad tile {tile}")
+
+
+@pytest.mark.parametrize("name,B,H,W", [("l64", 1, 16, 16), ("l64", 2, 32, 32),
+                                        ("l32", 1, 16, 16), ("l32", 1, 32, 32)])
+def test_halo_conv(name, B, H, W, monkeypatch):
+    """The halo-reuse conv kernel (whole-row 256-pixel tiles, one halo load
+    per 64-channel chunk for all taps), forced on at sizes the oracle runs
+    in seconds: single- and two-source inputs, the K-extended 1x1 shortcut,
+    tiles of 16, 8 and 4 image rows, zero halo at image borders."""
+    monkeypatch.setenv("PULSE_HALO", "2")
+    d = configs.shrink(configs.get(name), batch=B, hw=H, width=W)
+    _case(d, configs.SEEDS[name], f"{name} halo {B}x{H}x{W}")
