@@ -206,6 +206,73 @@ pulse_status pulse_stage_timing_read(pulse_stage* st, int64_t* launches,
  * timestep linear. */
 double pulse_stage_flops(const pulse_stage* st);
 
+/* ---- pipeline schedule (Sec. V) ----------------------------------------
+ *
+ * A model cut into P = 2D partitions runs on D devices; partition p and its
+ * skip partner P-1-p are collocated (Sec. IV-B) together with their
+ * backward passes, so device q holds the skip-collocated stage made of
+ * encoder partition q and decoder partition 2D-1-q (Sec. V-B; one
+ * pulse_stage).  One microbatch is the chain of S = 4D unit-time stages
+ * s = 0..P-1 (forward of partition s) and s = P..2P-1 (backward of partition
+ * 2P-1-s).  A schedule is a table[d * T + t] over devices d and steps t
+ * holding s * M + m (stage s of microbatch m) or -1 (idle); the caller owns
+ * it.  Stage-to-device placement is the symmetric one: pair q on device q. */
+
+/* Build the wave schedule of (D, M) (Sec. V-A objective: fewest steps).  For
+ * D <= 3 and a state space of at most 2e5 progress vectors the schedule is
+ * an exact minimum, found by breadth-first search over the microbatches each
+ * stage has finished (*exact = 1); otherwise a list schedule that always
+ * runs a device's deepest runnable stage (*exact = 0).  With table == NULL
+ * only *T (the number of steps) is returned; otherwise table must hold
+ * D * cap entries with cap >= *T (else PULSE_E_SHAPE) and receives the
+ * schedule as table[d * T + t].  PULSE_E_INVALID_ARG
+ * for D outside [1, 64], M outside [1, 4096] or T == NULL. */
+pulse_status pulse_sched_build(int32_t D, int32_t M, int32_t* table, int32_t cap, int32_t* T,
+                               int32_t* exact);
+
+/* Check a schedule against the constraints of the scheduling formulation
+ * (Sec. V-A): *violated receives a bit mask with bit k set when constraint
+ * (k) fails -- (1) unique assignment, (3) fixed device mapping, (4)
+ * collocation of the four stages of a skip pair, (5) sequential execution,
+ * (6) monotonic microbatch order -- and bit 0 when the first stage is not on
+ * device 0.  (2), one stage per device and step, holds by the table's
+ * shape.  0 means valid. */
+pulse_status pulse_sched_check(int32_t D, int32_t M, const int32_t* table, int32_t T,
+                               int32_t* violated);
+
+/* Per-microbatch boundary tensors of one device (device pointers in the
+ * stage dtype unless noted): x (encoder input), u (decoder upstream input),
+ * temb, g_enc and g_dec (output gradients) in; y_enc, y_dec, dx, du out;
+ * dtemb (fp32, accumulated) may be NULL. */
+typedef struct {
+  const void* x;
+  const void* u;
+  const void* temb;
+  const void* g_enc;
+  const void* g_dec;
+  void* y_enc;
+  void* y_dec;
+  void* dx;
+  void* du;
+  float* dtemb;
+} pulse_mb_io;
+
+/* Execute steps [t0, t1) of device d's row of a schedule on its stage: each
+ * cell becomes pulse_stage_forward/backward of the stage's ENC half (stage
+ * s = d forward, s = 4D-1-d backward) or DEC half (s = 2D-1-d forward,
+ * s = 2D+d backward) for that microbatch, in step order, on `stream` (io: M
+ * entries, read only for the microbatches the steps touch).  A host runtime
+ * that moves boundary tensors between devices calls it one step at a time
+ * and exchanges at the step boundaries; one call over [0, T) runs the whole
+ * row when all inputs are already resident.  The stage needs max_inflight
+ * >= the microbatches the row keeps in flight.  PULSE_E_INVALID_ARG when
+ * 0 <= t0 <= t1 <= T fails or a cell in the range is not one of the device's
+ * four stages (nothing is enqueued then); otherwise the first failing stage
+ * call's status. */
+pulse_status pulse_sched_run_device(pulse_stage* st, int32_t D, int32_t d, int32_t M,
+                                    const int32_t* table, int32_t T, int32_t t0, int32_t t1,
+                                    const pulse_mb_io* io, void* stream);
+
 /* Measurement helper, not part of the method: `blocks` workgroups of 256
  * threads each run `iters` iterations of independent bf16 MFMAs of the given
  * shape (32: 32x32x16, 16: 16x16x32) on register operands, with no memory

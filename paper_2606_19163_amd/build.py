@@ -37,7 +37,8 @@ CFLAGS = [
     "-I", CSRC,
 ]
 
-SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "stage.cpp"]
+SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "stage.cpp",
+           "sched.cpp"]
 
 
 def _compile(src: str) -> str:

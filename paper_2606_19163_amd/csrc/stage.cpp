@@ -13,6 +13,7 @@
 #include <string>
 #include <vector>
 
+#include "error.hpp"
 #include "kernels.hpp"
 #include "pulse_stage.h"
 
@@ -86,6 +87,11 @@ struct TimedLaunch {
 };
 
 }  // namespace
+
+pulse_status pulse::set_last_error(pulse_status s, const char* msg) {
+  g_err = msg;
+  return s;
+}
 
 struct pulse_stage {
   // descriptor

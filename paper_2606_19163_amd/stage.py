@@ -116,6 +116,14 @@ def lib():
         L.pulse_stage_timing_read.restype = st
         L.pulse_stage_flops.argtypes = [_vp]
         L.pulse_stage_flops.restype = ctypes.c_double
+        _ip = ctypes.POINTER(_i32)
+        L.pulse_sched_build.argtypes = [_i32, _i32, _ip, _i32, _ip, _ip]
+        L.pulse_sched_build.restype = st
+        L.pulse_sched_check.argtypes = [_i32, _i32, _ip, _i32, _ip]
+        L.pulse_sched_check.restype = st
+        L.pulse_sched_run_device.argtypes = [_vp, _i32, _i32, _i32, _ip, _i32, _i32, _i32,
+                                             ctypes.POINTER(MbIO), _vp]
+        L.pulse_sched_run_device.restype = st
         L.pulse_mfma_probe.argtypes = [_i32, _i32, _i32, _vp, ctypes.POINTER(ctypes.c_double),
                                        _vp]
         L.pulse_mfma_probe.restype = st
@@ -306,6 +314,51 @@ class Stage:
         _check(lib().pulse_stage_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms),
                                              ctypes.byref(fl), ctypes.byref(by)))
         return n.value, ms.value, fl.value, by.value
+
+
+class MbIO(ctypes.Structure):
+    _fields_ = [("x", _vp), ("u", _vp), ("temb", _vp), ("g_enc", _vp), ("g_dec", _vp),
+                ("y_enc", _vp), ("y_dec", _vp), ("dx", _vp), ("du", _vp), ("dtemb", _vp)]
+
+
+def sched_build(D, M):
+    """The wave schedule of (D, M): (table as a [D][T] list of lists of
+    s*M+m or -1, exact flag)."""
+    T = _i32()
+    ex = _i32()
+    _check(lib().pulse_sched_build(D, M, None, 0, ctypes.byref(T), ctypes.byref(ex)))
+    buf = (_i32 * (D * T.value))()
+    _check(lib().pulse_sched_build(D, M, buf, T.value, ctypes.byref(T), ctypes.byref(ex)))
+    t = T.value
+    return [[buf[d * t + i] for i in range(t)] for d in range(D)], bool(ex.value)
+
+
+def sched_check(D, M, table):
+    """Bit mask of violated schedule constraints (0: valid)."""
+    T = len(table[0]) if table else 0
+    buf = (_i32 * (D * T))(*[v for row in table for v in row])
+    bad = _i32()
+    _check(lib().pulse_sched_check(D, M, buf, T, ctypes.byref(bad)))
+    return bad.value
+
+
+def sched_run_device(stage, D, d, M, table, io=None, t0=0, t1=None, stream=None):
+    """Run steps [t0, t1) of device d's row of the schedule on ``stage``.
+    ``io``: M dicts of device tensors (x, u, temb, g_enc, g_dec in; y_enc,
+    y_dec, dx, du out; dtemb optional); None for a dry-run stage."""
+    T = len(table[0])
+    t1 = T if t1 is None else t1
+    buf = (_i32 * (D * T))(*[v for row in table for v in row])
+    arr = (MbIO * M)()
+    keep = []
+    if io is not None:
+        for m in range(M):
+            for k, _ in MbIO._fields_:
+                t = io[m].get(k)
+                setattr(arr[m], k, t.data_ptr() if t is not None else None)
+                keep.append(t)
+    s = None if stage.dry else _stream_handle(stream)
+    _check(lib().pulse_sched_run_device(stage.h, D, d, M, buf, T, t0, t1, arr, s))
 
 
 def mfma_probe(shape, blocks, iters, out, stream=None):
