@@ -9,6 +9,10 @@ decoder forward (reading [upstream || skip] from the cache), decoder
 backward (skip gradient buffered), encoder backward (skip gradient added).
 The ``wave`` workload's step is one wave iteration of the four SD levels
 with 4 microbatches in flight (all forwards, then backwards in reverse).
+``wave-sched`` runs the same four levels as the four devices of a 4-device
+pipeline: each level's stage executes its device's row of the collocated
+wave schedule for 4 microbatches (pulse_sched_run_device), one row after
+another on this GPU.
 
 Prints ONE JSON line (rank 0): stage fwd+bwd TFLOP/s with the fraction of
 the bf16 MFMA peak, microbatches/s, the roofline of the implicit-GEMM conv
@@ -36,7 +40,7 @@ METRIC = "stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s, 64x64x320
 
 def workload_desc(name):
     from paper_2606_19163_amd import configs
-    if name == "wave":
+    if name in ("wave", "wave-sched"):
         return configs.wave_levels()
     return [configs.get(name)]
 
@@ -48,6 +52,12 @@ def describe(name, descs):
                             "8x8x1280) at batch 8, 4 microbatches in flight, all forwards "
                             "then backwards in reverse",
                 "batch": 8, "microbatches": 4, "levels": 4}
+    if name == "wave-sched":
+        return {"workload": "wave-sched: 4 collocated stages (64x64x320, 32x32x640, "
+                            "16x16x1280, 8x8x1280) at batch 8 as devices 0-3 of a 4-device "
+                            "pipeline, each running its row of the wave schedule for 4 "
+                            "microbatches",
+                "batch": 8, "microbatches": 4, "levels": 4, "devices": 4}
     chans = sorted({b["c_out"] for b in d["enc"]} | {b["c_in"] for b in d["enc"]})
     return {"workload": f"{name}: one collocated stage, batch {d['batch']}, "
                         f"{d['height']}x{d['width']}, channels {chans}, "
@@ -150,7 +160,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="l64",
-                    choices=["l64", "l32", "l16", "l8", "tiny", "wave"])
+                    choices=["l64", "l32", "l16", "l8", "tiny", "wave", "wave-sched"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
     ap.add_argument("--serial", action="store_true",
@@ -177,9 +187,15 @@ def main():
 
     torch.cuda.set_device(0)
     descs = workload_desc(args.workload)
-    n_mb = 4 if args.workload == "wave" else 1
-    seed = configs.SEEDS["wave" if args.workload == "wave" else args.workload]
-    if args.workload == "wave":
+    multi = args.workload in ("wave", "wave-sched")
+    n_mb = 4 if multi else 1
+    seed = configs.SEEDS["wave" if multi else args.workload]
+    sched = None
+    if args.workload == "wave-sched":
+        sched, sched_exact = S.sched_build(len(descs), n_mb)
+        for d, need in zip(descs, S.sched_inflight(len(descs), n_mb, sched)):
+            d["max_inflight"] = need
+    if multi:
         params, bounds = synth.make_wave(descs, seed, n_mb)
     else:
         p0, b0 = synth.make_all(descs[0], seed)
@@ -207,7 +223,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    io = [[dict(dev[i][m], **outs[i][m], dtemb=dtembs[i]) for m in range(n_mb)]
+          for i in range(len(descs))]
+
+    def step_sched():
+        for i, st in enumerate(stages):
+            S.sched_run_device(st, len(stages), i, n_mb, sched, io[i])
+
     def step():
+        if sched is not None:
+            return step_sched()
         for i, st in enumerate(stages):
             for m in range(n_mb):
                 b = dev[i][m]
@@ -285,6 +310,11 @@ def main():
             "launches": launches, "avg_launch_us": round(kms * 1e3 / launches, 2),
             "avg_gflop_per_launch": round(kflops / launches / 1e9, 3),
         }
+    if sched is not None:
+        T = len(sched[0])
+        line["schedule"] = {"devices": len(stages), "microbatches": n_mb, "steps": T,
+                            "exact_minimum": bool(sched_exact),
+                            "device_busy_frac": round(4 * n_mb / T, 4)}
     if bf16:
         line["mfma_probe_tflops"] = mfma_probe_tflops()
     if not args.no_cpu_baseline:

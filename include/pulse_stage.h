@@ -218,15 +218,18 @@ double pulse_stage_flops(const pulse_stage* st);
  * holding s * M + m (stage s of microbatch m) or -1 (idle); the caller owns
  * it.  Stage-to-device placement is the symmetric one: pair q on device q. */
 
-/* Build the wave schedule of (D, M) (Sec. V-A objective: fewest steps).  For
- * D <= 3 and a state space of at most 2e5 progress vectors the schedule is
- * an exact minimum, found by breadth-first search over the microbatches each
- * stage has finished (*exact = 1); otherwise a list schedule that always
- * runs a device's deepest runnable stage (*exact = 0).  With table == NULL
- * only *T (the number of steps) is returned; otherwise table must hold
- * D * cap entries with cap >= *T (else PULSE_E_SHAPE) and receives the
- * schedule as table[d * T + t].  PULSE_E_INVALID_ARG
- * for D outside [1, 64], M outside [1, 4096] or T == NULL. */
+/* Build the wave schedule of (D, M) (Sec. V-A objective: fewest steps).
+ * Candidates are two list schedules (each step, every device runs one
+ * runnable stage: backward-first deepest-first, or forward-first
+ * deepest-first) and, for D <= 4 and a state space of at most 2e5 progress
+ * vectors, an exact minimum found by breadth-first search over the
+ * microbatches each stage has finished.  The fewest steps win, then the
+ * fewest microbatches in flight on any device; *exact = 1 when the search
+ * ran, so that the result is a proven minimum.  With table == NULL only *T
+ * (the number of steps) is returned; otherwise table must hold D * cap
+ * entries with cap >= *T (else PULSE_E_SHAPE) and receives the schedule as
+ * table[d * T + t].  PULSE_E_INVALID_ARG for D outside [1, 64], M outside
+ * [1, 4096] or T == NULL. */
 pulse_status pulse_sched_build(int32_t D, int32_t M, int32_t* table, int32_t cap, int32_t* T,
                                int32_t* exact);
 
@@ -239,6 +242,13 @@ pulse_status pulse_sched_build(int32_t D, int32_t M, int32_t* table, int32_t cap
  * shape.  0 means valid. */
 pulse_status pulse_sched_check(int32_t D, int32_t M, const int32_t* table, int32_t T,
                                int32_t* violated);
+
+/* Microbatches each device holds at once under a schedule: peak[d] (D
+ * entries, caller-owned) receives the largest number of microbatches whose
+ * encoder forward on device d has run and whose encoder backward has not,
+ * which is the max_inflight that device's stage needs. */
+pulse_status pulse_sched_inflight(int32_t D, int32_t M, const int32_t* table, int32_t T,
+                                  int32_t* peak);
 
 /* Per-microbatch boundary tensors of one device (device pointers in the
  * stage dtype unless noted): x (encoder input), u (decoder upstream input),

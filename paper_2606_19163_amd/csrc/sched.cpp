@@ -106,25 +106,33 @@ bool exact_schedule(int D, int M, size_t max_states, std::vector<std::vector<int
   return true;
 }
 
-// List schedule: at every step each device runs its runnable stage with the
-// largest s (backward before forward, deeper before shallower), the lowest
-// microbatch first.
-void list_schedule(int D, int M, std::vector<std::vector<int>>& rows) {
-  const int S = 4 * D;
+// List schedules: at every step each device runs one of its runnable stages,
+// the lowest microbatch of that stage first.  BWD_FIRST takes the stage with
+// the largest s (backward before forward, deeper before shallower): it keeps
+// at most 2D-1-d microbatches in flight on device d and reaches the
+// minimum when D divides M.  FWD_FIRST takes forwards before backwards, each
+// deepest first: every microbatch's forward finishes early, which reaches
+// the minimum for every (D, M) tried, with all M microbatches in flight.
+enum Rule { BWD_FIRST, FWD_FIRST };
+
+void list_schedule(int D, int M, Rule rule, std::vector<std::vector<int>>& rows) {
+  const int S = 4 * D, P = 2 * D;
   std::vector<int> dev(S), k(S, 0);
   for (int s = 0; s < S; ++s) dev[s] = pair_of(D, partition_of(D, s));
   std::vector<std::vector<int>> done_at(S, std::vector<int>(M, -1));
   rows.assign(D, {});
+  auto rank = [&](int s) { return rule == FWD_FIRST && s < P ? s + S : s; };
   for (int t = 0;; ++t) {
     bool left = false;
     for (int s = 0; s < S; ++s) left |= k[s] < M;
     if (!left) break;
     std::vector<int> pick(D, -1);
-    for (int s = S - 1; s >= 0; --s) {
+    for (int s = 0; s < S; ++s) {
       if (k[s] >= M) continue;
       const int m = k[s];
       if (s > 0 && !(k[s - 1] > m && done_at[s - 1][m] <= t - 1)) continue;
-      if (pick[dev[s]] < 0) pick[dev[s]] = s;
+      int& p = pick[dev[s]];
+      if (p < 0 || rank(s) > rank(p)) p = s;
     }
     for (int d = 0; d < D; ++d) {
       const int s = pick[d];
@@ -140,6 +148,29 @@ void list_schedule(int D, int M, std::vector<std::vector<int>>& rows) {
   }
 }
 
+// Largest number of microbatches device d holds between its encoder forward
+// (stage d) and its encoder backward (stage 4D-1-d), over a table[d * T + t].
+int peak_inflight(int D, int M, const int32_t* table, int T, int d) {
+  int cur = 0, peak = 0;
+  for (int t = 0; t < T; ++t) {
+    const int v = table[(long)d * T + t];
+    if (v < 0) continue;
+    const int s = v / M;
+    if (s == d) peak = std::max(peak, ++cur);
+    if (s == 4 * D - 1 - d) --cur;
+  }
+  return peak;
+}
+
+int max_inflight_of(int D, int M, const std::vector<std::vector<int>>& rows) {
+  const int T = (int)rows[0].size();
+  std::vector<int32_t> flat((size_t)D * T);
+  for (int d = 0; d < D; ++d) std::copy(rows[d].begin(), rows[d].end(), flat.begin() + (long)d * T);
+  int worst = 0;
+  for (int d = 0; d < D; ++d) worst = std::max(worst, peak_inflight(D, M, flat.data(), T, d));
+  return worst;
+}
+
 }  // namespace
 
 extern "C" {
@@ -148,13 +179,31 @@ pulse_status pulse_sched_build(int32_t D, int32_t M, int32_t* table, int32_t cap
                                int32_t* exact) {
   if (!args_ok(D, M)) return bad_arg(kDM);
   if (!T) return bad_arg("T is NULL");
-  std::vector<std::vector<int>> rows;
-  // the progress vectors are non-increasing sequences of S = 4D values in
-  // [0, M]: C(M + S, S) of them; search only when that is small
+  // candidates: both list schedules, and the exact search when its state
+  // space is small (the progress vectors are non-increasing sequences of
+  // S = 4D values in [0, M]: C(M + S, S) of them).  The fewest steps win;
+  // among equals, the fewest microbatches in flight on any device.
+  std::vector<std::vector<int>> rows, cand;
+  int best_t = 0, best_mem = 0;
+  auto consider = [&](std::vector<std::vector<int>>& c) {
+    const int t = (int)c[0].size(), mem = max_inflight_of(D, M, c);
+    if (rows.empty() || t < best_t || (t == best_t && mem < best_mem)) {
+      rows.swap(c);
+      best_t = t;
+      best_mem = mem;
+    }
+  };
+  list_schedule(D, M, BWD_FIRST, cand);
+  consider(cand);
+  list_schedule(D, M, FWD_FIRST, cand);
+  consider(cand);
   double states = 1.0;
   for (int i = 1; i <= 4 * D; ++i) states = states * (M + i) / i;
-  const bool ex = D <= 3 && M <= 200 && states <= 2e5 && exact_schedule(D, M, 200000, rows);
-  if (!ex) list_schedule(D, M, rows);
+  bool ex = false;
+  if (D <= 4 && M <= 200 && states <= 2e5 && exact_schedule(D, M, 200000, cand)) {
+    ex = true;  // best_t can only tie or lose to the exact minimum
+    consider(cand);
+  }
   const int t = (int)rows[0].size();
   *T = t;
   if (exact) *exact = ex ? 1 : 0;
@@ -212,6 +261,14 @@ pulse_status pulse_sched_check(int32_t D, int32_t M, const int32_t* table, int32
       if (a >= 0 && b >= 0 && b < a) bad |= 1 << 6;  // (6) monotonic microbatch order
     }
   *violated = bad;
+  return PULSE_OK;
+}
+
+pulse_status pulse_sched_inflight(int32_t D, int32_t M, const int32_t* table, int32_t T,
+                                  int32_t* peak) {
+  if (!args_ok(D, M)) return bad_arg(kDM);
+  if (!table || !peak || T < 0) return bad_arg("table or peak is NULL, or T < 0");
+  for (int d = 0; d < D; ++d) peak[d] = peak_inflight(D, M, table, T, d);
   return PULSE_OK;
 }
 

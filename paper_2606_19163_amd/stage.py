@@ -121,6 +121,8 @@ def lib():
         L.pulse_sched_build.restype = st
         L.pulse_sched_check.argtypes = [_i32, _i32, _ip, _i32, _ip]
         L.pulse_sched_check.restype = st
+        L.pulse_sched_inflight.argtypes = [_i32, _i32, _ip, _i32, _ip]
+        L.pulse_sched_inflight.restype = st
         L.pulse_sched_run_device.argtypes = [_vp, _i32, _i32, _i32, _ip, _i32, _i32, _i32,
                                              ctypes.POINTER(MbIO), _vp]
         L.pulse_sched_run_device.restype = st
@@ -340,6 +342,15 @@ def sched_check(D, M, table):
     bad = _i32()
     _check(lib().pulse_sched_check(D, M, buf, T, ctypes.byref(bad)))
     return bad.value
+
+
+def sched_inflight(D, M, table):
+    """Peak microbatches in flight per device under the schedule."""
+    T = len(table[0]) if table else 0
+    buf = (_i32 * (D * T))(*[v for row in table for v in row])
+    peak = (_i32 * D)()
+    _check(lib().pulse_sched_inflight(D, M, buf, T, peak))
+    return list(peak)
 
 
 def sched_run_device(stage, D, d, M, table, io=None, t0=0, t1=None, stream=None):

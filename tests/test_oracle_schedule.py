@@ -32,6 +32,25 @@ def test_bounds(D, M):
     assert t <= 4 * D * M
 
 
+def test_forward_turnaround_bound():
+    """Device D-1 runs the forwards of partitions D-1 and D (stages D-1 and
+    D).  Before stage D of the last microbatch it has run stage D-1 for all M
+    microbatches and stage D for the M-1 before it (constraints (5), (6)),
+    starting no earlier than step D-1; 3D-1 stages follow.  So every schedule
+    takes at least 4D + 2M - 2 steps."""
+    for D, M in [(1, 1), (1, 4), (2, 1), (2, 2), (2, 3), (2, 4), (3, 1), (3, 2), (3, 3)]:
+        assert so.optimal_makespan(D, M) >= 4 * D + 2 * M - 2
+
+
+@pytest.mark.parametrize("D,M", [(1, 2), (1, 4), (2, 1), (2, 2), (2, 3), (2, 4), (2, 5),
+                                 (3, 1), (3, 2), (3, 3), (4, 2)])
+def test_optimum_follows_the_wave_pattern(D, M):
+    """The exhaustive optimum equals max(4D + 2M - 2, 4M + 2D - 2): the
+    turnaround bound above while M <= D, and four steps per added
+    microbatch, i.e. full devices in steady state, beyond it."""
+    assert so.optimal_makespan(D, M) == max(4 * D + 2 * M - 2, 4 * M + 2 * D - 2)
+
+
 def _greedy(D, M, dev=None):
     """A schedule built step by step (deepest runnable stage first) on the
     stage-to-device map `dev` (default: the symmetric placement)."""

@@ -34,7 +34,7 @@ def _mask(bad):
     return sum(1 << k for k in bad)
 
 
-EXACT = [(1, 1), (1, 3), (2, 1), (2, 2), (2, 3), (2, 4), (3, 1), (3, 2), (3, 3)]
+EXACT = [(1, 1), (1, 3), (2, 1), (2, 2), (2, 3), (2, 4), (3, 1), (3, 2), (3, 3), (4, 2), (4, 3)]
 
 
 @pytest.mark.parametrize("D,M", EXACT)
@@ -56,13 +56,50 @@ def test_large_schedules_are_valid(D, M):
     assert S.sched_check(D, M, table) == 0
 
 
-def test_list_schedule_is_near_the_bound():
-    # every device holds 4M unit stages: a wave schedule of many microbatches
-    # keeps the devices busy except during fill and drain
-    for D, M in [(4, 64), (8, 64)]:
+def _wave_steps(D, M):
+    return max(4 * D + 2 * M - 2, 4 * M + 2 * D - 2)
+
+
+def test_large_schedules_reach_the_wave_pattern():
+    """Beyond the exhaustive search the builder still reaches the step count
+    of the exact optimum's pattern, max(4D + 2M - 2, 4M + 2D - 2), whose
+    first term is a lower bound for every schedule."""
+    for D in range(1, 9):
+        for M in (1, 2, 3, 5, 7, 8, 12, 13, 16, 31, 32):
+            table, _ = S.sched_build(D, M)
+            assert len(table[0]) == _wave_steps(D, M), (D, M)
+    for D, M in [(16, 64), (32, 96)]:
         table, _ = S.sched_build(D, M)
-        T = len(table[0])
-        assert T <= 4 * M + 4 * D * 2, (D, M, T)
+        assert len(table[0]) == _wave_steps(D, M)
+        assert S.sched_check(D, M, table) == 0
+
+
+def _peak(D, M, cells):
+    """Microbatches between device d's encoder forward (stage d) and encoder
+    backward (stage 4D-1-d), at most, from the oracle-format table."""
+    out = []
+    for d, row in enumerate(cells):
+        cur = peak = 0
+        for c in row:
+            if c is None:
+                continue
+            if c[0] == d:
+                cur += 1
+                peak = max(peak, cur)
+            if c[0] == 4 * D - 1 - d:
+                cur -= 1
+        out.append(peak)
+    return out
+
+
+@pytest.mark.parametrize("D,M", [(1, 3), (2, 3), (2, 8), (3, 4), (4, 4), (4, 16), (8, 32)])
+def test_inflight(D, M):
+    table, _ = S.sched_build(D, M)
+    peak = S.sched_inflight(D, M, table)
+    assert peak == _peak(D, M, _to_cells(table, M))
+    if M % D == 0 and M > D:
+        # backward-first order: device d holds 2D-1-d microbatches at most
+        assert peak == [min(M, 2 * D - 1 - d) for d in range(D)]
 
 
 def _mutations(D, M, cells):
