@@ -28,8 +28,8 @@ constraints of the scheduling formulation are checked as written there:
 plus the anchor of the first stage on device 0.  The objective is the last
 occupied step T_max (makespan T_max + 1).
 
-Readings (the paper leaves them open): the "S stages corresponding to
-forward and backward passes" are the 2P forward/backward stages above; a
+Readings (the paper leaves them open): the formulation's S stages, which
+cover forward and backward passes, are the 2P forward/backward stages above; a
 partition's forward and backward are collocated (its weights and saved
 activations live on one device); stages take one step each.
 """

@@ -38,7 +38,7 @@ CFLAGS = [
 ]
 
 SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "stage.cpp",
-           "sched.cpp"]
+           "sched.cpp", "partition.cpp"]
 
 
 def _compile(src: str) -> str:

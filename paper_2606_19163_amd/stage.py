@@ -60,10 +60,13 @@ _lib = None
 
 
 def header_functions():
-    """Names of the functions declared in include/pulse_stage.h."""
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(pulse_\w+)\s*\(", src)))
+    """Names of the functions declared in the headers under include/."""
+    import glob
+    names = set()
+    for h in sorted(glob.glob(os.path.join(os.path.dirname(HEADER), "*.h"))):
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"\b(pulse_\w+)\s*\(", src))
+    return sorted(names)
 
 
 def lib():
