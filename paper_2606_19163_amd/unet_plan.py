@@ -1,0 +1,155 @@
+"""Skip-aware partition of a UNet built from the four measured stage levels.
+
+    python -m paper_2606_19163_amd.unet_plan [--batch 8] [--reps 20]
+
+The UNet is the sixteen ResBlocks of the 64x64x320, 32x32x640, 16x16x1280
+and 8x8x1280 levels in model order (encoder blocks of each level going down,
+then decoder blocks coming up), with the long skips of those levels: each
+decoder block reads the encoder output its level caches for it, and the
+second 32x32 decoder block reads the 32x32 level's input, the output of the
+last 64x64 encoder block.  Every block's forward time is measured on this
+GPU through the stage ABI (a one-block stage per ResBlock shape, HIP events
+around the forward call), every block's output size is its bf16 activation.
+The partitioner (pulse_partition, Sec. IV-B) then splits the sequence for
+2 and 4 devices, beside the block-wise split (equal ResBlocks per stage),
+and one JSON line reports both.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+
+from . import configs, plan, synth
+from . import stage as S
+
+XGMI_BYTES_PER_S = 153e9   # one MI355X xGMI link
+T_LAT_S = 10e-6            # per-transfer latency taken for the link
+
+
+def unet_ops(batch=8):
+    """(ops, skips): ops in model order as dicts (name, half, level desc,
+    block), skips as op-index pairs."""
+    levels = [("64", configs.l64(batch)), ("32", configs.l32(batch)),
+              ("16", configs.l16(batch)), ("8", configs.l8(batch))]
+    ops, enc_index, slot_owner = [], {}, {}
+    for name, d in levels:
+        for k, b in enumerate(d["enc"]):
+            enc_index[(name, k)] = len(ops)
+            ops.append(dict(name=f"E{name}.{k}", half=S.ENC, level=d, block=b))
+    skips = []
+    prev_level_out = None  # op whose output enters the level
+    for name, d in levels:
+        owner = {}
+        if d.get("input_skip_slot", -1) >= 0:
+            owner[d["input_skip_slot"]] = prev_level_out
+        for k, b in enumerate(d["enc"]):
+            if b["skip_slot_out"] >= 0:
+                owner[b["skip_slot_out"]] = enc_index[(name, k)]
+        slot_owner[name] = owner
+        prev_level_out = enc_index[(name, len(d["enc"]) - 1)]
+    for name, d in reversed(levels):
+        for k, b in enumerate(d["dec"]):
+            i = len(ops)
+            ops.append(dict(name=f"D{name}.{k}", half=S.DEC, level=d, block=b))
+            src = slot_owner[name].get(b["skip_slot_in"])
+            if src is not None:
+                skips.append((src, i))
+    return ops, skips
+
+
+def out_bytes(op):
+    d, b = op["level"], op["block"]
+    return d["batch"] * d["height"] * d["width"] * b["c_out"] * 2
+
+
+def block_stage(op):
+    """A stage holding the op's block and the smallest partner the ABI needs
+    (a decoder block reading the encoder block's output, or an encoder
+    block producing the decoder block's skip)."""
+    d, b = op["level"], op["block"]
+    desc = {k: d[k] for k in ("batch", "height", "width", "groups", "eps", "temb_dim", "dtype")}
+    desc["input_skip_slot"] = -1
+    desc["max_inflight"] = 1
+    if op["half"] == S.ENC:
+        desc["enc"] = [dict(c_in=b["c_in"], c_out=b["c_out"], skip_slot_out=0)]
+        desc["dec"] = [dict(c_up=b["c_out"], c_skip=b["c_out"], c_out=b["c_out"],
+                            skip_slot_in=0)]
+    else:
+        desc["enc"] = [dict(c_in=b["c_skip"], c_out=b["c_skip"], skip_slot_out=0)]
+        desc["dec"] = [dict(c_up=b["c_up"], c_skip=b["c_skip"], c_out=b["c_out"],
+                            skip_slot_in=0)]
+    return desc
+
+
+def time_forward(op, reps=20, warmup=3, seed=0):
+    """Median forward time (s) of the op's block at its level's batch."""
+    import torch
+    desc = block_stage(op)
+    params, b = synth.make_all(desc, seed)
+    st = S.Stage(desc)
+    st.set_params(params)
+    db = {k: st.to_dev(v) for k, v in b.items()}
+    times = []
+    for r in range(warmup + reps):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if op["half"] == S.ENC:
+            a.record()
+            st.forward(S.ENC, 0, db["x"], db["temb"])
+            e.record()
+        else:
+            st.forward(S.ENC, 0, db["x"], db["temb"])
+            a.record()
+            st.forward(S.DEC, 0, db["u"], db["temb"])
+            e.record()
+        e.synchronize()
+        st.release(0)
+        if r >= warmup:
+            times.append(a.elapsed_time(e) * 1e-3)
+    times.sort()
+    return times[len(times) // 2]
+
+
+def blockwise_cuts(n, p):
+    per = n // p
+    return [per * (k + 1) - 1 for k in range(p - 1)]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--batch", type=int, default=8)
+    ap.add_argument("--reps", type=int, default=20)
+    args = ap.parse_args()
+    import torch
+    torch.cuda.set_device(0)
+    ops, skips = unet_ops(args.batch)
+    t_f = []
+    for op in ops:
+        t_f.append(time_forward(op, args.reps))
+        print(f"# {op['name']}: {t_f[-1] * 1e6:.1f} us", flush=True)
+    m_a = [float(out_bytes(op)) for op in ops]
+    n = len(ops)
+    out = {"batch": args.batch, "ops": [o["name"] for o in ops],
+           "forward_us": [round(t * 1e6, 2) for t in t_f],
+           "skips": skips, "plans": []}
+    for p in (4, 8):
+        for lam in (0.0, 1.0):
+            kw = dict(lam=lam, t_lat=T_LAT_S, b_inter=XGMI_BYTES_PER_S)
+            cuts, cost = plan.partition(t_f, m_a, skips, p, **kw)
+            _, _, sc = plan.partition_cost(t_f, m_a, skips, p, cuts, **kw)
+            bw = blockwise_cuts(n, p)
+            bcost, bvalid, bsc = plan.partition_cost(t_f, m_a, skips, p, bw, **kw)
+            out["plans"].append({
+                "stages": p, "devices": p // 2, "lambda": lam,
+                "balanced": {"cuts": cuts, "max_stage_us": round(cost * 1e6, 2),
+                             "stage_us": [round(v * 1e6, 2) for v in sc]},
+                "blockwise": {"cuts": bw, "valid": bvalid,
+                              "max_stage_us": round(max(bsc) * 1e6, 2),
+                              "stage_us": [round(v * 1e6, 2) for v in bsc]},
+                "reduction_pct": round(100.0 * (1.0 - cost / max(bsc)), 1),
+            })
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
