@@ -65,6 +65,61 @@ pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* c
 pulse_status pulse_partition_cost(const pulse_part_problem* pb, int32_t p, const int32_t* cuts,
                                   double* cost, int32_t* valid, double* stage_costs);
 
+/* Hybrid data/pipeline parallelism (Sec. VI).  N devices run G replicas of
+ * a P-device pipeline (N = P G) of 2P collocated stages, on microbatches of
+ * b samples.  Per stage s (1-based), summed over the ops the skip-aware
+ * partition puts in it: T_f^s(b) forward time at b, M_theta^s parameter
+ * bytes, M_a^s activation bytes kept per sample; M_o^s the output bytes per
+ * sample of its last op.  The models of Sec. VI:
+ *
+ *   M_peak  = 7 (M_theta^P + M_theta^(P+1)) + P (M_a^P + M_a^(P+1)) b
+ *             + P M_o^(P-1)                       (no last term for P = 1)
+ *   T_sched = (10P - 4) max_s T_f^s(b)
+ *             + max(0, 10P - 12) (t_lat + b max_s M_o^s / b_inter) + T_AR
+ *   T_AR    = t_lat + 2 (G - 1) max_s M_theta^s / (G b_intra)
+ *   T_sample = T_sched / (b P G)
+ *
+ * The partition for (P, b) is pulse_partition of the op forward times at b
+ * into 2P stages, with boundary bytes b * m_o and the problem's lambda,
+ * t_lat and b_inter. */
+typedef struct {
+  int32_t n_ops;          /* 2 .. 512 */
+  int32_t n_b;            /* 1 .. 32 candidate microbatch sizes */
+  const int32_t* b;       /* [n_b] strictly increasing, >= 1 */
+  const double* t_f;      /* [n_b][n_ops] forward time of each op at each b (seconds) */
+  const double* m_theta;  /* [n_ops] parameter bytes */
+  const double* m_a;      /* [n_ops] activation bytes kept per sample */
+  const double* m_o;      /* [n_ops] output bytes per sample */
+  int32_t n_skips;
+  const int32_t* skips;   /* [n_skips][2] op index pairs */
+  double lambda;          /* partition communication weight (>= 0) */
+  double t_lat;           /* seconds per transfer (>= 0) */
+  double b_inter;         /* bytes/s of the pipeline link (> 0) */
+  double b_intra;         /* bytes/s of the all-reduce (> 0) */
+  double m_limit;         /* bytes of memory per device (> 0, may be +infinity) */
+} pulse_tune_problem;
+
+typedef struct {
+  int32_t P, G, b;
+  int32_t feasible;       /* M_peak < m_limit */
+  double t_sample, t_sched, m_peak, t_ar;
+} pulse_tune_row;
+
+/* Enumerate every factorisation N = P G with 2P <= n_ops; for each, keep
+ * the largest candidate b whose partition exists and fits in memory, and
+ * return the configuration with the smallest T_sample in *best (*found = 0
+ * when nothing fits; ties go to the smaller P).  rows (cap entries, may be
+ * NULL) receives one row per (P, b) evaluated, P ascending then b
+ * ascending; *n_rows their count (all of them, even beyond cap).
+ * PULSE_E_INVALID_ARG for a NULL pointer, N < 1 or a bad problem. */
+pulse_status pulse_tune(const pulse_tune_problem* pb, int32_t n_devices, pulse_tune_row* best,
+                        int32_t* found, pulse_tune_row* rows, int32_t cap, int32_t* n_rows);
+
+/* The models above for one configuration whose 2P stages are given by cuts
+ * (2P - 1 entries, as pulse_partition returns them), at candidate b_index. */
+pulse_status pulse_tune_eval(const pulse_tune_problem* pb, int32_t P, int32_t G, int32_t b_index,
+                             const int32_t* cuts, pulse_tune_row* row);
+
 #ifdef __cplusplus
 }
 #endif

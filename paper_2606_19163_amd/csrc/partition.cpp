@@ -87,14 +87,8 @@ Costs make_costs(const pulse_part_problem* pb) {
   return c;
 }
 
-}  // namespace
-
-extern "C" {
-
-pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* cuts,
-                             double* cost) {
-  if (pulse_status st = check_problem(pb, p)) return st;
-  if (!cuts || !cost) return bad("cuts or cost is NULL");
+// The dynamic program; arguments already checked.
+void partition_dp(const pulse_part_problem* pb, int32_t p, int32_t* cuts, double* cost) {
   const int n = pb->n_ops, H = p / 2;
   const Skips sk = fold_skips(pb);
   const Costs cs = make_costs(pb);
@@ -163,7 +157,7 @@ pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* c
   }
   *cost = best;
   for (int k = 0; k < p - 1; ++k) cuts[k] = -1;
-  if (bi < 0) return PULSE_OK;
+  if (bi < 0) return;
   // walk back outward: level h fixes the last op of stage h-1 (i) and of
   // stage p-h-1 (j-1, the op before stage p-h)
   int i = bi, j = bi + 1;
@@ -174,6 +168,17 @@ pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* c
     i = a / W - 1;
     j = a % W;
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* cuts,
+                             double* cost) {
+  if (pulse_status st = check_problem(pb, p)) return st;
+  if (!cuts || !cost) return bad("cuts or cost is NULL");
+  partition_dp(pb, p, cuts, cost);
   return PULSE_OK;
 }
 
@@ -206,6 +211,150 @@ pulse_status pulse_partition_cost(const pulse_part_problem* pb, int32_t p, const
   }
   *valid = ok ? 1 : 0;
   *cost = ok ? worst : kInf;
+  return PULSE_OK;
+}
+
+}  // extern "C"
+
+// ---- hybrid data/pipeline parallelism (Sec. VI) ---------------------------
+
+namespace {
+
+pulse_status check_tune(const pulse_tune_problem* tp) {
+  if (!tp) return bad("problem is NULL");
+  if (tp->n_ops < 2 || tp->n_ops > kMaxOps) return bad("n_ops must be in [2, 512]");
+  if (tp->n_b < 1 || tp->n_b > 32 || !tp->b) return bad("n_b must be in [1, 32] and b set");
+  for (int k = 0; k < tp->n_b; ++k)
+    if (tp->b[k] < 1 || (k && tp->b[k] <= tp->b[k - 1]))
+      return bad("b must be strictly increasing and >= 1");
+  if (!tp->t_f || !tp->m_theta || !tp->m_a || !tp->m_o) return bad("a per-op array is NULL");
+  for (long k = 0; k < (long)tp->n_b * tp->n_ops; ++k)
+    if (!finite_nonneg(tp->t_f[k])) return bad("t_f must be finite and >= 0");
+  for (int l = 0; l < tp->n_ops; ++l)
+    if (!finite_nonneg(tp->m_theta[l]) || !finite_nonneg(tp->m_a[l]) ||
+        !finite_nonneg(tp->m_o[l]))
+      return bad("memory sizes must be finite and >= 0");
+  if (!(std::isfinite(tp->b_intra) && tp->b_intra > 0.0)) return bad("b_intra must be > 0");
+  if (!(tp->m_limit > 0.0)) return bad("m_limit must be > 0");
+  return PULSE_OK;
+}
+
+// The partition problem of candidate k: op times at b[k], boundary bytes
+// b[k] * m_o.
+struct PartAtB {
+  std::vector<double> ma;
+  pulse_part_problem pp;
+};
+
+PartAtB part_at_b(const pulse_tune_problem* tp, int k) {
+  PartAtB r;
+  r.ma.resize(tp->n_ops);
+  for (int l = 0; l < tp->n_ops; ++l) r.ma[l] = tp->b[k] * tp->m_o[l];
+  r.pp.n_ops = tp->n_ops;
+  r.pp.t_f = tp->t_f + (long)k * tp->n_ops;
+  r.pp.m_a = r.ma.data();
+  r.pp.n_skips = tp->n_skips;
+  r.pp.skips = tp->skips;
+  r.pp.lambda = tp->lambda;
+  r.pp.t_lat = tp->t_lat;
+  r.pp.b_inter = tp->b_inter;
+  return r;
+}
+
+// The models of Sec. VI for one configuration (stages from `cuts`).
+pulse_tune_row eval_config(const pulse_tune_problem* tp, int P, int G, int k,
+                           const int32_t* cuts) {
+  const int n = tp->n_ops, S = 2 * P;
+  const double* tf = tp->t_f + (long)k * n;
+  const double b = tp->b[k];
+  std::vector<double> Tf(S, 0.0), Mth(S, 0.0), Ma(S, 0.0), Mo(S, 0.0);
+  for (int s = 0, l = 0; s < S; ++s) {
+    const int last = s < S - 1 ? cuts[s] : n - 1;
+    for (; l <= last; ++l) {
+      Tf[s] += tf[l];
+      Mth[s] += tp->m_theta[l];
+      Ma[s] += tp->m_a[l];
+    }
+    Mo[s] = tp->m_o[last];
+  }
+  // stage s of the formulas (1-based) is index s-1
+  double m_peak = 7.0 * (Mth[P - 1] + Mth[P]) + P * (Ma[P - 1] + Ma[P]) * b;
+  if (P >= 2) m_peak += P * Mo[P - 2];
+  const double mth_max = *std::max_element(Mth.begin(), Mth.end());
+  const double t_ar = tp->t_lat + 2.0 * (G - 1) * mth_max / (G * tp->b_intra);
+  const double tf_max = *std::max_element(Tf.begin(), Tf.end());
+  const double mo_max = *std::max_element(Mo.begin(), Mo.end());
+  const double steps = std::max(0, 10 * P - 12);
+  const double t_sched = (10.0 * P - 4.0) * tf_max +
+                         steps * (tp->t_lat + b * mo_max / tp->b_inter) + t_ar;
+  pulse_tune_row r;
+  r.P = P;
+  r.G = G;
+  r.b = tp->b[k];
+  r.feasible = m_peak < tp->m_limit ? 1 : 0;
+  r.t_sample = t_sched / (b * P * G);
+  r.t_sched = t_sched;
+  r.m_peak = m_peak;
+  r.t_ar = t_ar;
+  return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+pulse_status pulse_tune(const pulse_tune_problem* tp, int32_t n_devices, pulse_tune_row* best,
+                        int32_t* found, pulse_tune_row* rows, int32_t cap, int32_t* n_rows) {
+  if (pulse_status st = check_tune(tp)) return st;
+  if (n_devices < 1 || n_devices > 1 << 20) return bad("n_devices must be in [1, 2^20]");
+  if (!best || !found || !n_rows || (cap > 0 && !rows) || cap < 0)
+    return bad("best, found or n_rows is NULL, or rows missing for cap > 0");
+  {
+    // the problem's partition fields must hold for every candidate b
+    PartAtB pa = part_at_b(tp, 0);
+    if (pulse_status st = check_problem(&pa.pp, 2)) return st;
+  }
+  *found = 0;
+  int count = 0;
+  for (int P = 1; P <= n_devices && 2 * P <= tp->n_ops; ++P) {
+    if (n_devices % P) continue;
+    if (2 * P > kMaxStages) break;
+    const int G = n_devices / P;
+    pulse_tune_row chosen{};
+    bool have = false;
+    std::vector<int32_t> cuts(2 * P - 1);
+    for (int k = 0; k < tp->n_b; ++k) {
+      PartAtB pa = part_at_b(tp, k);
+      double cost;
+      partition_dp(&pa.pp, 2 * P, cuts.data(), &cost);
+      if (!std::isfinite(cost)) continue;
+      const pulse_tune_row r = eval_config(tp, P, G, k, cuts.data());
+      if (count < cap) rows[count] = r;
+      ++count;
+      if (r.feasible) {
+        chosen = r;  // candidates ascend: the last feasible one has the largest b
+        have = true;
+      }
+    }
+    if (have && (!*found || chosen.t_sample < best->t_sample)) {
+      *best = chosen;
+      *found = 1;
+    }
+  }
+  *n_rows = count;
+  return PULSE_OK;
+}
+
+pulse_status pulse_tune_eval(const pulse_tune_problem* tp, int32_t P, int32_t G, int32_t b_index,
+                             const int32_t* cuts, pulse_tune_row* row) {
+  if (pulse_status st = check_tune(tp)) return st;
+  if (!cuts || !row) return bad("cuts or row is NULL");
+  if (P < 1 || 2 * P > tp->n_ops || G < 1) return bad("P or G out of range");
+  if (b_index < 0 || b_index >= tp->n_b) return bad("b_index out of range");
+  for (int s = 0; s < 2 * P - 1; ++s)
+    if (cuts[s] < 0 || cuts[s] >= tp->n_ops - 1 || (s && cuts[s] <= cuts[s - 1]))
+      return bad("cuts must increase strictly and lie in [0, n_ops - 2]");
+  *row = eval_config(tp, P, G, b_index, cuts);
   return PULSE_OK;
 }
 

@@ -110,6 +110,35 @@ def time_forward(op, reps=20, warmup=3, seed=0):
     return times[len(times) // 2]
 
 
+def param_bytes(op):
+    """Bytes of the block's parameters at 2 bytes each (the half-precision
+    weights the memory model's factor 7 counts)."""
+    d, b = op["level"], op["block"]
+    c_in = b["c_in"] if op["half"] == S.ENC else b["c_up"] + b["c_skip"]
+    c_out = b["c_out"]
+    n = 9 * c_in * c_out + c_out            # conv1
+    n += d["temb_dim"] * c_out + c_out      # timestep linear
+    n += 2 * c_in + 2 * c_out               # GroupNorm affines
+    n += 9 * c_out * c_out + c_out          # conv2
+    if c_in != c_out:
+        n += c_in * c_out + c_out           # 1x1 shortcut
+    return 2.0 * n
+
+
+def act_bytes_per_sample(op):
+    """Bytes the stage keeps per sample for the block's backward: its
+    GroupNorm+SiLU input a1 (all input channels), h1, a2 and the output, in
+    bf16."""
+    d, b = op["level"], op["block"]
+    c_in = b["c_in"] if op["half"] == S.ENC else b["c_up"] + b["c_skip"]
+    return 2.0 * d["height"] * d["width"] * (c_in + 3 * b["c_out"])
+
+
+def out_bytes_per_sample(op):
+    d, b = op["level"], op["block"]
+    return 2.0 * d["height"] * d["width"] * b["c_out"]
+
+
 def blockwise_cuts(n, p):
     per = n // p
     return [per * (k + 1) - 1 for k in range(p - 1)]
@@ -119,6 +148,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--tune", action="store_true",
+                    help="also time every block at microbatch 1, 2, 4, 8, 16 and run the "
+                         "hybrid tuner for 8, 16 and 32 devices")
     args = ap.parse_args()
     import torch
     torch.cuda.set_device(0)
@@ -148,7 +180,38 @@ def main():
                               "stage_us": [round(v * 1e6, 2) for v in bsc]},
                 "reduction_pct": round(100.0 * (1.0 - cost / max(bsc)), 1),
             })
+    if args.tune:
+        out["tune"] = tune_report(args.reps)
     print(json.dumps(out), flush=True)
+
+
+B_INTER_NODE = 50e9    # one 400 Gb/s network port per device between nodes
+B_INTRA_NODE = 300e9   # ring all-reduce over the xGMI mesh of one node
+M_LIMIT = 288e9        # HBM3E per MI355X
+
+
+def tune_report(reps, bs=(1, 2, 4, 8, 16)):
+    ops, skips = unet_ops(8)
+    t_f = []
+    for b in bs:
+        row = []
+        for op in ops:
+            o = dict(op, level=dict(op["level"], batch=b))
+            row.append(time_forward(o, reps))
+        t_f.append(row)
+        print(f"# b={b}: " + " ".join(f"{v * 1e6:.0f}" for v in row), flush=True)
+    m_theta = [param_bytes(o) for o in ops]
+    m_a = [act_bytes_per_sample(o) for o in ops]
+    m_o = [out_bytes_per_sample(o) for o in ops]
+    res = {"bs": list(bs), "forward_us": [[round(v * 1e6, 2) for v in r] for r in t_f],
+           "b_inter": B_INTER_NODE, "b_intra": B_INTRA_NODE, "t_lat": T_LAT_S,
+           "m_limit": M_LIMIT, "choices": []}
+    for N in (8, 16, 32):
+        best, rows = plan.tune(N, list(bs), t_f, m_theta, m_a, m_o, skips, lam=1.0,
+                               t_lat=T_LAT_S, b_inter=B_INTER_NODE, b_intra=B_INTRA_NODE,
+                               m_limit=M_LIMIT)
+        res["choices"].append({"devices": N, "best": best, "rows": rows})
+    return res
 
 
 if __name__ == "__main__":
