@@ -150,7 +150,7 @@ def main():
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--tune", action="store_true",
                     help="also time every block at microbatch 1, 2, 4, 8, 16 and run the "
-                         "hybrid tuner for 8, 16 and 32 devices")
+                         "hybrid tuner for 8, 16 and 32 devices at two memory limits")
     args = ap.parse_args()
     import torch
     torch.cuda.set_device(0)
@@ -187,7 +187,7 @@ def main():
 
 B_INTER_NODE = 50e9    # one 400 Gb/s network port per device between nodes
 B_INTRA_NODE = 300e9   # ring all-reduce over the xGMI mesh of one node
-M_LIMIT = 288e9        # HBM3E per MI355X
+M_LIMITS = (288e9, 6e9)  # HBM3E per MI355X, and a tight budget that binds
 
 
 def tune_report(reps, bs=(1, 2, 4, 8, 16)):
@@ -205,12 +205,14 @@ def tune_report(reps, bs=(1, 2, 4, 8, 16)):
     m_o = [out_bytes_per_sample(o) for o in ops]
     res = {"bs": list(bs), "forward_us": [[round(v * 1e6, 2) for v in r] for r in t_f],
            "b_inter": B_INTER_NODE, "b_intra": B_INTRA_NODE, "t_lat": T_LAT_S,
-           "m_limit": M_LIMIT, "choices": []}
-    for N in (8, 16, 32):
-        best, rows = plan.tune(N, list(bs), t_f, m_theta, m_a, m_o, skips, lam=1.0,
-                               t_lat=T_LAT_S, b_inter=B_INTER_NODE, b_intra=B_INTRA_NODE,
-                               m_limit=M_LIMIT)
-        res["choices"].append({"devices": N, "best": best, "rows": rows})
+           "choices": []}
+    for m_limit in M_LIMITS:
+        for N in (8, 16, 32):
+            best, rows = plan.tune(N, list(bs), t_f, m_theta, m_a, m_o, skips, lam=1.0,
+                                   t_lat=T_LAT_S, b_inter=B_INTER_NODE, b_intra=B_INTRA_NODE,
+                                   m_limit=m_limit)
+            res["choices"].append({"devices": N, "m_limit": m_limit, "best": best,
+                                   "rows": rows})
     return res
 
 
