@@ -124,6 +124,40 @@ def mfma_probe_tflops():
     return res
 
 
+def library_gemm_tflops():
+    """The vendor GEMM (torch.matmul, bf16) on plain GEMMs of the stage's
+    shapes and on large squares, median of 5 timed runs of 20 calls each:
+    the conv forward of the 64x64x320 stage (M = 32768 pixels, N = 320,
+    K = 2880 or 5760), its weight gradient (M = 320, N = 2880, K = 32768,
+    A transposed), and 8192^3 / 16384^2 x 8192."""
+    import torch
+    shapes = [("conv 32768x320x2880", 32768, 320, 2880, False),
+              ("conv 32768x320x5760", 32768, 320, 5760, False),
+              ("wgrad 320x2880x32768", 320, 2880, 32768, True),
+              ("square 8192^3", 8192, 8192, 8192, False),
+              ("16384x16384x8192", 16384, 16384, 8192, False)]
+    res = {}
+    for name, M, N, K, ta in shapes:
+        a = (torch.randn(K, M, device="cuda", dtype=torch.bfloat16).t() if ta else
+             torch.randn(M, K, device="cuda", dtype=torch.bfloat16))
+        b = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            a @ b
+        times = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                a @ b
+            e1.record()
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1) / 20)
+        times.sort()
+        res[name] = round(2.0 * M * N * K / (times[2] * 1e-3) / 1e12, 1)
+        del a, b
+    return res
+
+
 def cpu_baseline(name, descs, seed, sample_batch, min_seconds=10.0):
     """The oracle, as it stands, on `sample_batch` images of the workload's
     first stage (forward + backward), repeated until at least `min_seconds`
@@ -167,6 +201,8 @@ def main():
                     help="keep the whole backward on the stage stream (no side stream)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket the conv launches with HIP events")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor GEMM on plain GEMMs of the stage's shapes")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device-to-device copy of this many MiB before "
                          "the warmup (the known-size kernel that scales HBM counters)")
@@ -317,6 +353,8 @@ def main():
                             "device_busy_frac": round(4 * n_mb / T, 4)}
     if bf16:
         line["mfma_probe_tflops"] = mfma_probe_tflops()
+    if args.library_gemm:
+        line["library_gemm_tflops"] = library_gemm_tflops()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, descs, seed,
                                             min(args.cpu_sample_batch, descs[0]["batch"]))

@@ -56,6 +56,89 @@ __device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, Red
   }
 }
 
+// ---- per-thread resolved channel vectors ------------------------------------
+// Every streaming kernel below gives each thread one vector of 8 channels
+// [c, c+8) for all the pixels it visits.  The source tensor of those
+// channels (one of a virtual input's two sources), their offset and the
+// pixel stride are resolved once, the element type is a template argument,
+// and the pixel loop issues all its loads before any use, without branches,
+// so that they stay in flight together.
+
+struct Ch8 {
+  const void* p;  // tensor base
+  long c;         // channel offset inside a pixel
+  long stride;    // elements per pixel
+};
+
+__device__ __forceinline__ Ch8 resolve(const Src& s, int c) { return Ch8{s.ptr, c, s.C}; }
+
+__device__ __forceinline__ Ch8 resolve(const VIn& v, int c) {
+  return c < v.c0 ? Ch8{v.s0.ptr, c, v.s0.C} : Ch8{v.s1.ptr, c - v.c0, v.s1.C};
+}
+
+// channels of pixel `pix` as fp32 (DT: element type of the tensor)
+template <int DT>
+__device__ __forceinline__ void rd8(const Ch8& h, long pix, float v[8]) {
+  const long e = pix * h.stride + h.c;
+  if constexpr (DT == DT_BF16) {
+    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(h.p) + e);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+    const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(h.p) + e);
+    const float4 a = q[0], b = q[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
+// fp32 addend of pixel `pix` (add: tensor base offset by the channel)
+__device__ __forceinline__ void add8(const float* add, long stride, long pix, float v[8]) {
+  const float4* q = reinterpret_cast<const float4*>(add + pix * stride);
+  const float4 a = q[0], b = q[1];
+  v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+  v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+}
+
+// A thread's view of a virtual input: resolved source plus optional addend.
+struct VCh8 {
+  Ch8 h;
+  const float* add;
+  long astride;
+};
+
+__device__ __forceinline__ VCh8 resolve_v(const VIn& v, int c) {
+  return VCh8{resolve(v, c), v.add ? v.add + c : nullptr, v.C};
+}
+
+template <int DT, bool ADD>
+__device__ __forceinline__ void rdv8(const VCh8& h, long pix, float v[8]) {
+  rd8<DT>(h.h, pix, v);
+  if constexpr (ADD) add8(h.add, h.astride, pix, v);
+}
+
+// The U pixels p, p + py, ... of one loop step: absolute pixel indices with
+// the ones past p1 clamped to the last valid pixel (they are loaded but
+// weighted 0), and their weights.
+template <int U>
+__device__ __forceinline__ void step_pixels(int p, int py, int p1, long img0, long (&pix)[U],
+                                            float (&w)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int pu = p + u * py;
+    pix[u] = img0 + (pu < p1 ? pu : p1 - 1);
+    w[u] = pu < p1 ? 1.f : 0.f;
+  }
+}
+
+constexpr int U_STATS = 4;  // pixels per loop step of the reductions
+constexpr int U_BWD = 2;    // of the backward kernels (more live constants)
+
+template <int DT, bool ADD, int U = U_STATS>
 __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid rg,
                                                           float* partial) {
   __shared__ float sm[256 * 16];
@@ -64,25 +147,21 @@ __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid 
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   if (r.active) {
-    // four pixels per iteration keep four loads in flight per thread
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += 4 * rg.py) {
-      float f[4][8];
+    const VCh8 h = resolve_v(x, r.c);
+    const long img0 = (long)r.b * g.hw();
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U * rg.py) {
+      long pix[U];
+      float w[U], f[U][8];
+      step_pixels<U>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int pu = p + u * rg.py;
-        if (pu < r.p1) {
-          ld8v(x, (long)r.b * g.hw() + pu, r.c, f[u]);
-        } else {
+      for (int u = 0; u < U; ++u) rdv8<DT, ADD>(h, pix[u], f[u]);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) f[u][i] = 0.f;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          acc[i] += f[u][i];
-          acc[8 + i] += f[u][i] * f[u][i];
+          const float v = w[u] * f[u][i];
+          acc[i] += v;
+          acc[8 + i] += v * f[u][i];
         }
     }
   }
@@ -142,30 +221,43 @@ __global__ __launch_bounds__(256) void k_gn_stats_finalize(const float* partial,
   }
 }
 
-__global__ __launch_bounds__(256) void k_gn_apply(VIn x, Geo g, const float* scale,
-                                                  const float* shift, void* dst0, void* dst1,
-                                                  int dtype) {
-  const int NV = x.C / 8;
-  const long total = g.pixels() * NV;
-  const int HW = g.hw();
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (long)gridDim.x * blockDim.x) {
-    const long pix = i / NV;
-    const int c = (int)(i - pix * NV) * 8;
-    const int b = (int)(pix / HW);
-    float f[8];
-    ld8v(x, pix, c, f);
-    const float4* sc = reinterpret_cast<const float4*>(scale + (long)b * x.C + c);
-    const float4* sh = reinterpret_cast<const float4*>(shift + (long)b * x.C + c);
+// a = SiLU(x * scale + shift) for the channels of one thread over its
+// chunk of pixels; channels below x.c0 go to dst0 (x.c0 channels per pixel),
+// the others to dst1 (x.C - x.c0 per pixel).
+template <int DT, bool ADD>
+__global__ __launch_bounds__(256) void k_gn_apply(VIn x, Geo g, RedGrid rg, const float* scale,
+                                                  const float* shift, void* dst0, void* dst1) {
+  const Range r = block_range(g, rg, x.C);
+  if (!r.active) return;
+  const VCh8 h = resolve_v(x, r.c);
+  const bool first = r.c < x.c0;
+  void* dst = first ? dst0 : dst1;
+  const long dstride = first ? x.c0 : x.C - x.c0;
+  const long dc = first ? r.c : r.c - x.c0;
+  float ss[8], hh[8];
+  {
+    const float4* sc = reinterpret_cast<const float4*>(scale + (long)r.b * x.C + r.c);
+    const float4* sh = reinterpret_cast<const float4*>(shift + (long)r.b * x.C + r.c);
     const float4 s0 = sc[0], s1 = sc[1], h0 = sh[0], h1 = sh[1];
-    const float ss[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-    const float hh[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+    ss[0] = s0.x; ss[1] = s0.y; ss[2] = s0.z; ss[3] = s0.w;
+    ss[4] = s1.x; ss[5] = s1.y; ss[6] = s1.z; ss[7] = s1.w;
+    hh[0] = h0.x; hh[1] = h0.y; hh[2] = h0.z; hh[3] = h0.w;
+    hh[4] = h1.x; hh[5] = h1.y; hh[6] = h1.z; hh[7] = h1.w;
+  }
+  const long img0 = (long)r.b * g.hw();
+  for (int p = r.p0 + threadIdx.y; p < r.p1; p += U_STATS * rg.py) {
+    long pix[U_STATS];
+    float w[U_STATS], f[U_STATS][8];
+    step_pixels<U_STATS>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) f[j] = silu_f(f[j] * ss[j] + hh[j]);
-    if (c < x.c0)
-      st8(dst0, dtype, x.c0, pix, c, f);
-    else
-      st8(dst1, dtype, x.C - x.c0, pix, c - x.c0, f);
+    for (int u = 0; u < U_STATS; ++u) rdv8<DT, ADD>(h, pix[u], f[u]);
+#pragma unroll
+    for (int u = 0; u < U_STATS; ++u) {
+      if (p + u * rg.py >= r.p1) break;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[u][j] = silu_f(f[u][j] * ss[j] + hh[j]);
+      st8(dst, DT, (int)dstride, pix[u], (int)dc, f[u]);
+    }
   }
 }
 
@@ -207,6 +299,7 @@ __device__ __forceinline__ void load_gn_const(GnConst& k, int b, int c, int C, i
   load_group_pair(rstd, b, G, c, cg, k.rs);
 }
 
+template <int DT, bool ADD, int U = U_BWD>
 __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
                                                         RedGrid rg, const float* scale,
                                                         const float* shift, const float* mean,
@@ -220,26 +313,24 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
   if (r.active) {
     GnConst k;
     load_gn_const(k, r.b, r.c, x.C, G, scale, shift, mean, rstd);
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
-      float f[1][8], d[1][8];
+    const VCh8 hx = resolve_v(x, r.c);
+    const Ch8 hd = resolve(da, r.c);
+    const long img0 = (long)r.b * g.hw();
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U * rg.py) {
+      long pix[U];
+      float w[U], f[U][8], d[U][8];
+      step_pixels<U>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-      for (int u = 0; u < 1; ++u) {
-        const int pu = p + u * rg.py;
-        if (pu < r.p1) {
-          const long pix = (long)r.b * g.hw() + pu;
-          ld8v(x, pix, r.c, f[u]);
-          ld8(da, pix, r.c, d[u]);
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) f[u][j] = d[u][j] = 0.f;
-        }
+      for (int u = 0; u < U; ++u) {
+        rdv8<DT, ADD>(hx, pix[u], f[u]);
+        rd8<DT>(hd, pix[u], d[u]);
       }
 #pragma unroll
-      for (int u = 0; u < 1; ++u)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float z = f[u][j] * k.sc[j] + k.sh[j];
-          const float dz = d[u][j] * dsilu_f(z);
+          const float dz = w[u] * d[u][j] * dsilu_f(z);
           const float xh = (f[u][j] - k.mu[j]) * k.rs[j];
           acc[j] += dz;
           acc[8 + j] += dz * xh;
@@ -410,9 +501,10 @@ __global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, 
 }
 
 // CHAN: the output's per-chunk channel sums are written (the timestep-
-// embedding gradient); ADD: the addends add0/add1 exist.  Each instance keeps
-// only the registers it needs.
-template <bool CHAN, bool ADD>
+// embedding gradient); ADD0: the addend o.add0 (stage dtype) exists; NF: the
+// number of fp32 addends (o.add0's own and o.add1, in that order).  Each
+// instance keeps only the registers it needs.
+template <int DT, bool CHAN, bool ADD0, int NF>
 __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
                                                       RedGrid rg, const float* scale,
                                                       const float* shift, const float* mean,
@@ -461,35 +553,50 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
         Cq[j] = -k.rs[j] * c0[j] - Bq[j] * k.mu[j];
       }
     }
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
-      const long pix = (long)r.b * g.hw() + p;
-      float f[8], d[8], out[8];
-      ld8v(x, pix, r.c, f);
-      ld8(da, pix, r.c, d);
+    const Ch8 hx = resolve(x, r.c);
+    const Ch8 hd = resolve(da, r.c);
+    const Ch8 h0 = ADD0 ? resolve(o.add0, r.c) : hx;
+    // fp32 addends: o.add0's own first, then o.add1 (both C channels per pixel)
+    const bool own = ADD0 && o.add0.add;
+    const float* fa0 = own ? o.add0.add + r.c : (o.add1 ? o.add1 + r.c : nullptr);
+    const float* fa1 = own && o.add1 ? o.add1 + r.c : nullptr;
+    const bool first = r.c < o.c_split;
+    void* dst = first ? o.dst0 : o.dst1;
+    const int dtype = first ? o.dtype0 : o.dtype1;
+    const int dstride = first ? o.c_split : C - o.c_split;
+    const int dc = first ? r.c : r.c - o.c_split;
+    const long img0 = (long)r.b * g.hw();
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U_BWD * rg.py) {
+      long pix[U_BWD];
+      float w[U_BWD], f[U_BWD][8], d[U_BWD][8], e[U_BWD][8];
+      step_pixels<U_BWD>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float dz = d[j] * dsilu_f(f[j] * sc[j] + sh[j]);
-        out[j] = A[j] * dz + (Bq[j] * f[j] + Cq[j]);
-      }
-      if (ADD && o.add0.s0.ptr) {
-        float e[8];
-        ld8v(o.add0, pix, r.c, e);
+      for (int u = 0; u < U_BWD; ++u) {
+        rd8<DT>(hx, pix[u], f[u]);
+        rd8<DT>(hd, pix[u], d[u]);
+        if constexpr (ADD0) {
+          rd8<DT>(h0, pix[u], e[u]);
+        } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) out[j] += e[j];
+          for (int j = 0; j < 8; ++j) e[u][j] = 0.f;
+        }
+        if constexpr (NF >= 1) add8(fa0, C, pix[u], e[u]);
+        if constexpr (NF >= 2) add8(fa1, C, pix[u], e[u]);
       }
-      if (ADD && o.add1) {
-        const float4* ap = reinterpret_cast<const float4*>(o.add1 + pix * C + r.c);
-        const float4 a0 = ap[0], a1 = ap[1];
-        out[0] += a0.x; out[1] += a0.y; out[2] += a0.z; out[3] += a0.w;
-        out[4] += a1.x; out[5] += a1.y; out[6] += a1.z; out[7] += a1.w;
-      }
-      if (r.c < o.c_split)
-        st8(o.dst0, o.dtype0, o.c_split, pix, r.c, out);
-      else
-        st8(o.dst1, o.dtype1, C - o.c_split, pix, r.c - o.c_split, out);
-      if (CHAN) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] += out[j];
+      for (int u = 0; u < U_BWD; ++u) {
+        if (p + u * rg.py >= r.p1) break;
+        float out[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float dz = d[u][j] * dsilu_f(f[u][j] * sc[j] + sh[j]);
+          out[j] = A[j] * dz + (Bq[j] * f[u][j] + Cq[j]) + e[u][j];
+        }
+        st8(dst, dtype, dstride, pix[u], dc, out);
+        if (CHAN) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[j] += out[j];
+        }
       }
     }
   }
@@ -499,6 +606,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
   }
 }
 
+template <int DT, bool ADD>
 __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid rg,
                                                           float* partial) {
   __shared__ float sm[256 * 8];
@@ -507,11 +615,18 @@ __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid 
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   if (r.active) {
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += rg.py) {
-      float f[8];
-      ld8v(v, (long)r.b * g.hw() + p, r.c, f);
+    const VCh8 h = resolve_v(v, r.c);
+    const long img0 = (long)r.b * g.hw();
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U_STATS * rg.py) {
+      long pix[U_STATS];
+      float w[U_STATS], f[U_STATS][8];
+      step_pixels<U_STATS>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] += f[j];
+      for (int u = 0; u < U_STATS; ++u) rdv8<DT, ADD>(h, pix[u], f[u]);
+#pragma unroll
+      for (int u = 0; u < U_STATS; ++u)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] += w[u] * f[u][j];
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * v.C;
@@ -524,6 +639,13 @@ dim3 red_dims(const Geo& g, RedGrid rg, int C) {
 }
 
 dim3 red_block(RedGrid rg) { return dim3(rg.vx, rg.py); }
+
+// Element type shared by every tensor source of a launch (the stage dtype),
+// or -1 when they disagree (no kernel is instantiated for that).
+int common_dt(const VIn& v) {
+  if (v.s1.ptr && v.c0 < v.C && v.s1.dtype != v.s0.dtype) return -1;
+  return v.s0.dtype;
+}
 
 }  // namespace
 
@@ -546,8 +668,14 @@ RedGrid red_grid(const Geo& g, int C) {
 
 hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_stats_partial, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg,
-                     partial);
+  const int dt = common_dt(x);
+  if (dt < 0) return hipErrorInvalidValue;
+  const bool add = x.add != nullptr;
+  auto kern = dt == DT_BF16 ? (add ? k_gn_stats_partial<DT_BF16, true>
+                                   : k_gn_stats_partial<DT_BF16, false>)
+                            : (add ? k_gn_stats_partial<DT_F32, true>
+                                   : k_gn_stats_partial<DT_F32, false>);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg, partial);
   return hipGetLastError();
 }
 
@@ -562,19 +690,29 @@ hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid 
 
 hipError_t launch_gn_apply(const VIn& x, const Geo& g, const float* scale, const float* shift,
                            void* dst0, void* dst1, int dtype, hipStream_t st) {
-  const long total = g.pixels() * (x.C / 8);
-  long blocks = (total + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(k_gn_apply, dim3((unsigned)blocks), dim3(256), 0, st, x, g, scale, shift,
-                     dst0, dst1, dtype);
+  const int dt = common_dt(x);
+  if (dt < 0 || dt != dtype) return hipErrorInvalidValue;
+  const RedGrid rg = red_grid(g, x.C);
+  const bool add = x.add != nullptr;
+  auto kern = dt == DT_BF16 ? (add ? k_gn_apply<DT_BF16, true> : k_gn_apply<DT_BF16, false>)
+                            : (add ? k_gn_apply<DT_F32, true> : k_gn_apply<DT_F32, false>);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg, scale, shift,
+                     dst0, dst1);
   return hipGetLastError();
 }
 
 hipError_t launch_gn_bwd_partial(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                  const float* scale, const float* shift, const float* mean,
                                  const float* rstd, int G, float* partial, hipStream_t st) {
-  hipLaunchKernelGGL(k_gn_bwd_partial, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
-                     scale, shift, mean, rstd, G, partial);
+  const int dt = common_dt(x);
+  if (dt < 0 || da.dtype != dt) return hipErrorInvalidValue;
+  const bool add = x.add != nullptr;
+  auto kern = dt == DT_BF16 ? (add ? k_gn_bwd_partial<DT_BF16, true>
+                                   : k_gn_bwd_partial<DT_BF16, false>)
+                            : (add ? k_gn_bwd_partial<DT_F32, true>
+                                   : k_gn_bwd_partial<DT_F32, false>);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg, scale,
+                     shift, mean, rstd, G, partial);
   return hipGetLastError();
 }
 
@@ -594,22 +732,51 @@ hipError_t launch_chan_totals(const float* partial, const Geo& g, RedGrid rg, in
   return hipGetLastError();
 }
 
+namespace {
+
+template <int DT, bool CHAN, bool ADD0>
+auto bwd_apply_kernel(int nf) {
+  return nf == 0 ? k_gn_bwd_apply<DT, CHAN, ADD0, 0>
+                 : nf == 1 ? k_gn_bwd_apply<DT, CHAN, ADD0, 1> : k_gn_bwd_apply<DT, CHAN, ADD0, 2>;
+}
+
+template <int DT>
+auto bwd_apply_kernel(bool chan, bool add0, int nf) {
+  return chan ? (add0 ? bwd_apply_kernel<DT, true, true>(nf) : bwd_apply_kernel<DT, true, false>(nf))
+              : (add0 ? bwd_apply_kernel<DT, false, true>(nf)
+                      : bwd_apply_kernel<DT, false, false>(nf));
+}
+
+}  // namespace
+
 hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
                                int G, const GnBwdOut& o, hipStream_t st) {
-  const bool chan = o.chan_partial != nullptr, add = o.add0.s0.ptr || o.add1;
-  auto kern = chan ? (add ? k_gn_bwd_apply<true, true> : k_gn_bwd_apply<true, false>)
-                   : (add ? k_gn_bwd_apply<false, true> : k_gn_bwd_apply<false, false>);
-  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg,
-                     scale, shift, mean, rstd, gamma, coef, G, o);
+  const int dt = common_dt(x);
+  const bool add0 = o.add0.s0.ptr != nullptr;
+  // x is a forward activation (no addend); add0 shares the stage dtype
+  if (dt < 0 || da.dtype != dt || x.add || (add0 && common_dt(o.add0) != dt))
+    return hipErrorInvalidValue;
+  const int nf = (add0 && o.add0.add ? 1 : 0) + (o.add1 ? 1 : 0);
+  const bool chan = o.chan_partial != nullptr;
+  auto kern = dt == DT_BF16 ? bwd_apply_kernel<DT_BF16>(chan, add0, nf)
+                            : bwd_apply_kernel<DT_F32>(chan, add0, nf);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg, scale, shift,
+                     mean, rstd, gamma, coef, G, o);
   return hipGetLastError();
 }
 
 hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st) {
-  hipLaunchKernelGGL(k_chan_sum_partial, red_dims(g, rg, v.C), red_block(rg), 0, st, v, g, rg,
-                     partial);
+  const int dt = common_dt(v);
+  if (dt < 0) return hipErrorInvalidValue;
+  const bool add = v.add != nullptr;
+  auto kern = dt == DT_BF16 ? (add ? k_chan_sum_partial<DT_BF16, true>
+                                   : k_chan_sum_partial<DT_BF16, false>)
+                            : (add ? k_chan_sum_partial<DT_F32, true>
+                                   : k_chan_sum_partial<DT_F32, false>);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, v.C), red_block(rg), 0, st, v, g, rg, partial);
   return hipGetLastError();
 }
 

@@ -131,11 +131,14 @@ struct pulse_stage {
   size_t part_cap = 0;   // weight-gradient split partials (elements)
   size_t kpart_cap = 0;  // conv K-split partials (elements)
   size_t s_kpart = 0, s_red2 = 0;
+  size_t s_chp[2] = {0, 0};  // per-chunk channel sums of dh1 (GN2 backward), by block parity
+  int cmax = 0;              // widest channel count of any block
   // side stream: the weight-gradient GEMMs of the backward pass run on it,
   // concurrently with the data-gradient chain on the caller's stream
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_w2[2] = {nullptr, nullptr}, ev_w1[2] = {nullptr, nullptr};
+  hipEvent_t ev_temb = nullptr;  // the forward's timestep projections are ready
   // binding
   const float* prm = nullptr;
   float* grd = nullptr;
@@ -421,9 +424,16 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_kpart = sc; sc += align256(kpart * 4);
   s->s_red = sc; sc += align256(red * 4);
   s->s_red2 = sc; sc += align256(red * 4);  // reductions on the side stream
+  for (int i = 0; i < 2; ++i) {
+    s->s_chp[i] = sc;
+    sc += align256(red * 4);
+  }
   s->s_coef = sc; sc += align256((size_t)s->geo.B * s->G * 2 * 4);
   s->s_pi = sc; sc += align256((size_t)2 * s->geo.B * cmax * 4);
-  s->s_e = sc; sc += align256((size_t)s->geo.B * cmax * 4);
+  s->cmax = cmax;
+  // one timestep projection per block of the larger half
+  const size_t nblk = std::max(s->eb.size(), s->db.size());
+  s->s_e = sc; sc += align256(nblk * s->geo.B * cmax * 4);
   s->s_zero = sc; sc += 256;  // zero bytes read in place of out-of-image taps
   s->ws_bytes = s->off_scratch + sc;
   return PULSE_OK;
@@ -743,9 +753,7 @@ pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& 
   const float* shift = reinterpret_cast<const float*>(row + g.shift);
   HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
   HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta, st));
-  GnBwdOut oo = o;
-  if (oo.chan_partial) oo.chan_partial = red;  // reuse: the partials above are consumed
-  HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, oo,
+  HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, o,
                              st));
   return PULSE_OK;
 }
@@ -769,9 +777,18 @@ VIn block_input(pulse_stage* s, int r, const Block& b, int k, const void* dec_up
   return vin2(up, dt, b.c0, row + s->row_act[b.slot], dt, b.cin - b.c0);
 }
 
+// The side stream is used unless per-kernel timing is on: timed conv
+// launches then run alone on the caller's stream, so their events measure
+// the kernel and not its overlap with the weight-gradient GEMMs.
+bool use_side(const pulse_stage* s) { return s->side && !s->timing; }
+
+float* temb_slice(pulse_stage* s, int k) {
+  return s->sf(s->s_e) + (size_t)k * s->geo.B * s->cmax;
+}
+
 // One ResBlock forward.  `out` receives the block output, `out2` a copy.
 pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin, void* out,
-                           void* out2, hipStream_t st) {
+                           void* out2, const float* e, bool wait_temb, hipStream_t st) {
   char* row = s->row_base(r);
   const int dt = s->dtype;
   void* a1_0 = row + b.a1_0;
@@ -780,10 +797,9 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
   // a1 = SiLU(GN1(x)), one tensor per source
   if ((ps = gn_forward(s, row, b.gn1, xin, s->pp(b.g1), s->pp(b.be1), a1_0, a1_1, st)) != PULSE_OK)
     return ps;
-  // e = b1 + bl + Wl SiLU(temb)
-  float* e = s->sf(s->s_e);
-  HIPCHK(launch_temb_fwd(row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
-                         s->pp(b.b1), s->pp(b.bl), e, st));
+  // e = b1 + bl + Wl SiLU(temb), computed for every block of the half on
+  // the side stream (temb_prefetch)
+  if (wait_temb && use_side(s)) HIPCHK(hipStreamWaitEvent(st, s->ev_temb, 0));
   const VIn a1 = (b.cin > b.c0) ? vin2(a1_0, dt, b.c0, a1_1, dt, b.cin - b.c0)
                                 : vin1(a1_0, dt, b.cin);
   void* h1 = row + b.h1;
@@ -806,10 +822,6 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
 }
 
 // One ResBlock backward.  dout: gradient w.r.t. the block output.  o: where
-// The side stream is used unless per-kernel timing is on: timed conv
-// launches then run alone on the caller's stream, so their events measure
-// the kernel and not its overlap with the weight-gradient GEMMs.
-bool use_side(const pulse_stage* s) { return s->side && !s->timing; }
 
 // Fork: work enqueued on the side stream after this starts once everything
 // enqueued on `st` so far has finished.  Join: `st` continues once the side
@@ -847,6 +859,26 @@ pulse_status join_side(pulse_stage* s, hipStream_t st) {
   if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(s->ev_join, s->side));
   HIPCHK(hipStreamWaitEvent(st, s->ev_join, 0));
+  return PULSE_OK;
+}
+
+// Timestep projections e_k = b1 + bl + Wl SiLU(temb) of every block of one
+// half, into consecutive [B][cmax] slices of the e buffer.  They run on the
+// side stream while the first block's GroupNorm runs here; the first conv1
+// waits for ev_temb.  The fork orders them after this stream's earlier
+// work, which includes every read of the previous call's projections.
+pulse_status temb_prefetch(pulse_stage* s, int r, const std::vector<Block>& blocks, int half,
+                           hipStream_t st) {
+  char* row = s->row_base(r);
+  hipStream_t sd = use_side(s) ? s->side : st;
+  pulse_status ps;
+  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;
+  for (size_t k = 0; k < blocks.size(); ++k) {
+    const Block& b = blocks[k];
+    HIPCHK(launch_temb_fwd(row + s->row_temb[half], s->dtype, s->geo.B, s->D, b.cout,
+                           s->pp(b.Wl), s->pp(b.b1), s->pp(b.bl), temb_slice(s, (int)k), sd));
+  }
+  if (use_side(s)) HIPCHK(hipEventRecord(s->ev_temb, s->side));
   return PULSE_OK;
 }
 
@@ -908,22 +940,26 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     o2.dtype0 = dt;
     o2.c_split = b.cout;
     o2.add0 = vnone();
-    o2.chan_partial = s->sf(s->s_red);
+    o2.chan_partial = s->sf(s->s_chp[par]);
     const VIn h1v = vin1(row + b.h1, dt, b.cout);
     if ((ps = gn_backward(s, row, b.gn2, h1v, s->pp(b.g2), s->gp(b.g2), s->gp(b.be2), da, o2,
                           st)) != PULSE_OK)
       return ps;
-    const RedGrid rg = red_grid(s->geo, b.cout);
-    float* de = s->sf(s->s_pi);  // per-image sums of dh1: [B][cout]
-    HIPCHK(launch_chan_per_image(s->sf(s->s_red), s->geo, rg, b.cout, 1, de, st));
-    HIPCHK(launch_temb_bwd(de, row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout, s->pp(b.Wl),
-                           s->gp(b.Wl), s->gp(b.bl), s->gp(b.b1), dtemb, st));
   }
   // conv1 weight and data gradients
   const VIn a1 = (b.cin > b.c0) ? vin2(row + b.a1_0, dt, b.c0, row + b.a1_1, dt, b.cin - b.c0)
                                 : vin1(row + b.a1_0, dt, b.cin);
   const VIn dh1v = vin1(dh1, dt, b.cout);
-  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;  // dh1 is complete
+  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;  // dh1 and its sums are complete
+  {
+    // the timestep-embedding gradient from the per-image sums of dh1, on the
+    // side stream (the next write of this parity's sums waits for ev_w1)
+    const RedGrid rg = red_grid(s->geo, b.cout);
+    float* de = s->sf(s->s_pi);  // [B][cout]
+    HIPCHK(launch_chan_per_image(s->sf(s->s_chp[par]), s->geo, rg, b.cout, 1, de, sd));
+    HIPCHK(launch_temb_bwd(de, row + s->row_temb[b.dec ? 1 : 0], dt, s->geo.B, s->D, b.cout,
+                           s->pp(b.Wl), s->gp(b.Wl), s->gp(b.bl), s->gp(b.b1), dtemb, sd));
+  }
   if ((ps = wgrad(s, b.cout, {seg3(0, b.cin, a1, s->gp(b.W1))}, dh1v, sd)) != PULSE_OK)
     return ps;
   if ((ps = mark_side(s, s->ev_w1[par])) != PULSE_OK) return ps;
@@ -1003,6 +1039,7 @@ void pulse_stage_destroy(pulse_stage* s) {
     if (s->ev_w2[i]) (void)hipEventDestroy(s->ev_w2[i]);
     if (s->ev_w1[i]) (void)hipEventDestroy(s->ev_w1[i]);
   }
+  if (s->ev_temb) (void)hipEventDestroy(s->ev_temb);
   if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
 }
@@ -1057,6 +1094,7 @@ pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads,
       HIPCHK(hipEventCreateWithFlags(&s->ev_w2[i], hipEventDisableTiming));
       HIPCHK(hipEventCreateWithFlags(&s->ev_w1[i], hipEventDisableTiming));
     }
+    HIPCHK(hipEventCreateWithFlags(&s->ev_temb, hipEventDisableTiming));
   }
   s->prm = params;
   s->grd = grads;
@@ -1147,6 +1185,7 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
                                                : row + s->row_xin;
       HIPCHK(hipMemcpyAsync(xin_store, in, act_bytes(s, s->eb[0].cin), hipMemcpyDeviceToDevice,
                             st));
+      if ((ps = temb_prefetch(s, r, s->eb, 0, st)) != PULSE_OK) return ps;
       const int n = (int)s->eb.size();
       for (int k = 0; k < n; ++k) {
         const Block& b = s->eb[k];
@@ -1159,18 +1198,22 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
         } else {
           o1 = (k == n - 1) ? out : row + b.out_saved;
         }
-        if ((ps = block_forward(s, r, b, xin, o1, o2, st)) != PULSE_OK) return ps;
+        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, st)) != PULSE_OK)
+          return ps;
       }
       (void)dt;
     } else {
       HIPCHK(hipMemcpyAsync(row + s->row_u, in, act_bytes(s, s->db[0].c0),
                             hipMemcpyDeviceToDevice, st));
+      if ((ps = temb_prefetch(s, r, s->db, 1, st)) != PULSE_OK) return ps;
       const int n = (int)s->db.size();
       for (int k = 0; k < n; ++k) {
         const Block& b = s->db[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
         void* o1 = (k == n - 1) ? out : row + b.out_saved;
-        if ((ps = block_forward(s, r, b, xin, o1, nullptr, st)) != PULSE_OK) return ps;
+        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, st)) !=
+            PULSE_OK)
+          return ps;
       }
     }
   }
