@@ -496,9 +496,15 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   __syncthreads();
 
   // epilogue in 16-row slices: accumulators -> LDS -> 8-channel rows
-  // (+bias, +rowvec, +residual) -> 16-byte stores
+  // (+bias, +rowvec, +residual) -> 16-byte stores.  With a.stats the stored
+  // (bf16-rounded) values go back to the slice in LDS and thread t < BN adds
+  // column t of every slice to its running sum and sum of squares: the
+  // GroupNorm statistics of the output, one row per (image, M-tile).
   float* ct = reinterpret_cast<float*>(smem);
   constexpr int NV8 = C::BN / 8;
+  static_assert(C::BN <= C::NT, "one thread per output column for the statistics");
+  const bool stats = a.stats != nullptr;
+  float csum = 0.f, csq = 0.f;
 #pragma unroll 1
   for (int g = 0; g < C::WAVES_M; ++g) {
 #pragma unroll
@@ -510,7 +516,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         const int n = n0 + (e - row * NV8) * 8;
         const long m = m0 + g * C::WM + i * 16 + row;
         if (m >= P || n >= a.N) continue;
-        const float* src = ct + row * C::LDC + (n - n0);
+        float* src = ct + row * C::LDC + (n - n0);
         const float4 s0 = reinterpret_cast<const float4*>(src)[0];
         const float4 s1 = reinterpret_cast<const float4*>(src)[1];
         if (a.ksplit > 1) {  // raw partial; the finalize adds the epilogue terms
@@ -537,9 +543,35 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         }
         st8(a.out, a.out_dtype, a.ldo, m, n, v);
         if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
+        if (stats) {
+          float4* w = reinterpret_cast<float4*>(src);
+          w[0] = make_float4(bf2f(f2bf(v[0])), bf2f(f2bf(v[1])), bf2f(f2bf(v[2])),
+                             bf2f(f2bf(v[3])));
+          w[1] = make_float4(bf2f(f2bf(v[4])), bf2f(f2bf(v[5])), bf2f(f2bf(v[6])),
+                             bf2f(f2bf(v[7])));
+        }
       }
       __syncthreads();
+      if (stats) {
+        if (tid < C::BN) {
+#pragma unroll 4
+          for (int row = 0; row < 16; ++row) {
+            const float x = ct[row * C::LDC + tid];
+            csum += x;
+            csq += x * x;
+          }
+        }
+        __syncthreads();
+      }
     }
+  }
+  if (stats && tid < C::BN && n0 + tid < a.N) {
+    // the launcher guarantees H*W % BM == 0: the tile lies in one image
+    const int img = (int)(m0 / HW);
+    const int chunk = (int)(m0 - (long)img * HW) / C::BM;
+    float* dst = a.stats + ((long)img * (HW / C::BM) + chunk) * 2 * a.N + n0 + tid;
+    dst[0] = csum;
+    dst[a.N] = csq;
   }
 #else
   (void)a;
@@ -1128,6 +1160,8 @@ using W2_160x128 = CfgW<160, 128, 80, 64>;   // 4 waves
 
 template <class C>
 static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
+  // output statistics need whole tiles inside one image and no K split
+  if (a.stats && (a.ksplit > 1 || a.g.hw() % C::BM != 0)) return hipErrorInvalidValue;
   const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
   const int ks = a.ksplit > 1 ? a.ksplit : 1;

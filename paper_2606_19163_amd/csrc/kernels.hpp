@@ -45,6 +45,10 @@ struct GemmArgs {
   VIn gy;              // output gradient, M channels
   int kchunk;          // pixels per split
   float* part;         // [splits][M][N] fp32 partials (both modes)
+  // CONV mode of the LDS-DMA kernels without a K split, when H*W % BM == 0:
+  // per-channel sum and sum of squares of the output as stored (bf16), one
+  // row per (image, M-tile): [B][H*W / BM][2][N]; null: not computed
+  float* stats;
 };
 
 // implicit GEMM (igemm.hip): tile shapes (block M x block N; bf16, 64

@@ -133,6 +133,7 @@ struct pulse_stage {
   size_t s_kpart = 0, s_red2 = 0;
   size_t s_chp[2] = {0, 0};  // per-chunk channel sums of dh1 (GN2 backward), by block parity
   int cmax = 0;              // widest channel count of any block
+  size_t red_cap = 0;        // floats in each reduction buffer
   // side stream: the weight-gradient GEMMs of the backward pass run on it,
   // concurrently with the data-gradient chain on the caller's stream
   hipStream_t side = nullptr;
@@ -422,6 +423,7 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_part = sc; sc += align256(part * 4);
   s->kpart_cap = kpart;
   s->s_kpart = sc; sc += align256(kpart * 4);
+  s->red_cap = red;
   s->s_red = sc; sc += align256(red * 4);
   s->s_red2 = sc; sc += align256(red * 4);  // reductions on the side stream
   for (int i = 0; i < 2; ++i) {
@@ -605,7 +607,8 @@ double conv_bytes(const pulse_stage* s, const GemmArgs& a) {
   return b;
 }
 
-pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
+pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_chunks = nullptr) {
+  if (stats_chunks) *stats_chunks = 0;
   const int tile = conv_tile(s, a.N);
   const int ks = conv_ksplit(s, tile, a.N, a.K);
   const int kt = a.K / info_of(s, tile).bk;
@@ -628,6 +631,18 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st) {
   const bool halo = uses_v2(s) && s->conv_tile_force < 0 && ks == 1 && s->halo > 0 &&
                     halo_conv_fits(s->geo, a.N) &&
                     (s->halo == 2 || (s->P / 256) * (a.N / 160) >= 256);
+  // output statistics from the epilogue: LDS-DMA tiles, no K split, whole
+  // tiles per image, and room in the reduction buffer; else the caller's
+  // GroupNorm computes them itself (stats_chunks stays 0)
+  if (a.stats) {
+    const int bm = info_of(s, tile).bm;
+    const long rows = s->geo.hw() % bm == 0 ? (long)s->geo.B * (s->geo.hw() / bm) : 0;
+    if (stats_chunks && !halo && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
+        (size_t)rows * 2 * a.N <= s->red_cap)
+      *stats_chunks = s->geo.hw() / bm;
+    else
+      a.stats = nullptr;
+  }
   if (halo)
     HIPCHK(launch_conv_halo(a, st));
   else if (uses_v2(s))
@@ -673,9 +688,13 @@ Seg seg1(int begin, int C, const VIn& in, float* grad = nullptr) {
 }
 
 // forward conv: out[P][N] = sum_seg conv(seg) (+bias, +rowvec, +resid)
+// With `stats`, the output's GroupNorm partial sums come from the conv's
+// epilogue when the kernel can produce them: *stats_chunks receives their
+// chunks per image, or 0 when they were not computed.
 pulse_status conv_fwd(pulse_stage* s, int N, std::initializer_list<Seg> segs, const void* W,
                       int ldb, const float* bias, const float* rowvec, const VIn& resid,
-                      void* out, void* out2, int out_dtype, hipStream_t st) {
+                      void* out, void* out2, int out_dtype, hipStream_t st,
+                      float* stats = nullptr, int* stats_chunks = nullptr) {
   GemmArgs a = gemm_base(s);
   a.M = (int)s->P;
   a.N = N;
@@ -694,7 +713,8 @@ pulse_status conv_fwd(pulse_stage* s, int N, std::initializer_list<Seg> segs, co
   a.out2 = out2;
   a.out_dtype = out_dtype;
   a.ldo = N;
-  return run_conv(s, a, st);
+  a.stats = stats;
+  return run_conv(s, a, st, stats_chunks);
 }
 
 pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const VIn& gy,
@@ -723,12 +743,18 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
   return PULSE_OK;
 }
 
+// GroupNorm+SiLU forward of x into dst0/dst1.  pre_chunks > 0: the
+// per-chunk channel sums of x are already in the reduction buffer, with that
+// many chunks per image (written by the producing conv's epilogue).
 pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
                         const float* gamma, const float* beta, void* dst0, void* dst1,
-                        hipStream_t st) {
-  const RedGrid rg = red_grid(s->geo, x.C);
+                        hipStream_t st, int pre_chunks = 0) {
+  RedGrid rg = red_grid(s->geo, x.C);
   float* red = s->sf(s->s_red);
-  HIPCHK(launch_gn_stats_partial(x, s->geo, rg, red, st));
+  if (pre_chunks > 0)
+    rg.chunks = pre_chunks;
+  else
+    HIPCHK(launch_gn_stats_partial(x, s->geo, rg, red, st));
   float* mean = reinterpret_cast<float*>(row + g.mean);
   float* rstd = reinterpret_cast<float*>(row + g.rstd);
   float* scale = reinterpret_cast<float*>(row + g.scale);
@@ -803,14 +829,15 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
   const VIn a1 = (b.cin > b.c0) ? vin2(a1_0, dt, b.c0, a1_1, dt, b.cin - b.c0)
                                 : vin1(a1_0, dt, b.cin);
   void* h1 = row + b.h1;
+  int h1_chunks = 0;  // GN2 statistics of h1 from conv1's epilogue, when it can
   if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cin, a1)}, s->ws + b.wf1, 9 * b.cin, nullptr, e,
-                     vnone(), h1, nullptr, dt, st)) != PULSE_OK)
+                     vnone(), h1, nullptr, dt, st, s->sf(s->s_red), &h1_chunks)) != PULSE_OK)
     return ps;
   // a2 = SiLU(GN2(h1))
   const VIn h1v = vin1(h1, dt, b.cout);
   void* a2 = row + b.a2;
-  if ((ps = gn_forward(s, row, b.gn2, h1v, s->pp(b.g2), s->pp(b.be2), a2, nullptr, st)) !=
-      PULSE_OK)
+  if ((ps = gn_forward(s, row, b.gn2, h1v, s->pp(b.g2), s->pp(b.be2), a2, nullptr, st,
+                       h1_chunks)) != PULSE_OK)
     return ps;
   const VIn a2v = vin1(a2, dt, b.cout);
   const float* bias2 = reinterpret_cast<const float*>(s->ws + b.bias2);
