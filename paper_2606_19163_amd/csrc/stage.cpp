@@ -103,6 +103,7 @@ struct pulse_stage {
   size_t esz = 4;
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
+  int conv_ksplit_cap = 16;  // largest conv K split (env PULSE_CONV_KSPLIT_MAX)
   // halo-reuse conv: 0 never (default: it measured slower in the full step,
   // where its 147 KB of LDS keeps the side stream's GEMMs off its CUs), 1
   // when its grid fills the GPU, 2 whenever it fits
@@ -254,7 +255,7 @@ int conv_ksplit(const pulse_stage* s, int tile, int N, int K) {
   if (tiles >= want) return 1;
   long ks = (want + tiles - 1) / tiles;
   ks = std::min(ks, std::max(1L, (long)(K / ti.bk) / 4));
-  return (int)std::min(ks, 16L);
+  return (int)std::min(ks, (long)s->conv_ksplit_cap);
 }
 
 // Pixel split of a weight-gradient GEMM.  With s splits the grid holds
@@ -343,6 +344,7 @@ pulse_status build_layout(pulse_stage* s) {
     s->v2 = env_int("PULSE_GEMM_V1", 0) == 0;
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
     s->halo = env_int("PULSE_HALO", 0);
+    s->conv_ksplit_cap = std::max(1, std::min(16, env_int("PULSE_CONV_KSPLIT_MAX", 16)));
     if (s->v2) {
       s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
       s->wgrad_tile_force = (wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
@@ -813,15 +815,21 @@ float* temb_slice(pulse_stage* s, int k) {
 }
 
 // One ResBlock forward.  `out` receives the block output, `out2` a copy.
+// in_chunks > 0: the GN1 statistics of xin are
+// already in the reduction buffer (from the previous block's conv2);
+// out_chunks non-null: ask conv2 for the statistics of `out` (receives their
+// chunks per image, 0 when not computed).
 pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin, void* out,
-                           void* out2, const float* e, bool wait_temb, hipStream_t st) {
+                           void* out2, const float* e, bool wait_temb, int in_chunks,
+                           int* out_chunks, hipStream_t st) {
   char* row = s->row_base(r);
   const int dt = s->dtype;
   void* a1_0 = row + b.a1_0;
   void* a1_1 = row + b.a1_1;
   pulse_status ps;
   // a1 = SiLU(GN1(x)), one tensor per source
-  if ((ps = gn_forward(s, row, b.gn1, xin, s->pp(b.g1), s->pp(b.be1), a1_0, a1_1, st)) != PULSE_OK)
+  if ((ps = gn_forward(s, row, b.gn1, xin, s->pp(b.g1), s->pp(b.be1), a1_0, a1_1, st,
+                       in_chunks)) != PULSE_OK)
     return ps;
   // e = b1 + bl + Wl SiLU(temb), computed for every block of the half on
   // the side stream (temb_prefetch)
@@ -841,11 +849,13 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
     return ps;
   const VIn a2v = vin1(a2, dt, b.cout);
   const float* bias2 = reinterpret_cast<const float*>(s->ws + b.bias2);
+  float* ostats = out_chunks ? s->sf(s->s_red) : nullptr;  // GN2 has consumed it
   if (b.conv_sc)
     return conv_fwd(s, b.cout, {seg3(0, b.cout, a2v), seg1(9 * b.cout, b.cin, xin)},
-                    s->ws + b.wf2, b.ldb2, bias2, nullptr, vnone(), out, out2, dt, st);
+                    s->ws + b.wf2, b.ldb2, bias2, nullptr, vnone(), out, out2, dt, st, ostats,
+                    out_chunks);
   return conv_fwd(s, b.cout, {seg3(0, b.cout, a2v)}, s->ws + b.wf2, b.ldb2, bias2, nullptr, xin,
-                  out, out2, dt, st);
+                  out, out2, dt, st, ostats, out_chunks);
 }
 
 // One ResBlock backward.  dout: gradient w.r.t. the block output.  o: where
@@ -1214,6 +1224,7 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
                             st));
       if ((ps = temb_prefetch(s, r, s->eb, 0, st)) != PULSE_OK) return ps;
       const int n = (int)s->eb.size();
+      int chunks = 0;  // GN1 statistics of the next block's input, from conv2
       for (int k = 0; k < n; ++k) {
         const Block& b = s->eb[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
@@ -1225,7 +1236,10 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
         } else {
           o1 = (k == n - 1) ? out : row + b.out_saved;
         }
-        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, st)) != PULSE_OK)
+        // the next encoder block normalises exactly this output
+        const int in_chunks = chunks;
+        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, in_chunks,
+                                k + 1 < n ? &chunks : nullptr, st)) != PULSE_OK)
           return ps;
       }
       (void)dt;
@@ -1238,8 +1252,8 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
         const Block& b = s->db[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
         void* o1 = (k == n - 1) ? out : row + b.out_saved;
-        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, st)) !=
-            PULSE_OK)
+        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, 0, nullptr,
+                                st)) != PULSE_OK)
           return ps;
       }
     }

@@ -83,6 +83,19 @@ def test_every_conv_tile(tile, monkeypatch):
     _case(configs.shrink(configs.l64(), batch=2, hw=12, width=10), 2, f"l64s conv tile {tile}")
 
 
+@pytest.mark.parametrize("tile", [-1, 0, 2, 3, 4])
+def test_conv_epilogue_statistics(tile, monkeypatch):
+    """Convs without a K split whose tiles lie inside one image compute the
+    GroupNorm statistics of their output in the epilogue (GN2 after conv1,
+    the next encoder block's GN1 after conv2): 16x16 images hold whole
+    128- and 256-pixel tiles; the K split is switched off so that the path
+    runs at a size the oracle finishes quickly."""
+    monkeypatch.setenv("PULSE_CONV_KSPLIT_MAX", "1")
+    if tile >= 0:
+        monkeypatch.setenv("PULSE_CONV_TILE", str(tile))
+    _case(configs.shrink(configs.l64(), batch=2, hw=16), 2, f"l64s epilogue stats tile {tile}")
+
+
 @pytest.mark.parametrize("tile", [10, 11, 12, 13])
 def test_every_wgrad_tile(tile, monkeypatch):
     """Every weight-gradient tile shape of the LDS-DMA path."""
