@@ -31,28 +31,30 @@ __device__ __forceinline__ Range block_range(const Geo& g, RedGrid rg, int C) {
   return r;
 }
 
-// Sum the pixel lanes of NV values per thread through LDS (fixed order) and
-// let lane 0 write 8 of them to out0 (and the next 8 to out1).
+// Sum the pixel lanes of NV values per thread through LDS and store the
+// block's totals: component i < 8 of channel vector v to row0[8 v + i],
+// component 8 + i to row1[8 v + i] (v = this block's channel vectors, those
+// below C / 8).  Values go to LDS component-major (conflict-free), and
+// every thread of the block then sums some of the vx * NV totals over the
+// py lanes in a fixed order.  sm holds NV * 256 floats.
 template <int NV>
-__device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, RedGrid rg,
-                                                  bool active, float* out0, float* out1) {
-  const int tx = threadIdx.x, ty = threadIdx.y;
+__device__ __forceinline__ void lane_reduce_store(float (&v)[NV], float* sm, RedGrid rg, int C,
+                                                  float* row0, float* row1) {
+  const int t = threadIdx.y * rg.vx + threadIdx.x;
+  const int nt = rg.vx * rg.py;
 #pragma unroll
-  for (int i = 0; i < NV; ++i) sm[(ty * rg.vx + tx) * NV + i] = v[i];
+  for (int i = 0; i < NV; ++i) sm[i * 256 + t] = v[i];
   __syncthreads();
-  if (ty == 0 && active) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      float s = sm[tx * NV + i];
-      for (int y = 1; y < rg.py; ++y) s += sm[(y * rg.vx + tx) * NV + i];
-      v[i] = s;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) out0[i] = v[i];
-    if (out1) {
-#pragma unroll
-      for (int i = 0; i < 8 && 8 + i < NV; ++i) out1[i] = v[8 + i];
-    }
+  for (int q = t; q < rg.vx * NV; q += nt) {
+    const int i = q / rg.vx, tx = q - i * rg.vx;
+    float s = 0.f;
+    for (int y = 0; y < rg.py; ++y) s += sm[i * 256 + y * rg.vx + tx];
+    const int c = ((int)blockIdx.z * rg.vx + tx) * 8;
+    if (c >= C) continue;
+    if (i < 8)
+      row0[c + i] = s;
+    else
+      row1[c + i - 8] = s;
   }
 }
 
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid 
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
-  lane_reduce_store<16>(acc, sm, rg, r.active, base + r.c, base + x.C + r.c);
+  lane_reduce_store<16>(acc, sm, rg, x.C, base, base + x.C);
 }
 
 // Fixed-order block sum of two fp64 values (256 threads).
@@ -338,7 +340,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * x.C;
-  lane_reduce_store<16>(acc, sm, rg, r.active, base + r.c, base + x.C + r.c);
+  lane_reduce_store<16>(acc, sm, rg, x.C, base, base + x.C);
 }
 
 // Per-image channel sums of the partials: pi[s][b][c] = sum_chunk
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
   }
   if (CHAN) {
     float* base = o.chan_partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * C;
-    lane_reduce_store<8>(acc, sm, rg, r.active, base + r.c, nullptr);
+    lane_reduce_store<8>(acc, sm, rg, C, base, nullptr);
   }
 }
 
@@ -630,7 +632,7 @@ __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid 
     }
   }
   float* base = partial + ((long)r.b * rg.chunks + blockIdx.y) * 2 * v.C;
-  lane_reduce_store<8>(acc, sm, rg, r.active, base + r.c, nullptr);
+  lane_reduce_store<8>(acc, sm, rg, v.C, base, nullptr);
 }
 
 dim3 red_dims(const Geo& g, RedGrid rg, int C) {
