@@ -877,6 +877,12 @@ __global__ __launch_bounds__(512) void igemm_halo_conv(GemmArgs a) {
 // WGRAD mode
 // ---------------------------------------------------------------------------
 
+// Balanced weight-gradient split: block b of nb owns units [b U / nb,
+// (b + 1) U / nb) of the U = tiles x K-steps units; the block owning unit v.
+__host__ __device__ __forceinline__ int sk_block_of(long v, long U, int nb) {
+  return (int)(((v + 1) * nb - 1) / U);
+}
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* zero16) {
   // the body exists for the device pass only (the host pass emits the launch stub)
@@ -888,19 +894,45 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
-  // block -> (split, tile), split-major over a contiguous range per XCD, so
-  // the blocks of one pixel split share that XCD's L2
+  // Work of this block, as segments (tile, pixel range, partial slot z).
+  // Uniform splits: block -> (split z, tile), split-major over a contiguous
+  // range per XCD, so the blocks of one pixel split share that XCD's L2; one
+  // segment of kchunk pixels.  Balanced (a.sk_blocks > 0): the tiles' K-steps
+  // in tile-major order are dealt out as equal contiguous ranges, one per
+  // block; a range may end in one tile and continue in the next, and the
+  // i-th block touching a tile writes partial slot i (sk_plan).
   const int tilesN = (a.N + C::BN - 1) / C::BN;
   const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
-  const int z = lb / ntiles;
-  const int tile = lb - z * ntiles;
-  const int m0 = (tile / tilesN) * C::BM;
-  const int n0 = (tile % tilesN) * C::BN;
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
   const long P = a.g.pixels();
-  const long pbeg = (long)z * a.kchunk;
-  const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
+  const long KTT = (P + C::BK - 1) / C::BK;  // K-steps of a whole tile
+  const long U = (long)ntiles * KTT;
+  long u = 0, uend = 0;
+  if (a.sk_blocks > 0) {
+    u = (long)lb * U / a.sk_blocks;
+    uend = (long)(lb + 1) * U / a.sk_blocks;
+  }
+  for (;;) {
+  int tile, z;
+  long pbeg, pend, kdone = 0;
+  if (a.sk_blocks > 0) {
+    if (u >= uend) break;
+    tile = (int)(u / KTT);
+    const long k0 = u - (long)tile * KTT;
+    const long k1 = k0 + (uend - u) < KTT ? k0 + (uend - u) : KTT;
+    kdone = k1 - k0;
+    pbeg = k0 * C::BK;
+    pend = k1 * C::BK < P ? k1 * C::BK : P;
+    z = lb - sk_block_of((long)tile * KTT, U, a.sk_blocks);
+  } else {
+    z = lb / ntiles;
+    tile = lb - z * ntiles;
+    pbeg = (long)z * a.kchunk;
+    pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
+  }
+  const int m0 = (tile / tilesN) * C::BM;
+  const int n0 = (tile % tilesN) * C::BN;
 
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gy.s0.ptr, P * a.gy.s0.C * 2);
   const uint32_t gpitch = (uint32_t)(a.gy.s0.C * 2);
@@ -1086,6 +1118,9 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
       __syncthreads();
     }
   }
+  if (a.sk_blocks <= 0) break;
+  u += kdone;  // the LDS stages are free again: the epilogue ended in a barrier
+  }
 #else
   (void)a;
   (void)zero16;
@@ -1179,8 +1214,8 @@ template <class C>
 static hipError_t wgrad2_t(const GemmArgs& a, int splits, const void* zero16, hipStream_t st) {
   const long tilesM = (a.M + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL(igemm2_wgrad<C>, dim3((unsigned)(tilesM * tilesN * splits)), dim3(C::NT),
-                     0, st, a, zero16);
+  const long blocks = a.sk_blocks > 0 ? a.sk_blocks : tilesM * tilesN * splits;
+  hipLaunchKernelGGL(igemm2_wgrad<C>, dim3((unsigned)blocks), dim3(C::NT), 0, st, a, zero16);
   return hipGetLastError();
 }
 
@@ -1234,6 +1269,43 @@ hipError_t launch_conv_halo(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Balanced-split finalize: every element of tile t sums the partial slots
+// of the blocks that touched t, in slot order, into the gradient.  Four
+// consecutive columns per thread.
+__global__ void wgrad_finalize_sk(GemmArgs a, int bm, int bn, long KTT) {
+  const long idx = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (idx >= (long)a.M * a.N) return;
+  const int m = (int)(idx / a.N);
+  const int n = (int)(idx - (long)m * a.N);
+  const int tilesN = (a.N + bn - 1) / bn;
+  const long ntiles = (long)((a.M + bm - 1) / bm) * tilesN;
+  const long U = ntiles * KTT;
+  const long tile = (long)(m / bm) * tilesN + n / bn;
+  const int cnt = sk_block_of((tile + 1) * KTT - 1, U, a.sk_blocks) -
+                  sk_block_of(tile * KTT, U, a.sk_blocks) + 1;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int z = 0; z < cnt; ++z) {
+    const float4 v = *reinterpret_cast<const float4*>(a.part + (long)z * a.M * a.N + idx);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  const int si = seg_of(a.nseg, a.seg[1].begin, a.seg[2].begin, n);
+  const Seg& sg = si == 0 ? a.seg[0] : (si == 1 ? a.seg[1] : a.seg[2]);
+  const int len = sg.end - sg.begin;
+  float* g = sg.grad + (long)m * len + (n - sg.begin);
+  g[0] += s.x; g[1] += s.y; g[2] += s.z; g[3] += s.w;
+}
+
+int sk_max_slots(int M, int N, int bm, int bn, long P, int bk, int nb) {
+  const int tilesN = (N + bn - 1) / bn;
+  const long ntiles = (long)((M + bm - 1) / bm) * tilesN;
+  const long KTT = (P + bk - 1) / bk;
+  const long U = ntiles * KTT;
+  int mx = 0;
+  for (long t = 0; t < ntiles; ++t)
+    mx = std::max(mx, sk_block_of((t + 1) * KTT - 1, U, nb) - sk_block_of(t * KTT, U, nb) + 1);
+  return mx;
+}
+
 hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero16,
                          hipStream_t st) {
   hipError_t e;
@@ -1244,6 +1316,13 @@ hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero1
     default: e = wgrad2_t<W2_128x128>(a, splits, zero16, st); break;
   }
   if (e != hipSuccess) return e;
+  if (a.sk_blocks > 0) {
+    const TileInfo ti = tile2_info(t);
+    const long total = (long)a.M * a.N / 4;
+    hipLaunchKernelGGL(wgrad_finalize_sk, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+                       a, ti.bm, ti.bn, (a.g.pixels() + ti.bk - 1) / ti.bk);
+    return hipGetLastError();
+  }
   return launch_wgrad_finalize(a, splits, st);
 }
 

@@ -45,6 +45,10 @@ struct GemmArgs {
   VIn gy;              // output gradient, M channels
   int kchunk;          // pixels per split
   float* part;         // [splits][M][N] fp32 partials (both modes)
+  int sk_blocks;       // WGRAD (LDS-DMA path): > 0 deals the tiles' K-steps out in
+                       // equal ranges to this many blocks (partial slot = the
+                       // block's rank among those touching the tile); 0: uniform
+                       // splits of kchunk pixels
   // CONV mode of the LDS-DMA kernels without a K split, when H*W % BM == 0:
   // per-channel sum and sum of squares of the output as stored (bf16), one
   // row per (image, M-tile): [B][H*W / BM][2][N]; null: not computed
@@ -102,6 +106,10 @@ bool halo_conv_fits(const Geo& g, int N);
 hipError_t launch_conv_halo(const GemmArgs& a, hipStream_t st);
 hipError_t launch_wgrad2(const GemmArgs& a, int tile, int splits, const void* zero16,
                          hipStream_t st);
+// Largest number of partial slots a tile needs when nb blocks share the
+// K-steps of an M x N weight gradient over P pixels (bm x bn tiles, bk
+// pixels per K-step).
+int sk_max_slots(int M, int N, int bm, int bn, long P, int bk, int nb);
 
 // ---- GroupNorm / reductions (norm.hip) -----------------------------------
 

@@ -104,6 +104,10 @@ struct pulse_stage {
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
   int conv_ksplit_cap = 16;  // largest conv K split (env PULSE_CONV_KSPLIT_MAX)
+  int wgrad_balance = 0;     // balanced weight-gradient split: 0 never (default: it
+                             // measured slower, its blocks share no pixel rows in L2),
+                             // 1 when the uniform split idles slots, 2 always
+                             // (env PULSE_WGRAD_BALANCE)
   // halo-reuse conv: 0 never (default: it measured slower in the full step,
   // where its 147 KB of LDS keeps the side stream's GEMMs off its CUs), 1
   // when its grid fills the GPU, 2 whenever it fits
@@ -289,6 +293,39 @@ int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
   return (int)((s->P + kc - 1) / kc);
 }
 
+// Weight-gradient work split: uniform pixel splits (pick_splits); with the
+// balanced split switched on (PULSE_WGRAD_BALANCE=1, when the uniform split
+// leaves more than a tenth of the resident-block slots idle, or 2, always)
+// the tiles' K-steps are dealt out evenly to one block per slot, at least 8
+// K-steps each.  It keeps every CU busy, but the blocks running together no
+// longer share pixel rows in L2, and it measured slower on every stage, so
+// it is off by default.  slots = partial slots the split writes per element.
+struct WgradPlan {
+  int splits = 1, kchunk = 0, sk_blocks = 0, slots = 1;
+};
+
+WgradPlan wgrad_plan(const pulse_stage* s, int tile, int M, int N) {
+  WgradPlan w;
+  w.splits = pick_splits(s, tile, M, N, w.kchunk);
+  w.slots = w.splits;
+  if (!uses_v2(s) || s->wgrad_balance == 0) return w;
+  const TileInfo ti = info_of(s, tile);
+  const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
+  const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : 1;
+  const long nslots = 256L * per_cu;
+  const long blocks = tiles * w.splits;
+  const long rounds = (blocks + nslots - 1) / nslots;
+  const double util = (double)blocks / (double)(rounds * nslots);
+  if (util >= 0.9 && s->wgrad_balance < 2) return w;
+  const long ktt = (s->P + ti.bk - 1) / ti.bk;
+  const long units = tiles * ktt;
+  const long nb = std::min(nslots, units / 8);
+  if (nb < 1) return w;
+  w.sk_blocks = (int)nb;
+  w.slots = sk_max_slots(M, N, ti.bm, ti.bn, s->P, ti.bk, (int)nb);
+  return w;
+}
+
 int env_int(const char* name, int dflt) {
   const char* v = getenv(name);
   if (!v || !*v) return dflt;
@@ -345,6 +382,7 @@ pulse_status build_layout(pulse_stage* s) {
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
     s->halo = env_int("PULSE_HALO", 0);
     s->conv_ksplit_cap = std::max(1, std::min(16, env_int("PULSE_CONV_KSPLIT_MAX", 16)));
+    s->wgrad_balance = std::max(0, std::min(2, env_int("PULSE_WGRAD_BALANCE", 0)));
     if (s->v2) {
       s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
       s->wgrad_tile_force = (wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
@@ -408,10 +446,9 @@ pulse_status build_layout(pulse_stage* s) {
   size_t part = 0, kpart = 0, red = 0;
   for (auto* v : {&s->eb, &s->db})
     for (auto& b : *v) {
-      int kc;
-      int sp = pick_splits(s, wgrad_tile(s, b.cout, b.ldb2), b.cout, b.ldb2, kc);
+      int sp = wgrad_plan(s, wgrad_tile(s, b.cout, b.ldb2), b.cout, b.ldb2).slots;
       part = std::max(part, (size_t)sp * b.cout * b.ldb2);
-      sp = pick_splits(s, wgrad_tile(s, b.cout, 9 * b.cin), b.cout, 9 * b.cin, kc);
+      sp = wgrad_plan(s, wgrad_tile(s, b.cout, 9 * b.cin), b.cout, 9 * b.cin).slots;
       part = std::max(part, (size_t)sp * b.cout * 9 * b.cin);
       for (int c : {b.cin, b.cout}) {
         RedGrid rg = red_grid(s->geo, c);
@@ -731,12 +768,13 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
   a.N = n;
   a.K = (int)s->P;
   a.gy = gy;
-  int kchunk;
   const int tile = wgrad_tile(s, M, n);
-  const int splits = pick_splits(s, tile, M, n, kchunk);
-  if ((size_t)splits * M * n > s->part_cap)
+  const WgradPlan w = wgrad_plan(s, tile, M, n);
+  const int splits = w.splits;
+  if ((size_t)w.slots * M * n > s->part_cap)
     return fail(PULSE_E_SHAPE, "internal: wgrad partial buffer too small");
-  a.kchunk = kchunk;
+  a.kchunk = w.kchunk;
+  a.sk_blocks = w.sk_blocks;
   a.part = s->sf(s->s_part);
   if (uses_v2(s))
     HIPCHK(launch_wgrad2(a, tile, splits, s->scratch(s->s_zero), st));

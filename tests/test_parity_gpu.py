@@ -103,6 +103,18 @@ def test_every_wgrad_tile(tile, monkeypatch):
     _case(configs.shrink(configs.l32(), batch=2, hw=6, width=7), 3, f"l32s wgrad tile {tile}")
 
 
+@pytest.mark.parametrize("tile", [10, 11, 12, 13])
+@pytest.mark.parametrize("name,B,H,W", [("l64", 2, 12, 10), ("l32", 2, 6, 7)])
+def test_balanced_wgrad_split(tile, name, B, H, W, monkeypatch):
+    """The balanced weight-gradient split (the tiles' K-steps dealt out in
+    equal ranges, ranges crossing tile boundaries, per-tile partial slots
+    summed in order) forced on for every weight-gradient tile."""
+    monkeypatch.setenv("PULSE_WGRAD_BALANCE", "2")
+    monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
+    d = configs.shrink(configs.get(name), batch=B, hw=H, width=W)
+    _case(d, configs.SEEDS[name], f"{name} balanced wgrad tile {tile}")
+
+
 @pytest.mark.parametrize("name,B,H,W", [("l64", 1, 16, 16), ("l64", 2, 32, 32),
                                         ("l32", 1, 16, 16), ("l32", 1, 32, 32)])
 def test_halo_conv(name, B, H, W, monkeypatch):
