@@ -65,6 +65,23 @@ pulse_status pulse_partition(const pulse_part_problem* pb, int32_t p, int32_t* c
 pulse_status pulse_partition_cost(const pulse_part_problem* pb, int32_t p, const int32_t* cuts,
                                   double* cost, int32_t* valid, double* stage_costs);
 
+/* Forward point-to-point bytes of one sample through a cut model
+ * (Sec. II-C, Sec. V-B).  Stage s of n_stages holds ops cuts[s-1]+1 ..
+ * cuts[s].  With collocated = 0 stage s runs on device s, as a sequential
+ * pipeline places it: every stage boundary is one transfer of the boundary
+ * op's output, and a skip (c1, c2) crossing devices is passed on from
+ * stage to stage, one transfer of c1's output per device it crosses.  With
+ * collocated = 1, n_stages is even and stage s runs on device
+ * min(s, n_stages-1-s): boundaries between stages on different devices
+ * are transferred once, and skips between non-adjacent ops, which a valid
+ * partition keeps on one device, cost nothing (PULSE_E_INVALID_ARG if one
+ * would cross).  A skip between adjacent ops is charged like any other
+ * when it crosses devices (the traffic model of Sec. II-C counts it apart
+ * from the boundary).  Backward passes send the same volume of gradients
+ * again. */
+pulse_status pulse_comm_volume(const pulse_part_problem* pb, int32_t n_stages,
+                               const int32_t* cuts, int32_t collocated, double* bytes);
+
 /* Hybrid data/pipeline parallelism (Sec. VI).  N devices run G replicas of
  * a P-device pipeline (N = P G) of 2P collocated stages, on microbatches of
  * b samples.  Per stage s (1-based), summed over the ops the skip-aware

@@ -87,3 +87,30 @@ def optimum(n, p, t_f, m_a, skips, lam=0.0, t_lat=0.0, b_inter=1.0):
         elif c == best and c < math.inf:
             arg.append(cuts)
     return best, arg
+
+
+def comm_volume(n, m_a, skips, n_stages, cuts, collocated):
+    """Forward point-to-point bytes of one sample: stage boundaries between
+    devices, plus every skip that crosses devices, forwarded stage by stage
+    from its source device to its destination device (the traffic model of
+    Sec. II-C counts a skip between adjacent ops apart from the boundary).
+    Collocated placement puts stage s on device min(s, n_stages - 1 - s)."""
+    def dev_of_stage(st):
+        return min(st, n_stages - 1 - st) if collocated else st
+    dev = [0] * n
+    for st, (a, b) in enumerate(stages_of(n, cuts)):
+        for l in range(a, b + 1):
+            dev[l] = dev_of_stage(st)
+    v = 0.0
+    for st in range(n_stages - 1):
+        if dev_of_stage(st) != dev_of_stage(st + 1):
+            v += m_a[cuts[st]]
+    for c1, c2 in skips:
+        c1, c2 = min(c1, c2), max(c1, c2)
+        if dev[c1] == dev[c2]:
+            continue
+        # a valid collocated partition keeps non-adjacent skips on one device
+        assert not (collocated and c2 - c1 > 1), "a skip crosses devices"
+        v += m_a[c1] * abs(dev[c2] - dev[c1])
+    return v
+

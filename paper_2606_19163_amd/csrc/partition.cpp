@@ -214,6 +214,39 @@ pulse_status pulse_partition_cost(const pulse_part_problem* pb, int32_t p, const
   return PULSE_OK;
 }
 
+pulse_status pulse_comm_volume(const pulse_part_problem* pb, int32_t n_stages,
+                               const int32_t* cuts, int32_t collocated, double* bytes) {
+  if (pulse_status st = check_problem(pb, 2)) return st;
+  if (!cuts || !bytes) return bad("cuts or bytes is NULL");
+  const int n = pb->n_ops;
+  if (n_stages < 1 || n_stages > n || (collocated && n_stages % 2))
+    return bad("n_stages must be in [1, n_ops], and even when collocated");
+  for (int k = 0; k < n_stages - 1; ++k)
+    if (cuts[k] < 0 || cuts[k] >= n - 1 || (k && cuts[k] <= cuts[k - 1]))
+      return bad("cuts must increase strictly and lie in [0, n_ops - 2]");
+  std::vector<int> dev(n);
+  auto dev_of_stage = [&](int st) {
+    return collocated ? std::min(st, n_stages - 1 - st) : st;
+  };
+  for (int st = 0, l = 0; st < n_stages; ++st) {
+    const int last = st < n_stages - 1 ? cuts[st] : n - 1;
+    for (; l <= last; ++l) dev[l] = dev_of_stage(st);
+  }
+  double v = 0.0;
+  for (int st = 0; st + 1 < n_stages; ++st)
+    if (dev_of_stage(st) != dev_of_stage(st + 1)) v += pb->m_a[cuts[st]];
+  for (int k = 0; k < pb->n_skips; ++k) {
+    int a = pb->skips[2 * k], b = pb->skips[2 * k + 1];
+    if (a > b) std::swap(a, b);
+    if (dev[a] == dev[b]) continue;
+    if (collocated && b - a > 1)
+      return bad("a skip crosses devices: the cuts violate the collocation rule");
+    v += pb->m_a[a] * std::abs(dev[b] - dev[a]);
+  }
+  *bytes = v;
+  return PULSE_OK;
+}
+
 }  // extern "C"
 
 // ---- hybrid data/pipeline parallelism (Sec. VI) ---------------------------

@@ -56,6 +56,22 @@ def partition(t_f, m_a, skips, p, lam=0.0, t_lat=0.0, b_inter=1.0):
     return [cuts[k] for k in range(p - 1)], cost.value
 
 
+def comm_volume(m_a, skips, n_stages, cuts, collocated):
+    """Forward point-to-point bytes of one sample (pulse_comm_volume)."""
+    n = len(m_a)
+    pb, keep = _problem([0.0] * n, m_a, skips, 0.0, 0.0, 1.0)
+    L = _lib()
+    if not getattr(L, "_cv_bound", False):
+        L.pulse_comm_volume.argtypes = [ctypes.POINTER(PartProblem), _i32, _ip, _i32, _dp]
+        L.pulse_comm_volume.restype = ctypes.c_int
+        L._cv_bound = True
+    c = (_i32 * max(1, n_stages - 1))(*cuts)
+    v = _d()
+    _S._check(L.pulse_comm_volume(ctypes.byref(pb), n_stages, c, 1 if collocated else 0,
+                                  ctypes.byref(v)))
+    return v.value
+
+
 def partition_cost(t_f, m_a, skips, p, cuts, lam=0.0, t_lat=0.0, b_inter=1.0):
     """(cost, valid, stage costs) of a given partition."""
     pb, keep = _problem(t_f, m_a, skips, lam, t_lat, b_inter)

@@ -171,8 +171,21 @@ def main():
             _, _, sc = plan.partition_cost(t_f, m_a, skips, p, cuts, **kw)
             bw = blockwise_cuts(n, p)
             bcost, bvalid, bsc = plan.partition_cost(t_f, m_a, skips, p, bw, **kw)
+            # forward point-to-point bytes per sample: this collocated plan
+            # against a sequential pipeline of p / 2 stages balanced on the
+            # same forward times (skips forwarded stage to stage)
+            D = p // 2
+            per = 1.0 / args.batch
+            pulse_b = plan.comm_volume(m_a, skips, p, cuts, True) * per
+            seq_cuts, _ = plan.partition(t_f, m_a, [], D) if D % 2 == 0 else \
+                (blockwise_cuts(n, D), 0.0)
+            seq_b = plan.comm_volume(m_a, skips, D, seq_cuts, False) * per
             out["plans"].append({
-                "stages": p, "devices": p // 2, "lambda": lam,
+                "stages": p, "devices": D, "lambda": lam,
+                "comm_mb_per_sample": {"sequential": round(seq_b / 1e6, 3),
+                                       "sequential_cuts": seq_cuts,
+                                       "collocated": round(pulse_b / 1e6, 3),
+                                       "reduction_pct": round(100 * (1 - pulse_b / seq_b), 1)},
                 "balanced": {"cuts": cuts, "max_stage_us": round(cost * 1e6, 2),
                              "stage_us": [round(v * 1e6, 2) for v in sc]},
                 "blockwise": {"cuts": bw, "valid": bvalid,

@@ -117,3 +117,22 @@ def test_invariants():
         for cuts in po.optimum(n, p, t, [0.0] * n, skips)[1]:
             assert po.is_valid(n, p, cuts, skips)
             assert po.cost(n, p, cuts, t, [0.0] * n, skips) == best
+
+
+@pytest.mark.parametrize("K,D", [(8, 4), (8, 2), (16, 4), (16, 8), (24, 4), (12, 2), (32, 8)])
+def test_sequential_skip_volume_closed_form(K, D):
+    """K blocks (K/2 encoder, K/2 decoder, block i's skip feeding block
+    K-1-i), each producing `a` bytes, cut sequentially into D stages of K/D
+    blocks: forward traffic ((K+4)D/4 - 1) a (Sec. II-C); the collocated
+    placement of the same model over 2D stages on D devices sends only its
+    2(D-1) boundaries (Sec. V-B)."""
+    a = 3.0
+    m_a = [a] * K
+    skips = [(i, K - 1 - i) for i in range(K // 2)]
+    seq = [K // D * (s + 1) - 1 for s in range(D - 1)]
+    want = ((K + 4) * D / 4 - 1) * a
+    assert po.comm_volume(K, m_a, skips, D, seq, collocated=False) == pytest.approx(want)
+    if K % (2 * D) == 0:
+        col = [K // (2 * D) * (s + 1) - 1 for s in range(2 * D - 1)]
+        assert po.is_valid(K, 2 * D, col, skips)
+        assert po.comm_volume(K, m_a, skips, 2 * D, col, collocated=True) == 2 * (D - 1) * a

@@ -100,3 +100,21 @@ def test_arguments():
         plan.partition([1.0] * 4, [0.0] * 4, [], 2, b_inter=0.0)
     with pytest.raises(S.PulseError):
         plan.partition_cost([1.0] * 4, [0.0] * 4, [], 2, [3])  # cut at the last op
+
+
+def test_comm_volume_matches_the_oracle():
+    rng = random.Random(13)
+    for _ in range(200):
+        n = rng.randint(2, 12)
+        m = [rng.choice([0.0, 1.0, 4.0, 9.0]) for _ in range(n)]
+        skips = [(i, n - 1 - i) for i in range(n // 2) if rng.random() < 0.6]
+        p = rng.randint(1, n)
+        cuts = sorted(rng.sample(range(n - 1), p - 1))
+        assert plan.comm_volume(m, skips, p, cuts, False) == \
+            pytest.approx(po.comm_volume(n, m, skips, p, cuts, False))
+        if p % 2 == 0 and po.is_valid(n, p, cuts, skips):
+            assert plan.comm_volume(m, skips, p, cuts, True) == \
+                pytest.approx(po.comm_volume(n, m, skips, p, cuts, True))
+    # a collocated placement whose skip crosses devices is rejected
+    with pytest.raises(S.PulseError):
+        plan.comm_volume([1.0] * 8, [(0, 3)], 4, [1, 3, 5], True)
