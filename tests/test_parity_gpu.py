@@ -58,20 +58,22 @@ def test_bf16_k32_path():
     _case(d, 17, "c96")
 
 
-def test_l64_full_size_sampled():
-    """The headline stage at its real size (B=8, 64x64x320) in the launch
-    configuration the bench times; the oracle recomputes two samples of the
-    batch (every output but the parameter gradients is per sample)."""
-    desc = configs.l64()
-    params, b = synth.make_all(desc, configs.SEEDS["l64"])
-    log("case l64 full: GPU run")
+@pytest.mark.parametrize("name", ["l64", "l32", "l16", "l8"])
+def test_full_size_sampled(name):
+    """Every stage at its real size (64x64x320 and 32x32x640 at batch 8,
+    16x16 and 8x8 at 1280 channels and batch 16) in the launch configuration
+    the bench times; the oracle recomputes two samples of the batch (every
+    output but the parameter gradients is per sample)."""
+    desc = configs.get(name)
+    params, b = synth.make_all(desc, configs.SEEDS[name])
+    log(f"case {name} full: GPU run")
     gpu, _ = run_gpu(desc, params, b)
-    for n in (0, 5):
-        log(f"case l64 full: oracle sample {n}")
+    for n in (0, desc["batch"] - 3):
+        log(f"case {name} full: oracle sample {n}")
         d1 = configs.shrink(desc, batch=1)
         b1 = {k: v[n:n + 1] for k, v in b.items()}
         ref = _oracle(d1, params, b1)
-        compare(desc, gpu, ref, grads=False, skip_rows=slice(n, n + 1), label=f"l64 n={n}")
+        compare(desc, gpu, ref, grads=False, skip_rows=slice(n, n + 1), label=f"{name} n={n}")
 
 
 @pytest.mark.parametrize("tile", range(7))
