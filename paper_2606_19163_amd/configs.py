@@ -134,3 +134,47 @@ def param_names(desc):
         if ci != co:
             out += [(pre + "Ws", (co, ci)), (pre + "bs", (co,))]
     return out
+
+
+# ---- transformer-block stages -----------------------------------------------
+
+T_BLOCK = ("ln1.g", "ln1.b", "qkv.W", "qkv.b", "proj.W", "proj.b",
+           "ln2.g", "ln2.b", "fc1.W", "fc1.b", "fc2.W", "fc2.b")
+
+
+def _tstage(batch, tokens, width, heads, n_enc, n_dec, dtype=BF16):
+    return dict(kind="transformer", batch=batch, tokens=tokens, width=width, heads=heads,
+                eps=1e-5, mlp=4, n_enc=n_enc, n_dec=n_dec, dtype=dtype, max_inflight=1)
+
+
+def t_tiny():
+    """Small transformer stage: 2 x 16 tokens of 64 channels, 2 heads of 32."""
+    return _tstage(2, 16, 64, 2, 1, 1)
+
+
+def t768(batch=16):
+    """UViT-like stage: 256 tokens (a 32x32 latent in 2x2 patches) of 768
+    channels, 12 heads of 64, 2 encoder and 2 decoder blocks."""
+    return _tstage(batch, 256, 768, 12, 2, 2)
+
+
+CONFIGS["t_tiny"] = t_tiny
+CONFIGS["t768"] = t768
+SEEDS["t_tiny"] = 6
+SEEDS["t768"] = 7
+
+
+def tparam_names(desc):
+    """Transformer-stage parameter names and shapes in generation order:
+    encoder blocks, then decoder blocks (skip linear first)."""
+    C, M = desc["width"], desc["width"] * desc["mlp"]
+    shapes = {"ln1.g": (C,), "ln1.b": (C,), "qkv.W": (3 * C, C), "qkv.b": (3 * C,),
+              "proj.W": (C, C), "proj.b": (C,), "ln2.g": (C,), "ln2.b": (C,),
+              "fc1.W": (M, C), "fc1.b": (M,), "fc2.W": (C, M), "fc2.b": (C,)}
+    out = []
+    for k in range(desc["n_enc"]):
+        out += [(f"enc{k}.{n}", shapes[n]) for n in T_BLOCK]
+    for k in range(desc["n_dec"]):
+        out += [(f"dec{k}.skip.W", (C, 2 * C)), (f"dec{k}.skip.b", (C,))]
+        out += [(f"dec{k}.{n}", shapes[n]) for n in T_BLOCK]
+    return out

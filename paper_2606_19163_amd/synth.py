@@ -120,3 +120,34 @@ def make_wave(levels, seed, n_mb):
     params = [make_params(d, rng) for d in levels]
     bounds = [[make_boundary(d, rng) for _ in range(n_mb)] for d in levels]
     return params, bounds
+
+
+def make_tstage(desc, seed):
+    """(params, boundary) of a transformer stage from ``default_rng(seed)``:
+    parameters in tparam_names order (a weight [out, in] is N(0, 1/in), its
+    bias uses the same fan-in; LayerNorm gains 1 + 0.1 N(0,1), shifts
+    0.1 N(0,1)), then x, u, g_enc, g_dec [B, L, C] ~ N(0,1); bf16-rounded
+    for bf16 stages."""
+    rng = np.random.default_rng(seed)
+    names = _cfg.tparam_names(desc)
+    shapes = dict(names)
+    params = {}
+    for name, shape in names:
+        leaf = name.split(".")[-1]
+        z = rng.standard_normal(shape, dtype=np.float32)
+        if leaf == "W":
+            v = z / np.float32(np.sqrt(shape[1]))
+        elif leaf == "b" and not name.split(".")[-2].startswith("ln"):
+            fan = shapes[name[:-1] + "W"][1]
+            v = z / np.float32(np.sqrt(fan))
+        elif leaf == "g":
+            v = np.float32(1.0) + np.float32(0.1) * z
+        else:
+            v = np.float32(0.1) * z
+        params[name] = v.astype(np.float32)
+    shp = (desc["batch"], desc["tokens"], desc["width"])
+    bound = {k: rng.standard_normal(shp, dtype=np.float32) for k in ("x", "u", "g_enc", "g_dec")}
+    if desc["dtype"] == _cfg.BF16:
+        params = {k: round_bf16(v) for k, v in params.items()}
+        bound = {k: round_bf16(v) for k, v in bound.items()}
+    return params, bound
