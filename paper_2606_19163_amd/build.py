@@ -37,8 +37,8 @@ CFLAGS = [
     "-I", CSRC,
 ]
 
-SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "stage.cpp",
-           "sched.cpp", "partition.cpp"]
+SOURCES = ["igemm.hip", "igemm2.hip", "norm.hip", "misc.hip", "probe.hip", "attn.hip",
+           "tnorm.hip", "stage.cpp", "tstage.cpp", "sched.cpp", "partition.cpp"]
 
 
 def _compile(src: str) -> str:

@@ -148,8 +148,8 @@ def _tstage(batch, tokens, width, heads, n_enc, n_dec, dtype=BF16):
 
 
 def t_tiny():
-    """Small transformer stage: 2 x 16 tokens of 64 channels, 2 heads of 32."""
-    return _tstage(2, 16, 64, 2, 1, 1)
+    """Small transformer stage: 2 x 64 tokens of 128 channels, 2 heads of 64."""
+    return _tstage(2, 64, 128, 2, 1, 1)
 
 
 def t768(batch=16):

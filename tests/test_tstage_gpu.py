@@ -1,0 +1,120 @@
+"""GPU parity of the transformer-block stage (C ABI) against the fp64 oracle:
+outputs, boundary gradients, every parameter gradient and the buffered skip
+gradients, element by element (relative L2 within the bf16 bound)."""
+
+import numpy as np
+import pytest
+
+from oracle import transformer_oracle as TO
+from paper_2606_19163_amd import configs, synth
+from paper_2606_19163_amd import tstage as TS
+
+from gpu_util import log, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2  # bf16 storage of activations and weights, fp32 accumulation
+
+
+def _mid():
+    """Ragged tiles: 576 tokens (4.5 row tiles of 128), width 192 (3 heads;
+    192- and 576-column GEMMs end in half tiles), 2 + 2 blocks."""
+    d = configs._tstage(3, 192, 192, 3, 2, 2)
+    return d
+
+
+CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t768": (configs.t768, 7)}
+
+
+def run_gpu(desc, params, b, mbs=(0,)):
+    import torch
+    st = TS.TStage(desc)
+    st.set_params(params)
+    st.zero_grads()
+    dev = {k: st.to_dev(v) for k, v in b.items()}
+    res = {}
+    for mb in mbs:
+        ye = st.forward(TS.ENC, mb, dev["x"])
+        yd = st.forward(TS.DEC, mb, dev["u"])
+        du = st.backward(TS.DEC, mb, dev["g_dec"])
+        dsk = {k: st.skip_grad(mb, k) for k in range(desc["n_enc"])}
+        dx = st.backward(TS.ENC, mb, dev["g_enc"])
+        torch.cuda.synchronize()
+        res = dict(y_enc=ye.float().cpu().numpy(), y_dec=yd.float().cpu().numpy(),
+                   du=du.float().cpu().numpy(), dx=dx.float().cpu().numpy(),
+                   dskips={k: v.cpu().numpy() for k, v in dsk.items()})
+    res["grads"] = st.grads_dict()
+    assert st.inflight() == 0
+    return res, st
+
+
+def _compare(name, got, ref, scale=1.0):
+    worst = 0.0
+    for k in ("y_enc", "y_dec", "dx", "du"):
+        e = rel_l2(got[k], ref[k])
+        log(f"{name} {k}: rel {e:.3e}")
+        assert e < TOL, (k, e)
+    for k in ref["dskips"]:
+        e = rel_l2(got["dskips"][k], ref["dskips"][k])
+        log(f"{name} dskip[{k}]: rel {e:.3e}")
+        assert e < TOL, ("dskip", k, e)
+    for k, v in ref["grads"].items():
+        e = rel_l2(got["grads"][k], scale * np.asarray(v))
+        worst = max(worst, e)
+        assert e < TOL, (k, e)
+    log(f"{name} worst parameter-gradient rel {worst:.3e}")
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_tstage_matches_oracle(name):
+    make, seed = CASES[name]
+    d = make()
+    log(f"case {name}: batch {d['batch']} tokens {d['tokens']} width {d['width']} "
+        f"heads {d['heads']} blocks {d['n_enc']}+{d['n_dec']}")
+    p, b = synth.make_tstage(d, seed)
+    ref = TO.tstage_run(d, p, b["x"], b["u"], b["g_enc"], b["g_dec"])
+    got, _ = run_gpu(d, p, b)
+    _compare(name, got, ref)
+
+
+def test_gradients_accumulate_over_microbatches():
+    d = configs.t_tiny()
+    d["max_inflight"] = 2
+    p, b = synth.make_tstage(d, 6)
+    ref = TO.tstage_run(d, p, b["x"], b["u"], b["g_enc"], b["g_dec"])
+    got, _ = run_gpu(d, p, b, mbs=(3, 5))
+    _compare("two microbatches", got, ref, scale=2.0)
+
+
+def test_interleaved_microbatches_keep_their_skips():
+    """Two microbatches in flight with different inputs, run in a pipeline
+    order (F_enc 0, F_enc 1, F_dec 1, F_dec 0, B_dec 0, B_dec 1, B_enc 1,
+    B_enc 0): each microbatch's outputs and gradients match its own oracle."""
+    import torch
+    d = configs.t_tiny()
+    d["max_inflight"] = 2
+    p, b0 = synth.make_tstage(d, 6)
+    _, b1 = synth.make_tstage(d, 16)
+    refs = [TO.tstage_run(d, p, bb["x"], bb["u"], bb["g_enc"], bb["g_dec"]) for bb in (b0, b1)]
+    st = TS.TStage(d)
+    st.set_params(p)
+    st.zero_grads()
+    dev = [{k: st.to_dev(v) for k, v in bb.items()} for bb in (b0, b1)]
+    ye = [st.forward(TS.ENC, m, dev[m]["x"]) for m in (0, 1)]
+    yd = [None, None]
+    yd[1] = st.forward(TS.DEC, 1, dev[1]["u"])
+    yd[0] = st.forward(TS.DEC, 0, dev[0]["u"])
+    du = [st.backward(TS.DEC, m, dev[m]["g_dec"]) for m in (0, 1)]
+    dx = [None, None]
+    dx[1] = st.backward(TS.ENC, 1, dev[1]["g_enc"])
+    dx[0] = st.backward(TS.ENC, 0, dev[0]["g_enc"])
+    torch.cuda.synchronize()
+    for m in (0, 1):
+        for k, t in (("y_enc", ye[m]), ("y_dec", yd[m]), ("du", du[m]), ("dx", dx[m])):
+            e = rel_l2(t.float().cpu().numpy(), refs[m][k])
+            log(f"mb {m} {k}: rel {e:.3e}")
+            assert e < TOL, (m, k, e)
+    g = st.grads_dict()
+    for k in refs[0]["grads"]:
+        e = rel_l2(g[k], np.asarray(refs[0]["grads"][k]) + np.asarray(refs[1]["grads"][k]))
+        assert e < TOL, (k, e)
