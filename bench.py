@@ -188,13 +188,111 @@ def cpu_baseline(name, descs, seed, sample_batch, min_seconds=10.0):
                       f"fp64; {dt:.2f} s"}
 
 
+def tstage_cpu_baseline(desc, seed, sample_batch, min_seconds=10.0):
+    """The transformer-stage oracle, as it stands, on `sample_batch` images of
+    the workload (forward + backward), repeated until `min_seconds` have
+    passed, scaled to TFLOP/s."""
+    from oracle import transformer_oracle as TO
+    from paper_2606_19163_amd import synth
+    from paper_2606_19163_amd import tstage as TS
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    d = dict(desc, batch=sample_batch)
+    params, b = synth.make_tstage(d, seed)
+    flops = TS.TStage(d, dry_run=True).flops()
+    runs, t0 = 0, time.perf_counter()
+    while runs == 0 or time.perf_counter() - t0 < min_seconds:
+        TO.tstage_run(d, params, b["x"], b["u"], b["g_enc"], b["g_dec"])
+        runs += 1
+    dt = time.perf_counter() - t0
+    return {"value": runs * flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{runs} x {sample_batch} of {desc['batch']} images of one microbatch, "
+                      f"forward + backward, numpy fp64; {dt:.2f} s"}
+
+
+def bench_tstage(args):
+    """One transformer-block stage (UViT-like, 256 tokens of 768 channels,
+    12 heads, 2 + 2 blocks, batch 16): the same step and JSON line as the
+    ResBlock stages, with the roofline of the token-major GEMM launches."""
+    import torch
+    from paper_2606_19163_amd import configs, synth
+    from paper_2606_19163_amd import tstage as TS
+
+    torch.cuda.set_device(0)
+    d = configs.get(args.workload)
+    seed = configs.SEEDS[args.workload]
+    params, b = synth.make_tstage(d, seed)
+    st = TS.TStage(d)
+    st.set_params(params)
+    dev = {k: st.to_dev(v) for k, v in b.items()}
+    outs = {k: st.act() for k in ("y_enc", "y_dec", "dx", "du")}
+
+    def step():
+        st.forward(TS.ENC, 0, dev["x"], out=outs["y_enc"])
+        st.forward(TS.DEC, 0, dev["u"], out=outs["y_dec"])
+        st.backward(TS.DEC, 0, dev["g_dec"], din=outs["du"])
+        st.backward(TS.ENC, 0, dev["g_enc"], din=outs["dx"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launches, kms, kflops, kbytes = 0, 0.0, 0.0, 0.0
+    if not args.no_kernel_events:
+        st.timing(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        launches, kms, kflops, kbytes = st.timing_read()
+        st.timing(False)
+    flops_step = st.flops()
+    tflops = flops_step * args.steps / elapsed / 1e12
+    line = {
+        "metric": "transformer stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s",
+        "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) tokens, N(0,1/fan_in) weights)",
+        "config": {"workload": f"{args.workload}: one collocated transformer stage, batch "
+                               f"{d['batch']}, {d['tokens']} tokens of {d['width']} channels, "
+                               f"{d['heads']} heads of 64, MLP x{d['mlp']}, {d['n_enc']} "
+                               f"encoder + {d['n_dec']} decoder blocks",
+                   "batch": d["batch"], "tokens": d["tokens"], "width": d["width"],
+                   "heads": d["heads"], "blocks": [d["n_enc"], d["n_dec"]]},
+        "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
+        "microbatches_per_s": round(args.steps / elapsed, 2),
+        "gflop_per_step": round(flops_step / 1e9, 2),
+    }
+    if launches:
+        achieved = kflops / (kms * 1e-3) / 1e12
+        line["roofline"] = {
+            "kernel": "igemm_conv in its token-major 1x1 form (linear forward / data gradient)",
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": round(kbytes / launches), "launches": launches,
+            "avg_launch_us": round(kms * 1e3 / launches, 2),
+            "avg_gflop_per_launch": round(kflops / launches / 1e9, 3)}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = tstage_cpu_baseline(d, seed, min(args.cpu_sample_batch, 2))
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="l64",
-                    choices=["l64", "l32", "l16", "l8", "tiny", "wave", "wave-sched"])
+                    choices=["l64", "l32", "l16", "l8", "tiny", "wave", "wave-sched",
+                             "t768", "t_tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
     ap.add_argument("--serial", action="store_true",
@@ -214,6 +312,8 @@ def main():
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.workload in ("t768", "t_tiny"):
+        return bench_tstage(args)
     if args.serial:
         os.environ["PULSE_SERIAL"] = "1"
     import numpy as np

@@ -992,6 +992,10 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
     }
   }
 
+  // one K-step of BK pixels moves a pixel by kdw columns and kdh rows
+  // (kdh < H; the carry of the columns adds at most one more row)
+  const int kdw = C::BK % W;
+  const int kdh = (C::BK / W) % H;
   auto issue = [&](int kt, char* base) __attribute__((always_inline)) {
     const long p0 = pbeg + (long)kt * C::BK;
 #pragma unroll
@@ -1007,12 +1011,14 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
         const void* g = ok ? (const void*)(bsrc[u] + (long)(p + bshift[u]) * bpitch[u]) : zero16;
         __builtin_amdgcn_global_load_lds(g, lds(base + C::A_BYTES + (wl - C::WLA) * 1024), 16, 0,
                                          0);
-        // advance this lane's pixel by one K-step
-        int w = bw[u] + C::BK, h = bh[u];
-        while (w >= W) {
+        // advance this lane's pixel by one K-step: BK = kdh rows + kdw
+        // columns, the row taken modulo H (the next image starts at row 0)
+        int w = bw[u] + kdw, h = bh[u] + kdh;
+        if (w >= W) {
           w -= W;
-          if (++h == H) h = 0;
+          ++h;
         }
+        if (h >= H) h -= H;
         bw[u] = w;
         bh[u] = h;
       }

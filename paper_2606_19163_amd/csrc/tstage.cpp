@@ -3,7 +3,7 @@
 // every forward / backward half.  Implements include/pulse_tstage.h.
 //
 // Every linear layer runs on the implicit-GEMM kernels (igemm2.hip) in their
-// 1x1 form over a [batch, tokens, 1] geometry: the forward and the data
+// 1x1 form over a [batch, 1, tokens] geometry: the forward and the data
 // gradient in conv mode (out[T][N] = in[T][K] W^T with W given as [N][K]),
 // the weight gradient in wgrad mode.  The decoder's skip linear reads
 // [v || skip] as one two-source operand, so the concatenation never exists
@@ -617,7 +617,9 @@ pulse_status pulse_tstage_create(const pulse_tstage_desc* desc, pulse_tstage** o
   s->H = desc->heads;
   s->R = desc->mlp_ratio * desc->width;
   s->T = (long)s->B * s->L;
-  s->geo = Geo{s->B, s->L, 1};
+  // each image's tokens as one row of L pixels: the weight-gradient kernel
+  // steps its pixel coordinates 64 at a time, one wrap per row
+  s->geo = Geo{s->B, 1, s->L};
   build_layout(s);
   s->rows.resize(desc->max_inflight);
   *out = s;
