@@ -88,7 +88,10 @@ enum Tile2 : int {
   TILE2_C256x160S3 = 4,  // three LDS stages, 8 waves, one block per CU
   TILE2_C128x160S3 = 5,  // three LDS stages, 4 waves, one block per CU
   TILE2_C128x160K32S4 = 6,  // four LDS stages of 32 channels, two blocks per CU
-  TILE2_CONV_LAST = 6,
+  TILE2_C128x192 = 7,       // 4 waves of 64 x 96, two blocks per CU
+  TILE2_C64x128 = 8,        // 4 waves of 32 x 64, three blocks per CU
+  TILE2_C128x64 = 9,        // 4 waves of 64 x 32, three blocks per CU
+  TILE2_CONV_LAST = 9,
   TILE2_W320x192 = 10,
   TILE2_W320x128 = 11,
   TILE2_W128x128 = 12,

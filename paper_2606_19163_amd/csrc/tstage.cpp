@@ -103,6 +103,14 @@ struct pulse_tstage {
   size_t s_dy[2] = {0, 0}, s_dm = 0, s_da2 = 0, s_dh = 0, s_do = 0, s_dqkv = 0, s_da = 0,
          s_dsx = 0, s_dv = 0, s_ds = 0, s_kpart = 0, s_wpart = 0, s_red = 0, s_zero = 0;
   size_t kpart_cap = 0, wpart_cap = 0, red_cap = 0;
+  size_t s_red2 = 0;  // reduction buffer of the side stream
+  // side stream: the weight-gradient GEMMs and bias-gradient sums of the
+  // backward pass run on it, concurrently with the data-gradient chain
+  hipStream_t side = nullptr;
+  std::vector<hipEvent_t> sev;  // synchronisation events, reused per call
+  size_t sev_used = 0;
+  // GEMM tuning overrides (env, read at create; -1: the default choice)
+  int conv_tile_force = -1, conv_ks_cap = 16, wgrad_tile_force = -1;
   // binding
   const float* prm = nullptr;
   float* grd = nullptr;
@@ -158,29 +166,75 @@ void layout_block_params(pulse_tstage* s, TBlock& b, const std::string& pre) {
   b.fc2b = add_param(s, pre + "fc2.b", C);
 }
 
-// conv-mode tile for N output columns, weight-gradient tile for M rows
-int tconv_tile(int N) { return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128; }
-int twgrad_tile(int M) { return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128; }
+int env_or(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
 
-// K splits of a conv-mode GEMM: enough blocks for two per CU, each split
-// keeping at least 4 K-steps (at most 16 splits)
-int tconv_ksplit(long M, int N, int K) {
-  const TileInfo ti = tile2_info(tconv_tile(N));
-  const long tiles = ((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
-  if (tiles >= 512) return 1;
-  long ks = (512 + tiles - 1) / tiles;
-  ks = std::min(ks, std::max(1L, (long)(K / ti.bk) / 4));
-  ks = std::min(ks, 16L);
-  const long kt = K / ti.bk;
-  const long steps = (kt + ks - 1) / ks;
-  return (int)((kt + steps - 1) / steps);  // no empty split
+// Tile and K split of a conv-mode GEMM (M x N over K).  Token-major GEMMs
+// are short (K of one to four widths), so per-block set-up and the last,
+// partly filled round of blocks weigh as much as the MFMA work, and a K
+// split costs an fp32 partial of M x N per split.  Default, from sweeps of
+// every tile and split on the 768-wide stage: the largest 128-row tile whose
+// tile count still fits one round of two blocks per CU (at least 400 tiles
+// of 128 x 192, 128 x 160 or 128 x 128), without a K split; otherwise
+// 64 x 128 tiles (three blocks per CU), split in two when K exceeds 1536.
+// Overrides (for sweeps): PULSE_TCONV_TILE forces a tile (with the split
+// rule of two blocks per CU, at least 4 K-steps per split),
+// PULSE_TCONV_KSPLIT_MAX caps the split.
+struct ConvPlan {
+  int tile, ks, ksteps;
+};
+
+long tile_count(int tile, long M, int N) {
+  const TileInfo ti = tile2_info(tile);
+  return ((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
+}
+
+ConvPlan tconv_plan(int tile_force, int ks_cap, long M, int N, int K) {
+  ConvPlan p;
+  long ks = 1;
+  if (tile_force >= 0) {
+    p.tile = tile_force;
+    const long tiles = tile_count(p.tile, M, N);
+    const long kt = K / tile2_info(p.tile).bk;
+    if (tiles < 512) {
+      ks = (512 + tiles - 1) / tiles;
+      ks = std::min(ks, std::max(1L, kt / 4));
+    }
+  } else {
+    p.tile = -1;
+    long best = 0;
+    for (int t : {TILE2_C128x192, TILE2_C128x160, TILE2_C128x128}) {
+      const long n = tile_count(t, M, N);
+      if (n <= 512 && n >= 400 && n > best) {
+        best = n;
+        p.tile = t;
+      }
+    }
+    if (p.tile < 0) {
+      p.tile = TILE2_C64x128;
+      ks = K > 1536 ? 2 : 1;
+    }
+  }
+  ks = std::min(ks, (long)std::max(1, ks_cap));
+  const long kt = K / tile2_info(p.tile).bk;
+  p.ksteps = (int)((kt + ks - 1) / ks);
+  p.ks = (int)((kt + p.ksteps - 1) / p.ksteps);  // no empty split
+  return p;
+}
+
+// weight-gradient tile for M rows (PULSE_TWGRAD_TILE forces one)
+int twgrad_tile(int tile_force, int M) {
+  if (tile_force >= TILE2_WGRAD_FIRST && tile_force <= TILE2_WGRAD_LAST) return tile_force;
+  return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128;
 }
 
 // Token splits of a weight-gradient GEMM (M x N over P tokens): the count
 // that minimises rounds(s) * T_tile / s + s * M * N * 8 / HBM, as for the
 // ResBlock stage; kchunk receives the tokens per split
-int twgrad_splits(long P, int M, int N, int& kchunk) {
-  const TileInfo ti = tile2_info(twgrad_tile(M));
+int twgrad_splits(int tile, long P, int M, int N, int& kchunk) {
+  const TileInfo ti = tile2_info(tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
   const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : 1;
   const long slots = 256L * per_cu;
@@ -284,10 +338,10 @@ void build_layout(pulse_tstage* s) {
   for (const auto& g : gemms) {
     // as a conv: N = g[0] columns over K = g[1]; as a weight gradient: M = g[0]
     const int N = g[0], K = g[1];
-    const int ks = tconv_ksplit(T, N, K);
-    if (ks > 1) kcap = std::max(kcap, (size_t)ks * T * N);
+    const ConvPlan cp = tconv_plan(s->conv_tile_force, s->conv_ks_cap, T, N, K);
+    if (cp.ks > 1) kcap = std::max(kcap, (size_t)cp.ks * T * N);
     int kc = 0;
-    const int sp = twgrad_splits(T, N, K, kc);
+    const int sp = twgrad_splits(twgrad_tile(s->wgrad_tile_force, N), T, N, K, kc);
     wcap = std::max(wcap, (size_t)sp * N * K);
   }
   s->kpart_cap = kcap;
@@ -300,6 +354,7 @@ void build_layout(pulse_tstage* s) {
                               (size_t)128 * 2 * std::max(3 * C, R));
   s->red_cap = red;
   s->s_red = take(red * 4);
+  s->s_red2 = take(red * 4);
   s->s_zero = take(256);
   // per-microbatch rows
   s->off_rows = off;
@@ -415,13 +470,12 @@ pulse_status linear(pulse_tstage* s, int N, const Seg& in, const void* W, int ld
   a.out2 = out2;
   a.out_dtype = out_dtype;
   a.ldo = N;
-  const int tile = tconv_tile(N);
-  const int ks = tconv_ksplit(s->T, N, a.K);
-  const int kt = a.K / tile2_info(tile).bk;
-  a.ksplit = ks;
-  a.ksteps = (kt + ks - 1) / ks;
-  if (ks > 1) {
-    if ((size_t)ks * a.M * N > s->kpart_cap)
+  const ConvPlan cp = tconv_plan(s->conv_tile_force, s->conv_ks_cap, s->T, N, a.K);
+  const int tile = cp.tile;
+  a.ksplit = cp.ks;
+  a.ksteps = cp.ksteps;
+  if (cp.ks > 1) {
+    if ((size_t)cp.ks * a.M * N > s->kpart_cap)
       return tfail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
     a.part = s->fat(s->s_kpart);
   }
@@ -453,22 +507,23 @@ pulse_status linear_wgrad(pulse_tstage* s, int M, const Seg& in, const void* gy,
   a.seg[0] = in;
   a.gy = tvin(gy, M);
   int kc = 0;
-  const int splits = twgrad_splits(s->T, M, a.N, kc);
+  const int wtile = twgrad_tile(s->wgrad_tile_force, M);
+  const int splits = twgrad_splits(wtile, s->T, M, a.N, kc);
   if ((size_t)splits * M * a.N > s->wpart_cap)
     return tfail(PULSE_E_SHAPE, "internal: weight-gradient partial buffer too small");
   a.kchunk = kc;
   a.part = s->fat(s->s_wpart);
-  THIP(launch_wgrad2(a, twgrad_tile(M), splits, s->at(s->s_zero), st));
+  THIP(launch_wgrad2(a, wtile, splits, s->at(s->s_zero), st));
   return PULSE_OK;
 }
 
-// acc[n] += sum over the T tokens of v[t][n]
-pulse_status col_sum(pulse_tstage* s, const void* v, int N, float* acc, hipStream_t st) {
+// acc[n] += sum over the T tokens of v[t][n] (part: a reduction buffer)
+pulse_status col_sum(pulse_tstage* s, const void* v, int N, float* acc, float* part,
+                     hipStream_t st) {
   const Geo g{1, (int)s->T, 1};
   const RedGrid rg = red_grid(g, N);
   if ((size_t)rg.chunks * 2 * N > s->red_cap)
     return tfail(PULSE_E_SHAPE, "internal: reduction buffer too small");
-  float* part = s->fat(s->s_red);
   THIP(launch_chan_sum_partial(tvin(v, N), g, rg, part, st));
   THIP(launch_chan_totals(part, g, rg, N, 1, acc, nullptr, nullptr, st));
   return PULSE_OK;
@@ -520,9 +575,88 @@ pulse_status block_fwd(pulse_tstage* s, char* row, const TBlock& b, const void* 
   return PULSE_OK;
 }
 
+// Stream plumbing of the backward pass.  With the side stream, each
+// parameter gradient (weight-gradient GEMM and bias sum) is handed to it as
+// soon as its output gradient exists; the caller's stream goes on with the
+// data gradient.  Scratch that the side stream reads is not overwritten by
+// the caller's stream before the side stream's event for it has fired.
+struct BwdSync {
+  pulse_tstage* s;
+  hipStream_t st;     // the caller's stream
+  hipStream_t work;   // where parameter gradients run: side or st
+  float* red;         // their reduction buffer
+  bool on_side;
+  hipEvent_t last = nullptr;  // the side stream's latest recorded event
+};
+
+hipEvent_t sync_event(pulse_tstage* s) {
+  if (s->sev_used == s->sev.size()) {
+    hipEvent_t e;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+    s->sev.push_back(e);
+  }
+  return s->sev[s->sev_used++];
+}
+
+BwdSync bwd_sync(pulse_tstage* s, hipStream_t st) {
+  BwdSync y;
+  y.s = s;
+  y.st = st;
+  y.on_side = s->side != nullptr && !s->timing;
+  y.work = y.on_side ? s->side : st;
+  y.red = s->fat(y.on_side ? s->s_red2 : s->s_red);
+  s->sev_used = 0;
+  return y;
+}
+
+// make the side stream wait for everything enqueued on the caller's stream
+pulse_status fork(BwdSync& y) {
+  if (!y.on_side) return PULSE_OK;
+  hipEvent_t e = sync_event(y.s);
+  if (!e) return tfail(PULSE_E_HIP, "hipEventCreate failed");
+  THIP(hipEventRecord(e, y.st));
+  THIP(hipStreamWaitEvent(y.s->side, e, 0));
+  return PULSE_OK;
+}
+
+// an event after the side stream's work so far (null without a side stream)
+pulse_status mark(BwdSync& y, hipEvent_t* out) {
+  *out = nullptr;
+  if (!y.on_side) return PULSE_OK;
+  hipEvent_t e = sync_event(y.s);
+  if (!e) return tfail(PULSE_E_HIP, "hipEventCreate failed");
+  THIP(hipEventRecord(e, y.s->side));
+  *out = y.last = e;
+  return PULSE_OK;
+}
+
+pulse_status wait_for(BwdSync& y, hipEvent_t e) {
+  if (e) THIP(hipStreamWaitEvent(y.st, e, 0));
+  return PULSE_OK;
+}
+
+// the caller's stream waits for all side work
+pulse_status join(BwdSync& y) { return wait_for(y, y.last); }
+
+// parameter gradients of one linear layer: bias += colsum(gy), W += gy^T in
+pulse_status param_grads(BwdSync& y, int M, const Seg& in, const void* gy, float* bias) {
+  TCHK(fork(y));
+  TCHK(col_sum(y.s, gy, M, bias, y.red, y.work));
+  TCHK(linear_wgrad(y.s, M, in, gy, y.work));
+  return PULSE_OK;
+}
+
+// Scratch buffers that the side stream may still read, with the event that
+// frees each (null: free).
+struct SideReads {
+  hipEvent_t dy = nullptr, dm = nullptr, dh = nullptr, dqkv = nullptr, dsx = nullptr;
+};
+
 // dx = d(block)/dx^T dy for the block input x; parameter gradients +=
-pulse_status block_bwd(pulse_tstage* s, char* row, const TBlock& b, const void* x,
-                       const void* dy, void* dx, hipStream_t st) {
+pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, const void* x,
+                       const void* dy, void* dx) {
+  pulse_tstage* s = y.s;
+  hipStream_t st = y.st;
   const int C = s->C, R = s->R;
   const long T = s->T;
   void* a = row + b.r_a;
@@ -541,24 +675,27 @@ pulse_status block_bwd(pulse_tstage* s, char* row, const TBlock& b, const void* 
   void* dqkv = s->at(s->s_dqkv);
   void* da = s->at(s->s_da);
   // MLP: y = h + Fc2(GELU(Fc1(LN2(h))))
-  TCHK(col_sum(s, dy, C, s->gp(b.fc2b), st));
-  TCHK(linear_wgrad(s, C, tseg(R, tvin(m, R), s->gp(b.fc2W)), dy, st));
+  TCHK(param_grads(y, C, tseg(R, tvin(m, R), s->gp(b.fc2W)), dy, s->gp(b.fc2b)));
+  TCHK(mark(y, &rd.dy));
+  TCHK(wait_for(y, rd.dm));
   TCHK(linear(s, R, tseg(C, tvin(dy, C)), s->at(b.t_fc2), C, nullptr, nullptr, dm, nullptr,
               DT_BF16, st));
   THIP(launch_gelu_bwd(dm, z, dm, T * R, st));
-  TCHK(col_sum(s, dm, R, s->gp(b.fc1b), st));
-  TCHK(linear_wgrad(s, R, tseg(C, tvin(a2, C), s->gp(b.fc1W)), dm, st));
+  TCHK(param_grads(y, R, tseg(C, tvin(a2, C), s->gp(b.fc1W)), dm, s->gp(b.fc1b)));
+  TCHK(mark(y, &rd.dm));
   TCHK(linear(s, C, tseg(R, tvin(dm, R)), s->at(b.t_fc1), R, nullptr, nullptr, da2, nullptr,
               DT_BF16, st));
+  TCHK(wait_for(y, rd.dh));
   TCHK(ln_backward(s, da2, h, st2, b.ln2g, b.ln2b, dy, dh, st));
   // attention: h = x + Proj(MHA(LN1(x)))
-  TCHK(col_sum(s, dh, C, s->gp(b.projb), st));
-  TCHK(linear_wgrad(s, C, tseg(C, tvin(o, C), s->gp(b.projW)), dh, st));
+  TCHK(param_grads(y, C, tseg(C, tvin(o, C), s->gp(b.projW)), dh, s->gp(b.projb)));
+  TCHK(mark(y, &rd.dh));
   TCHK(linear(s, C, tseg(C, tvin(dh, C)), s->at(b.t_proj), C, nullptr, nullptr, dO, nullptr,
               DT_BF16, st));
+  TCHK(wait_for(y, rd.dqkv));
   THIP(launch_attn_bwd(qkv, dO, row + b.r_p, s->B, s->L, C, s->H, dqkv, s->at(s->s_ds), st));
-  TCHK(col_sum(s, dqkv, 3 * C, s->gp(b.qkvb), st));
-  TCHK(linear_wgrad(s, 3 * C, tseg(C, tvin(a, C), s->gp(b.qkvW)), dqkv, st));
+  TCHK(param_grads(y, 3 * C, tseg(C, tvin(a, C), s->gp(b.qkvW)), dqkv, s->gp(b.qkvb)));
+  TCHK(mark(y, &rd.dqkv));
   TCHK(linear(s, C, tseg(3 * C, tvin(dqkv, 3 * C)), s->at(b.t_qkv), 3 * C, nullptr, nullptr, da,
               nullptr, DT_BF16, st));
   TCHK(ln_backward(s, da, x, st1, b.ln1g, b.ln1b, dh, dx, st));
@@ -620,6 +757,10 @@ pulse_status pulse_tstage_create(const pulse_tstage_desc* desc, pulse_tstage** o
   // each image's tokens as one row of L pixels: the weight-gradient kernel
   // steps its pixel coordinates 64 at a time, one wrap per row
   s->geo = Geo{s->B, 1, s->L};
+  const int ct = env_or("PULSE_TCONV_TILE", -1);
+  s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
+  s->conv_ks_cap = std::max(1, std::min(16, env_or("PULSE_TCONV_KSPLIT_MAX", 16)));
+  s->wgrad_tile_force = env_or("PULSE_TWGRAD_TILE", -1);
   build_layout(s);
   s->rows.resize(desc->max_inflight);
   *out = s;
@@ -629,6 +770,8 @@ pulse_status pulse_tstage_create(const pulse_tstage_desc* desc, pulse_tstage** o
 void pulse_tstage_destroy(pulse_tstage* s) {
   if (!s) return;
   for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+  for (hipEvent_t e : s->sev) (void)hipEventDestroy(e);
+  if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
 }
 
@@ -672,6 +815,10 @@ pulse_status pulse_tstage_bind(pulse_tstage* s, const float* params, float* grad
     return tfail(PULSE_E_INVALID_ARG, "workspace %zu bytes < required %zu", ws_bytes, s->ws_bytes);
   if (pulse_tstage_inflight(s) > 0)
     return tfail(PULSE_E_STATE, "cannot rebind with microbatches in flight");
+  if (!s->side && env_or("PULSE_SERIAL", 0) == 0) {
+    // default priority, no implicit synchronisation with the null stream
+    THIP(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
+  }
   s->prm = params;
   s->grd = grads;
   s->ws = static_cast<char*>(ws);
@@ -780,19 +927,26 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
     char* row = s->row(r);
     const int C = s->C, ne = s->d.n_enc, nd = s->d.n_dec;
     const long T = s->T;
+    BwdSync y = bwd_sync(s, st);
+    SideReads rd;
     if (half == PULSE_DEC) {
       const void* dy = dout;
+      hipEvent_t dy_read = nullptr;  // the side stream has read the previous block's dy
       for (int k = nd - 1; k >= 0; --k) {
         const TBlock& b = s->db[k];
         void* dsx = s->at(s->s_dsx);
-        TCHK(block_bwd(s, row, b, row + b.r_x, dy, dsx, st));
+        TCHK(wait_for(y, rd.dsx));
+        TCHK(block_bwd(y, rd, row, b, row + b.r_x, dy, dsx));
         // skip linear over [v || skip]
         const int slot = ne - 1 - k;
         const void* skip = row + s->row_slot[slot];
-        TCHK(col_sum(s, dsx, C, s->gp(b.skb), st));
-        TCHK(linear_wgrad(s, C, tseg(2 * C, tvin2(row + b.r_v, C, skip, C), s->gp(b.skW)), dsx,
-                          st));
+        TCHK(param_grads(y, C, tseg(2 * C, tvin2(row + b.r_v, C, skip, C), s->gp(b.skW)), dsx,
+                         s->gp(b.skb)));
+        TCHK(mark(y, &rd.dsx));
         void* dv = k == 0 ? din : s->at(s->s_dy[k & 1]);
+        // dv's buffer held the dy of block k + 1, which the side stream reads
+        TCHK(wait_for(y, dy_read));
+        dy_read = rd.dy;
         const char* tsk = s->at(b.t_sk);
         TCHK(linear(s, C, tseg(C, tvin(dsx, C)), tsk, C, nullptr, nullptr, dv, nullptr, DT_BF16,
                     st));
@@ -807,14 +961,16 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
         // the gradient reaching x_k: from its encoder consumer and from the
         // buffered skip gradient of its decoder consumer
         void* dy = s->at(s->s_dy[0]);
+        TCHK(wait_for(y, rd.dy));
         THIP(launch_add_cast(g, DT_BF16, reinterpret_cast<const float*>(row + s->row_sgrad[k]),
                              dy, DT_BF16, T * C, st));
         const void* x = k == 0 ? row + b.r_x : row + s->row_slot[k - 1];
         void* dx = k == 0 ? din : s->at(s->s_dy[1]);
-        TCHK(block_bwd(s, row, b, x, dy, dx, st));
+        TCHK(block_bwd(y, rd, row, b, x, dy, dx));
         g = dx;
       }
     }
+    TCHK(join(y));
   }
   if (half == PULSE_DEC) {
     s->rows[r].state = T_DEC_BWD;

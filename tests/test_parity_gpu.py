@@ -76,7 +76,7 @@ def test_full_size_sampled(name):
         compare(desc, gpu, ref, grads=False, skip_rows=slice(n, n + 1), label=f"{name} n={n}")
 
 
-@pytest.mark.parametrize("tile", range(7))
+@pytest.mark.parametrize("tile", range(10))
 def test_every_conv_tile(tile, monkeypatch):
     """Every implicit-GEMM conv tile shape of the LDS-DMA path (1-, 2- and
     3/4-stage rings, 64- and 32-channel K-steps, with and without K splits)

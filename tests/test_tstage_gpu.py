@@ -118,3 +118,25 @@ def test_interleaved_microbatches_keep_their_skips():
     for k in refs[0]["grads"]:
         e = rel_l2(g[k], np.asarray(refs[0]["grads"][k]) + np.asarray(refs[1]["grads"][k]))
         assert e < TOL, (k, e)
+
+
+@pytest.mark.parametrize("tile", range(10))
+def test_tstage_every_conv_tile(tile, monkeypatch):
+    """Every conv-mode tile shape on the token-major linear layers (ragged
+    rows and columns)."""
+    monkeypatch.setenv("PULSE_TCONV_TILE", str(tile))
+    d = _mid()
+    p, b = synth.make_tstage(d, 11)
+    ref = TO.tstage_run(d, p, b["x"], b["u"], b["g_enc"], b["g_dec"])
+    got, _ = run_gpu(d, p, b)
+    _compare(f"conv tile {tile}", got, ref)
+
+
+@pytest.mark.parametrize("tile", [10, 11, 12, 13])
+def test_tstage_every_wgrad_tile(tile, monkeypatch):
+    monkeypatch.setenv("PULSE_TWGRAD_TILE", str(tile))
+    d = _mid()
+    p, b = synth.make_tstage(d, 11)
+    ref = TO.tstage_run(d, p, b["x"], b["u"], b["g_enc"], b["g_dec"])
+    got, _ = run_gpu(d, p, b)
+    _compare(f"wgrad tile {tile}", got, ref)
