@@ -1,18 +1,27 @@
 // Multi-head self-attention of the transformer-block stage (gfx950, bf16
 // MFMA 16x16x32, fp32 accumulation).  Head dimension 64; L tokens per image
-// with L a multiple of 64 and at most 256, so a head's keys and values fit
+// with L a multiple of 64 and at most 256, so one head's keys and values fit
 // in LDS whole.  q, k and v are the three C-channel thirds of the qkv rows
 // [B*L][3C]; head h owns channels [64 h, 64 h + 64) of each third.
 //
-//   forward  : s = q k^T / 8, p = softmax_rows(s), o = p v; p is kept (bf16)
-//              for the backward pass
-//   backward : dp = do v^T, ds = p (dp - rowsum(p dp)) / 8,
-//              dq = ds k, dk = ds^T q, dv = p^T do
+//   forward : s = q k^T / 8, p = softmax_rows(s), o = p v; the row's
+//             log-sum-exp lse = log sum_j exp(s_j) is kept (fp32), not p
+//   backward: p is recomputed from q, k and lse; with D = rowsum(do o),
+//             dp = do v^T, ds = p (dp - D) / 8, dq = ds k, dk = ds^T q,
+//             dv = p^T do.  One kernel per query tile computes dq (and D),
+//             one per key tile computes dk and dv from s^T = k q^T, so that
+//             neither p nor ds ever goes to memory and no result is
+//             accumulated across blocks.
 //
-// Every product runs on MFMA with operands read from LDS as 16-byte rows of
-// 8 consecutive k values.  Operands whose k index is not the contiguous one
-// in memory (v and k in the forward/backward products over keys, p^T, ds^T,
-// q^T and do^T) are transposed on their way into LDS.
+// LDS tiles are row-major [rows][64] bf16 with the 16-byte chunks of each
+// row permuted (chunk c of row r stored at c ^ swz(r)).  An MFMA operand
+// whose k index runs along a tile row is one 16-byte read; one whose k index
+// runs down the rows (v and k as the B operand of p v and ds k, q and do in
+// dk and dv) comes from two ds_read_b64_tr_b16: within 16 lanes, lane j
+// receives element j % 4 of the rows addressed by lanes 4 t + j / 4
+// (t = 0..3).  swz keeps both read shapes free of bank conflicts: 16
+// consecutive rows of one chunk, and rows {0-3, 8-11} (+16 k) of a 32-byte
+// column pair, fall on distinct banks.
 #include <hip/hip_runtime.h>
 
 #include "common.hpp"
@@ -24,19 +33,87 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 constexpr int HD = 64;        // head dimension
 constexpr int QT = 64;        // queries (or keys) per block: 4 waves x 16
 constexpr int LMAX = 256;     // tokens per image, at most
 constexpr float SCALE = 0.125f;  // 1 / sqrt(64)
+constexpr float LOG2E = 1.44269504088896341f;
 
 __device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// 8 consecutive bf16 at p (16-byte aligned) as an MFMA operand
-__device__ __forceinline__ bf16x8 ld8lds(const uint16_t* p) {
-  return *reinterpret_cast<const bf16x8*>(p);
+__device__ __forceinline__ uint16_t bf(float f) { return f2bf(f); }
+
+// chunk permutation of tile row r: bit 1 of r -> bit 1, bit 2 -> bit 0,
+// bit 3 -> bit 2
+__device__ __forceinline__ int swz(int r) {
+  return (((r >> 1) & 1) << 1) | ((r >> 2) & 1) | (((r >> 3) & 1) << 2);
+}
+
+// element offset of chunk c (8 channels) of row r in a [rows][64] tile
+__device__ __forceinline__ int toff(int r, int c) { return r * HD + ((c ^ swz(r)) << 3); }
+
+// rows [0, n) x 64 channels of a token-major tensor (row stride `stride`)
+// into a tile
+__device__ __forceinline__ void load_tile(uint16_t* t, const uint16_t* src, long stride, int n) {
+  for (int e = threadIdx.x; e < n * 8; e += blockDim.x) {
+    const int r = e >> 3, c = e & 7;
+    *reinterpret_cast<uint4*>(t + toff(r, c)) =
+        *reinterpret_cast<const uint4*>(src + (long)r * stride + c * 8);
+  }
+}
+
+// operand of 8 consecutive channels: row r, channels 32 kk + 8 g .. + 7
+__device__ __forceinline__ bf16x8 frag_row(const uint16_t* t, int r, int kk, int g) {
+  return *reinterpret_cast<const bf16x8*>(t + toff(r, 4 * kk + g));
+}
+
+__device__ __forceinline__ v4s rd_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
+}
+
+// operand whose k index runs down the tile: k = rows [r0, r0 + 32), the
+// other index = channels [d0, d0 + 16); lane (g, j) receives rows
+// r0 + 8 g .. + 7 of channel d0 + j
+__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* t, int r0, int d0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const int col = d0 + 4 * (j & 3);
+  const int r = r0 + 8 * g + (j >> 2);
+  const v4s lo = rd_tr(t + toff(r, col >> 3) + (col & 7));
+  const v4s hi = rd_tr(t + toff(r + 4, col >> 3) + (col & 7));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// A wave's strip of 16 rows x W columns (W / 8 chunks per row), chunk c of
+// row r at c ^ (r & mask) with mask + 1 the largest power of two <= 16
+// dividing the chunk count: 16 rows of one chunk fall on distinct banks.
+struct Strip {
+  uint16_t* p;
+  int chunks, mask;
+  __device__ __forceinline__ int off(int r, int c) const {
+    return r * chunks * 8 + ((c ^ (r & mask)) << 3);
+  }
+  // C-layout value of row r, column col
+  __device__ __forceinline__ void put(int r, int col, float v) const {
+    p[off(r, col >> 3) + (col & 7)] = bf(v);
+  }
+  // A operand: row m, k = columns 32 ks + 8 g .. + 7
+  __device__ __forceinline__ bf16x8 frag(int m, int ks, int g) const {
+    return *reinterpret_cast<const bf16x8*>(p + off(m, 4 * ks + g));
+  }
+};
+
+__device__ __forceinline__ Strip make_strip(uint16_t* p, int width) {
+  Strip s;
+  s.p = p;
+  s.chunks = width / 8;
+  const int low = s.chunks & -s.chunks;
+  s.mask = (low < 16 ? low : 16) - 1;
+  return s;
 }
 
 // Reduce over the 16 lanes that share lane / 16 (one row of a 16x16 block).
@@ -51,246 +128,274 @@ __device__ __forceinline__ float row_sum16(float v) {
   return v;
 }
 
-// Copy rows [r0, r0 + n) of 64 bf16 (a head's channels) from a token-major
-// tensor into LDS rows of 64 (row stride 64 elements).
-__device__ __forceinline__ void load_rows(uint16_t* dst, const uint16_t* src, long stride, int n) {
-  for (int e = threadIdx.x; e < n * 8; e += blockDim.x) {
-    const int r = e >> 3, c = (e & 7) * 8;
-    *reinterpret_cast<uint4*>(dst + r * HD + c) =
-        *reinterpret_cast<const uint4*>(src + (long)r * stride + c);
-  }
-}
-
-// Transposed copy: the same rows land as columns of dst [64][ld] (dst[c][r]).
-__device__ __forceinline__ void load_rows_t(uint16_t* dst, int ld, const uint16_t* src,
-                                            long stride, int n) {
-  for (int e = threadIdx.x; e < n * 8; e += blockDim.x) {
-    const int r = e >> 3, c = (e & 7) * 8;
-    const uint4 q = *reinterpret_cast<const uint4*>(src + (long)r * stride + c);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+__device__ __forceinline__ float dot8(bf16x8 a, bf16x8 b) {
+  float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      dst[(c + 2 * i) * ld + r] = (uint16_t)(w[i] & 0xffffu);
-      dst[(c + 2 * i + 1) * ld + r] = (uint16_t)(w[i] >> 16);
-    }
-  }
+  for (int i = 0; i < 8; ++i) s += (float)a[i] * (float)b[i];
+  return s;
 }
-
-// Transposed copy of an L x L bf16 matrix block: rows [0, L) and columns
-// [c0, c0 + 64) of src (row stride L) into dst[64][L] (dst[c][r]).
-__device__ __forceinline__ void load_cols_t(uint16_t* dst, const uint16_t* src, int L, int c0) {
-  for (int e = threadIdx.x; e < L * 8; e += blockDim.x) {
-    const int r = e >> 3, c = (e & 7) * 8;
-    const uint4 q = *reinterpret_cast<const uint4*>(src + (long)r * L + c0 + c);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      dst[(c + 2 * i) * L + r] = (uint16_t)(w[i] & 0xffffu);
-      dst[(c + 2 * i + 1) * L + r] = (uint16_t)(w[i] >> 16);
-    }
-  }
-}
-
-__device__ __forceinline__ uint16_t bf(float f) { return f2bf(f); }
 
 // ---------------------------------------------------------------------------
-// forward: block (query tile, head, image); wave w owns queries 16 w .. +15
+// forward: block (query tile, head, image); wave w owns queries 16 w .. + 15
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, int C,
-                                                  uint16_t* o, uint16_t* pbuf) {
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[QT * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[LMAX * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t VT[HD * LMAX];   // [d][key]
-  __shared__ __attribute__((aligned(16))) uint16_t Ps[4][16 * LMAX];  // per wave [q][key]
+                                                  uint16_t* o, float* lse) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[LMAX * HD];  // then the p strips
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[LMAX * HD];
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
   const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_rows(Qs, base + (long)qt * QT * C3, C3, QT);
-  load_rows(Ks, base + C, C3, L);
-  load_rows_t(VT, L, base + 2 * C, C3, L);
-  __syncthreads();
-
+  load_tile(Ks, base + C, C3, L);
+  load_tile(Vs, base + 2 * C, C3, L);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
+  const int q0 = qt * QT + w * 16;  // the wave's first query in the image
+  bf16x8 qa[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
+  __syncthreads();
+
   const int nb = L / 16;
   f32x4 s[LMAX / 16];
 #pragma unroll
-  for (int j = 0; j < LMAX / 16; ++j) s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < LMAX / 16; ++j) {
+    s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (j < nb) {
 #pragma unroll
-  for (int ks = 0; ks < HD / 32; ++ks) {
-    const bf16x8 a = ld8lds(Qs + (w * 16 + m) * HD + ks * 32 + g * 8);
-#pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) s[j] = mma(a, ld8lds(Ks + (j * 16 + m) * HD + ks * 32 + g * 8), s[j]);
+      for (int kk = 0; kk < 2; ++kk) s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
+    }
   }
   // softmax of rows 4 g + i (the lane holds column m of every 16-key block)
-  uint16_t* P = Ps[w];
+  float inv[4], ls[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) mx = fmaxf(mx, s[j][i] * SCALE);
+      if (j < nb) mx = fmaxf(mx, s[j][i]);
     mx = row_max16(mx);
     float sum = 0.f;
 #pragma unroll
     for (int j = 0; j < LMAX / 16; ++j)
       if (j < nb) {
-        const float e = __expf(s[j][i] * SCALE - mx);
+        const float e = exp2f((s[j][i] - mx) * (SCALE * LOG2E));
         s[j][i] = e;
         sum += e;
       }
     sum = row_sum16(sum);
-    const float inv = 1.0f / sum;
+    inv[i] = 1.0f / sum;
+    ls[i] = mx * SCALE + logf(sum);
+  }
+  __syncthreads();  // every wave is done with Ks: it now holds the p strips
+  const Strip P = make_strip(Ks + w * 16 * L, L);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) P[(4 * g + i) * L + j * 16 + m] = bf(s[j][i] * inv);
-  }
-  __syncthreads();
-  // o = p v: A = p rows (k = key), B = v^T rows (k = key)
+      if (j < nb) P.put(4 * g + i, 16 * j + m, s[j][i] * inv[i]);
+  // o = p v: A = p rows (k = key), B = v rows read down the tile (k = key)
   f32x4 acc[HD / 16];
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int ks = 0; ks < L / 32; ++ks) {
-    const bf16x8 a = ld8lds(P + m * L + ks * 32 + g * 8);
+    const bf16x8 a = P.frag(m, ks, g);
 #pragma unroll
     for (int jd = 0; jd < HD / 16; ++jd)
-      acc[jd] = mma(a, ld8lds(VT + (jd * 16 + m) * L + ks * 32 + g * 8), acc[jd]);
+      acc[jd] = mma(a, frag_tr(Vs, 32 * ks, 16 * jd, lane), acc[jd]);
   }
-  const long q0 = row0 + (long)qt * QT + w * 16;
+  const long orow = row0 + q0 + 4 * g;
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      o[(q0 + 4 * g + i) * C + h * HD + jd * 16 + m] = bf(acc[jd][i]);
-  // keep p for the backward pass: [b][h][q][key]
-  uint16_t* pg = pbuf + (((long)b * H + h) * L + (long)qt * QT + w * 16) * L;
-  for (int e = lane; e < 16 * L / 8; e += 64)
-    *reinterpret_cast<uint4*>(pg + e * 8) = *reinterpret_cast<const uint4*>(P + e * 8);
+    for (int i = 0; i < 4; ++i) o[(orow + i) * C + h * HD + jd * 16 + m] = bf(acc[jd][i]);
+  if (m == 0) {
+    float* l = lse + ((long)b * H + h) * L + q0 + 4 * g;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) l[i] = ls[i];
+  }
 }
 
 // ---------------------------------------------------------------------------
-// backward, per query tile: dp = do v^T, ds = p (dp - rowsum(p dp)) / 8,
-// dq = ds k; ds kept (bf16) for the key-side kernel
+// backward, per query tile: dq = ds k, and D = rowsum(do o) for the key tiles
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const uint16_t* dout,
-                                                    const uint16_t* pbuf, int L, int C,
-                                                    uint16_t* dqkv, uint16_t* dsbuf) {
-  __shared__ __attribute__((aligned(16))) uint16_t dOs[QT * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[LMAX * HD];    // [key][d]
-  __shared__ __attribute__((aligned(16))) uint16_t KT[HD * LMAX];    // [d][key]
-  __shared__ __attribute__((aligned(16))) uint16_t Ss[4][16 * LMAX];  // per wave ds [q][key]
+__global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const uint16_t* o,
+                                                    const uint16_t* dout, const float* lse,
+                                                    int L, int C, uint16_t* dqkv,
+                                                    float* dsum) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[LMAX * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[LMAX * HD];  // then the ds strips
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
   const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_rows(dOs, dout + (row0 + (long)qt * QT) * C + h * HD, C, QT);
-  load_rows(Vs, base + 2 * C, C3, L);
-  load_rows_t(KT, L, base + C, C3, L);
-  __syncthreads();
-
+  load_tile(Ks, base + C, C3, L);
+  load_tile(Vs, base + 2 * C, C3, L);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
-  const int nb = L / 16;
-  f32x4 dp[LMAX / 16];
+  const int q0 = qt * QT + w * 16;
+  const long lrow = ((long)b * H + h) * L + q0;  // lse / D index of the wave's first row
+  bf16x8 qa[2], da[2];
+  float dpart = 0.f;
 #pragma unroll
-  for (int j = 0; j < LMAX / 16; ++j) dp[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < HD / 32; ++ks) {
-    const bf16x8 a = ld8lds(dOs + (w * 16 + m) * HD + ks * 32 + g * 8);
-#pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) dp[j] = mma(a, ld8lds(Vs + (j * 16 + m) * HD + ks * 32 + g * 8), dp[j]);
+  for (int kk = 0; kk < 2; ++kk) {
+    const long r = row0 + q0 + m;
+    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
+    da[kk] = *reinterpret_cast<const bf16x8*>(dout + r * C + h * HD + 32 * kk + 8 * g);
+    const bf16x8 ov = *reinterpret_cast<const bf16x8*>(o + r * C + h * HD + 32 * kk + 8 * g);
+    dpart += dot8(da[kk], ov);
   }
-  const long q0 = (long)qt * QT + w * 16;  // within the image
-  const uint16_t* pr = pbuf + (((long)b * H + h) * L + q0) * L;
-  uint16_t* S = Ss[w];
+  // D of row m: the lanes m, m + 16, m + 32, m + 48 hold its 64 channels
+  dpart += __shfl_xor(dpart, 16, 64);
+  dpart += __shfl_xor(dpart, 32, 64);
+  if (g == 0) dsum[lrow + m] = dpart;
+  float Di[4], li[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int r = 4 * g + i;
-    float pv[LMAX / 16];
-    float t = 0.f;
+    Di[i] = __shfl(dpart, 4 * g + i, 64);
+    li[i] = lse[lrow + 4 * g + i];
+  }
+  __syncthreads();
+
+  const int nb = L / 16;
+  f32x4 s[LMAX / 16], dp[LMAX / 16];
+#pragma unroll
+  for (int j = 0; j < LMAX / 16; ++j) {
+    s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dp[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (j < nb) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
+        dp[j] = mma(da[kk], frag_row(Vs, 16 * j + m, kk, g), dp[j]);
+      }
+    }
+  }
+  __syncthreads();  // every wave is done with Vs: it now holds the ds strips
+  const Strip S = make_strip(Vs + w * 16 * L, L);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < LMAX / 16; ++j)
       if (j < nb) {
-        pv[j] = bf2f(pr[(long)r * L + j * 16 + m]);
-        t += pv[j] * dp[j][i];
+        const float p = exp2f((s[j][i] * SCALE - li[i]) * LOG2E);
+        S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
       }
-    t = row_sum16(t);
-#pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) S[r * L + j * 16 + m] = bf(pv[j] * (dp[j][i] - t) * SCALE);
-  }
-  __syncthreads();
-  // dq = ds k: A = ds rows (k = key), B = k^T rows (k = key)
+  // dq = ds k: A = ds rows (k = key), B = k rows read down the tile
   f32x4 acc[HD / 16];
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int ks = 0; ks < L / 32; ++ks) {
-    const bf16x8 a = ld8lds(S + m * L + ks * 32 + g * 8);
+    const bf16x8 a = S.frag(m, ks, g);
 #pragma unroll
     for (int jd = 0; jd < HD / 16; ++jd)
-      acc[jd] = mma(a, ld8lds(KT + (jd * 16 + m) * L + ks * 32 + g * 8), acc[jd]);
+      acc[jd] = mma(a, frag_tr(Ks, 32 * ks, 16 * jd, lane), acc[jd]);
   }
+  const long orow = row0 + q0 + 4 * g;
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      dqkv[(row0 + q0 + 4 * g + i) * C3 + h * HD + jd * 16 + m] = bf(acc[jd][i]);
-  uint16_t* dg = dsbuf + (((long)b * H + h) * L + q0) * L;
-  for (int e = lane; e < 16 * L / 8; e += 64)
-    *reinterpret_cast<uint4*>(dg + e * 8) = *reinterpret_cast<const uint4*>(S + e * 8);
+    for (int i = 0; i < 4; ++i) dqkv[(orow + i) * C3 + h * HD + jd * 16 + m] = bf(acc[jd][i]);
 }
 
 // ---------------------------------------------------------------------------
-// backward, per key tile: dv = p^T do, dk = ds^T q; wave w owns keys
-// 16 w .. +15 of the tile
+// backward, per key tile: wave w owns keys 16 w .. + 15 of the tile and runs
+// over the queries 64 at a time: s^T = k q^T, p^T, dp^T = v do^T,
+// ds^T = p^T (dp^T - D) / 8, dv += p^T do, dk += ds^T q
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const uint16_t* dout,
-                                                     const uint16_t* pbuf,
-                                                     const uint16_t* dsbuf, int L, int C,
-                                                     uint16_t* dqkv) {
-  __shared__ __attribute__((aligned(16))) uint16_t PT[QT * LMAX];   // [key][q]
-  __shared__ __attribute__((aligned(16))) uint16_t ST[QT * LMAX];   // [key][q]
-  __shared__ __attribute__((aligned(16))) uint16_t dOT[HD * LMAX];  // [d][q]
-  __shared__ __attribute__((aligned(16))) uint16_t QTs[HD * LMAX];  // [d][q]
+                                                     const float* lse, const float* dsum,
+                                                     int L, int C, uint16_t* dqkv) {
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[LMAX * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t dOs[LMAX * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ws[4][16 * QT];  // p^T, then ds^T, per wave
   const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
-  const long mat = ((long)b * H + h) * L * L;
-  load_cols_t(PT, pbuf + mat, L, kt * QT);
-  load_cols_t(ST, dsbuf + mat, L, kt * QT);
-  load_rows_t(dOT, L, dout + row0 * C + h * HD, C, L);
-  load_rows_t(QTs, L, qkv + row0 * C3 + h * HD, C3, L);
-  __syncthreads();
-
+  const uint16_t* base = qkv + row0 * C3 + h * HD;
+  load_tile(Qs, base, C3, L);
+  load_tile(dOs, dout + row0 * C + h * HD, C, L);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
+  const int k0 = kt * QT + w * 16;  // the wave's first key in the image
+  const float* lrow = lse + ((long)b * H + h) * L;
+  const float* drow = dsum + ((long)b * H + h) * L;
+  bf16x8 ka[2], va[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    ka[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + C + 32 * kk + 8 * g);
+    va[kk] =
+        *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + 2 * C + 32 * kk + 8 * g);
+  }
+  __syncthreads();
+
+  const Strip W = make_strip(Ws[w], QT);
   f32x4 dv[HD / 16], dk[HD / 16];
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd) {
     dv[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
     dk[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  for (int ks = 0; ks < L / 32; ++ks) {
-    const bf16x8 ap = ld8lds(PT + (w * 16 + m) * L + ks * 32 + g * 8);
-    const bf16x8 as = ld8lds(ST + (w * 16 + m) * L + ks * 32 + g * 8);
+  for (int qc = 0; qc < L / QT; ++qc) {
+    f32x4 st[4], dpt[4];
 #pragma unroll
-    for (int jd = 0; jd < HD / 16; ++jd) {
-      dv[jd] = mma(ap, ld8lds(dOT + (jd * 16 + m) * L + ks * 32 + g * 8), dv[jd]);
-      dk[jd] = mma(as, ld8lds(QTs + (jd * 16 + m) * L + ks * 32 + g * 8), dk[jd]);
+    for (int jq = 0; jq < 4; ++jq) {
+      st[jq] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dpt[jq] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int r = qc * QT + 16 * jq + m;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        st[jq] = mma(ka[kk], frag_row(Qs, r, kk, g), st[jq]);
+        dpt[jq] = mma(va[kk], frag_row(dOs, r, kk, g), dpt[jq]);
+      }
+    }
+    // the lane holds keys 4 g + i and query column qc * 64 + 16 jq + m
+    float lq[4], dq[4];
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      lq[jq] = lrow[qc * QT + 16 * jq + m];
+      dq[jq] = drow[qc * QT + 16 * jq + m];
+    }
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f((st[jq][i] * SCALE - lq[jq]) * LOG2E);
+        st[jq][i] = p;
+        dpt[jq][i] = p * (dpt[jq][i] - dq[jq]) * SCALE;
+        W.put(4 * g + i, 16 * jq + m, p);
+      }
+    // dv += p^T do: A = p^T rows (k = query), B = do rows read down the tile
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 a = W.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        dv[jd] = mma(a, frag_tr(dOs, qc * QT + 32 * ks, 16 * jd, lane), dv[jd]);
+    }
+    // the strip now takes ds^T (this wave's reads of p^T are issued before)
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) W.put(4 * g + i, 16 * jq + m, dpt[jq][i]);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 a = W.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        dk[jd] = mma(a, frag_tr(Qs, qc * QT + 32 * ks, 16 * jd, lane), dk[jd]);
     }
   }
-  const long k0 = row0 + (long)kt * QT + w * 16;
+  const long krow = row0 + k0 + 4 * g;
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const long r = (k0 + 4 * g + i) * C3 + h * HD + jd * 16 + m;
+      const long r = (krow + i) * C3 + h * HD + jd * 16 + m;
       dqkv[r + C] = bf(dk[jd][i]);
       dqkv[r + 2 * C] = bf(dv[jd][i]);
     }
@@ -302,28 +407,27 @@ bool attn_fits(int L, int C, int heads) {
   return L >= QT && L % QT == 0 && L <= LMAX && C == heads * HD;
 }
 
-hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, void* pbuf,
+hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, float* lse,
                            hipStream_t st) {
   if (!attn_fits(L, C, heads)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_attn_fwd, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o),
-                     static_cast<uint16_t*>(pbuf));
+                     static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o), lse);
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bwd(const void* qkv, const void* dout, const void* pbuf, int B, int L,
-                           int C, int heads, void* dqkv, void* dsbuf, hipStream_t st) {
+hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse,
+                           int B, int L, int C, int heads, void* dqkv, float* dsum,
+                           hipStream_t st) {
   if (!attn_fits(L, C, heads)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_attn_bwd_q, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout),
-                     static_cast<const uint16_t*>(pbuf), L, C, static_cast<uint16_t*>(dqkv),
-                     static_cast<uint16_t*>(dsbuf));
+                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(o),
+                     static_cast<const uint16_t*>(dout), lse, L, C, static_cast<uint16_t*>(dqkv),
+                     dsum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_attn_bwd_kv, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout),
-                     static_cast<const uint16_t*>(pbuf), static_cast<const uint16_t*>(dsbuf), L,
-                     C, static_cast<uint16_t*>(dqkv));
+                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout), lse,
+                     dsum, L, C, static_cast<uint16_t*>(dqkv));
   return hipGetLastError();
 }
 

@@ -14,13 +14,14 @@ namespace pulse {
 bool attn_fits(int L, int C, int heads);
 // o[b*L + i][64 h + e] = sum_j p[b][h][i][j] v[b*L + j][64 h + e] with
 // p = softmax_j(q_i . k_j / 8); q, k, v are channel thirds of qkv [B*L][3C].
-// pbuf [B][heads][L][L] receives p (bf16).
-hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, void* pbuf,
+// lse [B][heads][L] receives log sum_j exp(q_i . k_j / 8) (fp32).
+hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, float* lse,
                            hipStream_t st);
-// dqkv [B*L][3C] from dout [B*L][C], the saved p and qkv; dsbuf
-// [B][heads][L][L] is scratch (receives ds).
-hipError_t launch_attn_bwd(const void* qkv, const void* dout, const void* pbuf, int B, int L,
-                           int C, int heads, void* dqkv, void* dsbuf, hipStream_t st);
+// dqkv [B*L][3C] from dout [B*L][C], the forward's o and lse and qkv; dsum
+// [B][heads][L] (fp32) is scratch (receives rowsum(dout o)).
+hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse,
+                           int B, int L, int C, int heads, void* dqkv, float* dsum,
+                           hipStream_t st);
 
 // ---- LayerNorm, GELU, adds (tnorm.hip) -----------------------------------
 

@@ -71,7 +71,7 @@ struct TBlock {
   size_t r_x = 0;  // block input kept in the row (encoder block 0: the stage input;
                    // decoder block: the skip linear's output)
   size_t r_v = 0;  // decoder: upstream input v of the skip linear
-  size_t r_a, r_st1, r_qkv, r_p, r_o, r_h, r_a2, r_st2, r_z, r_m;
+  size_t r_a, r_st1, r_qkv, r_lse, r_o, r_h, r_a2, r_st2, r_z, r_m;
 };
 
 enum TRowState { T_FREE = 0, T_ENC_FWD = 1, T_DEC_FWD = 2, T_DEC_BWD = 3 };
@@ -101,7 +101,7 @@ struct pulse_tstage {
   size_t ws_bytes = 0, off_rows = 0, row_size = 0;
   size_t row_slot[64] = {}, row_sgrad[64] = {};
   size_t s_dy[2] = {0, 0}, s_dm = 0, s_da2 = 0, s_dh = 0, s_do = 0, s_dqkv = 0, s_da = 0,
-         s_dsx = 0, s_dv = 0, s_ds = 0, s_kpart = 0, s_wpart = 0, s_red = 0, s_zero = 0;
+         s_dsx = 0, s_dv = 0, s_dsum = 0, s_kpart = 0, s_wpart = 0, s_red = 0, s_zero = 0;
   size_t kpart_cap = 0, wpart_cap = 0, red_cap = 0;
   size_t s_red2 = 0;  // reduction buffer of the side stream
   // side stream: the weight-gradient GEMMs and bias-gradient sums of the
@@ -319,7 +319,7 @@ void build_layout(pulse_tstage* s) {
     }
   // shared scratch of the backward pass
   const size_t act = (size_t)T * C * 2;
-  const size_t pbytes = (size_t)s->B * s->H * s->L * s->L * 2;
+  const size_t lbytes = (size_t)s->B * s->H * s->L * 4;  // one fp32 per (image, head, token)
   s->s_dy[0] = take(act);
   s->s_dy[1] = take(act);
   s->s_dm = take((size_t)T * R * 2);
@@ -330,7 +330,7 @@ void build_layout(pulse_tstage* s) {
   s->s_da = take(act);
   s->s_dsx = take(act);
   s->s_dv = take(act);
-  s->s_ds = take(pbytes);
+  s->s_dsum = take(lbytes);
   // partial buffers: the largest conv K split and weight-gradient split
   size_t kcap = 0, wcap = 0;
   const int gemms[][3] = {{3 * C, C, 0}, {C, C, 0}, {R, C, 0}, {C, R, 0}, {C, 2 * C, 0},
@@ -369,7 +369,7 @@ void build_layout(pulse_tstage* s) {
     b.r_a = rtake(act);
     b.r_st1 = rtake(stb);
     b.r_qkv = rtake(3 * act);
-    b.r_p = rtake(pbytes);
+    b.r_lse = rtake(lbytes);
     b.r_o = rtake(act);
     b.r_h = rtake(act);
     b.r_a2 = rtake(act);
@@ -563,7 +563,7 @@ pulse_status block_fwd(pulse_tstage* s, char* row, const TBlock& b, const void* 
   THIP(launch_ln_fwd(x, s->T, C, eps, s->pp(b.ln1g), s->pp(b.ln1b), a, st1, st));
   TCHK(linear(s, 3 * C, tseg(C, tvin(a, C)), s->at(b.w_qkv), C, s->pp(b.qkvb), nullptr, qkv,
               nullptr, DT_BF16, st));
-  THIP(launch_attn_fwd(qkv, s->B, s->L, C, s->H, o, row + b.r_p, st));
+  THIP(launch_attn_fwd(qkv, s->B, s->L, C, s->H, o, reinterpret_cast<float*>(row + b.r_lse), st));
   TCHK(linear(s, C, tseg(C, tvin(o, C)), s->at(b.w_proj), C, s->pp(b.projb), x, h, nullptr,
               DT_BF16, st));
   THIP(launch_ln_fwd(h, s->T, C, eps, s->pp(b.ln2g), s->pp(b.ln2b), a2, st2, st));
@@ -693,7 +693,8 @@ pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, co
   TCHK(linear(s, C, tseg(C, tvin(dh, C)), s->at(b.t_proj), C, nullptr, nullptr, dO, nullptr,
               DT_BF16, st));
   TCHK(wait_for(y, rd.dqkv));
-  THIP(launch_attn_bwd(qkv, dO, row + b.r_p, s->B, s->L, C, s->H, dqkv, s->at(s->s_ds), st));
+  THIP(launch_attn_bwd(qkv, o, dO, reinterpret_cast<const float*>(row + b.r_lse), s->B, s->L, C,
+                       s->H, dqkv, s->fat(s->s_dsum), st));
   TCHK(param_grads(y, 3 * C, tseg(C, tvin(a, C), s->gp(b.qkvW)), dqkv, s->gp(b.qkvb)));
   TCHK(mark(y, &rd.dqkv));
   TCHK(linear(s, C, tseg(3 * C, tvin(dqkv, 3 * C)), s->at(b.t_qkv), 3 * C, nullptr, nullptr, da,
