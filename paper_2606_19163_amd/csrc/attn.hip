@@ -57,13 +57,28 @@ __device__ __forceinline__ int swz(int r) {
 // element offset of chunk c (8 channels) of row r in a [rows][64] tile
 __device__ __forceinline__ int toff(int r, int c) { return r * HD + ((c ^ swz(r)) << 3); }
 
-// rows [0, n) x 64 channels of a token-major tensor (row stride `stride`)
-// into a tile
-__device__ __forceinline__ void load_tile(uint16_t* t, const uint16_t* src, long stride, int n) {
-  for (int e = threadIdx.x; e < n * 8; e += blockDim.x) {
+// rows [0, N) x 64 channels of two token-major tensors (row strides s0,
+// s1) into two tiles, 256 threads; every global load is issued before the
+// first LDS store, so the block waits for one round trip, not one per chunk
+template <int N>
+__device__ __forceinline__ void load_tiles(uint16_t* t0, const uint16_t* src0, long s0,
+                                           uint16_t* t1, const uint16_t* src1, long s1) {
+  constexpr int PER = N * 8 / 256;  // 16-byte chunks per thread and tile
+  static_assert(N * 8 % 256 == 0, "whole rounds of 256 chunks");
+  uint4 v0[PER], v1[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u;
     const int r = e >> 3, c = e & 7;
-    *reinterpret_cast<uint4*>(t + toff(r, c)) =
-        *reinterpret_cast<const uint4*>(src + (long)r * stride + c * 8);
+    v0[u] = *reinterpret_cast<const uint4*>(src0 + (long)r * s0 + c * 8);
+    v1[u] = *reinterpret_cast<const uint4*>(src1 + (long)r * s1 + c * 8);
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    const int r = e >> 3, c = e & 7;
+    *reinterpret_cast<uint4*>(t0 + toff(r, c)) = v0[u];
+    *reinterpret_cast<uint4*>(t1 + toff(r, c)) = v1[u];
   }
 }
 
@@ -138,17 +153,17 @@ __device__ __forceinline__ float dot8(bf16x8 a, bf16x8 b) {
 // ---------------------------------------------------------------------------
 // forward: block (query tile, head, image); wave w owns queries 16 w .. + 15
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, int C,
-                                                  uint16_t* o, float* lse) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[LMAX * HD];  // then the p strips
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[LMAX * HD];
+template <int L>
+__global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int C, uint16_t* o,
+                                                  float* lse) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[L * HD];  // then the p strips
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[L * HD];
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
   const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_tile(Ks, base + C, C3, L);
-  load_tile(Vs, base + 2 * C, C3, L);
+  load_tiles<L>(Ks, base + C, C3, Vs, base + 2 * C, C3);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
   const int q0 = qt * QT + w * 16;  // the wave's first query in the image
@@ -158,15 +173,13 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, in
     qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
   __syncthreads();
 
-  const int nb = L / 16;
-  f32x4 s[LMAX / 16];
+  constexpr int nb = L / 16;
+  f32x4 s[nb];
 #pragma unroll
-  for (int j = 0; j < LMAX / 16; ++j) {
+  for (int j = 0; j < nb; ++j) {
     s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (j < nb) {
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
-    }
+    for (int kk = 0; kk < 2; ++kk) s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
   }
   // softmax of rows 4 g + i (the lane holds column m of every 16-key block)
   float inv[4], ls[4];
@@ -174,17 +187,17 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, in
   for (int i = 0; i < 4; ++i) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) mx = fmaxf(mx, s[j][i]);
+    for (int j = 0; j < nb; ++j)
+      mx = fmaxf(mx, s[j][i]);
     mx = row_max16(mx);
     float sum = 0.f;
 #pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) {
-        const float e = exp2f((s[j][i] - mx) * (SCALE * LOG2E));
-        s[j][i] = e;
-        sum += e;
-      }
+    for (int j = 0; j < nb; ++j)
+    {
+      const float e = exp2f((s[j][i] - mx) * (SCALE * LOG2E));
+      s[j][i] = e;
+      sum += e;
+    }
     sum = row_sum16(sum);
     inv[i] = 1.0f / sum;
     ls[i] = mx * SCALE + logf(sum);
@@ -194,12 +207,13 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, in
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) P.put(4 * g + i, 16 * j + m, s[j][i] * inv[i]);
+    for (int j = 0; j < nb; ++j)
+      P.put(4 * g + i, 16 * j + m, s[j][i] * inv[i]);
   // o = p v: A = p rows (k = key), B = v rows read down the tile (k = key)
   f32x4 acc[HD / 16];
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
   for (int ks = 0; ks < L / 32; ++ks) {
     const bf16x8 a = P.frag(m, ks, g);
 #pragma unroll
@@ -221,19 +235,18 @@ __global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int L, in
 // ---------------------------------------------------------------------------
 // backward, per query tile: dq = ds k, and D = rowsum(do o) for the key tiles
 // ---------------------------------------------------------------------------
+template <int L>
 __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const uint16_t* o,
                                                     const uint16_t* dout, const float* lse,
-                                                    int L, int C, uint16_t* dqkv,
-                                                    float* dsum) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[LMAX * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[LMAX * HD];  // then the ds strips
+                                                    int C, uint16_t* dqkv, float* dsum) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[L * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[L * HD];  // then the ds strips
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
   const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_tile(Ks, base + C, C3, L);
-  load_tile(Vs, base + 2 * C, C3, L);
+  load_tiles<L>(Ks, base + C, C3, Vs, base + 2 * C, C3);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
   const int q0 = qt * QT + w * 16;
@@ -260,18 +273,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const u
   }
   __syncthreads();
 
-  const int nb = L / 16;
-  f32x4 s[LMAX / 16], dp[LMAX / 16];
+  constexpr int nb = L / 16;
+  f32x4 s[nb], dp[nb];
 #pragma unroll
-  for (int j = 0; j < LMAX / 16; ++j) {
+  for (int j = 0; j < nb; ++j) {
     s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     dp[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (j < nb) {
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
-        dp[j] = mma(da[kk], frag_row(Vs, 16 * j + m, kk, g), dp[j]);
-      }
+    for (int kk = 0; kk < 2; ++kk) {
+      s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
+      dp[j] = mma(da[kk], frag_row(Vs, 16 * j + m, kk, g), dp[j]);
     }
   }
   __syncthreads();  // every wave is done with Vs: it now holds the ds strips
@@ -279,15 +290,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const u
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < LMAX / 16; ++j)
-      if (j < nb) {
-        const float p = exp2f((s[j][i] * SCALE - li[i]) * LOG2E);
-        S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
-      }
+    for (int j = 0; j < nb; ++j)
+    {
+      const float p = exp2f((s[j][i] * SCALE - li[i]) * LOG2E);
+      S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
+    }
   // dq = ds k: A = ds rows (k = key), B = k rows read down the tile
   f32x4 acc[HD / 16];
 #pragma unroll
   for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
   for (int ks = 0; ks < L / 32; ++ks) {
     const bf16x8 a = S.frag(m, ks, g);
 #pragma unroll
@@ -306,19 +318,19 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const u
 // over the queries 64 at a time: s^T = k q^T, p^T, dp^T = v do^T,
 // ds^T = p^T (dp^T - D) / 8, dv += p^T do, dk += ds^T q
 // ---------------------------------------------------------------------------
+template <int L>
 __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const uint16_t* dout,
                                                      const float* lse, const float* dsum,
-                                                     int L, int C, uint16_t* dqkv) {
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[LMAX * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t dOs[LMAX * HD];
+                                                     int C, uint16_t* dqkv) {
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[L * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t dOs[L * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Ws[4][16 * QT];  // p^T, then ds^T, per wave
   const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
   const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_tile(Qs, base, C3, L);
-  load_tile(dOs, dout + row0 * C + h * HD, C, L);
+  load_tiles<L>(Qs, base, C3, dOs, dout + row0 * C + h * HD, C);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int m = lane & 15, g = lane >> 4;
   const int k0 = kt * QT + w * 16;  // the wave's first key in the image
@@ -340,6 +352,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
     dv[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
     dk[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+#pragma unroll 1
   for (int qc = 0; qc < L / QT; ++qc) {
     f32x4 st[4], dpt[4];
 #pragma unroll
@@ -407,28 +420,50 @@ bool attn_fits(int L, int C, int heads) {
   return L >= QT && L % QT == 0 && L <= LMAX && C == heads * HD;
 }
 
+template <int L>
+static hipError_t attn_fwd_t(const void* qkv, int B, int C, int heads, void* o, float* lse,
+                             hipStream_t st) {
+  hipLaunchKernelGGL(k_attn_fwd<L>, dim3(L / QT, heads, B), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(qkv), C, static_cast<uint16_t*>(o), lse);
+  return hipGetLastError();
+}
+
+template <int L>
+static hipError_t attn_bwd_t(const void* qkv, const void* o, const void* dout, const float* lse,
+                             int B, int C, int heads, void* dqkv, float* dsum, hipStream_t st) {
+  hipLaunchKernelGGL(k_attn_bwd_q<L>, dim3(L / QT, heads, B), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(o),
+                     static_cast<const uint16_t*>(dout), lse, C, static_cast<uint16_t*>(dqkv),
+                     dsum);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_attn_bwd_kv<L>, dim3(L / QT, heads, B), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout), lse,
+                     dsum, C, static_cast<uint16_t*>(dqkv));
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, float* lse,
                            hipStream_t st) {
   if (!attn_fits(L, C, heads)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_fwd, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o), lse);
-  return hipGetLastError();
+  switch (L) {
+    case 64: return attn_fwd_t<64>(qkv, B, C, heads, o, lse, st);
+    case 128: return attn_fwd_t<128>(qkv, B, C, heads, o, lse, st);
+    case 192: return attn_fwd_t<192>(qkv, B, C, heads, o, lse, st);
+    default: return attn_fwd_t<256>(qkv, B, C, heads, o, lse, st);
+  }
 }
 
 hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse,
                            int B, int L, int C, int heads, void* dqkv, float* dsum,
                            hipStream_t st) {
   if (!attn_fits(L, C, heads)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_bwd_q, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(o),
-                     static_cast<const uint16_t*>(dout), lse, L, C, static_cast<uint16_t*>(dqkv),
-                     dsum);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_attn_bwd_kv, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout), lse,
-                     dsum, L, C, static_cast<uint16_t*>(dqkv));
-  return hipGetLastError();
+  switch (L) {
+    case 64: return attn_bwd_t<64>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+    case 128: return attn_bwd_t<128>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+    case 192: return attn_bwd_t<192>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+    default: return attn_bwd_t<256>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+  }
 }
 
 }  // namespace pulse
