@@ -343,6 +343,13 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
     va[kk] =
         *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + 2 * C + 32 * kk + 8 * g);
   }
+  // lse and D of the query columns this lane holds: 16 t + m
+  float lq[L / 16], dq[L / 16];
+#pragma unroll
+  for (int t = 0; t < L / 16; ++t) {
+    lq[t] = lrow[16 * t + m];
+    dq[t] = drow[16 * t + m];
+  }
   __syncthreads();
 
   const Strip W = make_strip(Ws[w], QT);
@@ -352,7 +359,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
     dv[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
     dk[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-#pragma unroll 1
+#pragma unroll
   for (int qc = 0; qc < L / QT; ++qc) {
     f32x4 st[4], dpt[4];
 #pragma unroll
@@ -367,19 +374,13 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
       }
     }
     // the lane holds keys 4 g + i and query column qc * 64 + 16 jq + m
-    float lq[4], dq[4];
-#pragma unroll
-    for (int jq = 0; jq < 4; ++jq) {
-      lq[jq] = lrow[qc * QT + 16 * jq + m];
-      dq[jq] = drow[qc * QT + 16 * jq + m];
-    }
 #pragma unroll
     for (int jq = 0; jq < 4; ++jq)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = exp2f((st[jq][i] * SCALE - lq[jq]) * LOG2E);
+        const float p = exp2f((st[jq][i] * SCALE - lq[4 * qc + jq]) * LOG2E);
         st[jq][i] = p;
-        dpt[jq][i] = p * (dpt[jq][i] - dq[jq]) * SCALE;
+        dpt[jq][i] = p * (dpt[jq][i] - dq[4 * qc + jq]) * SCALE;
         W.put(4 * g + i, 16 * jq + m, p);
       }
     // dv += p^T do: A = p^T rows (k = query), B = do rows read down the tile
