@@ -116,4 +116,29 @@ __device__ __forceinline__ float dsilu_f(float z) {
   return s * (1.0f + z * (1.0f - s));
 }
 
+// erf(x) by Abramowitz and Stegun, Handbook of Mathematical Functions,
+// 7.1.26: erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e^(-x^2)
+// with t = 1 / (1 + p x) for x >= 0, odd in x; absolute error <= 1.5e-7,
+// branch-free.  e2 = e^(-x^2) is passed in so that callers can share it.
+__device__ __forceinline__ float erf_as(float x, float e2) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  const float poly =
+      t * (0.254829592f +
+           t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  return copysignf(1.0f - poly * e2, x);
+}
+
+// GELU(z) = z * Phi(z) with the standard normal CDF Phi (erf form)
+__device__ __forceinline__ float gelu_f(float z) {
+  const float e2 = __expf(-0.5f * z * z);
+  return 0.5f * z * (1.0f + erf_as(z * 0.70710678118654752f, e2));
+}
+
+// d GELU(z)/dz = Phi(z) + z * phi(z)
+__device__ __forceinline__ float gelu_d(float z) {
+  const float e2 = __expf(-0.5f * z * z);
+  return 0.5f * (1.0f + erf_as(z * 0.70710678118654752f, e2)) + z * 0.39894228040143268f * e2;
+}
+
 }  // namespace pulse

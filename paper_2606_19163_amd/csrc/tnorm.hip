@@ -11,7 +11,7 @@ namespace pulse {
 namespace {
 
 constexpr int LN_VEC = 4;        // 8-channel vectors per lane: C <= 64 * 8 * LN_VEC = 2048
-constexpr int LN_TOK = 4;        // tokens per wave in the backward pass
+constexpr int LN_TOK = 1;        // tokens per wave in the backward pass
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -166,11 +166,6 @@ __global__ __launch_bounds__(256) void k_ln_bwd(const uint16_t* dy, const uint16
   }
 }
 
-__device__ __forceinline__ float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678f)); }
-
-__device__ __forceinline__ float gelu_d(float z) {
-  return 0.5f * (1.0f + erff(z * 0.70710678f)) + z * 0.39894228f * __expf(-0.5f * z * z);
-}
 
 __global__ __launch_bounds__(256) void k_gelu_fwd(const uint16_t* z, uint16_t* m, long n8) {
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n8;
