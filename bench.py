@@ -188,6 +188,31 @@ def cpu_baseline(name, descs, seed, sample_batch, min_seconds=10.0):
                       f"fp64; {dt:.2f} s"}
 
 
+def timed_steps(step, steps):
+    """Run `steps` steps between two device synchronisations; returns the
+    wall time and the per-step times from HIP events recorded on the
+    current stream between steps (the stages join their side stream into it
+    at the end of every backward)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(steps):
+        step()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    return elapsed, per
+
+
+def step_stats(per):
+    n = len(per)
+    med = per[n // 2] if n % 2 else 0.5 * (per[n // 2 - 1] + per[n // 2])
+    return {"step_ms_median": round(med, 4), "step_ms_min": round(per[0], 4)}
+
+
 def tstage_cpu_baseline(desc, seed, sample_batch, min_seconds=10.0):
     """The transformer-stage oracle, as it stands, on `sample_batch` images of
     the workload (forward + backward), repeated until `min_seconds` have
@@ -240,11 +265,7 @@ def bench_tstage(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    elapsed, per = timed_steps(step, args.steps)
     launches, kms, kflops, kbytes = 0, 0.0, 0.0, 0.0
     if not args.no_kernel_events:
         st.timing(True)
@@ -270,6 +291,7 @@ def bench_tstage(args):
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "microbatches_per_s": round(args.steps / elapsed, 2),
         "gflop_per_step": round(flops_step / 1e9, 2),
+        **step_stats(per),
     }
     if launches:
         achieved = kflops / (kms * 1e-3) / 1e12
@@ -385,11 +407,7 @@ def main():
         step()
     torch.cuda.synchronize()
     # the timed steps: the stage as it runs in production
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    elapsed, per = timed_steps(step, args.steps)
     # the conv kernel's roofline: the same steps again with every conv launch
     # bracketed by HIP events on the stage stream (the backward then keeps
     # its weight-gradient GEMMs on that stream, so each event pair times the
@@ -432,6 +450,7 @@ def main():
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "microbatches_per_s": round(n_mb * args.steps / elapsed, 2),
         "gflop_per_step": round(flops_step / 1e9, 2),
+        **step_stats(per),
     }
     if events and launches:
         achieved = kflops / (kms * 1e-3) / 1e12

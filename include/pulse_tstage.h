@@ -125,6 +125,20 @@ pulse_status pulse_tstage_timing(pulse_tstage* st, int32_t enable);
 pulse_status pulse_tstage_timing_read(pulse_tstage* st, int64_t* launches, double* ms,
                                       double* flops, double* bytes);
 
+/* Execute steps [t0, t1) of device d's row of a collocated wave schedule
+ * (Sec. V; the table format of pulse_sched_build) on a transformer stage:
+ * each cell becomes pulse_tstage_forward/backward of the ENC half (stage
+ * s = d forward, s = 4D-1-d backward) or DEC half (s = 2D-1-d forward,
+ * s = 2D+d backward) for that microbatch, in step order, on `stream`.  The
+ * boundary tensors come from io[m] (x, u, g_enc, g_dec in; y_enc, y_dec, dx,
+ * du out; temb and dtemb are not used).  PULSE_E_INVALID_ARG when
+ * 0 <= t0 <= t1 <= T fails or a cell in the range is not one of the
+ * device's four stages (nothing is enqueued then); otherwise the first
+ * failing stage call's status. */
+pulse_status pulse_tsched_run_device(pulse_tstage* st, int32_t D, int32_t d, int32_t M,
+                                     const int32_t* table, int32_t T, int32_t t0, int32_t t1,
+                                     const pulse_mb_io* io, void* stream);
+
 /* FLOPs of one microbatch's ENC+DEC forward and backward: 2 M N K over every
  * linear-layer GEMM (forward, data and weight gradient) plus the attention
  * products (q k^T and p v forward; d p, d q, d k and d v backward). */

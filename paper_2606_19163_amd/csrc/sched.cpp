@@ -15,6 +15,7 @@
 
 #include "error.hpp"
 #include "pulse_stage.h"
+#include "pulse_tstage.h"
 
 namespace {
 
@@ -171,6 +172,41 @@ int max_inflight_of(int D, int M, const std::vector<std::vector<int>>& rows) {
   return worst;
 }
 
+// The four stages a device runs: the forward and backward of its encoder
+// partition d and of its decoder partition 2D - 1 - d.
+enum Cell { F_ENC, F_DEC, B_DEC, B_ENC };
+
+// Steps [t0, t1) of device d's row, each cell handed to call(cell, m) in
+// step order; every cell of the range is checked first, so that nothing
+// runs when one is not this device's.
+template <class Call>
+pulse_status run_row(int32_t D, int32_t d, int32_t M, const int32_t* table, int32_t T,
+                     int32_t t0, int32_t t1, Call call) {
+  if (!args_ok(D, M)) return bad_arg(kDM);
+  if (!table) return bad_arg("table is NULL");
+  if (d < 0 || d >= D) return bad_arg("device index out of range");
+  if (t0 < 0 || t0 > t1 || t1 > T) return bad_arg("step range outside [0, T]");
+  const int P = 2 * D;
+  const int f_enc = d, f_dec = P - 1 - d;                          // forward stages
+  const int b_dec = 2 * P - 1 - f_dec, b_enc = 2 * P - 1 - f_enc;  // their backwards
+  for (int t = t0; t < t1; ++t) {
+    const int v = table[(long)d * T + t];
+    if (v < 0) continue;
+    const int s = v / M;
+    if (v >= 4 * D * M || (s != f_enc && s != f_dec && s != b_dec && s != b_enc))
+      return bad_arg("a cell of the row is not one of this device's stages");
+  }
+  for (int t = t0; t < t1; ++t) {
+    const int v = table[(long)d * T + t];
+    if (v < 0) continue;
+    const int s = v / M, m = v - s * M;
+    const Cell c = s == f_enc ? F_ENC : s == f_dec ? F_DEC : s == b_dec ? B_DEC : B_ENC;
+    const pulse_status ps = call(c, m);
+    if (ps != PULSE_OK) return ps;
+  }
+  return PULSE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -275,38 +311,31 @@ pulse_status pulse_sched_inflight(int32_t D, int32_t M, const int32_t* table, in
 pulse_status pulse_sched_run_device(pulse_stage* st, int32_t D, int32_t d, int32_t M,
                                     const int32_t* table, int32_t T, int32_t t0, int32_t t1,
                                     const pulse_mb_io* io, void* stream) {
-  if (!args_ok(D, M)) return bad_arg(kDM);
-  if (!st || !table || !io) return bad_arg("stage, table or io is NULL");
-  if (d < 0 || d >= D) return bad_arg("device index out of range");
-  if (t0 < 0 || t0 > t1 || t1 > T) return bad_arg("step range outside [0, T]");
-  const int P = 2 * D;
-  const int f_enc = d, f_dec = P - 1 - d;             // forward stages of this device
-  const int b_dec = 2 * P - 1 - f_dec, b_enc = 2 * P - 1 - f_enc;  // their backwards
-  // every cell in the range must be one of this device's four stages
-  for (int t = t0; t < t1; ++t) {
-    const int v = table[(long)d * T + t];
-    if (v < 0) continue;
-    const int s = v / M;
-    if (v >= 4 * D * M || (s != f_enc && s != f_dec && s != b_dec && s != b_enc))
-      return bad_arg("a cell of the row is not one of this device's stages");
-  }
-  for (int t = t0; t < t1; ++t) {
-    const int v = table[(long)d * T + t];
-    if (v < 0) continue;
-    const int s = v / M, m = v - s * M;
+  if (!st || !io) return bad_arg("stage or io is NULL");
+  return run_row(D, d, M, table, T, t0, t1, [&](Cell c, int m) {
     const pulse_mb_io& b = io[m];
-    pulse_status ps;
-    if (s == f_enc)
-      ps = pulse_stage_forward(st, PULSE_ENC, m, b.x, b.temb, b.y_enc, stream);
-    else if (s == f_dec)
-      ps = pulse_stage_forward(st, PULSE_DEC, m, b.u, b.temb, b.y_dec, stream);
-    else if (s == b_dec)
-      ps = pulse_stage_backward(st, PULSE_DEC, m, b.g_dec, b.du, b.dtemb, stream);
-    else
-      ps = pulse_stage_backward(st, PULSE_ENC, m, b.g_enc, b.dx, b.dtemb, stream);
-    if (ps != PULSE_OK) return ps;
-  }
-  return PULSE_OK;
+    switch (c) {
+      case F_ENC: return pulse_stage_forward(st, PULSE_ENC, m, b.x, b.temb, b.y_enc, stream);
+      case F_DEC: return pulse_stage_forward(st, PULSE_DEC, m, b.u, b.temb, b.y_dec, stream);
+      case B_DEC: return pulse_stage_backward(st, PULSE_DEC, m, b.g_dec, b.du, b.dtemb, stream);
+      default: return pulse_stage_backward(st, PULSE_ENC, m, b.g_enc, b.dx, b.dtemb, stream);
+    }
+  });
+}
+
+pulse_status pulse_tsched_run_device(pulse_tstage* st, int32_t D, int32_t d, int32_t M,
+                                     const int32_t* table, int32_t T, int32_t t0, int32_t t1,
+                                     const pulse_mb_io* io, void* stream) {
+  if (!st || !io) return bad_arg("stage or io is NULL");
+  return run_row(D, d, M, table, T, t0, t1, [&](Cell c, int m) {
+    const pulse_mb_io& b = io[m];
+    switch (c) {
+      case F_ENC: return pulse_tstage_forward(st, PULSE_ENC, m, b.x, b.y_enc, stream);
+      case F_DEC: return pulse_tstage_forward(st, PULSE_DEC, m, b.u, b.y_dec, stream);
+      case B_DEC: return pulse_tstage_backward(st, PULSE_DEC, m, b.g_dec, b.du, stream);
+      default: return pulse_tstage_backward(st, PULSE_ENC, m, b.g_enc, b.dx, stream);
+    }
+  });
 }
 
 }  // extern "C"

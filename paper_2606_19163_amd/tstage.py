@@ -11,9 +11,9 @@ import ctypes
 import numpy as np
 
 from . import configs as _cfg
-from .stage import BF16, DEC, ENC, FLAG_DRY_RUN, _check, _ptr, _stream_handle, lib as _lib
+from .stage import BF16, DEC, ENC, FLAG_DRY_RUN, MbIO, _check, _ptr, _stream_handle, lib as _lib
 
-__all__ = ["TStageDesc", "TStage", "ENC", "DEC"]
+__all__ = ["TStageDesc", "TStage", "ENC", "DEC", "tsched_run_device"]
 
 _i32 = ctypes.c_int32
 _vp = ctypes.c_void_p
@@ -68,6 +68,9 @@ def lib():
         L.pulse_tstage_timing_read.restype = st
         L.pulse_tstage_flops.argtypes = [_vp]
         L.pulse_tstage_flops.restype = ctypes.c_double
+        L.pulse_tsched_run_device.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_i32), _i32,
+                                              _i32, _i32, ctypes.POINTER(MbIO), _vp]
+        L.pulse_tsched_run_device.restype = st
         _bound = True
     return L
 
@@ -203,3 +206,23 @@ class TStage:
         _check(lib().pulse_tstage_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms),
                                               ctypes.byref(fl), ctypes.byref(by)))
         return n.value, ms.value, fl.value, by.value
+
+
+def tsched_run_device(stage, D, d, M, table, io=None, t0=0, t1=None, stream=None):
+    """Run steps [t0, t1) of device d's row of the schedule on a transformer
+    stage.  ``io``: M dicts of device tensors (x, u, g_enc, g_dec in; y_enc,
+    y_dec, dx, du out); None for a dry-run stage."""
+    L = lib()
+    T = len(table[0])
+    t1 = T if t1 is None else t1
+    buf = (_i32 * (D * T))(*[v for row in table for v in row])
+    arr = (MbIO * M)()
+    keep = []
+    if io is not None:
+        for m in range(M):
+            for k, _ in MbIO._fields_:
+                t = io[m].get(k)
+                setattr(arr[m], k, t.data_ptr() if t is not None else None)
+                keep.append(t)
+    s = None if stage.dry else _stream_handle(stream)
+    _check(L.pulse_tsched_run_device(stage.h, D, d, M, buf, T, t0, t1, arr, s))

@@ -140,3 +140,97 @@ def test_tstage_every_wgrad_tile(tile, monkeypatch):
     ref = TO.tstage_run(d, p, b["x"], b["u"], b["g_enc"], b["g_dec"])
     got, _ = run_gpu(d, p, b)
     _compare(f"wgrad tile {tile}", got, ref)
+
+
+@pytest.mark.parametrize("D,M", [(2, 3), (3, 4)])
+def test_scheduled_transformer_pipeline(D, M):
+    """D transformer stages on this GPU wired as the devices of a D-device
+    pipeline (encoder outputs feed the next device's encoder, decoder
+    outputs the previous device's decoder, gradients flow back), driven one
+    step at a time through the wave schedule with pulse_tsched_run_device:
+    every boundary tensor and weight gradient equals bitwise the
+    microbatch-at-a-time run of the same chain, and the composed model
+    matches the oracle applied partition by partition."""
+    import torch
+    from paper_2606_19163_amd import stage as S
+    table, exact = S.sched_build(D, M)
+    need = max(S.sched_inflight(D, M, table))
+    log(f"case transformer schedule D={D} M={M} T={len(table[0])} in flight {need}")
+    desc = configs.t_tiny()
+    desc["max_inflight"] = need
+    sts, params = [], []
+    for d in range(D):
+        p, _ = synth.make_tstage(desc, 40 + d)
+        st = TS.TStage(desc)
+        st.set_params(p)
+        st.zero_grads()
+        sts.append(st)
+        params.append(p)
+    host = [synth.make_tstage(desc, 80 + m)[1] for m in range(M)]
+    io = [[{k: sts[d].act() for k in ("y_enc", "y_dec", "dx", "du")} for _ in range(M)]
+          for d in range(D)]
+    for m in range(M):
+        for d in range(D):
+            e = io[d][m]
+            e["x"] = sts[0].to_dev(host[m]["x"]) if d == 0 else io[d - 1][m]["y_enc"]
+            e["u"] = io[d + 1][m]["y_dec"] if d + 1 < D else e["y_enc"]
+            e["g_dec"] = sts[0].to_dev(host[m]["g_dec"]) if d == 0 else io[d - 1][m]["du"]
+            e["g_enc"] = io[d + 1][m]["dx"] if d + 1 < D else e["du"]
+
+    def snap():
+        torch.cuda.synchronize()
+        out = {}
+        for d in range(D):
+            out[("grads", d)] = sts[d].grads.cpu().numpy().tobytes()
+            for m in range(M):
+                for k in ("y_enc", "y_dec", "dx", "du"):
+                    out[(k, d, m)] = io[d][m][k].view(torch.uint16).cpu().numpy().tobytes()
+        return out
+
+    for t in range(len(table[0])):
+        for d in range(D):
+            TS.tsched_run_device(sts[d], D, d, M, table, io[d], t0=t, t1=t + 1)
+    for st in sts:
+        assert st.inflight() == 0
+    got = snap()
+    for d in range(D):
+        sts[d].zero_grads()
+    for m in range(M):
+        for d in range(D):
+            e = io[d][m]
+            sts[d].forward(TS.ENC, m, e["x"], out=e["y_enc"])
+        for d in reversed(range(D)):
+            e = io[d][m]
+            sts[d].forward(TS.DEC, m, e["u"], out=e["y_dec"])
+        for d in range(D):
+            e = io[d][m]
+            sts[d].backward(TS.DEC, m, e["g_dec"], din=e["du"])
+        for d in reversed(range(D)):
+            e = io[d][m]
+            sts[d].backward(TS.ENC, m, e["g_enc"], din=e["dx"])
+    ref = snap()
+    bad = [k for k in got if got[k] != ref[k]]
+    assert not bad, bad[:8]
+    # the composed model against the oracle (bf16 bound)
+    zeros = np.zeros_like(host[0]["x"])
+    for m in range(M):
+        x, ye = [None] * D, [None] * D
+        for d in range(D):
+            x[d] = host[m]["x"] if d == 0 else ye[d - 1]
+            ye[d] = TO.tstage_forward_only(desc, params[d], x[d], zeros)["y_enc"]
+        u, yd = [None] * D, [None] * D
+        for d in reversed(range(D)):
+            u[d] = yd[d + 1] if d + 1 < D else ye[d]
+            yd[d] = TO.tstage_forward_only(desc, params[d], x[d], u[d])["y_dec"]
+        gd, du = [None] * D, [None] * D
+        for d in range(D):
+            gd[d] = host[m]["g_dec"] if d == 0 else du[d - 1]
+            du[d] = TO.tstage_run(desc, params[d], x[d], u[d], zeros, gd[d])["du"]
+        dx = [None] * D
+        for d in reversed(range(D)):
+            ge = dx[d + 1] if d + 1 < D else du[d]
+            r = TO.tstage_run(desc, params[d], x[d], u[d], ge, gd[d])
+            dx[d] = r["dx"]
+            for k, v in (("y_enc", ye[d]), ("y_dec", yd[d]), ("du", r["du"]), ("dx", r["dx"])):
+                e = rel_l2(io[d][m][k].float().cpu().numpy(), v)
+                assert e < TOL, (d, m, k, e)

@@ -104,3 +104,46 @@ def test_bookkeeping_order_and_capacity():
 def test_dry_stage_binds_nothing():
     st = _dry(configs.t_tiny())
     assert st.ws_bytes == 0
+
+
+def test_skip_grad_exists_only_between_the_two_backward_halves():
+    import ctypes
+    d = configs.t_tiny()
+    st = _dry(d)
+    L = TS.lib()
+
+    def probe(mb, slot):
+        return L.pulse_tstage_skip_grad(st.h, mb, slot, None, None)
+
+    st.forward(TS.ENC, 4, None)
+    st.forward(TS.DEC, 4, None)
+    assert probe(4, 0) == S.E_CACHE_MISS       # before the decoder backward
+    st.backward(TS.DEC, 4, None)
+    assert probe(4, 0) == S.OK                 # buffered (dry run: no copy)
+    assert probe(4, 1) == S.E_INVALID_ARG      # slot out of range (one encoder block)
+    assert probe(5, 0) == S.E_CACHE_MISS       # unknown microbatch
+    st.backward(TS.ENC, 4, None)
+    assert probe(4, 0) == S.E_CACHE_MISS       # consumed by the encoder backward
+
+
+def test_schedule_rows_drive_a_dry_transformer_stage():
+    """Every device row of the collocated wave schedule runs through
+    pulse_tsched_run_device in dry-run mode: the state machine accepts the
+    schedule's order and every microbatch is released at the end; a cell of
+    another device is rejected before anything runs."""
+    from paper_2606_19163_amd import stage as S2
+    for D, M in [(1, 3), (2, 3), (3, 4)]:
+        table, _ = S2.sched_build(D, M)
+        need = S2.sched_inflight(D, M, table)
+        for d in range(D):
+            desc = configs.t_tiny()
+            desc["max_inflight"] = max(need)
+            st = _dry(desc)
+            TS.tsched_run_device(st, D, d, M, table)
+            assert st.inflight() == 0
+    table, _ = S2.sched_build(2, 2)
+    st = _dry(configs.t_tiny())
+    with pytest.raises(S.PulseError) as e:
+        TS.tsched_run_device(st, 2, 0, 2, [table[1], table[1]])  # device 1's cells as row 0
+    assert e.value.status == S.E_INVALID_ARG
+    assert st.inflight() == 0
