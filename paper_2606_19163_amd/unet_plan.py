@@ -144,25 +144,13 @@ def blockwise_cuts(n, p):
     return [per * (k + 1) - 1 for k in range(p - 1)]
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--batch", type=int, default=8)
-    ap.add_argument("--reps", type=int, default=20)
-    ap.add_argument("--tune", action="store_true",
-                    help="also time every block at microbatch 1, 2, 4, 8, 16 and run the "
-                         "hybrid tuner for 8, 16 and 32 devices at two memory limits")
-    args = ap.parse_args()
-    import torch
-    torch.cuda.set_device(0)
-    ops, skips = unet_ops(args.batch)
-    t_f = []
-    for op in ops:
-        t_f.append(time_forward(op, args.reps))
-        print(f"# {op['name']}: {t_f[-1] * 1e6:.1f} us", flush=True)
-    m_a = [float(out_bytes(op)) for op in ops]
-    n = len(ops)
-    out = {"batch": args.batch, "ops": [o["name"] for o in ops],
-           "forward_us": [round(t * 1e6, 2) for t in t_f],
+def partition_report(names, t_f, m_a, skips, batch):
+    """Balanced skip-aware partitions for 4 and 8 stages (with and without
+    the communication term) beside the block-wise split, and the forward
+    point-to-point bytes per sample of each collocated plan against a
+    sequential pipeline on the same devices."""
+    n = len(names)
+    out = {"batch": batch, "ops": list(names), "forward_us": [round(t * 1e6, 2) for t in t_f],
            "skips": skips, "plans": []}
     for p in (4, 8):
         for lam in (0.0, 1.0):
@@ -175,7 +163,7 @@ def main():
             # against a sequential pipeline of p / 2 stages balanced on the
             # same forward times (skips forwarded stage to stage)
             D = p // 2
-            per = 1.0 / args.batch
+            per = 1.0 / batch
             pulse_b = plan.comm_volume(m_a, skips, p, cuts, True) * per
             seq_cuts, _ = plan.partition(t_f, m_a, [], D) if D % 2 == 0 else \
                 (blockwise_cuts(n, D), 0.0)
@@ -193,6 +181,26 @@ def main():
                               "stage_us": [round(v * 1e6, 2) for v in bsc]},
                 "reduction_pct": round(100.0 * (1.0 - cost / max(bsc)), 1),
             })
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--batch", type=int, default=8)
+    ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--tune", action="store_true",
+                    help="also time every block at microbatch 1, 2, 4, 8, 16 and run the "
+                         "hybrid tuner for 8, 16 and 32 devices at two memory limits")
+    args = ap.parse_args()
+    import torch
+    torch.cuda.set_device(0)
+    ops, skips = unet_ops(args.batch)
+    t_f = []
+    for op in ops:
+        t_f.append(time_forward(op, args.reps))
+        print(f"# {op['name']}: {t_f[-1] * 1e6:.1f} us", flush=True)
+    m_a = [float(out_bytes(op)) for op in ops]
+    out = partition_report([o["name"] for o in ops], t_f, m_a, skips, args.batch)
     if args.tune:
         out["tune"] = tune_report(args.reps)
     print(json.dumps(out), flush=True)
@@ -216,6 +224,12 @@ def tune_report(reps, bs=(1, 2, 4, 8, 16)):
     m_theta = [param_bytes(o) for o in ops]
     m_a = [act_bytes_per_sample(o) for o in ops]
     m_o = [out_bytes_per_sample(o) for o in ops]
+    return tune_choices(bs, t_f, m_theta, m_a, m_o, skips)
+
+
+def tune_choices(bs, t_f, m_theta, m_a, m_o, skips):
+    """The hybrid tuner (Sec. VI) for 8, 16 and 32 devices at each memory
+    limit, from per-op forward times t_f[b_index][op] and byte counts."""
     res = {"bs": list(bs), "forward_us": [[round(v * 1e6, 2) for v in r] for r in t_f],
            "b_inter": B_INTER_NODE, "b_intra": B_INTRA_NODE, "t_lat": T_LAT_S,
            "choices": []}
