@@ -1197,6 +1197,9 @@ using C2_128x160K32 = CfgC<128, 160, 64, 80, 4, 32>;  // 4 waves, 4 stages of 32
 using C2_128x192 = CfgC<128, 192, 64, 96>;   // 4 waves
 using C2_64x128 = CfgC<64, 128, 32, 64>;     // 4 waves
 using C2_128x64 = CfgC<128, 64, 64, 32>;     // 4 waves
+using C2_64x128S3 = CfgC<64, 128, 32, 64, 3>;      // 4 waves, 3 stages
+using C2_64x128S4 = CfgC<64, 128, 32, 64, 4>;      // 4 waves, 4 stages
+using C2_64x128K32 = CfgC<64, 128, 32, 64, 4, 32>;  // 4 waves, 4 stages of 32 channels
 using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
 using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
@@ -1248,6 +1251,9 @@ TileInfo tile2_info(int t) {
     case TILE2_C128x192: return info2<C2_128x192>();
     case TILE2_C64x128: return info2<C2_64x128>();
     case TILE2_C128x64: return info2<C2_128x64>();
+    case TILE2_C64x128S3: return info2<C2_64x128S3>();
+    case TILE2_C64x128S4: return info2<C2_64x128S4>();
+    case TILE2_C64x128K32S4: return info2<C2_64x128K32>();
     case TILE2_W320x192: return info2<W2_320x192>();
     case TILE2_W320x128: return info2<W2_320x128>();
     case TILE2_W160x128: return info2<W2_160x128>();
@@ -1266,6 +1272,9 @@ hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
     case TILE2_C128x192: return conv2_t<C2_128x192>(a, st);
     case TILE2_C64x128: return conv2_t<C2_64x128>(a, st);
     case TILE2_C128x64: return conv2_t<C2_128x64>(a, st);
+    case TILE2_C64x128S3: return conv2_t<C2_64x128S3>(a, st);
+    case TILE2_C64x128S4: return conv2_t<C2_64x128S4>(a, st);
+    case TILE2_C64x128K32S4: return conv2_t<C2_64x128K32>(a, st);
     default: return conv2_t<C2_128x128>(a, st);
   }
 }

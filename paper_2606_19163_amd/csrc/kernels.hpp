@@ -91,13 +91,16 @@ enum Tile2 : int {
   TILE2_C128x192 = 7,       // 4 waves of 64 x 96, two blocks per CU
   TILE2_C64x128 = 8,        // 4 waves of 32 x 64, three blocks per CU
   TILE2_C128x64 = 9,        // 4 waves of 64 x 32, three blocks per CU
-  TILE2_CONV_LAST = 9,
-  TILE2_W320x192 = 10,
-  TILE2_W320x128 = 11,
-  TILE2_W128x128 = 12,
-  TILE2_W160x128 = 13,  // 4 waves, two blocks per CU
-  TILE2_WGRAD_FIRST = 10,
-  TILE2_WGRAD_LAST = 13
+  TILE2_C64x128S3 = 10,     // three LDS stages, two blocks per CU
+  TILE2_C64x128S4 = 11,     // four LDS stages, one block per CU
+  TILE2_C64x128K32S4 = 12,  // four LDS stages of 32 channels, three blocks per CU
+  TILE2_CONV_LAST = 12,
+  TILE2_W320x192 = 20,
+  TILE2_W320x128 = 21,
+  TILE2_W128x128 = 22,
+  TILE2_W160x128 = 23,  // 4 waves, two blocks per CU
+  TILE2_WGRAD_FIRST = 20,
+  TILE2_WGRAD_LAST = 23
 };
 TileInfo tile2_info(int tile);
 hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);

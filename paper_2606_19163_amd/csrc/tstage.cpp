@@ -178,7 +178,9 @@ int env_or(const char* name, int dflt) {
 // every tile and split on the 768-wide stage: the largest 128-row tile whose
 // tile count still fits one round of two blocks per CU (at least 400 tiles
 // of 128 x 192, 128 x 160 or 128 x 128), without a K split; otherwise
-// 64 x 128 tiles (three blocks per CU), split in two when K exceeds 1536.
+// 64 x 128 tiles with a three-stage LDS ring (two blocks per CU), no K split:
+// with 16 MFMAs per wave and K-step the deeper ring hides the operand
+// latency that two stages leave exposed, and beats splitting K.
 // Overrides (for sweeps): PULSE_TCONV_TILE forces a tile (with the split
 // rule of two blocks per CU, at least 4 K-steps per split),
 // PULSE_TCONV_KSPLIT_MAX caps the split.
@@ -212,10 +214,7 @@ ConvPlan tconv_plan(int tile_force, int ks_cap, long M, int N, int K) {
         p.tile = t;
       }
     }
-    if (p.tile < 0) {
-      p.tile = TILE2_C64x128;
-      ks = K > 1536 ? 2 : 1;
-    }
+    if (p.tile < 0) p.tile = TILE2_C64x128S3;
   }
   ks = std::min(ks, (long)std::max(1, ks_cap));
   const long kt = K / tile2_info(p.tile).bk;

@@ -120,7 +120,7 @@ def test_interleaved_microbatches_keep_their_skips():
         assert e < TOL, (k, e)
 
 
-@pytest.mark.parametrize("tile", range(10))
+@pytest.mark.parametrize("tile", range(13))
 def test_tstage_every_conv_tile(tile, monkeypatch):
     """Every conv-mode tile shape on the token-major linear layers (ragged
     rows and columns)."""
@@ -132,7 +132,7 @@ def test_tstage_every_conv_tile(tile, monkeypatch):
     _compare(f"conv tile {tile}", got, ref)
 
 
-@pytest.mark.parametrize("tile", [10, 11, 12, 13])
+@pytest.mark.parametrize("tile", [20, 21, 22, 23])
 def test_tstage_every_wgrad_tile(tile, monkeypatch):
     monkeypatch.setenv("PULSE_TWGRAD_TILE", str(tile))
     d = _mid()
