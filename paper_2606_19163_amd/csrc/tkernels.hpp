@@ -23,7 +23,7 @@ hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, con
                            int B, int L, int C, int heads, void* dqkv, float* dsum,
                            hipStream_t st);
 
-// ---- LayerNorm, GELU, adds (tnorm.hip) -----------------------------------
+// ---- LayerNorm, GELU (tnorm.hip) -----------------------------------
 
 // C % 8 == 0 and C <= 2048.
 // y = LN(x) * g + b per token; stats[2 t] = mean, stats[2 t + 1] = rstd.
@@ -38,8 +38,5 @@ hipError_t launch_ln_bwd(const void* dy, const void* x, const float* stats, cons
 hipError_t launch_gelu_fwd(const void* z, void* m, long n, hipStream_t st);
 // dz = dm * GELU'(z); dz may alias dm
 hipError_t launch_gelu_bwd(const void* dm, const void* z, void* dz, long n, hipStream_t st);
-// dst[r][c] = a[r * sa + c] + b[r * sb + c] for c < cols (cols % 8 == 0)
-hipError_t launch_add2(const void* a, long sa, const void* b, long sb, void* dst, int cols,
-                       long rows, hipStream_t st);
 
 }  // namespace pulse

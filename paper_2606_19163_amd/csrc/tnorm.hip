@@ -191,24 +191,6 @@ __global__ __launch_bounds__(256) void k_gelu_bwd(const uint16_t* dm, const uint
   }
 }
 
-// dst = a + b (bf16, n = 8 * n8 elements; a and b with row strides sa, sb
-// elements over rows of `cols` elements)
-__global__ __launch_bounds__(256) void k_add2(const uint16_t* a, long sa, const uint16_t* b,
-                                              long sb, uint16_t* dst, int cols, long rows) {
-  const int nv = cols / 8;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < rows * nv;
-       i += (long)gridDim.x * blockDim.x) {
-    const long r = i / nv;
-    const int c = (int)(i - r * nv) * 8;
-    float x[8], y[8];
-    ld8bf(a + r * sa + c, x);
-    ld8bf(b + r * sb + c, y);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) x[k] += y[k];
-    st8bf(dst + r * cols + c, x);
-  }
-}
-
 unsigned grid_of(long n, long cap = 8192) {
   long b = (n + 255) / 256;
   return (unsigned)(b < 1 ? 1 : (b > cap ? cap : b));
@@ -249,15 +231,6 @@ hipError_t launch_gelu_bwd(const void* dm, const void* z, void* dz, long n, hipS
   hipLaunchKernelGGL(k_gelu_bwd, dim3(grid_of(n / 8)), dim3(256), 0, st,
                      static_cast<const uint16_t*>(dm), static_cast<const uint16_t*>(z),
                      static_cast<uint16_t*>(dz), n / 8);
-  return hipGetLastError();
-}
-
-hipError_t launch_add2(const void* a, long sa, const void* b, long sb, void* dst, int cols,
-                       long rows, hipStream_t st) {
-  if (cols % 8) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_add2, dim3(grid_of(rows * (cols / 8))), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(a), sa, static_cast<const uint16_t*>(b), sb,
-                     static_cast<uint16_t*>(dst), cols, rows);
   return hipGetLastError();
 }
 
