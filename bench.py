@@ -185,7 +185,22 @@ def cpu_baseline(name, descs, seed, sample_batch, min_seconds=10.0):
             "kind": "oracle",
             "sample": f"{runs} x {sample_batch} of {descs[0]['batch']} images of one microbatch of "
                       f"the first stage ({d['height']}x{d['width']}), forward + backward, numpy "
-                      f"fp64; {dt:.2f} s"}
+                      f"fp64; {dt:.2f} s", **host_info()}
+
+
+def host_info():
+    """CPU model, logical CPU count and OMP thread setting of the host."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "cpu_count": os.cpu_count(),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
 
 def timed_steps(step, steps):
@@ -236,7 +251,7 @@ def tstage_cpu_baseline(desc, seed, sample_batch, min_seconds=10.0):
     return {"value": runs * flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{runs} x {sample_batch} of {desc['batch']} images of one microbatch, "
-                      f"forward + backward, numpy fp64; {dt:.2f} s"}
+                      f"forward + backward, numpy fp64; {dt:.2f} s", **host_info()}
 
 
 def bench_tstage(args):
