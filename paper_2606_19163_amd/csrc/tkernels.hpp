@@ -30,10 +30,14 @@ hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, con
 hipError_t launch_ln_fwd(const void* x, long T, int C, float eps, const float* g, const float* b,
                          void* y, float* stats, hipStream_t st);
 // dx = add + d LN / dx (add [T][C] bf16 or null); part[ln_bwd_blocks(T)][2][C]
-// receives per-block sums of dy * xhat (row 0) and dy (row 1).
+// receives per-block sums of dy * xhat (row 0) and dy (row 1); csum (or
+// null), [ln_bwd_blocks(T)][2][C], per-block column sums of dx as stored in
+// row 0.
 int ln_bwd_blocks(long T);
 hipError_t launch_ln_bwd(const void* dy, const void* x, const float* stats, const float* g,
-                         const void* add, long T, int C, void* dx, float* part, hipStream_t st);
+                         const void* add, long T, int C, void* dx, float* part, float* csum,
+                         hipStream_t st);
+
 // m = GELU(z) (erf form), n % 8 == 0 elements
 hipError_t launch_gelu_fwd(const void* z, void* m, long n, hipStream_t st);
 // dz = dm * GELU'(z); dz may alias dm

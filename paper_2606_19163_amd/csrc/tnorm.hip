@@ -87,15 +87,15 @@ __global__ __launch_bounds__(256) void k_ln_fwd(const uint16_t* x, long T, int C
 __global__ __launch_bounds__(256) void k_ln_bwd(const uint16_t* dy, const uint16_t* x,
                                                 const float2* stats, const float* g,
                                                 const uint16_t* add, long T, int C, uint16_t* dx,
-                                                float* part) {
+                                                float* part, float* csum) {
   __shared__ float sm[4][2][64 * LN_VEC * 8 / 4];  // per wave, [2][C / 4 per j] reused below
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nv = C / 8;
-  float accg[LN_VEC][8], accb[LN_VEC][8];
+  float accg[LN_VEC][8], accb[LN_VEC][8], accx[LN_VEC][8];
 #pragma unroll
   for (int j = 0; j < LN_VEC; ++j)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) accg[j][i] = accb[j][i] = 0.f;
+    for (int i = 0; i < 8; ++i) accg[j][i] = accb[j][i] = accx[j][i] = 0.f;
   for (int k = 0; k < LN_TOK; ++k) {
     const long t = ((long)blockIdx.x * 4 + w) * LN_TOK + k;
     if (t >= T) break;
@@ -133,7 +133,10 @@ __global__ __launch_bounds__(256) void k_ln_bwd(const uint16_t* dy, const uint16
           for (int i = 0; i < 8; ++i) a[i] = 0.f;
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] = a[i] + st.y * (gy[j][i] - m1 - xh[j][i] * m2);
+        for (int i = 0; i < 8; ++i) {
+          o[i] = a[i] + st.y * (gy[j][i] - m1 - xh[j][i] * m2);
+          accx[j][i] += bf2f(f2bf(o[i]));  // the value as stored
+        }
         st8bf(dx + t * C + vi * 8, o);
       }
     }
@@ -161,6 +164,26 @@ __global__ __launch_bounds__(256) void k_ln_bwd(const uint16_t* dy, const uint16
         }
         out[vi * 8 + i] = sg;
         out[C + vi * 8 + i] = sb;
+      }
+    }
+  }
+  if (!csum) return;
+  // column sums of dx as stored, to csum[block][0][C]
+  float* cs = csum + (long)blockIdx.x * 2 * C;
+#pragma unroll
+  for (int j = 0; j < LN_VEC; ++j) {
+    const int vi = lane + 64 * j;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sm[w][0][lane * 8 + i] = accx[j][i];
+    __syncthreads();
+    if (w == 0 && vi < nv) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float sx = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) sx += sm[ww][0][lane * 8 + i];
+        cs[vi * 8 + i] = sx;
       }
     }
   }
@@ -210,12 +233,13 @@ hipError_t launch_ln_fwd(const void* x, long T, int C, float eps, const float* g
 }
 
 hipError_t launch_ln_bwd(const void* dy, const void* x, const float* stats, const float* g,
-                         const void* add, long T, int C, void* dx, float* part, hipStream_t st) {
+                         const void* add, long T, int C, void* dx, float* part, float* csum,
+                         hipStream_t st) {
   if (C % 8 || C > 64 * 8 * LN_VEC) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_ln_bwd, dim3((unsigned)ln_bwd_blocks(T)), dim3(256), 0, st,
                      static_cast<const uint16_t*>(dy), static_cast<const uint16_t*>(x),
                      reinterpret_cast<const float2*>(stats), g, static_cast<const uint16_t*>(add),
-                     T, C, static_cast<uint16_t*>(dx), part);
+                     T, C, static_cast<uint16_t*>(dx), part, csum);
   return hipGetLastError();
 }
 
@@ -225,6 +249,7 @@ hipError_t launch_gelu_fwd(const void* z, void* m, long n, hipStream_t st) {
                      static_cast<const uint16_t*>(z), static_cast<uint16_t*>(m), n / 8);
   return hipGetLastError();
 }
+
 
 hipError_t launch_gelu_bwd(const void* dm, const void* z, void* dz, long n, hipStream_t st) {
   if (n % 8) return hipErrorInvalidValue;

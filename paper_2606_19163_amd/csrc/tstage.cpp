@@ -104,6 +104,10 @@ struct pulse_tstage {
          s_dsx = 0, s_dv = 0, s_dsum = 0, s_kpart = 0, s_wpart = 0, s_red = 0, s_zero = 0;
   size_t kpart_cap = 0, wpart_cap = 0, red_cap = 0;
   size_t s_red2 = 0;  // reduction buffer of the side stream
+  // column-sum partials of dh (LN2 backward) and of a decoder block's
+  // skip-linear output gradient (LN1 backward): the bias gradients of proj
+  // and skip without another pass over them
+  size_t s_cs_h = 0, s_cs_x = 0;
   // side stream: the weight-gradient GEMMs and bias-gradient sums of the
   // backward pass run on it, concurrently with the data-gradient chain
   hipStream_t side = nullptr;
@@ -354,6 +358,8 @@ void build_layout(pulse_tstage* s) {
   s->red_cap = red;
   s->s_red = take(red * 4);
   s->s_red2 = take(red * 4);
+  s->s_cs_h = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
+  s->s_cs_x = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
   s->s_zero = take(256);
   // per-microbatch rows
   s->off_rows = off;
@@ -528,13 +534,22 @@ pulse_status col_sum(pulse_tstage* s, const void* v, int N, float* acc, float* p
   return PULSE_OK;
 }
 
-// LayerNorm backward: dx = add + dLN(dy); g/b gradients accumulated
+// acc[n] += sum of rows [0, rows) of partials laid out [rows][2][N] (row 0)
+pulse_status totals(const float* part, int rows, int N, float* acc, hipStream_t st) {
+  RedGrid rg{};
+  rg.chunks = rows;
+  THIP(launch_chan_totals(part, Geo{1, 1, 1}, rg, N, 1, acc, nullptr, nullptr, st));
+  return PULSE_OK;
+}
+
+// LayerNorm backward: dx = add + dLN(dy); g/b gradients accumulated; csum
+// (or null) receives the column-sum partials of dx
 pulse_status ln_backward(pulse_tstage* s, const void* dy, const void* x, const float* stats,
                          int64_t goff, int64_t boff, const void* add, void* dx,
-                         hipStream_t st) {
+                         hipStream_t st, float* csum = nullptr) {
   const int nb = ln_bwd_blocks(s->T);
   float* part = s->fat(s->s_red);
-  THIP(launch_ln_bwd(dy, x, stats, s->pp(goff), add, s->T, s->C, dx, part, st));
+  THIP(launch_ln_bwd(dy, x, stats, s->pp(goff), add, s->T, s->C, dx, part, csum, st));
   RedGrid rg{};
   rg.chunks = nb;
   THIP(launch_chan_totals(part, Geo{1, 1, 1}, rg, s->C, 2, s->gp(goff), nullptr, s->gp(boff),
@@ -637,10 +652,16 @@ pulse_status wait_for(BwdSync& y, hipEvent_t e) {
 // the caller's stream waits for all side work
 pulse_status join(BwdSync& y) { return wait_for(y, y.last); }
 
-// parameter gradients of one linear layer: bias += colsum(gy), W += gy^T in
-pulse_status param_grads(BwdSync& y, int M, const Seg& in, const void* gy, float* bias) {
+// parameter gradients of one linear layer: bias += colsum(gy), W += gy^T in;
+// with `part` the column sums come from the producer of gy as partials
+// [rows][2][M]
+pulse_status param_grads(BwdSync& y, int M, const Seg& in, const void* gy, float* bias,
+                         const float* part = nullptr, int rows = 0) {
   TCHK(fork(y));
-  TCHK(col_sum(y.s, gy, M, bias, y.red, y.work));
+  if (part)
+    TCHK(totals(part, rows, M, bias, y.work));
+  else
+    TCHK(col_sum(y.s, gy, M, bias, y.red, y.work));
   TCHK(linear_wgrad(y.s, M, in, gy, y.work));
   return PULSE_OK;
 }
@@ -653,7 +674,7 @@ struct SideReads {
 
 // dx = d(block)/dx^T dy for the block input x; parameter gradients +=
 pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, const void* x,
-                       const void* dy, void* dx) {
+                       const void* dy, void* dx, float* dx_csum = nullptr) {
   pulse_tstage* s = y.s;
   hipStream_t st = y.st;
   const int C = s->C, R = s->R;
@@ -685,9 +706,11 @@ pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, co
   TCHK(linear(s, C, tseg(R, tvin(dm, R)), s->at(b.t_fc1), R, nullptr, nullptr, da2, nullptr,
               DT_BF16, st));
   TCHK(wait_for(y, rd.dh));
-  TCHK(ln_backward(s, da2, h, st2, b.ln2g, b.ln2b, dy, dh, st));
+  float* cs_h = s->fat(s->s_cs_h);
+  TCHK(ln_backward(s, da2, h, st2, b.ln2g, b.ln2b, dy, dh, st, cs_h));
   // attention: h = x + Proj(MHA(LN1(x)))
-  TCHK(param_grads(y, C, tseg(C, tvin(o, C), s->gp(b.projW)), dh, s->gp(b.projb)));
+  TCHK(param_grads(y, C, tseg(C, tvin(o, C), s->gp(b.projW)), dh, s->gp(b.projb), cs_h,
+                   ln_bwd_blocks(T)));
   TCHK(mark(y, &rd.dh));
   TCHK(linear(s, C, tseg(C, tvin(dh, C)), s->at(b.t_proj), C, nullptr, nullptr, dO, nullptr,
               DT_BF16, st));
@@ -698,7 +721,7 @@ pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, co
   TCHK(mark(y, &rd.dqkv));
   TCHK(linear(s, C, tseg(3 * C, tvin(dqkv, 3 * C)), s->at(b.t_qkv), 3 * C, nullptr, nullptr, da,
               nullptr, DT_BF16, st));
-  TCHK(ln_backward(s, da, x, st1, b.ln1g, b.ln1b, dh, dx, st));
+  TCHK(ln_backward(s, da, x, st1, b.ln1g, b.ln1b, dh, dx, st, dx_csum));
   return PULSE_OK;
 }
 
@@ -936,12 +959,13 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
         const TBlock& b = s->db[k];
         void* dsx = s->at(s->s_dsx);
         TCHK(wait_for(y, rd.dsx));
-        TCHK(block_bwd(y, rd, row, b, row + b.r_x, dy, dsx));
+        float* cs_x = s->fat(s->s_cs_x);
+        TCHK(block_bwd(y, rd, row, b, row + b.r_x, dy, dsx, cs_x));
         // skip linear over [v || skip]
         const int slot = ne - 1 - k;
         const void* skip = row + s->row_slot[slot];
         TCHK(param_grads(y, C, tseg(2 * C, tvin2(row + b.r_v, C, skip, C), s->gp(b.skW)), dsx,
-                         s->gp(b.skb)));
+                         s->gp(b.skb), cs_x, ln_bwd_blocks(s->T)));
         TCHK(mark(y, &rd.dsx));
         void* dv = k == 0 ? din : s->at(s->s_dy[k & 1]);
         // dv's buffer held the dy of block k + 1, which the side stream reads
