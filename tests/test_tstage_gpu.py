@@ -23,7 +23,16 @@ def _mid():
     return d
 
 
-CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t768": (configs.t768, 7)}
+def _narrow():
+    """128 tokens (the attention kernels' L = 128 instance), one image,
+    width 256 in 4 heads, a 2x MLP, 1 + 1 blocks."""
+    d = configs._tstage(1, 128, 256, 4, 1, 1)
+    d["mlp"] = 2
+    return d
+
+
+CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t_narrow": (_narrow, 12),
+         "t768": (configs.t768, 7)}
 
 
 def run_gpu(desc, params, b, mbs=(0,)):
