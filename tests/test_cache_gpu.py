@@ -116,3 +116,39 @@ def test_state_errors_enqueue_nothing():
         st.backward(S.ENC, 0, x)
     assert e.value.status == S.E_STATE
     assert st.inflight() == 0
+
+
+@pytest.mark.parametrize("level", [0, 1, 2, 3])
+def test_full_size_wave_order_matches_isolated_microbatches(level):
+    """The wave workload's launch configuration at full size: one level of
+    the four (64x64x320, 32x32x640, 16x16x1280, 8x8x1280 at batch 8) with 4
+    microbatches in flight, all forward passes, then the backward passes in
+    reverse.  Every per-microbatch output equals an isolated run bitwise (the
+    isolated runs are the ones the full-size parity tests compare with the
+    oracle), and so do the accumulated gradients."""
+    import torch
+    desc = configs.wave_levels()[level]
+    name = ["l64", "l32", "l16", "l8"][level]
+    params, bounds = synth.make_wave([desc], configs.SEEDS["wave"] + level, 4)
+    st = S.Stage(desc)
+    st.set_params(params[0])
+    dbs = [device_boundary(st, bb) for bb in bounds[0]]
+    log(f"case full-size wave level {name}: B={desc['batch']} {desc['height']}x{desc['width']}")
+    y = {}
+    for m in range(4):
+        y[("e", m)] = st.forward(S.ENC, m, dbs[m]["x"], dbs[m]["temb"])
+        y[("d", m)] = st.forward(S.DEC, m, dbs[m]["u"], dbs[m]["temb"])
+    assert st.inflight() == 4
+    for m in reversed(range(4)):
+        y[("du", m)] = st.backward(S.DEC, m, dbs[m]["g_dec"])
+        y[("dx", m)] = st.backward(S.ENC, m, dbs[m]["g_enc"])
+    torch.cuda.synchronize()
+    wave_grads = _bytes(st.grads)
+    st.zero_grads()
+    for m in reversed(range(4)):
+        out = S.run_microbatch(st, 100 + m, dbs[m])
+        torch.cuda.synchronize()
+        for k, t in (("e", "y_enc"), ("d", "y_dec"), ("du", "du"), ("dx", "dx")):
+            assert torch.equal(out[t].view(torch.int16), y[(k, m)].view(torch.int16)), (m, t)
+    assert _bytes(st.grads) == wave_grads
+    assert st.inflight() == 0
