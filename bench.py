@@ -255,9 +255,11 @@ def tstage_cpu_baseline(desc, seed, sample_batch, min_seconds=10.0):
 
 
 def bench_tstage(args):
-    """One transformer-block stage (UViT-like, 256 tokens of 768 channels,
-    12 heads, 2 + 2 blocks, batch 16): the same step and JSON line as the
-    ResBlock stages, with the roofline of the token-major GEMM launches."""
+    """One transformer-block stage (t768: UViT-like, 256 tokens of 768
+    channels, 12 heads, 2 + 2 blocks, batch 16; t1408: Hunyuan-DiT-like, 1024
+    tokens of 1408 channels, 22 heads, 1 + 1 blocks, batch 8): the same step
+    and JSON line as the ResBlock stages, with the roofline of the
+    token-major GEMM launches."""
     import torch
     from paper_2606_19163_amd import configs, synth
     from paper_2606_19163_amd import tstage as TS
@@ -318,7 +320,8 @@ def bench_tstage(args):
             "avg_launch_us": round(kms * 1e3 / launches, 2),
             "avg_gflop_per_launch": round(kflops / launches / 1e9, 3)}
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = tstage_cpu_baseline(d, seed, min(args.cpu_sample_batch, 2))
+        sample = 1 if d["tokens"] >= 1024 else min(args.cpu_sample_batch, 2)
+        line["cpu_baseline"] = tstage_cpu_baseline(d, seed, sample)
     print(json.dumps(line), flush=True)
 
 
@@ -329,7 +332,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="l64",
                     choices=["l64", "l32", "l16", "l8", "tiny", "wave", "wave-sched",
-                             "t768", "t_tiny"])
+                             "t768", "t1408", "t_tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
     ap.add_argument("--serial", action="store_true",
@@ -349,7 +352,7 @@ def main():
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
-    if args.workload in ("t768", "t_tiny"):
+    if args.workload in ("t768", "t1408", "t_tiny"):
         return bench_tstage(args)
     if args.serial:
         os.environ["PULSE_SERIAL"] = "1"

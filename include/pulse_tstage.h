@@ -46,7 +46,7 @@ typedef struct pulse_tstage pulse_tstage; /* opaque, library-owned */
 
 typedef struct {
   int32_t batch;        /* images per microbatch                              */
-  int32_t tokens;       /* tokens per image: a multiple of 64, at most 256     */
+  int32_t tokens;       /* tokens per image: a multiple of 64, at most 4096    */
   int32_t width;        /* channels C = 64 * heads, at most 2048               */
   int32_t heads;        /* attention heads of dimension 64                     */
   int32_t mlp_ratio;    /* MLP hidden width = mlp_ratio * width (1..8)         */

@@ -158,10 +158,19 @@ def t768(batch=16):
     return _tstage(batch, 256, 768, 12, 2, 2)
 
 
+def t1408(batch=8):
+    """Hunyuan-DiT-like stage: 1024 tokens (a 64x64x4 latent in 2x2 patches)
+    of 1408 channels, split into 22 heads of 64 (the attention kernels' head
+    dimension), a 4x MLP, 1 encoder and 1 decoder block."""
+    return _tstage(batch, 1024, 1408, 22, 1, 1)
+
+
 CONFIGS["t_tiny"] = t_tiny
 CONFIGS["t768"] = t768
+CONFIGS["t1408"] = t1408
 SEEDS["t_tiny"] = 6
 SEEDS["t768"] = 7
+SEEDS["t1408"] = 8
 
 
 def tparam_names(desc):

@@ -1,8 +1,10 @@
 // Multi-head self-attention of the transformer-block stage (gfx950, bf16
 // MFMA 16x16x32, fp32 accumulation).  Head dimension 64; L tokens per image
-// with L a multiple of 64 and at most 256, so one head's keys and values fit
-// in LDS whole.  q, k and v are the three C-channel thirds of the qkv rows
-// [B*L][3C]; head h owns channels [64 h, 64 h + 64) of each third.
+// with L a multiple of 64.  Up to 256 tokens one head's keys and values (or
+// queries and output gradients) are held in LDS whole; longer sequences, up
+// to 4096, stream them through LDS 64 tokens at a time.  q, k and v are the
+// three C-channel thirds of the qkv rows [B*L][3C]; head h owns channels
+// [64 h, 64 h + 64) of each third.
 //
 //   forward : s = q k^T / 8, p = softmax_rows(s), o = p v; the row's
 //             log-sum-exp lse = log sum_j exp(s_j) is kept (fp32), not p
@@ -38,7 +40,7 @@ typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 constexpr int HD = 64;        // head dimension
 constexpr int QT = 64;        // queries (or keys) per block: 4 waves x 16
-constexpr int LMAX = 256;     // tokens per image, at most
+constexpr int LMAX = 256;     // tokens per image held whole in LDS; longer ones stream
 constexpr float SCALE = 0.125f;  // 1 / sqrt(64)
 constexpr float LOG2E = 1.44269504088896341f;
 
@@ -415,10 +417,312 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Longer sequences (L > 256): the same products, streamed over 64-token
+// chunks of the other side.  The forward keeps a running row maximum and
+// sum (online softmax) and rescales its o accumulators when the maximum
+// grows; the backward kernels walk key (dq) or query (dk, dv) chunks.  Each
+// chunk is loaded into registers one iteration ahead and stored into a
+// single LDS tile per operand at the top of the next iteration.
+// ---------------------------------------------------------------------------
+
+constexpr int KC = 64;  // tokens per streamed chunk
+
+// the two 16-byte chunks this thread moves of a [64][64] tile
+__device__ __forceinline__ void chunk_regs(uint4 (&v)[2], const uint16_t* src, long stride) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    v[u] = *reinterpret_cast<const uint4*>(src + (long)(e >> 3) * stride + (e & 7) * 8);
+  }
+}
+
+__device__ __forceinline__ void chunk_store(uint16_t* t, const uint4 (&v)[2]) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    *reinterpret_cast<uint4*>(t + toff(e >> 3, e & 7)) = v[u];
+  }
+}
+
+__global__ __launch_bounds__(256) void k_attn_fwd_s(const uint16_t* qkv, int L, int C,
+                                                    uint16_t* o, float* lse) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ps[4][16 * KC];
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int H = gridDim.y;
+  const long row0 = (long)b * L;
+  const long C3 = 3L * C;
+  const uint16_t* base = qkv + row0 * C3 + h * HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  const int q0 = qt * QT + w * 16;
+  bf16x8 qa[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
+  uint4 rk[2], rv[2];
+  chunk_regs(rk, base + C, C3);
+  chunk_regs(rv, base + 2 * C, C3);
+  const Strip P = make_strip(Ps[w], KC);
+  float mrow[4], lrow[4];
+  f32x4 acc[HD / 16];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    mrow[i] = -INFINITY;
+    lrow[i] = 0.f;
+  }
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nch = L / KC;
+  for (int kc = 0; kc < nch; ++kc) {
+    __syncthreads();  // every wave is done with the previous chunk
+    chunk_store(Ks, rk);
+    chunk_store(Vs, rv);
+    __syncthreads();
+    if (kc + 1 < nch) {
+      chunk_regs(rk, base + (long)(kc + 1) * KC * C3 + C, C3);
+      chunk_regs(rv, base + (long)(kc + 1) * KC * C3 + 2 * C, C3);
+    }
+    f32x4 sc[KC / 16];
+#pragma unroll
+    for (int j = 0; j < KC / 16; ++j) {
+      sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) sc[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), sc[j]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float cm = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < KC / 16; ++j) cm = fmaxf(cm, sc[j][i]);
+      const float mn = fmaxf(mrow[i], row_max16(cm));
+      const float alpha = exp2f((mrow[i] - mn) * (SCALE * LOG2E));  // 0 for the first chunk
+      float rs = 0.f;
+#pragma unroll
+      for (int j = 0; j < KC / 16; ++j) {
+        const float e = exp2f((sc[j][i] - mn) * (SCALE * LOG2E));
+        sc[j][i] = e;
+        rs += e;
+      }
+      lrow[i] = lrow[i] * alpha + row_sum16(rs);
+      mrow[i] = mn;
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd) acc[jd][i] *= alpha;
+#pragma unroll
+      for (int j = 0; j < KC / 16; ++j) P.put(4 * g + i, 16 * j + m, sc[j][i]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < KC / 32; ++ks) {
+      const bf16x8 a = P.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        acc[jd] = mma(a, frag_tr(Vs, 32 * ks, 16 * jd, lane), acc[jd]);
+    }
+  }
+  const long orow = row0 + q0 + 4 * g;
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[(orow + i) * C + h * HD + jd * 16 + m] = bf(acc[jd][i] / lrow[i]);
+  if (m == 0) {
+    float* l = lse + ((long)b * H + h) * L + q0 + 4 * g;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) l[i] = mrow[i] * SCALE + logf(lrow[i]);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_attn_bwd_q_s(const uint16_t* qkv, const uint16_t* o,
+                                                      const uint16_t* dout, const float* lse,
+                                                      int L, int C, uint16_t* dqkv,
+                                                      float* dsum) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ss[4][16 * KC];
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int H = gridDim.y;
+  const long row0 = (long)b * L;
+  const long C3 = 3L * C;
+  const uint16_t* base = qkv + row0 * C3 + h * HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  const int q0 = qt * QT + w * 16;
+  const long lrow = ((long)b * H + h) * L + q0;
+  bf16x8 qa[2], da[2];
+  float dpart = 0.f;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const long r = row0 + q0 + m;
+    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
+    da[kk] = *reinterpret_cast<const bf16x8*>(dout + r * C + h * HD + 32 * kk + 8 * g);
+    const bf16x8 ov = *reinterpret_cast<const bf16x8*>(o + r * C + h * HD + 32 * kk + 8 * g);
+    dpart += dot8(da[kk], ov);
+  }
+  dpart += __shfl_xor(dpart, 16, 64);
+  dpart += __shfl_xor(dpart, 32, 64);
+  if (g == 0) dsum[lrow + m] = dpart;
+  float Di[4], li[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    Di[i] = __shfl(dpart, 4 * g + i, 64);
+    li[i] = lse[lrow + 4 * g + i];
+  }
+  uint4 rk[2], rv[2];
+  chunk_regs(rk, base + C, C3);
+  chunk_regs(rv, base + 2 * C, C3);
+  const Strip S = make_strip(Ss[w], KC);
+  f32x4 acc[HD / 16];
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nch = L / KC;
+  for (int kc = 0; kc < nch; ++kc) {
+    __syncthreads();
+    chunk_store(Ks, rk);
+    chunk_store(Vs, rv);
+    __syncthreads();
+    if (kc + 1 < nch) {
+      chunk_regs(rk, base + (long)(kc + 1) * KC * C3 + C, C3);
+      chunk_regs(rv, base + (long)(kc + 1) * KC * C3 + 2 * C, C3);
+    }
+    f32x4 sc[KC / 16], dp[KC / 16];
+#pragma unroll
+    for (int j = 0; j < KC / 16; ++j) {
+      sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        sc[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), sc[j]);
+        dp[j] = mma(da[kk], frag_row(Vs, 16 * j + m, kk, g), dp[j]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < KC / 16; ++j) {
+        const float p = exp2f((sc[j][i] * SCALE - li[i]) * LOG2E);
+        S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
+      }
+#pragma unroll
+    for (int ks = 0; ks < KC / 32; ++ks) {
+      const bf16x8 a = S.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        acc[jd] = mma(a, frag_tr(Ks, 32 * ks, 16 * jd, lane), acc[jd]);
+    }
+  }
+  const long orow = row0 + q0 + 4 * g;
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dqkv[(orow + i) * C3 + h * HD + jd * 16 + m] = bf(acc[jd][i]);
+}
+
+__global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, const uint16_t* dout,
+                                                       const float* lse, const float* dsum,
+                                                       int L, int C, uint16_t* dqkv) {
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t dOs[KC * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ws[4][16 * KC];
+  const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int H = gridDim.y;
+  const long row0 = (long)b * L;
+  const long C3 = 3L * C;
+  const uint16_t* base = qkv + row0 * C3 + h * HD;
+  const uint16_t* dbase = dout + row0 * C + h * HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  const int k0 = kt * QT + w * 16;
+  const float* lrow = lse + ((long)b * H + h) * L;
+  const float* drow = dsum + ((long)b * H + h) * L;
+  bf16x8 ka[2], va[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    ka[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + C + 32 * kk + 8 * g);
+    va[kk] =
+        *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + 2 * C + 32 * kk + 8 * g);
+  }
+  uint4 rq[2], rd[2];
+  chunk_regs(rq, base, C3);
+  chunk_regs(rd, dbase, C);
+  const Strip W = make_strip(Ws[w], KC);
+  f32x4 dv[HD / 16], dk[HD / 16];
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd) {
+    dv[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dk[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int nch = L / KC;
+  for (int qc = 0; qc < nch; ++qc) {
+    // lse and D of the query columns this lane holds in the chunk
+    float lq[KC / 16], dq[KC / 16];
+#pragma unroll
+    for (int jq = 0; jq < KC / 16; ++jq) {
+      lq[jq] = lrow[qc * KC + 16 * jq + m];
+      dq[jq] = drow[qc * KC + 16 * jq + m];
+    }
+    __syncthreads();
+    chunk_store(Qs, rq);
+    chunk_store(dOs, rd);
+    __syncthreads();
+    if (qc + 1 < nch) {
+      chunk_regs(rq, base + (long)(qc + 1) * KC * C3, C3);
+      chunk_regs(rd, dbase + (long)(qc + 1) * KC * C, C);
+    }
+    f32x4 st[KC / 16], dpt[KC / 16];
+#pragma unroll
+    for (int jq = 0; jq < KC / 16; ++jq) {
+      st[jq] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dpt[jq] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        st[jq] = mma(ka[kk], frag_row(Qs, 16 * jq + m, kk, g), st[jq]);
+        dpt[jq] = mma(va[kk], frag_row(dOs, 16 * jq + m, kk, g), dpt[jq]);
+      }
+    }
+#pragma unroll
+    for (int jq = 0; jq < KC / 16; ++jq)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f((st[jq][i] * SCALE - lq[jq]) * LOG2E);
+        dpt[jq][i] = p * (dpt[jq][i] - dq[jq]) * SCALE;
+        W.put(4 * g + i, 16 * jq + m, p);
+      }
+#pragma unroll
+    for (int ks = 0; ks < KC / 32; ++ks) {
+      const bf16x8 a = W.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        dv[jd] = mma(a, frag_tr(dOs, 32 * ks, 16 * jd, lane), dv[jd]);
+    }
+#pragma unroll
+    for (int jq = 0; jq < KC / 16; ++jq)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) W.put(4 * g + i, 16 * jq + m, dpt[jq][i]);
+#pragma unroll
+    for (int ks = 0; ks < KC / 32; ++ks) {
+      const bf16x8 a = W.frag(m, ks, g);
+#pragma unroll
+      for (int jd = 0; jd < HD / 16; ++jd)
+        dk[jd] = mma(a, frag_tr(Qs, 32 * ks, 16 * jd, lane), dk[jd]);
+    }
+  }
+  const long krow = row0 + k0 + 4 * g;
+#pragma unroll
+  for (int jd = 0; jd < HD / 16; ++jd)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long r = (krow + i) * C3 + h * HD + jd * 16 + m;
+      dqkv[r + C] = bf(dk[jd][i]);
+      dqkv[r + 2 * C] = bf(dv[jd][i]);
+    }
+}
+
 }  // namespace
 
 bool attn_fits(int L, int C, int heads) {
-  return L >= QT && L % QT == 0 && L <= LMAX && C == heads * HD;
+  return L >= QT && L % QT == 0 && L <= ATTN_LMAX && C == heads * HD;
 }
 
 template <int L>
@@ -451,7 +755,12 @@ hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void
     case 64: return attn_fwd_t<64>(qkv, B, C, heads, o, lse, st);
     case 128: return attn_fwd_t<128>(qkv, B, C, heads, o, lse, st);
     case 192: return attn_fwd_t<192>(qkv, B, C, heads, o, lse, st);
-    default: return attn_fwd_t<256>(qkv, B, C, heads, o, lse, st);
+    case 256: return attn_fwd_t<256>(qkv, B, C, heads, o, lse, st);
+    default:
+      hipLaunchKernelGGL(k_attn_fwd_s, dim3(L / QT, heads, B), dim3(256), 0, st,
+                         static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o),
+                         lse);
+      return hipGetLastError();
   }
 }
 
@@ -463,7 +772,19 @@ hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, con
     case 64: return attn_bwd_t<64>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
     case 128: return attn_bwd_t<128>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
     case 192: return attn_bwd_t<192>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
-    default: return attn_bwd_t<256>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+    case 256: return attn_bwd_t<256>(qkv, o, dout, lse, B, C, heads, dqkv, dsum, st);
+    default: {
+      hipLaunchKernelGGL(k_attn_bwd_q_s, dim3(L / QT, heads, B), dim3(256), 0, st,
+                         static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(o),
+                         static_cast<const uint16_t*>(dout), lse, L, C,
+                         static_cast<uint16_t*>(dqkv), dsum);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(k_attn_bwd_kv_s, dim3(L / QT, heads, B), dim3(256), 0, st,
+                         static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(dout),
+                         lse, dsum, L, C, static_cast<uint16_t*>(dqkv));
+      return hipGetLastError();
+    }
   }
 }
 

@@ -10,7 +10,10 @@ namespace pulse {
 
 // ---- multi-head attention (attn.hip) -------------------------------------
 
-// Head dimension 64, L % 64 == 0, 64 <= L <= 256, C == heads * 64.
+// Head dimension 64, L % 64 == 0, 64 <= L <= ATTN_LMAX, C == heads * 64.
+// Up to 256 tokens a head's keys and values sit in LDS whole; longer
+// sequences stream them in 64-token chunks (online softmax in the forward).
+constexpr int ATTN_LMAX = 4096;
 bool attn_fits(int L, int C, int heads);
 // o[b*L + i][64 h + e] = sum_j p[b][h][i][j] v[b*L + j][64 h + e] with
 // p = softmax_j(q_i . k_j / 8); q, k, v are channel thirds of qkv [B*L][3C].

@@ -264,8 +264,8 @@ pulse_status tvalidate(const pulse_tstage_desc* d) {
   if (!d) return tfail(PULSE_E_INVALID_ARG, "desc is NULL");
   if (d->dtype != PULSE_BF16) return tfail(PULSE_E_SHAPE, "the transformer stage runs bf16 only");
   if (d->batch < 1) return tfail(PULSE_E_SHAPE, "batch must be >= 1");
-  if (d->tokens < 64 || d->tokens > 256 || d->tokens % 64)
-    return tfail(PULSE_E_SHAPE, "tokens must be a multiple of 64 in [64, 256]");
+  if (d->tokens < 64 || d->tokens > ATTN_LMAX || d->tokens % 64)
+    return tfail(PULSE_E_SHAPE, "tokens must be a multiple of 64 in [64, %d]", ATTN_LMAX);
   if (d->heads < 1 || d->width != 64 * d->heads || d->width > 2048)
     return tfail(PULSE_E_SHAPE, "width must be 64 * heads and at most 2048");
   if (d->mlp_ratio < 1 || d->mlp_ratio > 8) return tfail(PULSE_E_SHAPE, "mlp_ratio must be in [1, 8]");

@@ -31,8 +31,27 @@ def _narrow():
     return d
 
 
+def _t320():
+    """320 tokens: the streamed attention kernels over five 64-token chunks
+    (an odd count), one image, 2 heads, 1 + 1 blocks."""
+    return configs._tstage(1, 320, 128, 2, 1, 1)
+
+
+def _long():
+    """1024 tokens per image (the Hunyuan-DiT-like sequence length), two
+    images, width 256 in 4 heads, 1 + 1 blocks."""
+    return configs._tstage(2, 1024, 256, 4, 1, 1)
+
+
+def _t1408_b2():
+    """The Hunyuan-DiT-like stage at its full per-image shape (1024 tokens,
+    width 1408 in 22 heads, MLP 5632) with two images."""
+    return configs.t1408(batch=2)
+
+
 CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t_narrow": (_narrow, 12),
-         "t768": (configs.t768, 7)}
+         "t768": (configs.t768, 7), "t_320": (_t320, 13), "t_long": (_long, 14),
+         "t1408_b2": (_t1408_b2, 8)}
 
 
 def run_gpu(desc, params, b, mbs=(0,)):

@@ -51,7 +51,7 @@ def test_flops_model_t768():
 
 
 @pytest.mark.parametrize("bad", [
-    dict(tokens=32), dict(tokens=320), dict(tokens=96), dict(width=96),
+    dict(tokens=32), dict(tokens=4160), dict(tokens=96), dict(tokens=1000), dict(width=96),
     dict(width=2112, heads=33), dict(mlp=0), dict(mlp=9), dict(n_dec=2),
     dict(n_enc=0, n_dec=0), dict(max_inflight=0), dict(max_inflight=65), dict(eps=-1.0),
     dict(dtype=configs.F32), dict(batch=0), dict(batch=8193, tokens=128),
@@ -63,6 +63,16 @@ def test_rejects_bad_descriptors(bad):
     with pytest.raises(S.PulseError) as e:
         _dry(d)
     assert e.value.status == S.E_SHAPE
+
+
+@pytest.mark.parametrize("tokens", [320, 1024, 4096])
+def test_accepts_long_sequences(tokens):
+    """Token counts past 256 take the streamed attention kernels; any
+    multiple of 64 up to 4096 is a valid stage."""
+    d = configs.t_tiny()
+    d.update(batch=1, tokens=tokens)
+    st = _dry(d)
+    assert st.L == tokens
 
 
 def test_bookkeeping_order_and_capacity():
