@@ -1,8 +1,9 @@
 // Multi-head self-attention of the transformer-block stage (gfx950, bf16
 // MFMA 16x16x32, fp32 accumulation).  Head dimension 64; L tokens per image
-// with L a multiple of 64.  Up to 256 tokens one head's keys and values (or
-// queries and output gradients) are held in LDS whole; longer sequences, up
-// to 4096, stream them through LDS 64 tokens at a time.  q, k and v are the
+// with L a multiple of 64, at most 4096.  The forward streams keys and
+// values through LDS 128 at a time for every L.  The backward holds one
+// head's keys and values (or queries and output gradients) in LDS whole up
+// to 256 tokens and streams them 64 at a time beyond.  q, k and v are the
 // three C-channel thirds of the qkv rows [B*L][3C]; head h owns channels
 // [64 h, 64 h + 64) of each third.
 //
@@ -37,10 +38,10 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16 staged bytes
 
 constexpr int HD = 64;        // head dimension
 constexpr int QT = 64;        // queries (or keys) per block: 4 waves x 16
-constexpr int LMAX = 256;     // tokens per image held whole in LDS; longer ones stream
 constexpr float SCALE = 0.125f;  // 1 / sqrt(64)
 constexpr float LOG2E = 1.44269504088896341f;
 
@@ -49,6 +50,26 @@ __device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 __device__ __forceinline__ uint16_t bf(float f) { return f2bf(f); }
+
+// 2^x as one v_exp_f32: results below 2^-126 flush to zero, which a
+// softmax weight relative to its row maximum (at most 1) can lose
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// (tile, head, image) of this block.  Blocks are dispatched round-robin
+// over the 8 XCDs in linear order; the tiles of one (image, head) read the
+// same keys and values, so consecutive dispatch slots of one XCD take
+// consecutive tiles (each XCD runs a contiguous range of the linear order)
+// and a head's K and V are fetched into one L2, not eight.
+__device__ __forceinline__ void tile_of(int& t, int& h, int& b) {
+  const int nb = gridDim.x * gridDim.y * gridDim.z;
+  const int bid = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int q = nb >> 3, r = nb & 7, x = bid & 7;
+  const int lb = x * q + (x < r ? x : r) + (bid >> 3);
+  t = lb % gridDim.x;
+  const int hb = lb / gridDim.x;
+  h = hb % gridDim.y;
+  b = hb / gridDim.y;
+}
 
 // chunk permutation of tile row r: bit 1 of r -> bit 1, bit 2 -> bit 0,
 // bit 3 -> bit 2
@@ -133,105 +154,11 @@ __device__ __forceinline__ Strip make_strip(uint16_t* p, int width) {
   return s;
 }
 
-// Reduce over the 16 lanes that share lane / 16 (one row of a 16x16 block).
-__device__ __forceinline__ float row_max16(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float row_sum16(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 __device__ __forceinline__ float dot8(bf16x8 a, bf16x8 b) {
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) s += (float)a[i] * (float)b[i];
   return s;
-}
-
-// ---------------------------------------------------------------------------
-// forward: block (query tile, head, image); wave w owns queries 16 w .. + 15
-// ---------------------------------------------------------------------------
-template <int L>
-__global__ __launch_bounds__(256) void k_attn_fwd(const uint16_t* qkv, int C, uint16_t* o,
-                                                  float* lse) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[L * HD];  // then the p strips
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[L * HD];
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int H = gridDim.y;
-  const long row0 = (long)b * L;
-  const long C3 = 3L * C;
-  const uint16_t* base = qkv + row0 * C3 + h * HD;
-  load_tiles<L>(Ks, base + C, C3, Vs, base + 2 * C, C3);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int m = lane & 15, g = lane >> 4;
-  const int q0 = qt * QT + w * 16;  // the wave's first query in the image
-  bf16x8 qa[2];
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
-  __syncthreads();
-
-  constexpr int nb = L / 16;
-  f32x4 s[nb];
-#pragma unroll
-  for (int j = 0; j < nb; ++j) {
-    s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) s[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), s[j]);
-  }
-  // softmax of rows 4 g + i (the lane holds column m of every 16-key block)
-  float inv[4], ls[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < nb; ++j)
-      mx = fmaxf(mx, s[j][i]);
-    mx = row_max16(mx);
-    float sum = 0.f;
-#pragma unroll
-    for (int j = 0; j < nb; ++j)
-    {
-      const float e = exp2f((s[j][i] - mx) * (SCALE * LOG2E));
-      s[j][i] = e;
-      sum += e;
-    }
-    sum = row_sum16(sum);
-    inv[i] = 1.0f / sum;
-    ls[i] = mx * SCALE + logf(sum);
-  }
-  __syncthreads();  // every wave is done with Ks: it now holds the p strips
-  const Strip P = make_strip(Ks + w * 16 * L, L);
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < nb; ++j)
-      P.put(4 * g + i, 16 * j + m, s[j][i] * inv[i]);
-  // o = p v: A = p rows (k = key), B = v rows read down the tile (k = key)
-  f32x4 acc[HD / 16];
-#pragma unroll
-  for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < L / 32; ++ks) {
-    const bf16x8 a = P.frag(m, ks, g);
-#pragma unroll
-    for (int jd = 0; jd < HD / 16; ++jd)
-      acc[jd] = mma(a, frag_tr(Vs, 32 * ks, 16 * jd, lane), acc[jd]);
-  }
-  const long orow = row0 + q0 + 4 * g;
-#pragma unroll
-  for (int jd = 0; jd < HD / 16; ++jd)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[(orow + i) * C + h * HD + jd * 16 + m] = bf(acc[jd][i]);
-  if (m == 0) {
-    float* l = lse + ((long)b * H + h) * L + q0 + 4 * g;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) l[i] = ls[i];
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -243,7 +170,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const u
                                                     int C, uint16_t* dqkv, float* dsum) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[L * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[L * HD];  // then the ds strips
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int qt, h, b;
+  tile_of(qt, h, b);
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
@@ -294,7 +222,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q(const uint16_t* qkv, const u
 #pragma unroll
     for (int j = 0; j < nb; ++j)
     {
-      const float p = exp2f((s[j][i] * SCALE - li[i]) * LOG2E);
+      const float p = ex2((s[j][i] * SCALE - li[i]) * LOG2E);
       S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
     }
   // dq = ds k: A = ds rows (k = key), B = k rows read down the tile
@@ -327,7 +255,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
   __shared__ __attribute__((aligned(16))) uint16_t Qs[L * HD];
   __shared__ __attribute__((aligned(16))) uint16_t dOs[L * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Ws[4][16 * QT];  // p^T, then ds^T, per wave
-  const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int kt, h, b;
+  tile_of(kt, h, b);
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
@@ -380,7 +309,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
     for (int jq = 0; jq < 4; ++jq)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = exp2f((st[jq][i] * SCALE - lq[4 * qc + jq]) * LOG2E);
+        const float p = ex2((st[jq][i] * SCALE - lq[4 * qc + jq]) * LOG2E);
         st[jq][i] = p;
         dpt[jq][i] = p * (dpt[jq][i] - dq[4 * qc + jq]) * SCALE;
         W.put(4 * g + i, 16 * jq + m, p);
@@ -429,108 +358,19 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
 constexpr int KC = 64;  // tokens per streamed chunk
 
 // the two 16-byte chunks this thread moves of a [64][64] tile
-__device__ __forceinline__ void chunk_regs(uint4 (&v)[2], const uint16_t* src, long stride) {
+__device__ __forceinline__ void chunk_regs(u32x4 (&v)[2], const uint16_t* src, long stride) {
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int e = threadIdx.x + 256 * u;
-    v[u] = *reinterpret_cast<const uint4*>(src + (long)(e >> 3) * stride + (e & 7) * 8);
+    v[u] = *reinterpret_cast<const u32x4*>(src + (long)(e >> 3) * stride + (e & 7) * 8);
   }
 }
 
-__device__ __forceinline__ void chunk_store(uint16_t* t, const uint4 (&v)[2]) {
+__device__ __forceinline__ void chunk_store(uint16_t* t, const u32x4 (&v)[2]) {
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int e = threadIdx.x + 256 * u;
-    *reinterpret_cast<uint4*>(t + toff(e >> 3, e & 7)) = v[u];
-  }
-}
-
-__global__ __launch_bounds__(256) void k_attn_fwd_s(const uint16_t* qkv, int L, int C,
-                                                    uint16_t* o, float* lse) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[KC * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Ps[4][16 * KC];
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int H = gridDim.y;
-  const long row0 = (long)b * L;
-  const long C3 = 3L * C;
-  const uint16_t* base = qkv + row0 * C3 + h * HD;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int m = lane & 15, g = lane >> 4;
-  const int q0 = qt * QT + w * 16;
-  bf16x8 qa[2];
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-    qa[kk] = *reinterpret_cast<const bf16x8*>(base + (long)(q0 + m) * C3 + 32 * kk + 8 * g);
-  uint4 rk[2], rv[2];
-  chunk_regs(rk, base + C, C3);
-  chunk_regs(rv, base + 2 * C, C3);
-  const Strip P = make_strip(Ps[w], KC);
-  float mrow[4], lrow[4];
-  f32x4 acc[HD / 16];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    mrow[i] = -INFINITY;
-    lrow[i] = 0.f;
-  }
-#pragma unroll
-  for (int jd = 0; jd < HD / 16; ++jd) acc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nch = L / KC;
-  for (int kc = 0; kc < nch; ++kc) {
-    __syncthreads();  // every wave is done with the previous chunk
-    chunk_store(Ks, rk);
-    chunk_store(Vs, rv);
-    __syncthreads();
-    if (kc + 1 < nch) {
-      chunk_regs(rk, base + (long)(kc + 1) * KC * C3 + C, C3);
-      chunk_regs(rv, base + (long)(kc + 1) * KC * C3 + 2 * C, C3);
-    }
-    f32x4 sc[KC / 16];
-#pragma unroll
-    for (int j = 0; j < KC / 16; ++j) {
-      sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) sc[j] = mma(qa[kk], frag_row(Ks, 16 * j + m, kk, g), sc[j]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float cm = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < KC / 16; ++j) cm = fmaxf(cm, sc[j][i]);
-      const float mn = fmaxf(mrow[i], row_max16(cm));
-      const float alpha = exp2f((mrow[i] - mn) * (SCALE * LOG2E));  // 0 for the first chunk
-      float rs = 0.f;
-#pragma unroll
-      for (int j = 0; j < KC / 16; ++j) {
-        const float e = exp2f((sc[j][i] - mn) * (SCALE * LOG2E));
-        sc[j][i] = e;
-        rs += e;
-      }
-      lrow[i] = lrow[i] * alpha + row_sum16(rs);
-      mrow[i] = mn;
-#pragma unroll
-      for (int jd = 0; jd < HD / 16; ++jd) acc[jd][i] *= alpha;
-#pragma unroll
-      for (int j = 0; j < KC / 16; ++j) P.put(4 * g + i, 16 * j + m, sc[j][i]);
-    }
-#pragma unroll
-    for (int ks = 0; ks < KC / 32; ++ks) {
-      const bf16x8 a = P.frag(m, ks, g);
-#pragma unroll
-      for (int jd = 0; jd < HD / 16; ++jd)
-        acc[jd] = mma(a, frag_tr(Vs, 32 * ks, 16 * jd, lane), acc[jd]);
-    }
-  }
-  const long orow = row0 + q0 + 4 * g;
-#pragma unroll
-  for (int jd = 0; jd < HD / 16; ++jd)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      o[(orow + i) * C + h * HD + jd * 16 + m] = bf(acc[jd][i] / lrow[i]);
-  if (m == 0) {
-    float* l = lse + ((long)b * H + h) * L + q0 + 4 * g;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) l[i] = mrow[i] * SCALE + logf(lrow[i]);
+    *reinterpret_cast<u32x4*>(t + toff(e >> 3, e & 7)) = v[u];
   }
 }
 
@@ -541,7 +381,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q_s(const uint16_t* qkv, const
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[KC * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Ss[4][16 * KC];
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int qt, h, b;
+  tile_of(qt, h, b);
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
@@ -569,7 +410,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q_s(const uint16_t* qkv, const
     Di[i] = __shfl(dpart, 4 * g + i, 64);
     li[i] = lse[lrow + 4 * g + i];
   }
-  uint4 rk[2], rv[2];
+  u32x4 rk[2], rv[2];
   chunk_regs(rk, base + C, C3);
   chunk_regs(rv, base + 2 * C, C3);
   const Strip S = make_strip(Ss[w], KC);
@@ -582,9 +423,10 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q_s(const uint16_t* qkv, const
     chunk_store(Ks, rk);
     chunk_store(Vs, rv);
     __syncthreads();
-    if (kc + 1 < nch) {
-      chunk_regs(rk, base + (long)(kc + 1) * KC * C3 + C, C3);
-      chunk_regs(rv, base + (long)(kc + 1) * KC * C3 + 2 * C, C3);
+    {
+      const int kn = min(kc + 1, nch - 1);  // unconditional: the wait stays at the store
+      chunk_regs(rk, base + (long)kn * KC * C3 + C, C3);
+      chunk_regs(rv, base + (long)kn * KC * C3 + 2 * C, C3);
     }
     f32x4 sc[KC / 16], dp[KC / 16];
 #pragma unroll
@@ -601,7 +443,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_q_s(const uint16_t* qkv, const
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < KC / 16; ++j) {
-        const float p = exp2f((sc[j][i] * SCALE - li[i]) * LOG2E);
+        const float p = ex2((sc[j][i] * SCALE - li[i]) * LOG2E);
         S.put(4 * g + i, 16 * j + m, p * (dp[j][i] - Di[i]) * SCALE);
       }
 #pragma unroll
@@ -625,7 +467,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, cons
   __shared__ __attribute__((aligned(16))) uint16_t Qs[KC * HD];
   __shared__ __attribute__((aligned(16))) uint16_t dOs[KC * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Ws[4][16 * KC];
-  const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int kt, h, b;
+  tile_of(kt, h, b);
   const int H = gridDim.y;
   const long row0 = (long)b * L;
   const long C3 = 3L * C;
@@ -643,7 +486,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, cons
     va[kk] =
         *reinterpret_cast<const bf16x8*>(base + (long)(k0 + m) * C3 + 2 * C + 32 * kk + 8 * g);
   }
-  uint4 rq[2], rd[2];
+  u32x4 rq[2], rd[2];
   chunk_regs(rq, base, C3);
   chunk_regs(rd, dbase, C);
   const Strip W = make_strip(Ws[w], KC);
@@ -666,9 +509,10 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, cons
     chunk_store(Qs, rq);
     chunk_store(dOs, rd);
     __syncthreads();
-    if (qc + 1 < nch) {
-      chunk_regs(rq, base + (long)(qc + 1) * KC * C3, C3);
-      chunk_regs(rd, dbase + (long)(qc + 1) * KC * C, C);
+    {
+      const int qn = min(qc + 1, nch - 1);
+      chunk_regs(rq, base + (long)qn * KC * C3, C3);
+      chunk_regs(rd, dbase + (long)qn * KC * C, C);
     }
     f32x4 st[KC / 16], dpt[KC / 16];
 #pragma unroll
@@ -685,7 +529,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, cons
     for (int jq = 0; jq < KC / 16; ++jq)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = exp2f((st[jq][i] * SCALE - lq[jq]) * LOG2E);
+        const float p = ex2((st[jq][i] * SCALE - lq[jq]) * LOG2E);
         dpt[jq][i] = p * (dpt[jq][i] - dq[jq]) * SCALE;
         W.put(4 * g + i, 16 * jq + m, p);
       }
@@ -719,18 +563,197 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv_s(const uint16_t* qkv, cons
     }
 }
 
+// ---------------------------------------------------------------------------
+// forward, key-split form (any L): block (64-query tile, head, image).  The
+// keys stream through LDS 128 at a time and wave w takes keys 32 w .. + 31
+// of every chunk for all 64 queries, so each K or V fragment read from LDS
+// feeds four MFMAs (one per 16-query block) and p never leaves registers:
+//   s^T = k q^T   A = k rows (LDS), B = q (registers); the output lane
+//                 (g, m) holds keys 8 g + 4 kb + i of query 16 qb + m
+//   o^T += v^T p^T  A = v read down the tile (lane (g, j): keys 8 g + t of
+//                 channel 16 db + j), B = p^T (lane (g, m): keys 8 g + t of
+//                 query m, t = 4 kb + i: exactly the values the lane holds)
+// For the first product to deliver keys 8 g + 4 kb + i on output row 4 g + i
+// of block kb, every 32-key group is stored with its rows permuted: key k at
+// row (k & 3) | ((k >> 3) & 3) << 2 | ((k >> 2) & 1) << 4, so that rows
+// 16 kb .. 16 kb + 15 hold keys 8 (m >> 2) + 4 kb + (m & 3), m = 0..15.
+// Every wave keeps a running maximum and sum per query (online softmax); at
+// the end the four partial states are merged through LDS.
+// ---------------------------------------------------------------------------
+
+constexpr int KS_CHUNK = 128;  // keys per chunk: 4 waves x 32
+constexpr int OPAD = 65;       // floats per row of the merge buffers
+
+__device__ __forceinline__ int kperm(int k) {
+  return (k & ~31) | (k & 3) | (((k >> 3) & 3) << 2) | (((k >> 2) & 1) << 4);
+}
+
+__global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int L, int C,
+                                                        uint16_t* o, float* lse) {
+  // K and V chunks during the key loop, then the four waves' o^T partials
+  __shared__ __attribute__((aligned(16))) float smem[4 * QT * OPAD];
+  __shared__ float ml[4][2][QT];
+  uint16_t* Ks = reinterpret_cast<uint16_t*>(smem);
+  uint16_t* Vs = Ks + KS_CHUNK * HD;
+  int qt, h, b;
+  tile_of(qt, h, b);
+  const int H = gridDim.y;
+  const long row0 = (long)b * L;
+  const long C3 = 3L * C;
+  const uint16_t* base = qkv + row0 * C3 + h * HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  const int q0 = qt * QT;
+  const float c = SCALE * LOG2E;
+
+  bf16x8 qa[4][2];
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      qa[qb][kk] =
+          *reinterpret_cast<const bf16x8*>(base + (long)(q0 + 16 * qb + m) * C3 + 32 * kk + 8 * g);
+
+  // this thread's share of a chunk: rows (t + 256 u) / 8, u = 0..3.  Rows
+  // past the image (a 64-key tail chunk, or the chunk after the last) are
+  // clamped to its last row and never stored: the loads stay unconditional,
+  // so that their wait falls at the LDS store of the next iteration.
+  u32x4 rk[4], rv[4];
+#define KS_LOAD(kc)                                                          \
+  _Pragma("unroll") for (int u = 0; u < 4; ++u) {                            \
+    const int e = threadIdx.x + 256 * u;                                     \
+    const int r = min((kc) * KS_CHUNK + (e >> 3), L - 1);                    \
+    const uint16_t* p = base + (long)r * C3 + (e & 7) * 8;                   \
+    rk[u] = *reinterpret_cast<const u32x4*>(p + C);                          \
+    rv[u] = *reinterpret_cast<const u32x4*>(p + 2 * C);                      \
+  }
+  KS_LOAD(0)
+
+  float mrow[4], lrow[4];
+  f32x4 acc[4][HD / 16];
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb) {
+    mrow[qb] = -INFINITY;
+    lrow[qb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int nch = (L + KS_CHUNK - 1) / KS_CHUNK;
+  for (int kc = 0; kc < nch; ++kc) {
+    const int rows = min(KS_CHUNK, L - kc * KS_CHUNK);
+    __syncthreads();  // every wave is done with the previous chunk
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int r = e >> 3;
+      if (r < rows) {
+        *reinterpret_cast<u32x4*>(Ks + toff(kperm(r), e & 7)) = rk[u];
+        *reinterpret_cast<u32x4*>(Vs + toff(r, e & 7)) = rv[u];
+      }
+    }
+    __syncthreads();
+    KS_LOAD(kc + 1)
+    if (32 * w >= rows) continue;  // no keys of this wave in a 64-key tail chunk
+
+    f32x4 sc[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const bf16x8 k0 = frag_row(Ks, 32 * w + 16 * kb + m, 0, g);
+      const bf16x8 k1 = frag_row(Ks, 32 * w + 16 * kb + m, 1, g);
+#pragma unroll
+      for (int qb = 0; qb < 4; ++qb) {
+        f32x4 t = mma(k0, qa[qb][0], f32x4{0.f, 0.f, 0.f, 0.f});
+        sc[qb][kb] = mma(k1, qa[qb][1], t);
+      }
+    }
+    bf16x8 pb[4];
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      float mx = fmaxf(fmaxf(fmaxf(sc[qb][0][0], sc[qb][0][1]), fmaxf(sc[qb][0][2], sc[qb][0][3])),
+                       fmaxf(fmaxf(sc[qb][1][0], sc[qb][1][1]), fmaxf(sc[qb][1][2], sc[qb][1][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(mrow[qb], mx);
+      const float alpha = ex2((mrow[qb] - mn) * c);  // 0 on the wave's first chunk
+      const float off = mn * c;
+      float rs = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = ex2(fmaf(sc[qb][kb][i], c, -off));
+          rs += e;
+          pb[qb][4 * kb + i] = (__bf16)e;
+        }
+      rs += __shfl_xor(rs, 16, 64);
+      rs += __shfl_xor(rs, 32, 64);
+      lrow[qb] = fmaf(lrow[qb], alpha, rs);
+      mrow[qb] = mn;
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[qb][db][i] *= alpha;
+    }
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db) {
+      const bf16x8 va = frag_tr(Vs, 32 * w, 16 * db, lane);
+#pragma unroll
+      for (int qb = 0; qb < 4; ++qb) acc[qb][db] = mma(va, pb[qb], acc[qb][db]);
+    }
+  }
+
+  // merge: M = max_w m_w, l = sum_w l_w 2^((m_w - M) c), o = sum_w f_w o_w
+  // with f_w = 2^((m_w - M) c) / l
+  if (g == 0) {
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      ml[w][0][16 * qb + m] = mrow[qb];
+      ml[w][1][16 * qb + m] = lrow[qb];
+    }
+  }
+  __syncthreads();  // also: every wave is done with the K and V chunks
+  float* part = smem + w * QT * OPAD;
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb) {
+    const int q = 16 * qb + m;
+    float M = ml[0][0][q];
+#pragma unroll
+    for (int v = 1; v < 4; ++v) M = fmaxf(M, ml[v][0][q]);
+    float l = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) l += ml[v][1][q] * ex2((ml[v][0][q] - M) * c);
+    const float f = ex2((mrow[qb] - M) * c) / l;
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) part[q * OPAD + 16 * db + 4 * g + i] = acc[qb][db][i] * f;
+    if (w == 0 && g == 0)
+      lse[((long)b * H + h) * L + q0 + q] = M * SCALE + logf(l);
+  }
+  __syncthreads();
+  // 64 queries x 64 channels: thread t writes 16 channels of query t / 4
+  {
+    const int q = threadIdx.x >> 2, d0 = (threadIdx.x & 3) * 16;
+    uint32_t pk[8];
+#pragma unroll
+    for (int j = 0; j < 16; j += 2) {
+      const int ix = q * OPAD + d0 + j;
+      const float v0 = smem[ix] + smem[QT * OPAD + ix] + smem[2 * QT * OPAD + ix] +
+                       smem[3 * QT * OPAD + ix];
+      const float v1 = smem[ix + 1] + smem[QT * OPAD + ix + 1] + smem[2 * QT * OPAD + ix + 1] +
+                       smem[3 * QT * OPAD + ix + 1];
+      pk[j / 2] = (uint32_t)bf(v0) | ((uint32_t)bf(v1) << 16);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(o + (row0 + q0 + q) * C + h * HD + d0);
+    dst[0] = uint4{pk[0], pk[1], pk[2], pk[3]};
+    dst[1] = uint4{pk[4], pk[5], pk[6], pk[7]};
+  }
+}
+
 }  // namespace
 
 bool attn_fits(int L, int C, int heads) {
   return L >= QT && L % QT == 0 && L <= ATTN_LMAX && C == heads * HD;
-}
-
-template <int L>
-static hipError_t attn_fwd_t(const void* qkv, int B, int C, int heads, void* o, float* lse,
-                             hipStream_t st) {
-  hipLaunchKernelGGL(k_attn_fwd<L>, dim3(L / QT, heads, B), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(qkv), C, static_cast<uint16_t*>(o), lse);
-  return hipGetLastError();
 }
 
 template <int L>
@@ -751,17 +774,9 @@ static hipError_t attn_bwd_t(const void* qkv, const void* o, const void* dout, c
 hipError_t launch_attn_fwd(const void* qkv, int B, int L, int C, int heads, void* o, float* lse,
                            hipStream_t st) {
   if (!attn_fits(L, C, heads)) return hipErrorInvalidValue;
-  switch (L) {
-    case 64: return attn_fwd_t<64>(qkv, B, C, heads, o, lse, st);
-    case 128: return attn_fwd_t<128>(qkv, B, C, heads, o, lse, st);
-    case 192: return attn_fwd_t<192>(qkv, B, C, heads, o, lse, st);
-    case 256: return attn_fwd_t<256>(qkv, B, C, heads, o, lse, st);
-    default:
-      hipLaunchKernelGGL(k_attn_fwd_s, dim3(L / QT, heads, B), dim3(256), 0, st,
-                         static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o),
-                         lse);
-      return hipGetLastError();
-  }
+  hipLaunchKernelGGL(k_attn_fwd_ks, dim3(L / QT, heads, B), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(qkv), L, C, static_cast<uint16_t*>(o), lse);
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse,
