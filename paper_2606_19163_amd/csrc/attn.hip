@@ -44,6 +44,7 @@ constexpr int HD = 64;        // head dimension
 constexpr int QT = 64;        // queries (or keys) per block: 4 waves x 16
 constexpr float SCALE = 0.125f;  // 1 / sqrt(64)
 constexpr float LOG2E = 1.44269504088896341f;
+constexpr float LN2 = 0.693147180559945309f;
 
 __device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -588,6 +589,51 @@ __device__ __forceinline__ int kperm(int k) {
   return (k & ~31) | (k & 3) | (((k >> 3) & 3) << 2) | (((k >> 2) & 1) << 4);
 }
 
+// Chunk staging of the key-split forward.  Thread t moves 16-byte piece
+// t % 8 of rows t / 8 + 32 u (u = 0..3) of a 128-row chunk.  Rows 0..63 of
+// a chunk always lie in the image (every chunk holds 128 rows but a tail,
+// which holds 64); rows 64..127 of a tail are fetched from the image's last
+// 64 rows instead (in bounds, never stored).  So every load is
+// unconditional, its wait falls at the LDS store of the next iteration, and
+// the per-lane offsets are computed once.
+__device__ __forceinline__ long piece(long stride) {
+  return (long)(threadIdx.x >> 3) * stride + (threadIdx.x & 7) * 8;
+}
+
+// chunk [c0, c0 + 128) of two tensors sharing row stride s (pa, pb: row 0
+// of each, po: piece(s)); c0 < L
+__device__ __forceinline__ void stage2(u32x4 (&a)[4], u32x4 (&b)[4], const uint16_t* pa,
+                                       const uint16_t* pb, long s, long po, int c0, int L) {
+  const int hi = min(c0 + 64, L - 64);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const long r = u < 2 ? c0 + 32 * u : hi + 32 * (u - 2);
+    a[u] = *reinterpret_cast<const u32x4*>(pa + r * s + po);
+    b[u] = *reinterpret_cast<const u32x4*>(pb + r * s + po);
+  }
+}
+
+// staged rows into two tiles at this thread's offsets oa, ob (row t / 8;
+// rows + 32 u sit 32 * 64 elements further: kperm and swz leave the bits
+// from 5 up alone); `full`: the chunk holds 128 rows
+__device__ __forceinline__ void put2(uint16_t* ta, int oa, uint16_t* tb, int ob,
+                                     const u32x4 (&a)[4], const u32x4 (&b)[4], bool full) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (u >= 2 && !full) break;
+    *reinterpret_cast<u32x4*>(ta + oa + 32 * HD * u) = a[u];
+    *reinterpret_cast<u32x4*>(tb + ob + 32 * HD * u) = b[u];
+  }
+}
+
+// Softmax of the key-split forward: each wave keeps, per query, a reference
+// r in the log2 domain (scores times SCALE * LOG2E).  Its weights are
+// p = 2^(s c - r) <= 2^RGROW: r moves up to the running maximum (and the
+// wave's sum and o accumulators are rescaled) only when a score of the
+// chunk exceeds it by more than RGROW, decided for the whole wave at once,
+// which skips the rescale on most chunks.
+constexpr float RGROW = 8.f;
+
 __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int L, int C,
                                                         uint16_t* o, float* lse) {
   // K and V chunks during the key loop, then the four waves' o^T partials
@@ -614,27 +660,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int
       qa[qb][kk] =
           *reinterpret_cast<const bf16x8*>(base + (long)(q0 + 16 * qb + m) * C3 + 32 * kk + 8 * g);
 
-  // this thread's share of a chunk: rows (t + 256 u) / 8, u = 0..3.  Rows
-  // past the image (a 64-key tail chunk, or the chunk after the last) are
-  // clamped to its last row and never stored: the loads stay unconditional,
-  // so that their wait falls at the LDS store of the next iteration.
+  const long po = piece(C3);
+  const int ko = toff(kperm(threadIdx.x >> 3), threadIdx.x & 7);
+  const int vo = toff(threadIdx.x >> 3, threadIdx.x & 7);
   u32x4 rk[4], rv[4];
-#define KS_LOAD(kc)                                                          \
-  _Pragma("unroll") for (int u = 0; u < 4; ++u) {                            \
-    const int e = threadIdx.x + 256 * u;                                     \
-    const int r = min((kc) * KS_CHUNK + (e >> 3), L - 1);                    \
-    const uint16_t* p = base + (long)r * C3 + (e & 7) * 8;                   \
-    rk[u] = *reinterpret_cast<const u32x4*>(p + C);                          \
-    rv[u] = *reinterpret_cast<const u32x4*>(p + 2 * C);                      \
-  }
-  KS_LOAD(0)
+  stage2(rk, rv, base + C, base + 2 * C, C3, po, 0, L);
 
-  float mrow[4], lrow[4];
+  float ref[4], lsum[4];  // per lane: the reference and its share of the sum
   f32x4 acc[4][HD / 16];
 #pragma unroll
   for (int qb = 0; qb < 4; ++qb) {
-    mrow[qb] = -INFINITY;
-    lrow[qb] = 0.f;
+    ref[qb] = -INFINITY;
+    lsum[qb] = 0.f;
 #pragma unroll
     for (int db = 0; db < HD / 16; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -642,17 +679,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int
   for (int kc = 0; kc < nch; ++kc) {
     const int rows = min(KS_CHUNK, L - kc * KS_CHUNK);
     __syncthreads();  // every wave is done with the previous chunk
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int e = threadIdx.x + 256 * u;
-      const int r = e >> 3;
-      if (r < rows) {
-        *reinterpret_cast<u32x4*>(Ks + toff(kperm(r), e & 7)) = rk[u];
-        *reinterpret_cast<u32x4*>(Vs + toff(r, e & 7)) = rv[u];
-      }
-    }
+    put2(Ks, ko, Vs, vo, rk, rv, rows == KS_CHUNK);
     __syncthreads();
-    KS_LOAD(kc + 1)
+    stage2(rk, rv, base + C, base + 2 * C, C3, po, min(kc + 1, nch - 1) * KS_CHUNK, L);
     if (32 * w >= rows) continue;  // no keys of this wave in a 64-key tail chunk
 
     f32x4 sc[4][2];
@@ -661,39 +690,44 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int
       const bf16x8 k0 = frag_row(Ks, 32 * w + 16 * kb + m, 0, g);
       const bf16x8 k1 = frag_row(Ks, 32 * w + 16 * kb + m, 1, g);
 #pragma unroll
+      for (int qb = 0; qb < 4; ++qb)
+        sc[qb][kb] = mma(k1, qa[qb][1], mma(k0, qa[qb][0], f32x4{0.f, 0.f, 0.f, 0.f}));
+    }
+    float mx[4];
+    bool grow = false;
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      float v = fmaxf(fmaxf(fmaxf(sc[qb][0][0], sc[qb][0][1]), fmaxf(sc[qb][0][2], sc[qb][0][3])),
+                      fmaxf(fmaxf(sc[qb][1][0], sc[qb][1][1]), fmaxf(sc[qb][1][2], sc[qb][1][3])));
+      v = fmaxf(v, __shfl_xor(v, 16, 64));
+      v = fmaxf(v, __shfl_xor(v, 32, 64));
+      mx[qb] = v * c;
+      grow |= mx[qb] > ref[qb] + RGROW;
+    }
+    if (__any(grow)) {
+#pragma unroll
       for (int qb = 0; qb < 4; ++qb) {
-        f32x4 t = mma(k0, qa[qb][0], f32x4{0.f, 0.f, 0.f, 0.f});
-        sc[qb][kb] = mma(k1, qa[qb][1], t);
+        const float nr = fmaxf(ref[qb], mx[qb]);
+        const float alpha = ex2(ref[qb] - nr);  // 0 on the wave's first chunk
+        ref[qb] = nr;
+        lsum[qb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[qb][db][i] *= alpha;
       }
     }
     bf16x8 pb[4];
 #pragma unroll
-    for (int qb = 0; qb < 4; ++qb) {
-      float mx = fmaxf(fmaxf(fmaxf(sc[qb][0][0], sc[qb][0][1]), fmaxf(sc[qb][0][2], sc[qb][0][3])),
-                       fmaxf(fmaxf(sc[qb][1][0], sc[qb][1][1]), fmaxf(sc[qb][1][2], sc[qb][1][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(mrow[qb], mx);
-      const float alpha = ex2((mrow[qb] - mn) * c);  // 0 on the wave's first chunk
-      const float off = mn * c;
-      float rs = 0.f;
+    for (int qb = 0; qb < 4; ++qb)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float e = ex2(fmaf(sc[qb][kb][i], c, -off));
-          rs += e;
+          const float e = ex2(fmaf(sc[qb][kb][i], c, -ref[qb]));
+          lsum[qb] += e;
           pb[qb][4 * kb + i] = (__bf16)e;
         }
-      rs += __shfl_xor(rs, 16, 64);
-      rs += __shfl_xor(rs, 32, 64);
-      lrow[qb] = fmaf(lrow[qb], alpha, rs);
-      mrow[qb] = mn;
-#pragma unroll
-      for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[qb][db][i] *= alpha;
-    }
 #pragma unroll
     for (int db = 0; db < HD / 16; ++db) {
       const bf16x8 va = frag_tr(Vs, 32 * w, 16 * db, lane);
@@ -702,13 +736,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int
     }
   }
 
-  // merge: M = max_w m_w, l = sum_w l_w 2^((m_w - M) c), o = sum_w f_w o_w
-  // with f_w = 2^((m_w - M) c) / l
+  // merge: R = max_w r_w, l = sum_w l_w 2^(r_w - R), o = sum_w f_w o_w with
+  // f_w = 2^(r_w - R) / l; lse = (R + log2 l) ln 2
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb) {
+    lsum[qb] += __shfl_xor(lsum[qb], 16, 64);
+    lsum[qb] += __shfl_xor(lsum[qb], 32, 64);
+  }
   if (g == 0) {
 #pragma unroll
     for (int qb = 0; qb < 4; ++qb) {
-      ml[w][0][16 * qb + m] = mrow[qb];
-      ml[w][1][16 * qb + m] = lrow[qb];
+      ml[w][0][16 * qb + m] = ref[qb];
+      ml[w][1][16 * qb + m] = lsum[qb];
     }
   }
   __syncthreads();  // also: every wave is done with the K and V chunks
@@ -716,19 +755,19 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd_ks(const uint16_t* qkv, int
 #pragma unroll
   for (int qb = 0; qb < 4; ++qb) {
     const int q = 16 * qb + m;
-    float M = ml[0][0][q];
+    float R = ml[0][0][q];
 #pragma unroll
-    for (int v = 1; v < 4; ++v) M = fmaxf(M, ml[v][0][q]);
+    for (int v = 1; v < 4; ++v) R = fmaxf(R, ml[v][0][q]);
     float l = 0.f;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) l += ml[v][1][q] * ex2((ml[v][0][q] - M) * c);
-    const float f = ex2((mrow[qb] - M) * c) / l;
+    for (int v = 0; v < 4; ++v) l += ml[v][1][q] * ex2(ml[v][0][q] - R);
+    const float f = ex2(ref[qb] - R) / l;
 #pragma unroll
     for (int db = 0; db < HD / 16; ++db)
 #pragma unroll
       for (int i = 0; i < 4; ++i) part[q * OPAD + 16 * db + 4 * g + i] = acc[qb][db][i] * f;
     if (w == 0 && g == 0)
-      lse[((long)b * H + h) * L + q0 + q] = M * SCALE + logf(l);
+      lse[((long)b * H + h) * L + q0 + q] = (R + log2f(l)) * LN2;
   }
   __syncthreads();
   // 64 queries x 64 channels: thread t writes 16 channels of query t / 4
