@@ -181,10 +181,12 @@ int env_or(const char* name, int dflt) {
 // split costs an fp32 partial of M x N per split.  Default, from sweeps of
 // every tile and split on the 768-wide stage: the largest 128-row tile whose
 // tile count still fits one round of two blocks per CU (at least 400 tiles
-// of 128 x 192, 128 x 160 or 128 x 128), without a K split; otherwise
-// 64 x 128 tiles with a three-stage LDS ring (two blocks per CU), no K split:
-// with 16 MFMAs per wave and K-step the deeper ring hides the operand
-// latency that two stages leave exposed, and beats splitting K.
+// of 128 x 192, 128 x 160 or 128 x 128), without a K split; a GEMM that
+// needs more than one round of 128-row tiles takes 128 x 192 (from the
+// sweep of the 1024-token, 1408-wide stage: +13 % step against 64 x 128);
+// otherwise 64 x 128 tiles with a three-stage LDS ring (two blocks per CU),
+// no K split: with 16 MFMAs per wave and K-step the deeper ring hides the
+// operand latency that two stages leave exposed, and beats splitting K.
 // Overrides (for sweeps): PULSE_TCONV_TILE forces a tile (with the split
 // rule of two blocks per CU, at least 4 K-steps per split),
 // PULSE_TCONV_KSPLIT_MAX caps the split.
@@ -218,7 +220,7 @@ ConvPlan tconv_plan(int tile_force, int ks_cap, long M, int N, int K) {
         p.tile = t;
       }
     }
-    if (p.tile < 0) p.tile = TILE2_C64x128S3;
+    if (p.tile < 0) p.tile = tile_count(TILE2_C128x192, M, N) > 512 ? TILE2_C128x192 : TILE2_C64x128S3;
   }
   ks = std::min(ks, (long)std::max(1, ks_cap));
   const long kt = K / tile2_info(p.tile).bk;
@@ -227,10 +229,15 @@ ConvPlan tconv_plan(int tile_force, int ks_cap, long M, int N, int K) {
   return p;
 }
 
-// weight-gradient tile for M rows (PULSE_TWGRAD_TILE forces one)
-int twgrad_tile(int tile_force, int M) {
+// weight-gradient tile for M rows summed over P tokens (PULSE_TWGRAD_TILE
+// forces one).  The 320 x 128 tile (8 waves, one block per CU) does the
+// most MFMA work per operand byte but quantises M in steps of 320; it wins
+// when M is a multiple of 320, or when every block's token loop is long
+// (P >= 8192: measured on the 1024-token, 1408-wide stage, where it cut the
+// step by 7 %; at 4096 tokens of the 768-wide stage 128 x 128 is 2 % faster).
+int twgrad_tile(int tile_force, int M, long P) {
   if (tile_force >= TILE2_WGRAD_FIRST && tile_force <= TILE2_WGRAD_LAST) return tile_force;
-  return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128;
+  return M % 320 == 0 || P >= 8192 ? TILE2_W320x128 : TILE2_W128x128;
 }
 
 // Token splits of a weight-gradient GEMM (M x N over P tokens): the count
@@ -344,7 +351,7 @@ void build_layout(pulse_tstage* s) {
     const ConvPlan cp = tconv_plan(s->conv_tile_force, s->conv_ks_cap, T, N, K);
     if (cp.ks > 1) kcap = std::max(kcap, (size_t)cp.ks * T * N);
     int kc = 0;
-    const int sp = twgrad_splits(twgrad_tile(s->wgrad_tile_force, N), T, N, K, kc);
+    const int sp = twgrad_splits(twgrad_tile(s->wgrad_tile_force, N, T), T, N, K, kc);
     wcap = std::max(wcap, (size_t)sp * N * K);
   }
   s->kpart_cap = kcap;
@@ -512,7 +519,7 @@ pulse_status linear_wgrad(pulse_tstage* s, int M, const Seg& in, const void* gy,
   a.seg[0] = in;
   a.gy = tvin(gy, M);
   int kc = 0;
-  const int wtile = twgrad_tile(s->wgrad_tile_force, M);
+  const int wtile = twgrad_tile(s->wgrad_tile_force, M, s->T);
   const int splits = twgrad_splits(wtile, s->T, M, a.N, kc);
   if ((size_t)splits * M * a.N > s->wpart_cap)
     return tfail(PULSE_E_SHAPE, "internal: weight-gradient partial buffer too small");

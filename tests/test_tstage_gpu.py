@@ -45,13 +45,16 @@ def _long():
 
 def _t1408_b2():
     """The Hunyuan-DiT-like stage at its full per-image shape (1024 tokens,
-    width 1408 in 22 heads, MLP 5632) with two images."""
+    width 1408 in 22 heads, MLP 5632) with two images (GEMMs that fit one
+    round of tiles).  The "t1408" case runs the benchmarked batch of 8, whose
+    GEMMs take the multi-round plan (128 x 192 conv tiles, 320 x 128
+    weight-gradient tiles over 8192 tokens)."""
     return configs.t1408(batch=2)
 
 
 CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t_narrow": (_narrow, 12),
          "t768": (configs.t768, 7), "t_320": (_t320, 13), "t_long": (_long, 14),
-         "t1408_b2": (_t1408_b2, 8)}
+         "t1408_b2": (_t1408_b2, 8), "t1408": (configs.t1408, 8)}
 
 
 def run_gpu(desc, params, b, mbs=(0,)):
