@@ -43,6 +43,12 @@ def _long():
     return configs._tstage(2, 1024, 256, 4, 1, 1)
 
 
+def _t4096():
+    """The longest sequence the stage takes: 4096 tokens, one image, 2 heads,
+    1 + 1 blocks (32 forward chunks, 64 streamed backward chunks)."""
+    return configs._tstage(1, 4096, 128, 2, 1, 1)
+
+
 def _t1408_b2():
     """The Hunyuan-DiT-like stage at its full per-image shape (1024 tokens,
     width 1408 in 22 heads, MLP 5632) with two images (GEMMs that fit one
@@ -54,7 +60,7 @@ def _t1408_b2():
 
 CASES = {"t_tiny": (configs.t_tiny, 6), "t_mid": (_mid, 11), "t_narrow": (_narrow, 12),
          "t768": (configs.t768, 7), "t_320": (_t320, 13), "t_long": (_long, 14),
-         "t1408_b2": (_t1408_b2, 8), "t1408": (configs.t1408, 8)}
+         "t_4096": (_t4096, 15), "t1408_b2": (_t1408_b2, 8), "t1408": (configs.t1408, 8)}
 
 
 def run_gpu(desc, params, b, mbs=(0,)):
