@@ -19,8 +19,8 @@
 // LDS tiles are row-major [rows][64] bf16 with the 16-byte chunks of each
 // row permuted (chunk c of row r stored at c ^ swz(r)).  An MFMA operand
 // whose k index runs along a tile row is one 16-byte read; one whose k index
-// runs down the rows (v and k as the B operand of p v and ds k, q and do in
-// dk and dv) comes from two ds_read_b64_tr_b16: within 16 lanes, lane j
+// runs down the rows (v in o = p v, k in dq = ds k, q and do in dk and dv)
+// comes from two ds_read_b64_tr_b16: within 16 lanes, lane j
 // receives element j % 4 of the rows addressed by lanes 4 t + j / 4
 // (t = 0..3).  swz keeps both read shapes free of bank conflicts: 16
 // consecutive rows of one chunk, and rows {0-3, 8-11} (+16 k) of a 32-byte
@@ -348,12 +348,11 @@ __global__ __launch_bounds__(256) void k_attn_bwd_kv(const uint16_t* qkv, const 
 }
 
 // ---------------------------------------------------------------------------
-// Longer sequences (L > 256): the same products, streamed over 64-token
-// chunks of the other side.  The forward keeps a running row maximum and
-// sum (online softmax) and rescales its o accumulators when the maximum
-// grows; the backward kernels walk key (dq) or query (dk, dv) chunks.  Each
-// chunk is loaded into registers one iteration ahead and stored into a
-// single LDS tile per operand at the top of the next iteration.
+// Backward for longer sequences (L > 256): the same products, streamed
+// over 64-token chunks of the other side: key chunks for dq, query chunks
+// for dk and dv.  Each chunk is loaded into registers one iteration ahead
+// and stored into a single LDS tile per operand at the top of the next
+// iteration.
 // ---------------------------------------------------------------------------
 
 constexpr int KC = 64;  // tokens per streamed chunk
