@@ -68,32 +68,42 @@ def describe(name, descs):
             "dec_blocks": [[b["c_up"], b["c_skip"], b["c_out"]] for b in d["dec"]]}
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "igemm2_conv_l64_traffic.md")
-KERNEL_SOURCES = ["igemm2.hip", "kernels.hpp", "common.hpp", "stage.cpp"]
+# committed FETCH_SIZE/WRITE_SIZE summaries of the conv-mode GEMM launches,
+# each valid for the kernel and planning sources it was taken on
+TRAFFIC_WORKLOADS = {
+    "l64": ["igemm2.hip", "kernels.hpp", "common.hpp", "stage.cpp"],
+    "t768": ["igemm2.hip", "kernels.hpp", "common.hpp", "tstage.cpp"],
+    "t1408": ["igemm2.hip", "kernels.hpp", "common.hpp", "tstage.cpp"],
+}
 
 
-def kernel_sources_sha256():
+def traffic_profile(name):
+    return os.path.join(ROOT, "profiles", f"igemm2_conv_{name}_traffic.md")
+
+
+def kernel_sources_sha256(name="l64"):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in TRAFFIC_WORKLOADS[name]:
         with open(os.path.join(ROOT, "paper_2606_19163_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
 def measured_traffic(name):
-    """HBM bytes per conv launch from the committed FETCH_SIZE/WRITE_SIZE
-    summary of the l64 stage; None when that summary was taken on other
-    kernel sources than the ones built here, or for another workload."""
-    if name != "l64" or not os.path.exists(TRAFFIC_PROFILE):
+    """HBM bytes per conv-mode launch from the committed FETCH_SIZE/WRITE_SIZE
+    summary of the workload; None when that summary was taken on other
+    kernel sources than the ones built here, or when there is none."""
+    path = traffic_profile(name) if name in TRAFFIC_WORKLOADS else None
+    if path is None or not os.path.exists(path):
         return None
     vals = {}
-    with open(TRAFFIC_PROFILE) as fh:
+    with open(path) as fh:
         for line in fh:
             if line.startswith("- ") and ": " in line:
                 k, v = line[2:].strip().split(": ", 1)
                 vals[k.strip("`")] = v.strip().strip("`")
-    if vals.get("kernel_sources_sha256") != kernel_sources_sha256():
+    if vals.get("kernel_sources_sha256") != kernel_sources_sha256(name):
         return None
     try:
         return int(vals["traffic_bytes_per_launch"])
@@ -272,6 +282,12 @@ def bench_tstage(args):
     st.set_params(params)
     dev = {k: st.to_dev(v) for k, v in b.items()}
     outs = {k: st.act() for k in ("y_enc", "y_dec", "dx", "du")}
+    if args.copy_calibration_mib > 0:
+        # one plain device copy of known size: the scale for HBM counters
+        src = torch.ones(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
+        torch.empty_like(src).copy_(src)
+        torch.cuda.synchronize()
+        del src
 
     def step():
         st.forward(TS.ENC, 0, dev["x"], out=outs["y_enc"])
@@ -315,7 +331,8 @@ def bench_tstage(args):
         line["roofline"] = {
             "kernel": "igemm_conv in its token-major 1x1 form (linear forward / data gradient)",
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": measured_traffic(args.workload),
             "algorithmic_bytes_per_launch": round(kbytes / launches), "launches": launches,
             "avg_launch_us": round(kms * 1e3 / launches, 2),
             "avg_gflop_per_launch": round(kflops / launches / 1e9, 3)}

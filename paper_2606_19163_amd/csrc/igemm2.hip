@@ -312,8 +312,25 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int z = lb / ntiles;
   const int bid = lb - z * ntiles;
-  const int tn = bid % tilesN;
-  const int tm = bid / tilesN;
+  // Tile order within the XCD's range.  Up to 8 column tiles: row-major, a
+  // row tile's A rows are reused across all of N and B is small.  Wider N:
+  // groups of 8 row tiles swept column by column, so that the blocks an XCD
+  // runs together share both their A rows and their B columns in its L2
+  // (row-major would stream the whole B through L2 once per row tile).
+  int tn, tm;
+  if (tilesN <= 8) {
+    tn = bid % tilesN;
+    tm = bid / tilesN;
+  } else {
+    constexpr int GM = 8;
+    const int tilesM = ntiles / tilesN;
+    const int grp = bid / (GM * tilesN);
+    const int first = grp * GM;
+    const int gm = min(GM, tilesM - first);
+    const int local = bid - grp * GM * tilesN;
+    tm = first + local % gm;
+    tn = local / gm;
+  }
   const long m0 = (long)tm * C::BM;
   const int n0 = tn * C::BN;
   const int KT_ALL = a.K / C::BK;
