@@ -35,7 +35,11 @@
  *    pulse_last_error() describes the cause.  No exception crosses the ABI.
  *    Kernel faults are asynchronous and surface at the caller's next
  *    synchronisation.
- *  - A stage is not thread-safe: serialise calls on one handle.
+ *  - A stage is not thread-safe: serialise calls on one handle.  Calls may
+ *    use different streams: every call shares the stage's scratch buffers,
+ *    so a call on a stream other than the previous call's first makes its
+ *    stream wait for the previous call's work (an event recorded at the end
+ *    of every call that enqueues work).
  */
 #ifndef PULSE_STAGE_H
 #define PULSE_STAGE_H

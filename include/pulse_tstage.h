@@ -31,7 +31,8 @@
  * the caller binds one workspace of pulse_tstage_sizes() bytes.  Every call
  * validates before it enqueues anything; on error it returns a status !=
  * PULSE_OK, changes no state and pulse_last_error() says why.  A stage is
- * not thread-safe.
+ * not thread-safe, and every call on one handle shares its scratch
+ * buffers: enqueue them on one stream, or order the streams yourself.
  */
 #ifndef PULSE_TSTAGE_H
 #define PULSE_TSTAGE_H

@@ -1,7 +1,8 @@
 """CPU oracle for a skip-collocated stage of transformer blocks (fp64, numpy).
 
-TEST INFRASTRUCTURE ONLY.  Only ``tests/`` may import or call this module;
-the GPU path shares no code with it.
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or call this module.  The
+product package never imports it, and the GPU path shares no code with it.
 
 What is computed
 ----------------

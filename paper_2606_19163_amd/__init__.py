@@ -7,4 +7,4 @@ this package does not load the library; ``paper_2606_19163_amd.stage`` does,
 and fails loudly when it has not been built.
 """
 
-__all__ = ["configs", "synth", "flops"]
+__all__ = ["configs", "synth"]

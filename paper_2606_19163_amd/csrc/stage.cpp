@@ -145,6 +145,12 @@ struct pulse_stage {
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_w2[2] = {nullptr, nullptr}, ev_w1[2] = {nullptr, nullptr};
   hipEvent_t ev_temb = nullptr;  // the forward's timestep projections are ready
+  // Every call shares the scratch buffers.  The stream of the last call that
+  // enqueued work and an event recorded at its end let a call on another
+  // stream wait for it first.
+  hipStream_t last_st = nullptr;
+  hipEvent_t ev_last = nullptr;
+  bool have_last = false;
   // binding
   const float* prm = nullptr;
   float* grd = nullptr;
@@ -486,8 +492,10 @@ pulse_status validate_desc(const pulse_stage_desc* d) {
     return fail(PULSE_E_INVALID_ARG, "dtype %d unknown", (int)d->dtype);
   if (d->batch < 1 || d->height < 1 || d->width < 1)
     return fail(PULSE_E_SHAPE, "batch/height/width must be >= 1");
-  if ((long)d->batch * d->height * d->width > (1L << 28))
-    return fail(PULSE_E_SHAPE, "too many pixels");
+  // The conv kernels address pixels with 24-bit products and every operand
+  // through a buffer range of at most 2^31 - 1 bytes.
+  const long P = (long)d->batch * d->height * d->width;
+  if (P >= (1L << 24)) return fail(PULSE_E_SHAPE, "batch*height*width must stay below 2^24 pixels");
   if (d->groups < 1 || d->groups > 256) return fail(PULSE_E_SHAPE, "groups must be in [1, 256]");
   if (!(d->eps >= 0.0f)) return fail(PULSE_E_SHAPE, "eps must be >= 0");
   if (d->temb_dim < 1) return fail(PULSE_E_SHAPE, "temb_dim must be >= 1");
@@ -518,6 +526,29 @@ pulse_status validate_desc(const pulse_stage_desc* d) {
   }
   if (d->input_skip_slot < -1 || d->input_skip_slot >= MAX_SLOTS)
     return fail(PULSE_E_SHAPE, "input_skip_slot out of range");
+  // Every [pixels][C] tensor (activations in the stage dtype, fp32 skip
+  // gradients and partial sums, counted at 4 bytes per value) and every
+  // weight copy ([C_out][9 C_in (+ C_in)] in the stage dtype) must stay
+  // below 2 GiB.
+  const long esz = d->dtype == PULSE_F32 ? 4 : 2;
+  long widest = 0, wbytes = 0;
+  for (int k = 0; k < d->n_enc; ++k) {
+    const auto& b = d->enc[k];
+    widest = std::max(widest, (long)std::max(b.c_in, b.c_out));
+    wbytes = std::max(wbytes, (long)b.c_out * (9L * b.c_out + b.c_in) * esz);
+    wbytes = std::max(wbytes, (long)b.c_in * 9L * b.c_out * esz);
+  }
+  for (int k = 0; k < d->n_dec; ++k) {
+    const auto& b = d->dec[k];
+    const long cin = (long)b.c_up + b.c_skip;
+    widest = std::max(widest, std::max(cin, (long)b.c_out));
+    wbytes = std::max(wbytes, (long)b.c_out * 9L * cin * esz);
+    wbytes = std::max(wbytes, (long)b.c_out * (9L * b.c_out + cin) * esz);
+    wbytes = std::max(wbytes, cin * 9L * b.c_out * esz);
+  }
+  if (P * widest * 4 >= (1L << 31))
+    return fail(PULSE_E_SHAPE, "a [pixels][%ld] tensor of 4-byte values reaches 2 GiB", widest);
+  if (wbytes >= (1L << 31)) return fail(PULSE_E_SHAPE, "a conv weight copy reaches 2 GiB");
   return PULSE_OK;
 }
 
@@ -930,6 +961,20 @@ pulse_status wait_mark(pulse_stage* s, hipEvent_t ev, bool recorded, hipStream_t
   return PULSE_OK;
 }
 
+// Calls may alternate streams: order this call's work after the previous
+// call's (a no-op on the same stream).
+pulse_status order_after_last(pulse_stage* s, hipStream_t st) {
+  if (s->have_last && s->last_st != st) HIPCHK(hipStreamWaitEvent(st, s->ev_last, 0));
+  return PULSE_OK;
+}
+
+pulse_status mark_last(pulse_stage* s, hipStream_t st) {
+  HIPCHK(hipEventRecord(s->ev_last, st));
+  s->last_st = st;
+  s->have_last = true;
+  return PULSE_OK;
+}
+
 pulse_status join_side(pulse_stage* s, hipStream_t st) {
   if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(s->ev_join, s->side));
@@ -1115,6 +1160,7 @@ void pulse_stage_destroy(pulse_stage* s) {
     if (s->ev_w1[i]) (void)hipEventDestroy(s->ev_w1[i]);
   }
   if (s->ev_temb) (void)hipEventDestroy(s->ev_temb);
+  if (s->ev_last) (void)hipEventDestroy(s->ev_last);
   if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
 }
@@ -1160,6 +1206,7 @@ pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads,
                 s->ws_bytes);
   if (pulse_stage_inflight(s) > 0)
     return fail(PULSE_E_STATE, "cannot rebind with microbatches in flight");
+  if (!s->ev_last) HIPCHK(hipEventCreateWithFlags(&s->ev_last, hipEventDisableTiming));
   if (!s->side && env_int("PULSE_SERIAL", 0) == 0) {
     // default priority, no implicit synchronisation with the null stream
     HIPCHK(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
@@ -1187,6 +1234,8 @@ pulse_status pulse_stage_sync_params(pulse_stage* s, void* stream) {
   }
   if (!s->bound) return fail(PULSE_E_NOT_BOUND, "stage is not bound");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  pulse_status ps;
+  if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
   const int dt = s->dtype;
   for (auto* v : {&s->eb, &s->db})
     for (auto& b : *v) {
@@ -1204,6 +1253,7 @@ pulse_status pulse_stage_sync_params(pulse_stage* s, void* stream) {
                             reinterpret_cast<float*>(s->ws + b.bias2), b.cout, st));
     }
   HIPCHK(hipMemsetAsync(s->scratch(s->s_zero), 0, 256, st));
+  if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
   s->synced = true;
   return PULSE_OK;
 }
@@ -1253,6 +1303,7 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
     hipStream_t st = static_cast<hipStream_t>(stream);
     char* row = s->row_base(r);
     const int dt = s->dtype;
+    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
     HIPCHK(hipMemcpyAsync(row + s->row_temb[half == PULSE_DEC ? 1 : 0], temb, (size_t)s->geo.B * s->D * s->esz,
                           hipMemcpyDeviceToDevice, st));
     if (half == PULSE_ENC) {
@@ -1295,6 +1346,7 @@ pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, co
           return ps;
       }
     }
+    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
   }
 
   Row& row = s->rows[r];
@@ -1349,6 +1401,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     hipStream_t st = static_cast<hipStream_t>(stream);
     char* row = s->row_base(r);
     const int dt = s->dtype;
+    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
     int cur = 0;
     BwdSync sy;
     if (half == PULSE_DEC) {
@@ -1398,6 +1451,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     }
     // the caller's stream sees every side-stream result
     if ((ps = join_side(s, st)) != PULSE_OK) return ps;
+    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
   }
 
   Row& row = s->rows[r];
@@ -1431,9 +1485,13 @@ pulse_status pulse_skip_cache_put(pulse_stage* s, int32_t mb, int32_t slot, cons
       return fail(PULSE_E_CACHE_FULL, "mb %d: %d microbatches already in flight", mb,
                   s->d.max_inflight);
   }
-  if (!s->dry)
+  if (!s->dry) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
     HIPCHK(hipMemcpyAsync(s->row_base(r) + s->row_act[slot], src, act_bytes(s, s->slot_ch[slot]),
-                          hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
+                          hipMemcpyDeviceToDevice, st));
+    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
+  }
   Row& row = s->rows[r];
   if (row.mb < 0) {
     row.mb = mb;
@@ -1466,8 +1524,10 @@ pulse_status pulse_skip_cache_take(pulse_stage* s, int32_t mb, int32_t slot,
     const size_t off = kind == PULSE_SKIP_ACT ? s->row_act[slot] : s->row_grad[slot];
     const size_t bytes = kind == PULSE_SKIP_ACT ? act_bytes(s, s->slot_ch[slot])
                                                 : (size_t)s->P * s->slot_ch[slot] * 4;
-    HIPCHK(hipMemcpyAsync(dst, s->row_base(r) + off, bytes, hipMemcpyDeviceToDevice,
-                          static_cast<hipStream_t>(stream)));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
+    HIPCHK(hipMemcpyAsync(dst, s->row_base(r) + off, bytes, hipMemcpyDeviceToDevice, st));
+    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
   }
   present = 0;
   if (!row.enc_done && (row.state == R_FRESH || row.state == R_DEC_BWD) && row_empty(s, row))

@@ -88,7 +88,10 @@ __global__ __launch_bounds__(256) void k_ln_bwd(const uint16_t* dy, const uint16
                                                 const float2* stats, const float* g,
                                                 const uint16_t* add, long T, int C, uint16_t* dx,
                                                 float* part, float* csum) {
-  __shared__ float sm[4][2][64 * LN_VEC * 8 / 4];  // per wave, [2][C / 4 per j] reused below
+  // per wave, [2][C / 4 per j] reused below; the partial-sum passes write
+  // lanes * 8 values per row whatever LN_VEC is
+  static_assert(64 * LN_VEC * 8 / 4 >= 64 * 8, "k_ln_bwd: LDS rows hold 64 lanes x 8 values");
+  __shared__ float sm[4][2][64 * LN_VEC * 8 / 4];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nv = C / 8;
   float accg[LN_VEC][8], accb[LN_VEC][8], accx[LN_VEC][8];

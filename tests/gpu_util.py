@@ -60,8 +60,9 @@ def run_gpu(desc, params, b, want_cache=True, mb=0):
     return res, st
 
 
-def compare(desc, gpu, ref, tol=None, grads=True, skip_rows=None, label=""):
-    """rel L2 per output; returns the dict of errors and asserts each <= tol."""
+def compare(desc, gpu, ref, tol=None, grads=True, skip_rows=None, label="", log_all=False):
+    """rel L2 per output; returns the dict of errors and asserts each <= tol.
+    ``log_all`` prints every tensor's error, not only the worst."""
     tol = tol_for(desc) if tol is None else tol
     errs = {}
     sl = (slice(None) if skip_rows is None else skip_rows)
@@ -77,6 +78,9 @@ def compare(desc, gpu, ref, tol=None, grads=True, skip_rows=None, label=""):
         if slot in gpu.get("dskips", {}):
             errs[f"dskip{slot}"] = rel_l2(gpu["dskips"][slot][sl], v)
     worst = max(errs, key=errs.get)
+    if log_all:
+        for k in sorted(errs):
+            log(f"  {label} {k} = {errs[k]:.3e}")
     log(f"  {label} worst {worst} = {errs[worst]:.3e} (tol {tol:g})")
     bad = {k: v for k, v in errs.items() if not (v <= tol)}
     assert not bad, bad

@@ -185,3 +185,41 @@ def test_input_slot_bookkeeping_l32():
     assert st.state(0, 1) & S.GRAD_PRESENT
     st.backward(S.ENC, 0, None)
     assert st.inflight() == 0
+
+
+def test_pixel_count_limit():
+    """The conv kernels form pixel offsets as 24-bit products: a stage of
+    2^24 pixels is refused at create, with the pixel count named.  (The
+    decoder's input gradient has at least 64 channels, so the 2 GiB tensor
+    limit below already binds from 2^23 pixels on.)"""
+    d = configs.shrink(configs.tiny(), batch=1, hw=4096, width=4096)
+    with pytest.raises(S.PulseError) as e:
+        _dry(d)
+    assert e.value.status == S.E_SHAPE and "2^24" in str(e.value)
+
+
+@pytest.mark.parametrize("width,ok", [(4095, True), (4096, False)])
+def test_tensor_bytes_limit(width, ok):
+    """Operands are addressed through buffer ranges of at most 2^31 - 1
+    bytes: the widest [pixels][C] tensor, counted at 4 bytes per value (the
+    fp32 skip gradients and partial sums), must stay below 2 GiB.  The tiny
+    stage's widest tensor is the decoder's 64-channel input gradient, so
+    2048 x 4096 pixels reach 2^31 bytes exactly."""
+    d = configs.shrink(configs.tiny(), batch=1, hw=2048, width=width)
+    if ok:
+        _dry(d)
+    else:
+        _expect_status(lambda: _dry(d), S.E_SHAPE)
+
+
+@pytest.mark.parametrize("dtype,ok", [(configs.BF16, True), (configs.F32, False)])
+def test_weight_bytes_limit(dtype, ok):
+    """A decoder conv2 copy with its shortcut appended, [8160][9*8160 + 8192],
+    is 1.33 GB in bf16 and 2.66 GB in fp32: the fp32 stage is refused."""
+    d = configs.tiny()
+    d["dtype"] = dtype
+    d["dec"][0].update(c_up=8160, c_out=8160)
+    if ok:
+        _dry(d)
+    else:
+        _expect_status(lambda: _dry(d), S.E_SHAPE)

@@ -123,9 +123,10 @@ def test_full_size_wave_order_matches_isolated_microbatches(level):
     """The wave workload's launch configuration at full size: one level of
     the four (64x64x320, 32x32x640, 16x16x1280, 8x8x1280 at batch 8) with 4
     microbatches in flight, all forward passes, then the backward passes in
-    reverse.  Every per-microbatch output equals an isolated run bitwise (the
-    isolated runs are the ones the full-size parity tests compare with the
-    oracle), and so do the accumulated gradients."""
+    reverse.  Every per-microbatch output equals an isolated run bitwise, and
+    so do the accumulated gradients.  (Isolated runs of each level at batch 8,
+    in this launch configuration, are compared with the oracle by
+    ``test_parity_gpu.py::test_full_size``.)"""
     import torch
     desc = configs.wave_levels()[level]
     name = ["l64", "l32", "l16", "l8"][level]
@@ -151,4 +152,34 @@ def test_full_size_wave_order_matches_isolated_microbatches(level):
         for k, t in (("e", "y_enc"), ("d", "y_dec"), ("du", "du"), ("dx", "dx")):
             assert torch.equal(out[t].view(torch.int16), y[(k, m)].view(torch.int16)), (m, t)
     assert _bytes(st.grads) == wave_grads
+    assert st.inflight() == 0
+
+
+def test_calls_on_alternating_streams_match_one_stream():
+    """Every call shares the stage's scratch buffers, so a call on a stream
+    other than the previous call's waits for that call's work first: the
+    four calls of a microbatch alternating between two side streams give
+    bitwise what the same calls give on one stream."""
+    import torch
+    desc = configs.shrink(configs.l64(), batch=2, hw=16)
+    st, _ = _wave_setup(desc, 2)
+    _, b = synth.make_all(desc, 2)
+    db = device_boundary(st, b)
+    st.zero_grads()
+    ref = S.run_microbatch(st, 0, db)
+    torch.cuda.synchronize()
+    g_ref = _bytes(st.grads)
+    st.zero_grads()
+    outs = {k: torch.empty_like(v) for k, v in ref.items()}
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    log("case alternating streams: F_enc s1, F_dec s2, B_dec s1, B_enc s2")
+    st.forward(S.ENC, 1, db["x"], db["temb"], out=outs["y_enc"], stream=s1)
+    st.forward(S.DEC, 1, db["u"], db["temb"], out=outs["y_dec"], stream=s2)
+    st.backward(S.DEC, 1, db["g_dec"], din=outs["du"], stream=s1)
+    st.backward(S.ENC, 1, db["g_enc"], din=outs["dx"], stream=s2)
+    torch.cuda.synchronize()
+    for k in ref:
+        assert _bytes(outs[k]) == _bytes(ref[k]), k
+    assert _bytes(st.grads) == g_ref
     assert st.inflight() == 0

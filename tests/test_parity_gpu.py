@@ -9,7 +9,7 @@ import pytest
 from oracle import pulse_oracle as O
 from paper_2606_19163_amd import configs, synth
 
-from gpu_util import compare, log, run_gpu
+from gpu_util import compare, log, rel_l2, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -58,22 +58,64 @@ def test_bf16_k32_path():
     _case(d, 17, "c96")
 
 
-@pytest.mark.parametrize("name", ["l64", "l32", "l16", "l8"])
-def test_full_size_sampled(name):
-    """Every stage at its real size (64x64x320 and 32x32x640 at batch 8,
-    16x16 and 8x8 at 1280 channels and batch 16) in the launch configuration
-    the bench times; the oracle recomputes two samples of the batch (every
-    output but the parameter gradients is per sample)."""
-    desc = configs.get(name)
-    params, b = synth.make_all(desc, configs.SEEDS[name])
-    log(f"case {name} full: GPU run")
+FULL = [("l64", None), ("l32", None), ("l16", None), ("l8", None), ("l16", 8), ("l8", 8)]
+
+
+@pytest.mark.parametrize("name,batch", FULL, ids=[f"{n}-b{b or 'bench'}" for n, b in FULL])
+def test_full_size(name, batch):
+    """Every stage at its real size in the launch configuration the bench
+    times (64x64x320 and 32x32x640 at batch 8, 16x16 and 8x8 at 1280
+    channels and batch 16), and the 16x16 and 8x8 levels also at batch 8,
+    the wave workload's shape, where the conv and weight-gradient plans pick
+    other K splits.  The oracle runs on the whole microbatch, so every
+    output, parameter gradient (the production weight-gradient split and its
+    finalize), cached skip and buffered skip gradient is compared."""
+    desc = configs.get(name) if batch is None else configs.get(name, batch=batch)
+    seed = configs.SEEDS[name]
+    log(f"case {name} full B={desc['batch']}: GPU run")
+    params, b = synth.make_all(desc, seed)
     gpu, _ = run_gpu(desc, params, b)
-    for n in (0, desc["batch"] - 3):
-        log(f"case {name} full: oracle sample {n}")
-        d1 = configs.shrink(desc, batch=1)
-        b1 = {k: v[n:n + 1] for k, v in b.items()}
-        ref = _oracle(d1, params, b1)
-        compare(desc, gpu, ref, grads=False, skip_rows=slice(n, n + 1), label=f"{name} n={n}")
+    log(f"case {name} full B={desc['batch']}: oracle")
+    ref = _oracle(desc, params, b)
+    compare(desc, gpu, ref, label=f"{name} B={desc['batch']}", log_all=True)
+
+
+def test_two_microbatch_accumulation():
+    """Parameter gradients accumulate (+=) over microbatches: two l64
+    microbatches with different inputs, run through one stage in the bench's
+    launch configuration, against the sum of two oracle runs; each
+    microbatch's outputs against its own oracle run."""
+    import torch
+    from paper_2606_19163_amd import stage as S
+    desc = configs.l64()
+    params, b0 = synth.make_all(desc, configs.SEEDS["l64"])
+    _, b1 = synth.make_all(desc, configs.SEEDS["l64"] + 100)
+    st = S.Stage(desc)
+    st.set_params(params)
+    st.zero_grads()
+    outs = []
+    dtemb = torch.zeros((desc["batch"], desc["temb_dim"]), dtype=torch.float32, device="cuda")
+    for mb, bb in enumerate((b0, b1)):
+        log(f"case l64 two microbatches: GPU microbatch {mb}")
+        db = {k: st.to_dev(v) for k, v in bb.items()}
+        dt = torch.zeros_like(dtemb)
+        o = S.run_microbatch(st, mb, db, dtemb=dt)
+        torch.cuda.synchronize()
+        res = {k: v.float().cpu().numpy() for k, v in o.items()}
+        res["dtemb"] = dt.cpu().numpy()
+        outs.append(res)
+    grads = st.grads_dict()
+    refs = []
+    for mb, bb in enumerate((b0, b1)):
+        log(f"case l64 two microbatches: oracle microbatch {mb}")
+        refs.append(_oracle(desc, params, bb))
+        compare(desc, outs[mb], refs[mb], grads=False, label=f"l64 mb{mb}")
+    total = {"grads": {k: refs[0]["grads"][k] + refs[1]["grads"][k] for k in refs[0]["grads"]}}
+    errs = {k: rel_l2(grads[k], v) for k, v in total["grads"].items()}
+    for k in sorted(errs):
+        log(f"  l64 two microbatches grad.{k} = {errs[k]:.3e}")
+    bad = {k: v for k, v in errs.items() if not (v <= 2e-2)}
+    assert not bad, bad
 
 
 @pytest.mark.parametrize("tile", range(13))

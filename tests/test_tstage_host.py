@@ -157,3 +157,32 @@ def test_schedule_rows_drive_a_dry_transformer_stage():
         TS.tsched_run_device(st, 2, 0, 2, [table[1], table[1]])  # device 1's cells as row 0
     assert e.value.status == S.E_INVALID_ARG
     assert st.inflight() == 0
+
+
+@pytest.mark.parametrize("batch,ok", [(1023, True), (1024, False)])
+def test_activation_bytes_limit(batch, ok):
+    """Width 2048 with an 8x MLP: the fc1 output holds 16384 bf16 values per
+    token, so 65536 tokens reach 2^31 bytes exactly and are refused, while
+    64 tokens fewer are accepted."""
+    d = configs.t_tiny()
+    d.update(batch=batch, tokens=64, width=2048, heads=32, mlp=8)
+    if ok:
+        _dry(d)
+    else:
+        with pytest.raises(S.PulseError) as e:
+            _dry(d)
+        assert e.value.status == S.E_SHAPE
+
+
+@pytest.mark.parametrize("batch,ok", [(16384, True), (16385, False)])
+def test_token_count_limit(batch, ok):
+    """The GEMM kernels form token offsets as 24-bit products; the stage
+    caps batch x tokens at 2^20."""
+    d = configs.t_tiny()
+    d.update(batch=batch, tokens=64)
+    if ok:
+        _dry(d)
+    else:
+        with pytest.raises(S.PulseError) as e:
+            _dry(d)
+        assert e.value.status == S.E_SHAPE
