@@ -494,6 +494,9 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     slot = slot + 1 == C::STAGES ? 0 : slot + 1;
 #pragma unroll
     for (int s = 0; s < C::KH; ++s) {
+      // the scheduler must not sink this half's MFMAs below the next
+      // half's wait (they would all wait for every fragment read)
+      __builtin_amdgcn_sched_barrier(0);
       if (s + 1 < C::KH)
         lgkm_wait<C::TM + C::TN>();
       else
@@ -509,6 +512,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
           acc[i][j] =
               __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
   __syncthreads();
 
@@ -825,6 +829,8 @@ __global__ __launch_bounds__(512) void igemm_halo_conv(GemmArgs a) {
       }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
+        // keep the first half's MFMAs above the second half's wait
+        __builtin_amdgcn_sched_barrier(0);
         if (s == 0)
           lgkm_wait<C::TM + C::TN>();
         else
@@ -840,6 +846,7 @@ __global__ __launch_bounds__(512) void igemm_halo_conv(GemmArgs a) {
             acc[i][j] =
                 __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
       ++step;
     }
     ck = nx;
@@ -1115,8 +1122,11 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
     lgkm_wait<0>();
     read(sb, af[1], bfr[1], std::integral_constant<int, 1>());
     mma(af[0], bfr[0]);
+    // keep the first half's MFMAs above the second half's wait
+    __builtin_amdgcn_sched_barrier(0);
     lgkm_wait<0>();
     mma(af[1], bfr[1]);
+    __builtin_amdgcn_sched_barrier(0);
   }
   __syncthreads();
 
