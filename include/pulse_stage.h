@@ -155,6 +155,26 @@ pulse_status pulse_stage_forward(pulse_stage* st, pulse_half half, int32_t mb,
                                  const void* in, const void* temb, void* out,
                                  void* stream);
 
+/* For callers that cannot allocate device memory per call or allocate at
+ * all (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid it): pulse_stage_forward with the forward pass's scratch (GroupNorm
+ * partial sums, timestep projections, conv K-split partials) taken from a
+ * device array of PULSE_FWD_STATIC_SCRATCH_BYTES that the library holds on
+ * each GPU it runs on until the process ends, instead of from the bound
+ * workspace.  Same arguments, semantics and results as pulse_stage_forward
+ * (bitwise); it makes no allocation of its own.  PULSE_E_SHAPE when the
+ * stage's forward scratch exceeds the array (the 64x64x320 stage at batch 8
+ * needs about 5.3 MB; stages with K-split convs or wide channels at large
+ * batch do not fit); PULSE_E_STATE while per-launch timing is on.  Every
+ * call on one GPU shares that GPU's array: calls that may overlap on one
+ * GPU (any stage, any stream) race and must be serialised by the caller.
+ * The array is written before it is read in every call, so it needs no
+ * clearing. */
+#define PULSE_FWD_STATIC_SCRATCH_BYTES (8u << 20)
+pulse_status pulse_stage_forward_static(pulse_stage* st, pulse_half half, int32_t mb,
+                                        const void* in, const void* temb, void* out,
+                                        void* stream);
+
 /* Backward of one half for microbatch `mb`.
  *  DEC: dout = dL/dy_dec, din = dL/du.  Writes the skip-gradient entry of
  *       every slot the decoder reads.

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -167,6 +168,21 @@ struct pulse_stage {
   char* row_base(int r) const { return ws + off_rows + (size_t)r * row_size; }
   void* scratch(size_t off) const { return ws + off_scratch + off; }
   float* sf(size_t off) const { return reinterpret_cast<float*>(scratch(off)); }
+  // Scratch of the forward pass (GroupNorm partial sums, timestep
+  // projections, conv K-split partials): the bound workspace's regions for
+  // every call but pulse_stage_forward_static, which points fwd_base at the
+  // library's static device array and the offsets at a compact layout.
+  char* fwd_base = nullptr;
+  size_t f_red = 0, f_e = 0, f_kpart = 0, f_kcap = 0;
+  size_t fs_red = 0, fs_e = 0, fs_kpart = 0, fs_kcap = 0, fs_bytes = 0;  // compact layout
+  float* fwd(size_t off) const { return reinterpret_cast<float*>(fwd_base + off); }
+  void use_workspace_scratch() {
+    fwd_base = ws + off_scratch;
+    f_red = s_red;
+    f_e = s_e;
+    f_kpart = s_kpart;
+    f_kcap = kpart_cap;
+  }
   const float* pp(int64_t off) const { return prm + off; }
   float* gp(int64_t off) const { return off < 0 ? nullptr : grd + off; }
 };
@@ -483,6 +499,23 @@ pulse_status build_layout(pulse_stage* s) {
   s->s_e = sc; sc += align256(nblk * s->geo.B * cmax * 4);
   s->s_zero = sc; sc += 256;  // zero bytes read in place of out-of-image taps
   s->ws_bytes = s->off_scratch + sc;
+  // the forward's scratch alone, packed (pulse_stage_forward_static), with
+  // the K-split partials of the forward convs only, at their own K
+  size_t fkpart = 0;
+  for (auto* v : {&s->eb, &s->db})
+    for (auto& b : *v) {
+      const int k2 = 9 * b.cout + (b.conv_sc ? b.cin : 0);
+      for (int K : {9 * b.cin, k2}) {
+        const int ks = conv_ksplit(s, conv_tile(s, b.cout), b.cout, K);
+        if (ks > 1) fkpart = std::max(fkpart, (size_t)ks * s->P * b.cout);
+      }
+    }
+  size_t fs = 0;
+  s->fs_red = fs; fs += align256(red * 4);
+  s->fs_e = fs; fs += align256(nblk * s->geo.B * cmax * 4);
+  s->fs_kpart = fs; fs += align256(fkpart * 4);
+  s->fs_kcap = fkpart;
+  s->fs_bytes = fs;
   return PULSE_OK;
 }
 
@@ -686,9 +719,9 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
   a.ksteps = (kt + ks - 1) / ks;
   if (ks > 1) {
     a.ksplit = (kt + a.ksteps - 1) / a.ksteps;  // no empty split
-    if ((size_t)a.ksplit * a.M * a.N > s->kpart_cap)
+    if ((size_t)a.ksplit * a.M * a.N > s->f_kcap)
       return fail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
-    a.part = s->sf(s->s_kpart);
+    a.part = s->fwd(s->f_kpart);
   }
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
@@ -821,7 +854,7 @@ pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x
                         const float* gamma, const float* beta, void* dst0, void* dst1,
                         hipStream_t st, int pre_chunks = 0) {
   RedGrid rg = red_grid(s->geo, x.C);
-  float* red = s->sf(s->s_red);
+  float* red = s->fwd(s->f_red);
   if (pre_chunks > 0)
     rg.chunks = pre_chunks;
   else
@@ -880,7 +913,7 @@ VIn block_input(pulse_stage* s, int r, const Block& b, int k, const void* dec_up
 bool use_side(const pulse_stage* s) { return s->side && !s->timing; }
 
 float* temb_slice(pulse_stage* s, int k) {
-  return s->sf(s->s_e) + (size_t)k * s->geo.B * s->cmax;
+  return s->fwd(s->f_e) + (size_t)k * s->geo.B * s->cmax;
 }
 
 // One ResBlock forward.  `out` receives the block output, `out2` a copy.
@@ -908,7 +941,7 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
   void* h1 = row + b.h1;
   int h1_chunks = 0;  // GN2 statistics of h1 from conv1's epilogue, when it can
   if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cin, a1)}, s->ws + b.wf1, 9 * b.cin, nullptr, e,
-                     vnone(), h1, nullptr, dt, st, s->sf(s->s_red), &h1_chunks)) != PULSE_OK)
+                     vnone(), h1, nullptr, dt, st, s->fwd(s->f_red), &h1_chunks)) != PULSE_OK)
     return ps;
   // a2 = SiLU(GN2(h1))
   const VIn h1v = vin1(h1, dt, b.cout);
@@ -918,7 +951,7 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
     return ps;
   const VIn a2v = vin1(a2, dt, b.cout);
   const float* bias2 = reinterpret_cast<const float*>(s->ws + b.bias2);
-  float* ostats = out_chunks ? s->sf(s->s_red) : nullptr;  // GN2 has consumed it
+  float* ostats = out_chunks ? s->fwd(s->f_red) : nullptr;  // GN2 has consumed it
   if (b.conv_sc)
     return conv_fwd(s, b.cout, {seg3(0, b.cout, a2v), seg1(9 * b.cout, b.cin, xin)},
                     s->ws + b.wf2, b.ldb2, bias2, nullptr, vnone(), out, out2, dt, st, ostats,
@@ -1124,6 +1157,163 @@ double block_flops(const pulse_stage* s, const Block& b) {
 // C ABI
 // ===========================================================================
 
+namespace {
+
+// The forward pass's scratch for pulse_stage_forward_static: one array per
+// GPU, held until the process ends.  Host code never uses its name as an
+// address: fwd_scratch_ptr[device] holds the device address, taken with
+// hipGetSymbolAddress on the call's device the first time that device is
+// used.
+constexpr size_t FWD_SCRATCH_BYTES = (size_t)PULSE_FWD_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) char fwd_scratch[FWD_SCRATCH_BYTES];
+constexpr int MAX_DEVICES = 64;
+std::mutex fwd_scratch_mu;
+void* fwd_scratch_ptr[MAX_DEVICES] = {};
+
+pulse_status fwd_scratch_of_current_device(char** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(PULSE_E_INVALID_ARG, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(fwd_scratch_mu);
+  if (!fwd_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(fwd_scratch));
+    if (e != hipSuccess || !p)
+      return fail(PULSE_E_HIP, "hipGetSymbolAddress of the forward scratch: %s",
+                  hipGetErrorString(e));
+    fwd_scratch_ptr[dev] = p;
+  }
+  *out = static_cast<char*>(fwd_scratch_ptr[dev]);
+  return PULSE_OK;
+}
+
+pulse_status forward_impl(pulse_stage* s, pulse_half half, int32_t mb, const void* in,
+                          const void* temb, void* out, void* stream, bool static_scratch) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (half != PULSE_ENC && half != PULSE_DEC) return fail(PULSE_E_INVALID_ARG, "bad half");
+  if (mb < 0) return fail(PULSE_E_INVALID_ARG, "mb must be >= 0");
+  pulse_status ps;
+  char* sbase = nullptr;
+  if (static_scratch && s->fs_bytes > FWD_SCRATCH_BYTES)
+    return fail(PULSE_E_SHAPE,
+                "the forward pass of this stage needs %zu bytes of scratch, more than the %zu "
+                "of the static array",
+                s->fs_bytes, FWD_SCRATCH_BYTES);
+  if (!s->dry) {
+    if ((ps = need_bound(s)) != PULSE_OK) return ps;
+    if ((ps = check_ptr(in, "in")) != PULSE_OK || (ps = check_ptr(temb, "temb")) != PULSE_OK ||
+        (ps = check_ptr(out, "out")) != PULSE_OK)
+      return ps;
+    if (static_scratch) {
+      if (s->timing)
+        return fail(PULSE_E_STATE, "per-launch timing creates events: switch it off first");
+      if ((ps = fwd_scratch_of_current_device(&sbase)) != PULSE_OK) return ps;
+    }
+  }
+  int r = find_row(s, mb);
+  const pulse_stage_desc& d = s->d;
+  if (half == PULSE_ENC) {
+    if (r >= 0 && s->rows[r].state != R_FRESH)
+      return fail(PULSE_E_STATE, "mb %d: encoder forward already ran", mb);
+    if (r >= 0) {
+      const Row& row = s->rows[r];
+      if (d.input_skip_slot >= 0 && row.act[d.input_skip_slot])
+        return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb,
+                    d.input_skip_slot);
+      for (auto& b : s->eb)
+        if (b.slot >= 0 && row.act[b.slot])
+          return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb, b.slot);
+    } else {
+      r = free_row(s);
+      if (r < 0)
+        return fail(PULSE_E_CACHE_FULL, "mb %d: %d microbatches already in flight", mb,
+                    d.max_inflight);
+    }
+  } else {
+    if (r < 0) return fail(PULSE_E_STATE, "mb %d: decoder forward before encoder forward", mb);
+    const Row& row = s->rows[r];
+    if (row.state != R_ENC_FWD && row.state != R_FRESH)
+      return fail(PULSE_E_STATE, "mb %d: decoder forward out of order (state %d)", mb, row.state);
+    for (auto& b : s->db)
+      if (!row.act[b.slot])
+        return fail(PULSE_E_CACHE_MISS, "mb %d: skip slot %d absent", mb, b.slot);
+  }
+
+  if (!s->dry) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* row = s->row_base(r);
+    const int dt = s->dtype;
+    if (static_scratch) {
+      s->fwd_base = sbase;
+      s->f_red = s->fs_red;
+      s->f_e = s->fs_e;
+      s->f_kpart = s->fs_kpart;
+      s->f_kcap = s->fs_kcap;
+    } else {
+      s->use_workspace_scratch();
+    }
+    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
+    HIPCHK(hipMemcpyAsync(row + s->row_temb[half == PULSE_DEC ? 1 : 0], temb, (size_t)s->geo.B * s->D * s->esz,
+                          hipMemcpyDeviceToDevice, st));
+    if (half == PULSE_ENC) {
+      void* xin_store = d.input_skip_slot >= 0 ? row + s->row_act[d.input_skip_slot]
+                                               : row + s->row_xin;
+      HIPCHK(hipMemcpyAsync(xin_store, in, act_bytes(s, s->eb[0].cin), hipMemcpyDeviceToDevice,
+                            st));
+      if ((ps = temb_prefetch(s, r, s->eb, 0, st)) != PULSE_OK) return ps;
+      const int n = (int)s->eb.size();
+      int chunks = 0;  // GN1 statistics of the next block's input, from conv2
+      for (int k = 0; k < n; ++k) {
+        const Block& b = s->eb[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        void* o1;
+        void* o2 = nullptr;
+        if (b.slot >= 0) {
+          o1 = row + s->row_act[b.slot];
+          if (k == n - 1) o2 = out;
+        } else {
+          o1 = (k == n - 1) ? out : row + b.out_saved;
+        }
+        // the next encoder block normalises exactly this output
+        const int in_chunks = chunks;
+        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, in_chunks,
+                                k + 1 < n ? &chunks : nullptr, st)) != PULSE_OK)
+          return ps;
+      }
+      (void)dt;
+    } else {
+      HIPCHK(hipMemcpyAsync(row + s->row_u, in, act_bytes(s, s->db[0].c0),
+                            hipMemcpyDeviceToDevice, st));
+      if ((ps = temb_prefetch(s, r, s->db, 1, st)) != PULSE_OK) return ps;
+      const int n = (int)s->db.size();
+      for (int k = 0; k < n; ++k) {
+        const Block& b = s->db[k];
+        const VIn xin = block_input(s, r, b, k, nullptr);
+        void* o1 = (k == n - 1) ? out : row + b.out_saved;
+        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, 0, nullptr,
+                                st)) != PULSE_OK)
+          return ps;
+      }
+    }
+    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
+  }
+
+  Row& row = s->rows[r];
+  if (half == PULSE_ENC) {
+    row.mb = mb;
+    row.state = R_ENC_FWD;
+    row.enc_done = true;
+    if (d.input_skip_slot >= 0) row.act[d.input_skip_slot] = 1;
+    for (auto& b : s->eb)
+      if (b.slot >= 0) row.act[b.slot] = 1;
+  } else {
+    row.state = R_DEC_FWD;
+  }
+  return PULSE_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* pulse_last_error(void) { return g_err.c_str(); }
@@ -1260,107 +1450,13 @@ pulse_status pulse_stage_sync_params(pulse_stage* s, void* stream) {
 
 pulse_status pulse_stage_forward(pulse_stage* s, pulse_half half, int32_t mb, const void* in,
                                  const void* temb, void* out, void* stream) {
-  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
-  if (half != PULSE_ENC && half != PULSE_DEC) return fail(PULSE_E_INVALID_ARG, "bad half");
-  if (mb < 0) return fail(PULSE_E_INVALID_ARG, "mb must be >= 0");
-  pulse_status ps;
-  if (!s->dry) {
-    if ((ps = need_bound(s)) != PULSE_OK) return ps;
-    if ((ps = check_ptr(in, "in")) != PULSE_OK || (ps = check_ptr(temb, "temb")) != PULSE_OK ||
-        (ps = check_ptr(out, "out")) != PULSE_OK)
-      return ps;
-  }
-  int r = find_row(s, mb);
-  const pulse_stage_desc& d = s->d;
-  if (half == PULSE_ENC) {
-    if (r >= 0 && s->rows[r].state != R_FRESH)
-      return fail(PULSE_E_STATE, "mb %d: encoder forward already ran", mb);
-    if (r >= 0) {
-      const Row& row = s->rows[r];
-      if (d.input_skip_slot >= 0 && row.act[d.input_skip_slot])
-        return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb,
-                    d.input_skip_slot);
-      for (auto& b : s->eb)
-        if (b.slot >= 0 && row.act[b.slot])
-          return fail(PULSE_E_CACHE_OCCUPIED, "mb %d slot %d already present", mb, b.slot);
-    } else {
-      r = free_row(s);
-      if (r < 0)
-        return fail(PULSE_E_CACHE_FULL, "mb %d: %d microbatches already in flight", mb,
-                    d.max_inflight);
-    }
-  } else {
-    if (r < 0) return fail(PULSE_E_STATE, "mb %d: decoder forward before encoder forward", mb);
-    const Row& row = s->rows[r];
-    if (row.state != R_ENC_FWD && row.state != R_FRESH)
-      return fail(PULSE_E_STATE, "mb %d: decoder forward out of order (state %d)", mb, row.state);
-    for (auto& b : s->db)
-      if (!row.act[b.slot])
-        return fail(PULSE_E_CACHE_MISS, "mb %d: skip slot %d absent", mb, b.slot);
-  }
+  return forward_impl(s, half, mb, in, temb, out, stream, false);
+}
 
-  if (!s->dry) {
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    char* row = s->row_base(r);
-    const int dt = s->dtype;
-    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
-    HIPCHK(hipMemcpyAsync(row + s->row_temb[half == PULSE_DEC ? 1 : 0], temb, (size_t)s->geo.B * s->D * s->esz,
-                          hipMemcpyDeviceToDevice, st));
-    if (half == PULSE_ENC) {
-      void* xin_store = d.input_skip_slot >= 0 ? row + s->row_act[d.input_skip_slot]
-                                               : row + s->row_xin;
-      HIPCHK(hipMemcpyAsync(xin_store, in, act_bytes(s, s->eb[0].cin), hipMemcpyDeviceToDevice,
-                            st));
-      if ((ps = temb_prefetch(s, r, s->eb, 0, st)) != PULSE_OK) return ps;
-      const int n = (int)s->eb.size();
-      int chunks = 0;  // GN1 statistics of the next block's input, from conv2
-      for (int k = 0; k < n; ++k) {
-        const Block& b = s->eb[k];
-        const VIn xin = block_input(s, r, b, k, nullptr);
-        void* o1;
-        void* o2 = nullptr;
-        if (b.slot >= 0) {
-          o1 = row + s->row_act[b.slot];
-          if (k == n - 1) o2 = out;
-        } else {
-          o1 = (k == n - 1) ? out : row + b.out_saved;
-        }
-        // the next encoder block normalises exactly this output
-        const int in_chunks = chunks;
-        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, in_chunks,
-                                k + 1 < n ? &chunks : nullptr, st)) != PULSE_OK)
-          return ps;
-      }
-      (void)dt;
-    } else {
-      HIPCHK(hipMemcpyAsync(row + s->row_u, in, act_bytes(s, s->db[0].c0),
-                            hipMemcpyDeviceToDevice, st));
-      if ((ps = temb_prefetch(s, r, s->db, 1, st)) != PULSE_OK) return ps;
-      const int n = (int)s->db.size();
-      for (int k = 0; k < n; ++k) {
-        const Block& b = s->db[k];
-        const VIn xin = block_input(s, r, b, k, nullptr);
-        void* o1 = (k == n - 1) ? out : row + b.out_saved;
-        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, 0, nullptr,
-                                st)) != PULSE_OK)
-          return ps;
-      }
-    }
-    if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
-  }
-
-  Row& row = s->rows[r];
-  if (half == PULSE_ENC) {
-    row.mb = mb;
-    row.state = R_ENC_FWD;
-    row.enc_done = true;
-    if (d.input_skip_slot >= 0) row.act[d.input_skip_slot] = 1;
-    for (auto& b : s->eb)
-      if (b.slot >= 0) row.act[b.slot] = 1;
-  } else {
-    row.state = R_DEC_FWD;
-  }
-  return PULSE_OK;
+pulse_status pulse_stage_forward_static(pulse_stage* s, pulse_half half, int32_t mb,
+                                        const void* in, const void* temb, void* out,
+                                        void* stream) {
+  return forward_impl(s, half, mb, in, temb, out, stream, true);
 }
 
 pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, const void* dout,
@@ -1401,6 +1497,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     hipStream_t st = static_cast<hipStream_t>(stream);
     char* row = s->row_base(r);
     const int dt = s->dtype;
+    s->use_workspace_scratch();
     if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
     int cur = 0;
     BwdSync sy;

@@ -96,6 +96,8 @@ def lib():
         L.pulse_stage_sync_params.restype = st
         L.pulse_stage_forward.argtypes = [_vp, ctypes.c_int, _i32, _vp, _vp, _vp, _vp]
         L.pulse_stage_forward.restype = st
+        L.pulse_stage_forward_static.argtypes = [_vp, ctypes.c_int, _i32, _vp, _vp, _vp, _vp]
+        L.pulse_stage_forward_static.restype = st
         L.pulse_stage_backward.argtypes = [_vp, ctypes.c_int, _i32, _vp, _vp, _vp, _vp]
         L.pulse_stage_backward.restype = st
         L.pulse_skip_cache_put.argtypes = [_vp, _i32, _i32, _vp, _vp]
@@ -261,6 +263,19 @@ class Stage:
             out = self.act(C)
         _check(lib().pulse_stage_forward(self.h, half, mb, _ptr(inp), _ptr(temb), _ptr(out),
                                          _stream_handle(stream)))
+        return out
+
+    def forward_static(self, half, mb, inp, temb, out=None, stream=None):
+        """pulse_stage_forward_static: the forward with its scratch in the
+        library's static device array (no allocation of any kind)."""
+        if self.dry:
+            _check(lib().pulse_stage_forward_static(self.h, half, mb, None, None, None, None))
+            return None
+        if out is None:
+            C = self.desc["enc"][-1]["c_out"] if half == ENC else self.desc["dec"][-1]["c_out"]
+            out = self.act(C)
+        _check(lib().pulse_stage_forward_static(self.h, half, mb, _ptr(inp), _ptr(temb),
+                                                _ptr(out), _stream_handle(stream)))
         return out
 
     def backward(self, half, mb, dout, din=None, dtemb=None, stream=None):

@@ -223,3 +223,15 @@ def test_weight_bytes_limit(dtype, ok):
         _dry(d)
     else:
         _expect_status(lambda: _dry(d), S.E_SHAPE)
+
+
+def test_forward_static_scratch_limit():
+    """The static-scratch forward takes stages whose forward scratch fits the
+    library's array (the 64x64x320 stage at batch 8) and refuses larger ones
+    (16x16x1280 at batch 16) before doing anything."""
+    st = _dry(configs.l64())
+    st.forward_static(S.ENC, 0, None, None)
+    st.forward_static(S.DEC, 0, None, None)
+    big = _dry(configs.l16())
+    _expect_status(lambda: big.forward_static(S.ENC, 0, None, None), S.E_SHAPE)
+    assert big.inflight() == 0
