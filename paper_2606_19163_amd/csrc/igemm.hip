@@ -277,7 +277,7 @@ __global__ __launch_bounds__(C::NT) void igemm_conv(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
@@ -438,7 +438,7 @@ __global__ __launch_bounds__(C::NT) void igemm_wgrad(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 

@@ -300,7 +300,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[C::STAGES * C::STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
@@ -667,7 +667,7 @@ __global__ __launch_bounds__(512) void igemm_halo_conv(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
   const int H = a.g.H, W = a.g.W, HW = H * W;
@@ -914,7 +914,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 

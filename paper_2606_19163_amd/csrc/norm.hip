@@ -199,12 +199,29 @@ __global__ __launch_bounds__(256) void k_gn_stats_finalize(const float* partial,
   const int b = blockIdx.x, gi = blockIdx.y;
   const int cg = C / G;
   double S = 0.0, Q = 0.0;
-  for (int i = threadIdx.x; i < rg.chunks * cg; i += 256) {
-    const int ch = i / cg;
-    const int c = gi * cg + (i - ch * cg);
-    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
-    S += base[c];
-    Q += base[C + c];
+  // NB loads in flight per thread, added in ascending i
+  constexpr int NB = 8;
+  const int n = rg.chunks * cg;
+  for (int i0 = threadIdx.x; i0 < n; i0 += NB * 256) {
+    float s[NB], q[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const int i = i0 + k * 256;
+      s[k] = q[k] = 0.f;
+      if (i < n) {
+        const int ch = i / cg;
+        const int c = gi * cg + (i - ch * cg);
+        const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+        s[k] = base[c];
+        q[k] = base[C + c];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k)
+      if (i0 + k * 256 < n) {
+        S += s[k];
+        Q += q[k];
+      }
   }
   block_sum2(S, Q, sm);
   const double cnt = (double)g.hw() * cg;
@@ -412,19 +429,22 @@ __device__ __forceinline__ void chan_totals_block(const float* partial, int rows
   if (c < C) {
     const long stride = 2L * C;
     const float* base = partial + c;
-    int i = ty;
-    for (; i + TY < rows; i += 2 * TY) {
-      const float a0 = base[i * stride], a1 = base[(i + TY) * stride];
-      const float e0 = nslot > 1 ? base[i * stride + C] : 0.f;
-      const float e1 = nslot > 1 ? base[(i + TY) * stride + C] : 0.f;
-      s0 += a0;
-      s0 += a1;
-      s1 += e0;
-      s1 += e1;
-    }
-    for (; i < rows; i += TY) {
-      s0 += base[i * stride];
-      if (nslot > 1) s1 += base[i * stride + C];
+    // NB rows in flight per lane, added in ascending row order
+    constexpr int NB = 16;
+    for (int i0 = ty; i0 < rows; i0 += NB * TY) {
+      float a[NB], e[NB];
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int i = i0 + k * TY;
+        a[k] = i < rows ? base[(long)i * stride] : 0.f;
+        e[k] = (nslot > 1 && i < rows) ? base[(long)i * stride + C] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < NB; ++k)
+        if (i0 + k * TY < rows) {
+          s0 += a[k];
+          s1 += e[k];
+        }
     }
   }
   sm[0][ty][tx] = s0;
@@ -487,12 +507,29 @@ __global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, 
   const int b = q / G, gi = q - b * G;
   const int cg = C / G;
   double S1 = 0.0, S2 = 0.0;
-  for (int i = threadIdx.x; i < rg.chunks * cg; i += 1024) {
-    const int ch = i / cg;
-    const int c = gi * cg + (i - ch * cg);
-    const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
-    S1 += (double)gamma[c] * base[c];
-    S2 += (double)gamma[c] * base[C + c];
+  constexpr int NB = 4;  // loads in flight per thread, added in ascending i
+  const int n = rg.chunks * cg;
+  for (int i0 = threadIdx.x; i0 < n; i0 += NB * 1024) {
+    float ga[NB], p1[NB], p2[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const int i = i0 + k * 1024;
+      ga[k] = p1[k] = p2[k] = 0.f;
+      if (i < n) {
+        const int ch = i / cg;
+        const int c = gi * cg + (i - ch * cg);
+        const float* base = partial + ((long)b * rg.chunks + ch) * 2 * C;
+        ga[k] = gamma[c];
+        p1[k] = base[c];
+        p2[k] = base[C + c];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k)
+      if (i0 + k * 1024 < n) {
+        S1 += (double)ga[k] * p1[k];
+        S2 += (double)ga[k] * p2[k];
+      }
   }
   block_sum2_1k(S1, S2, sm);
   if (threadIdx.x == 0) {
