@@ -630,13 +630,6 @@ __global__ void wgrad_finalize(GemmArgs a, int splits) {
 // ---------------------------------------------------------------------------
 
 // Tile shapes.  bf16 with 64 channels per K-step unless noted.
-using T128x128 = Cfg<128, 128, 64, 64, 64, false>;    // 4 waves of 64x64
-using T128x160 = Cfg<128, 160, 64, 64, 80, false>;    // 4 waves of 64x80
-using T256x160 = Cfg<256, 160, 64, 64, 80, false>;    // 8 waves of 64x80
-using T256x128 = Cfg<256, 128, 64, 64, 64, false>;    // 8 waves of 64x64
-using T128x320 = Cfg<128, 320, 64, 64, 80, false>;    // 8 waves of 64x80
-using T320x160 = Cfg<320, 160, 64, 80, 80, false>;    // 8 waves of 80x80
-using T160x160 = Cfg<160, 160, 64, 80, 80, false>;    // 4 waves of 80x80
 using T128x128K32 = Cfg<128, 128, 32, 64, 64, false>; // channel counts % 64 != 0
 using T64x64F32 = Cfg<64, 64, 32, 32, 32, true>;      // the fp32 stage
 
@@ -675,45 +668,16 @@ static TileInfo info_t() {
 }
 
 TileInfo tile_info(int t) {
-  switch (t) {
-    case TILE_128x128: return info_t<T128x128>();
-    case TILE_128x160: return info_t<T128x160>();
-    case TILE_256x160: return info_t<T256x160>();
-    case TILE_256x128: return info_t<T256x128>();
-    case TILE_128x320: return info_t<T128x320>();
-    case TILE_320x160: return info_t<T320x160>();
-    case TILE_160x160: return info_t<T160x160>();
-    case TILE_128x128_K32: return info_t<T128x128K32>();
-    default: return info_t<T64x64F32>();
-  }
+  return t == TILE_64x64_F32 ? info_t<T64x64F32>() : info_t<T128x128K32>();
 }
 
 hipError_t launch_conv(const GemmArgs& a, int t, hipStream_t st) {
-  switch (t) {
-    case TILE_128x128: return launch_conv_t<T128x128>(a, st);
-    case TILE_128x160: return launch_conv_t<T128x160>(a, st);
-    case TILE_256x160: return launch_conv_t<T256x160>(a, st);
-    case TILE_256x128: return launch_conv_t<T256x128>(a, st);
-    case TILE_128x320: return launch_conv_t<T128x320>(a, st);
-    case TILE_320x160: return launch_conv_t<T320x160>(a, st);
-    case TILE_160x160: return launch_conv_t<T160x160>(a, st);
-    case TILE_128x128_K32: return launch_conv_t<T128x128K32>(a, st);
-    default: return launch_conv_t<T64x64F32>(a, st);
-  }
+  return t == TILE_64x64_F32 ? launch_conv_t<T64x64F32>(a, st) : launch_conv_t<T128x128K32>(a, st);
 }
 
 hipError_t launch_wgrad(const GemmArgs& a, int t, int splits, hipStream_t st) {
-  switch (t) {
-    case TILE_128x128: return launch_wgrad_t<T128x128>(a, splits, st);
-    case TILE_128x160: return launch_wgrad_t<T128x160>(a, splits, st);
-    case TILE_256x160: return launch_wgrad_t<T256x160>(a, splits, st);
-    case TILE_256x128: return launch_wgrad_t<T256x128>(a, splits, st);
-    case TILE_128x320: return launch_wgrad_t<T128x320>(a, splits, st);
-    case TILE_320x160: return launch_wgrad_t<T320x160>(a, splits, st);
-    case TILE_160x160: return launch_wgrad_t<T160x160>(a, splits, st);
-    case TILE_128x128_K32: return launch_wgrad_t<T128x128K32>(a, splits, st);
-    default: return launch_wgrad_t<T64x64F32>(a, splits, st);
-  }
+  return t == TILE_64x64_F32 ? launch_wgrad_t<T64x64F32>(a, splits, st)
+                             : launch_wgrad_t<T128x128K32>(a, splits, st);
 }
 
 }  // namespace pulse

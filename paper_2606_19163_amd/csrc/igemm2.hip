@@ -51,10 +51,6 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// 128-byte rows of 8 chunks: chunk c of row r lives in slot c ^ swz(r).
-// Rows r and r+1 fall in opposite halves of a 256-byte bank period, so the
-// swizzle only has to separate rows of equal parity.
-__device__ __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
 
 }  // namespace
 
@@ -252,10 +248,6 @@ __device__ __forceinline__ SegRt seg_rt(const Seg& g, long P) {
   s.taps = g.taps;
   s.begin = g.begin;
   return s;
-}
-
-__device__ __forceinline__ SegRt pick(int s, const SegRt& a, const SegRt& b, const SegRt& c) {
-  return s == 0 ? a : (s == 1 ? b : c);
 }
 
 // field-wise select (a select of whole structs can end up in scratch memory)
@@ -600,312 +592,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// CONV mode with halo reuse
-// ---------------------------------------------------------------------------
-// A block owns 256 pixels = 256 / W whole rows of one image and 160 output
-// channels (8 waves of 64 x 80).  For each 64-channel chunk of the input it
-// loads the chunk's (rows + 2) x (W + 2) halo into LDS once -- zero outside
-// the image -- and runs every tap of that chunk from it, so only the weight
-// tile is loaded per tap.  Halo rows are 128 bytes (one pixel's 64 channels)
-// with the conv tiles' chunk swizzle.  The next chunk's halo goes out three
-// taps before the chunk ends (one tap before, for a 1x1 segment) into the
-// other halo buffer; weight tiles are double-buffered per tap.
-
-struct CfgH {
-  static constexpr int BM = 256, BN = 160, WM = 64, WN = 80;
-  static constexpr int WAVES_M = 4, WAVES_N = 2, NW = 8, NT = 512;
-  static constexpr int TM = 4, TN = 5;
-  static constexpr int HALO_MAX = 53248;             // bytes of one halo buffer
-  static constexpr int W_BYTES = BN * 128;            // weight tile of one tap
-  static constexpr int WLB = W_BYTES / 1024;          // its 1 KB wave loads (20)
-  static constexpr int NUB = (WLB + NW - 1) / NW;     // per wave (3 or 2)
-  static constexpr int HL_MAX = HALO_MAX / 1024;      // halo wave loads (<= 52)
-  static constexpr int NUH = (HL_MAX + NW - 1) / NW;  // per wave (<= 7)
-  static constexpr int LDC = BN + 4;
-  static constexpr int LDS_BYTES = 2 * HALO_MAX + 2 * W_BYTES;
-  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
-  static_assert(16 * LDC * 4 <= LDS_BYTES, "epilogue slice");
-};
-
-// Source of one 64-channel chunk of the K walk: segment fields, channel
-// offset within the segment and the segment's tap count.
-struct ChunkRt {
-  __amdgpu_buffer_rsrc_t rs;
-  uint32_t pitch, cbyte;  // source row pitch, byte offset of the chunk in a row
-  int taps;
-  int kcol;               // weight column of tap 0 of this chunk: begin + cb
-  int C;                  // segment channels (weight column step per tap)
-};
-
-__device__ __forceinline__ ChunkRt chunk_rt(int ci, const SegRt& q0, const SegRt& q1,
-                                            const SegRt& q2, int nseg) {
-  SegRt q = q0;
-  int c = ci;
-  if (nseg > 1 && c >= q0.C / 64) {
-    c -= q0.C / 64;
-    select_into(q, true, q1, q2);
-    if (nseg > 2 && c >= q1.C / 64) {
-      c -= q1.C / 64;
-      select_into(q, false, q1, q2);
-    }
-  }
-  const int cb = c * 64;
-  const bool second = cb >= q.c0;
-  ChunkRt r;
-  r.rs = second ? q.r1 : q.r0;
-  r.pitch = second ? q.pitch1 : q.pitch0;
-  r.cbyte = (uint32_t)((second ? cb - q.c0 : cb) * 2);
-  r.taps = q.taps;
-  r.kcol = q.begin + cb;
-  r.C = q.C;
-  return r;
-}
-
-__global__ __launch_bounds__(512) void igemm_halo_conv(GemmArgs a) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  using C = CfgH;
-  __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
-  const int wm = wave % C::WAVES_M;
-  const int wn = wave / C::WAVES_M;
-  const int H = a.g.H, W = a.g.W, HW = H * W;
-  const long P = a.g.pixels();
-  const int R = C::BM / W;            // image rows per tile
-  const int W2 = W + 2;
-  const int HPIX = (R + 2) * W2;      // halo pixels
-  const int HLOADS = (HPIX * 128 + 1023) / 1024;
-
-  const int tilesN = a.N / C::BN;
-  const int lb = xcd_remap(blockIdx.x, gridDim.x);
-  const int tn = lb % tilesN;
-  const int tm = lb / tilesN;
-  const long m0 = (long)tm * C::BM;
-  const int n0 = tn * C::BN;
-  const int img = (int)(m0 / HW);
-  const int row0 = (int)(m0 - (long)img * HW) / W;
-
-  // halo loads of this lane: wave load wl = wave + u*NW; slot q = wl*64 + lane
-  // is physical chunk q % 8 of halo pixel q / 8 and fetches logical chunk
-  // (q % 8) ^ swz(pixel)
-  int hpix[C::NUH];
-  uint32_t hcb[C::NUH];
-  int nh = 0;  // halo loads this wave issues
-#pragma unroll
-  for (int u = 0; u < C::NUH; ++u) {
-    const int wl = wave + u * C::NW;
-    const int hp = (wl * 64 + lane) >> 3;
-    hpix[u] = -1;
-    hcb[u] = (uint32_t)(((lane & 7) ^ swz128(hp)) * 16);
-    if (wl < HLOADS) {
-      ++nh;
-      if (hp < HPIX) {
-        const int hr = hp / W2, hc = hp - hr * W2;
-        const int r = row0 + hr - 1, c = hc - 1;
-        if (r >= 0 && r < H && c >= 0 && c < W) hpix[u] = img * HW + r * W + c;
-      }
-    }
-  }
-  // weight loads: wave load wl = wave + u*NW < WLB, row r = wl*8 + lane/8
-  uint32_t wco[C::NUB];
-#pragma unroll
-  for (int u = 0; u < C::NUB; ++u) {
-    const int wl = wave + u * C::NW;
-    const int r = wl * 8 + (lane >> 3);
-    wco[u] = (uint32_t)((long)(n0 + r) * a.ldb * 2 + ((lane & 7) ^ swz128(r)) * 16);
-  }
-
-  const SegRt q0 = seg_rt(a.seg[0], P);
-  const SegRt q1 = seg_rt(a.seg[1], P);
-  const SegRt q2 = seg_rt(a.seg[2], P);
-  const int nseg = a.nseg;
-  int NC = q0.C / 64;
-  if (nseg > 1) NC += q1.C / 64;
-  if (nseg > 2) NC += q2.C / 64;
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.Bw, (long)a.N * a.ldb * 2);
-  const uint32_t sbase = lds_u32(smem);
-  const uint32_t hbuf0 = sbase, wbuf0 = sbase + 2 * C::HALO_MAX;
-
-  auto issue_halo = [&](const ChunkRt& ck, int slot) __attribute__((always_inline)) {
-    char* dst = smem + slot * C::HALO_MAX;
-#pragma unroll
-    for (int u = 0; u < C::NUH; ++u) {
-      const int wl = wave + u * C::NW;
-      if (wl < HLOADS) {
-        const uint32_t off =
-            hpix[u] >= 0 ? __umul24((uint32_t)hpix[u], ck.pitch) + ck.cbyte + hcb[u] : OOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ck.rs, lds(dst + wl * 1024), 16, off, 0, 0, 0);
-      }
-    }
-  };
-  auto issue_w = [&](int kcol, int slot) __attribute__((always_inline)) {
-    char* dst = smem + 2 * C::HALO_MAX + slot * C::W_BYTES;
-    const uint32_t kb = (uint32_t)(kcol * 2);
-#pragma unroll
-    for (int u = 0; u < C::NUB; ++u) {
-      const int wl = wave + u * C::NW;
-      if (wl < C::WLB)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds(dst + wl * 1024), 16, wco[u] + kb, 0, 0,
-                                                 0);
-    }
-  };
-
-  f32x4_t acc[C::TM][C::TN];
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  // A fragment rows: pixel p = wm*64 + i*16 + r16 of the tile, halo index of
-  // its centre tap (lr + 1) * (W + 2) + col + 1
-  const int r16 = lane & 15;
-  const int g4 = lane >> 4;
-  int hc0[C::TM];
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
-    const int p = wm * C::WM + i * 16 + r16;
-    const int lr = p / W, col = p - lr * W;
-    hc0[i] = (lr + 1) * W2 + col + 1;
-  }
-  uint32_t fb[2];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int c = s * 4 + g4;
-    const int rb = wn * C::WN + r16;
-    fb[s] = (uint32_t)(rb * 128 + ((c ^ swz128(rb)) << 4));
-  }
-
-  bf16x8_t af[2][C::TM], bfr[2][C::TN];
-  ChunkRt ck = chunk_rt(0, q0, q1, q2, nseg);
-  issue_halo(ck, 0);
-  issue_w(ck.kcol, 0);
-  int step = 0;
-  bool halo_after_w = false;  // the last step issued a halo after its weight tile
-  for (int ci = 0; ci < NC; ++ci) {
-    const bool has_next = ci + 1 < NC;
-    ChunkRt nx = ck;
-    if (has_next) nx = chunk_rt(ci + 1, q0, q1, q2, nseg);
-    const int ntaps = ck.taps;
-    const int h_at = ntaps > 3 ? ntaps - 3 : 0;  // tap that sends the next halo
-    const uint32_t hb = hbuf0 + (uint32_t)((ci & 1) * C::HALO_MAX);
-    for (int t = 0; t < ntaps; ++t) {
-      // this step's weight tile (and, at a chunk's first tap, its halo)
-      if (t > 0 && halo_after_w) {
-        if (nh == 7) wait_vmcnt<7>();
-        else if (nh == 6) wait_vmcnt<6>();
-        else if (nh == 5) wait_vmcnt<5>();
-        else if (nh == 4) wait_vmcnt<4>();
-        else if (nh == 3) wait_vmcnt<3>();
-        else if (nh == 2) wait_vmcnt<2>();
-        else if (nh == 1) wait_vmcnt<1>();
-        else wait_vmcnt<0>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      __builtin_amdgcn_s_barrier();
-      // next weight tile into the slot read one step ago
-      if (t + 1 < ntaps)
-        issue_w(ck.kcol + (t + 1) * ck.C, (step + 1) & 1);
-      else if (has_next)
-        issue_w(nx.kcol, (step + 1) & 1);
-      halo_after_w = false;
-      if (has_next && t == h_at) {
-        issue_halo(nx, (ci + 1) & 1);
-        halo_after_w = true;
-      }
-      const int tap = ntaps == 9 ? t : 4;
-      const int sh = (tap / 3 - 1) * W2 + (tap % 3 - 1);
-      const uint32_t wb = wbuf0 + (uint32_t)((step & 1) * C::W_BYTES);
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int c = s * 4 + g4;
-#pragma unroll
-        for (int i = 0; i < C::TM; ++i) {
-          const int hi = hc0[i] + sh;
-          af[s][i] = ds_rd128<0>(hb + (uint32_t)(hi * 128 + ((c ^ swz128(hi)) << 4)));
-        }
-        ds_rd_n<C::TN, 2048, 0>(bfr[s], wb + fb[s]);
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        // keep the first half's MFMAs above the second half's wait
-        __builtin_amdgcn_sched_barrier(0);
-        if (s == 0)
-          lgkm_wait<C::TM + C::TN>();
-        else
-          lgkm_wait<0>();
-#pragma unroll
-        for (int i = 0; i < C::TM; ++i) tie(af[s][i]);
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j) tie(bfr[s][j]);
-#pragma unroll
-        for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < C::TN; ++j)
-            acc[i][j] =
-                __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      ++step;
-    }
-    ck = nx;
-  }
-  __syncthreads();
-
-  // epilogue in 16-row slices: accumulators -> LDS -> 8-channel rows
-  // (+bias, +rowvec, +residual) -> 16-byte stores
-  float* ct = reinterpret_cast<float*>(smem);
-  constexpr int NV8 = C::BN / 8;
-#pragma unroll 1
-  for (int g = 0; g < C::WAVES_M; ++g) {
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i) {
-      if (wm == g) acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct, wn, lane, i, acc);
-      __syncthreads();
-      for (int e = tid; e < 16 * NV8; e += C::NT) {
-        const int row = e / NV8;
-        const int n = n0 + (e - row * NV8) * 8;
-        const long m = m0 + g * C::WM + i * 16 + row;
-        const float* src = ct + row * C::LDC + (n - n0);
-        const float4 s0 = reinterpret_cast<const float4*>(src)[0];
-        const float4 s1 = reinterpret_cast<const float4*>(src)[1];
-        float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-        if (a.bias) {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
-        }
-        if (a.rowvec) {
-          const float* rv = a.rowvec + (long)img * a.N + n;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += rv[q];
-        }
-        if (a.resid.s0.ptr) {
-          float rr[8];
-          ld8(a.resid.s0, m, n, rr);
-#pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += rr[q];
-        }
-        st8(a.out, a.out_dtype, a.ldo, m, n, v);
-        if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
-      }
-      __syncthreads();
-    }
-  }
-#else
-  (void)a;
-#endif
-}
-
-// ---------------------------------------------------------------------------
 // WGRAD mode
 // ---------------------------------------------------------------------------
-
-// Balanced weight-gradient split: block b of nb owns units [b U / nb,
-// (b + 1) U / nb) of the U = tiles x K-steps units; the block owning unit v.
-__host__ __device__ __forceinline__ int sk_block_of(long v, long U, int nb) {
-  return (int)(((v + 1) * nb - 1) / U);
-}
 
 template <class C>
 __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* zero16) {
@@ -918,43 +606,18 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   const int wm = wave % C::WAVES_M;
   const int wn = wave / C::WAVES_M;
 
-  // Work of this block, as segments (tile, pixel range, partial slot z).
-  // Uniform splits: block -> (split z, tile), split-major over a contiguous
-  // range per XCD, so the blocks of one pixel split share that XCD's L2; one
-  // segment of kchunk pixels.  Balanced (a.sk_blocks > 0): the tiles' K-steps
-  // in tile-major order are dealt out as equal contiguous ranges, one per
-  // block; a range may end in one tile and continue in the next, and the
-  // i-th block touching a tile writes partial slot i (sk_plan).
+  // block -> (pixel split z, tile), split-major over a contiguous range per
+  // XCD, so the blocks of one pixel split share that XCD's L2; split z
+  // covers kchunk pixels
   const int tilesN = (a.N + C::BN - 1) / C::BN;
   const int ntiles = ((a.M + C::BM - 1) / C::BM) * tilesN;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
   const long P = a.g.pixels();
-  const long KTT = (P + C::BK - 1) / C::BK;  // K-steps of a whole tile
-  const long U = (long)ntiles * KTT;
-  long u = 0, uend = 0;
-  if (a.sk_blocks > 0) {
-    u = (long)lb * U / a.sk_blocks;
-    uend = (long)(lb + 1) * U / a.sk_blocks;
-  }
-  for (;;) {
-  int tile, z;
-  long pbeg, pend, kdone = 0;
-  if (a.sk_blocks > 0) {
-    if (u >= uend) break;
-    tile = (int)(u / KTT);
-    const long k0 = u - (long)tile * KTT;
-    const long k1 = k0 + (uend - u) < KTT ? k0 + (uend - u) : KTT;
-    kdone = k1 - k0;
-    pbeg = k0 * C::BK;
-    pend = k1 * C::BK < P ? k1 * C::BK : P;
-    z = lb - sk_block_of((long)tile * KTT, U, a.sk_blocks);
-  } else {
-    z = lb / ntiles;
-    tile = lb - z * ntiles;
-    pbeg = (long)z * a.kchunk;
-    pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
-  }
+  const int z = lb / ntiles;
+  const int tile = lb - z * ntiles;
+  const long pbeg = (long)z * a.kchunk;
+  const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
   const int m0 = (tile / tilesN) * C::BM;
   const int n0 = (tile % tilesN) * C::BN;
 
@@ -1151,9 +814,6 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
       __syncthreads();
     }
   }
-  if (a.sk_blocks <= 0) break;
-  u += kdone;  // the LDS stages are free again: the epilogue ended in a barrier
-  }
 #else
   (void)a;
   (void)zero16;
@@ -1214,23 +874,12 @@ __global__ __launch_bounds__(256) void conv_splitk_finalize(GemmArgs a) {
 // ---------------------------------------------------------------------------
 
 namespace launch2 {
-using C2_128x320 = CfgC<128, 320, 64, 80>;   // 8 waves
-using C2_128x160 = CfgC<128, 160, 64, 80>;   // 4 waves
-using C2_128x128 = CfgC<128, 128, 64, 64>;   // 4 waves
-using C2_256x128 = CfgC<256, 128, 64, 64>;   // 8 waves
-using C2_256x160S3 = CfgC<256, 160, 64, 80, 3>;  // 8 waves, 3 stages
-using C2_128x160S3 = CfgC<128, 160, 64, 80, 3>;  // 4 waves, 3 stages
-using C2_128x160K32 = CfgC<128, 160, 64, 80, 4, 32>;  // 4 waves, 4 stages of 32 channels
-using C2_128x192 = CfgC<128, 192, 64, 96>;   // 4 waves
-using C2_64x128 = CfgC<64, 128, 32, 64>;     // 4 waves
-using C2_128x64 = CfgC<128, 64, 64, 32>;     // 4 waves
-using C2_64x128S3 = CfgC<64, 128, 32, 64, 3>;      // 4 waves, 3 stages
-using C2_64x128S4 = CfgC<64, 128, 32, 64, 4>;      // 4 waves, 4 stages
-using C2_64x128K32 = CfgC<64, 128, 32, 64, 4, 32>;  // 4 waves, 4 stages of 32 channels
-using W2_320x192 = CfgW<320, 192, 80, 96>;   // 8 waves
-using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves
+using C2_128x160 = CfgC<128, 160, 64, 80>;   // 4 waves, two blocks per CU
+using C2_128x128 = CfgC<128, 128, 64, 64>;   // 4 waves, two blocks per CU
+using C2_128x192 = CfgC<128, 192, 64, 96>;   // 4 waves, two blocks per CU
+using C2_64x128S3 = CfgC<64, 128, 32, 64, 3>;  // 4 waves, 3 stages, two blocks per CU
+using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves, one block per CU
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
-using W2_160x128 = CfgW<160, 128, 80, 64>;   // 4 waves
 
 template <class C>
 static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
@@ -1253,7 +902,7 @@ template <class C>
 static hipError_t wgrad2_t(const GemmArgs& a, int splits, const void* zero16, hipStream_t st) {
   const long tilesM = (a.M + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
-  const long blocks = a.sk_blocks > 0 ? a.sk_blocks : tilesM * tilesN * splits;
+  const long blocks = tilesM * tilesN * splits;
   hipLaunchKernelGGL(igemm2_wgrad<C>, dim3((unsigned)blocks), dim3(C::NT), 0, st, a, zero16);
   return hipGetLastError();
 }
@@ -1268,112 +917,32 @@ using namespace launch2;
 
 TileInfo tile2_info(int t) {
   switch (t) {
-    case TILE2_C128x320: return info2<C2_128x320>();
     case TILE2_C128x160: return info2<C2_128x160>();
     case TILE2_C128x128: return info2<C2_128x128>();
-    case TILE2_C256x128: return info2<C2_256x128>();
-    case TILE2_C256x160S3: return info2<C2_256x160S3>();
-    case TILE2_C128x160S3: return info2<C2_128x160S3>();
-    case TILE2_C128x160K32S4: return info2<C2_128x160K32>();
     case TILE2_C128x192: return info2<C2_128x192>();
-    case TILE2_C64x128: return info2<C2_64x128>();
-    case TILE2_C128x64: return info2<C2_128x64>();
     case TILE2_C64x128S3: return info2<C2_64x128S3>();
-    case TILE2_C64x128S4: return info2<C2_64x128S4>();
-    case TILE2_C64x128K32S4: return info2<C2_64x128K32>();
-    case TILE2_W320x192: return info2<W2_320x192>();
     case TILE2_W320x128: return info2<W2_320x128>();
-    case TILE2_W160x128: return info2<W2_160x128>();
     default: return info2<W2_128x128>();
   }
 }
 
 hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
   switch (t) {
-    case TILE2_C128x320: return conv2_t<C2_128x320>(a, st);
     case TILE2_C128x160: return conv2_t<C2_128x160>(a, st);
-    case TILE2_C256x128: return conv2_t<C2_256x128>(a, st);
-    case TILE2_C256x160S3: return conv2_t<C2_256x160S3>(a, st);
-    case TILE2_C128x160S3: return conv2_t<C2_128x160S3>(a, st);
-    case TILE2_C128x160K32S4: return conv2_t<C2_128x160K32>(a, st);
     case TILE2_C128x192: return conv2_t<C2_128x192>(a, st);
-    case TILE2_C64x128: return conv2_t<C2_64x128>(a, st);
-    case TILE2_C128x64: return conv2_t<C2_128x64>(a, st);
     case TILE2_C64x128S3: return conv2_t<C2_64x128S3>(a, st);
-    case TILE2_C64x128S4: return conv2_t<C2_64x128S4>(a, st);
-    case TILE2_C64x128K32S4: return conv2_t<C2_64x128K32>(a, st);
     default: return conv2_t<C2_128x128>(a, st);
   }
-}
-
-bool halo_conv_fits(const Geo& g, int N) {
-  if (N % CfgH::BN != 0 || g.W % 16 != 0 || CfgH::BM % g.W != 0) return false;
-  if (g.hw() % CfgH::BM != 0 || g.pixels() >= (1L << 24)) return false;
-  const int rows = CfgH::BM / g.W;
-  const int bytes = (rows + 2) * (g.W + 2) * 128;
-  return (bytes + 1023) / 1024 * 1024 <= CfgH::HALO_MAX;
-}
-
-hipError_t launch_conv_halo(const GemmArgs& a, hipStream_t st) {
-  const long tiles = (a.g.pixels() / CfgH::BM) * (a.N / CfgH::BN);
-  hipLaunchKernelGGL(igemm_halo_conv, dim3((unsigned)tiles), dim3(CfgH::NT), 0, st, a);
-  return hipGetLastError();
-}
-
-// Balanced-split finalize: every element of tile t sums the partial slots
-// of the blocks that touched t, in slot order, into the gradient.  Four
-// consecutive columns per thread.
-__global__ void wgrad_finalize_sk(GemmArgs a, int bm, int bn, long KTT) {
-  const long idx = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (idx >= (long)a.M * a.N) return;
-  const int m = (int)(idx / a.N);
-  const int n = (int)(idx - (long)m * a.N);
-  const int tilesN = (a.N + bn - 1) / bn;
-  const long ntiles = (long)((a.M + bm - 1) / bm) * tilesN;
-  const long U = ntiles * KTT;
-  const long tile = (long)(m / bm) * tilesN + n / bn;
-  const int cnt = sk_block_of((tile + 1) * KTT - 1, U, a.sk_blocks) -
-                  sk_block_of(tile * KTT, U, a.sk_blocks) + 1;
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int z = 0; z < cnt; ++z) {
-    const float4 v = *reinterpret_cast<const float4*>(a.part + (long)z * a.M * a.N + idx);
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-  }
-  const int si = seg_of(a.nseg, a.seg[1].begin, a.seg[2].begin, n);
-  const Seg& sg = si == 0 ? a.seg[0] : (si == 1 ? a.seg[1] : a.seg[2]);
-  const int len = sg.end - sg.begin;
-  float* g = sg.grad + (long)m * len + (n - sg.begin);
-  g[0] += s.x; g[1] += s.y; g[2] += s.z; g[3] += s.w;
-}
-
-int sk_max_slots(int M, int N, int bm, int bn, long P, int bk, int nb) {
-  const int tilesN = (N + bn - 1) / bn;
-  const long ntiles = (long)((M + bm - 1) / bm) * tilesN;
-  const long KTT = (P + bk - 1) / bk;
-  const long U = ntiles * KTT;
-  int mx = 0;
-  for (long t = 0; t < ntiles; ++t)
-    mx = std::max(mx, sk_block_of((t + 1) * KTT - 1, U, nb) - sk_block_of(t * KTT, U, nb) + 1);
-  return mx;
 }
 
 hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero16,
                          hipStream_t st) {
   hipError_t e;
   switch (t) {
-    case TILE2_W320x192: e = wgrad2_t<W2_320x192>(a, splits, zero16, st); break;
     case TILE2_W320x128: e = wgrad2_t<W2_320x128>(a, splits, zero16, st); break;
-    case TILE2_W160x128: e = wgrad2_t<W2_160x128>(a, splits, zero16, st); break;
     default: e = wgrad2_t<W2_128x128>(a, splits, zero16, st); break;
   }
   if (e != hipSuccess) return e;
-  if (a.sk_blocks > 0) {
-    const TileInfo ti = tile2_info(t);
-    const long total = (long)a.M * a.N / 4;
-    hipLaunchKernelGGL(wgrad_finalize_sk, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
-                       a, ti.bm, ti.bn, (a.g.pixels() + ti.bk - 1) / ti.bk);
-    return hipGetLastError();
-  }
   return launch_wgrad_finalize(a, splits, st);
 }
 

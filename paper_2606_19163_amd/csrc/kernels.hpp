@@ -45,29 +45,18 @@ struct GemmArgs {
   VIn gy;              // output gradient, M channels
   int kchunk;          // pixels per split
   float* part;         // [splits][M][N] fp32 partials (both modes)
-  int sk_blocks;       // WGRAD (LDS-DMA path): > 0 deals the tiles' K-steps out in
-                       // equal ranges to this many blocks (partial slot = the
-                       // block's rank among those touching the tile); 0: uniform
-                       // splits of kchunk pixels
   // CONV mode of the LDS-DMA kernels without a K split, when H*W % BM == 0:
   // per-channel sum and sum of squares of the output as stored (bf16), one
   // row per (image, M-tile): [B][H*W / BM][2][N]; null: not computed
   float* stats;
 };
 
-// implicit GEMM (igemm.hip): tile shapes (block M x block N; bf16, 64
-// channels per K-step unless noted)
+// implicit GEMM, register-staged (igemm.hip): the fp32 stage and bf16
+// channel counts that are multiples of 32 but not of 64
 enum Tile : int {
-  TILE_128x128 = 0,
-  TILE_128x160 = 1,
-  TILE_256x160 = 2,
-  TILE_256x128 = 3,
-  TILE_128x320 = 4,
-  TILE_320x160 = 5,
-  TILE_160x160 = 6,
-  TILE_128x128_K32 = 7,  // bf16, 32 channels per K-step
-  TILE_64x64_F32 = 8,    // fp32, 32 channels per K-step
-  TILE_COUNT = 9
+  TILE_128x128_K32 = 0,  // bf16, 32 channels per K-step
+  TILE_64x64_F32 = 1,    // fp32, 32 channels per K-step
+  TILE_COUNT = 2
 };
 struct TileInfo {
   int bm, bn, bk;
@@ -79,43 +68,22 @@ hipError_t launch_wgrad(const GemmArgs& a, int tile, int splits, hipStream_t st)
 hipError_t launch_wgrad_finalize(const GemmArgs& a, int splits, hipStream_t st);
 
 // second generation (igemm2.hip): LDS-DMA operand loads, bf16 with 64
-// channels per K-step only.  zero16: 16 zero bytes of device memory.
+// channels per K-step.  zero16: 16 zero bytes of device memory.
 enum Tile2 : int {
-  TILE2_C128x320 = 0,
-  TILE2_C128x160 = 1,
-  TILE2_C128x128 = 2,
-  TILE2_C256x128 = 3,
-  TILE2_C256x160S3 = 4,  // three LDS stages, 8 waves, one block per CU
-  TILE2_C128x160S3 = 5,  // three LDS stages, 4 waves, one block per CU
-  TILE2_C128x160K32S4 = 6,  // four LDS stages of 32 channels, two blocks per CU
-  TILE2_C128x192 = 7,       // 4 waves of 64 x 96, two blocks per CU
-  TILE2_C64x128 = 8,        // 4 waves of 32 x 64, three blocks per CU
-  TILE2_C128x64 = 9,        // 4 waves of 64 x 32, three blocks per CU
-  TILE2_C64x128S3 = 10,     // three LDS stages, two blocks per CU
-  TILE2_C64x128S4 = 11,     // four LDS stages, one block per CU
-  TILE2_C64x128K32S4 = 12,  // four LDS stages of 32 channels, three blocks per CU
-  TILE2_CONV_LAST = 12,
-  TILE2_W320x192 = 20,
-  TILE2_W320x128 = 21,
-  TILE2_W128x128 = 22,
-  TILE2_W160x128 = 23,  // 4 waves, two blocks per CU
+  TILE2_C128x160 = 0,   // 4 waves of 64 x 80, two blocks per CU
+  TILE2_C128x128 = 1,   // 4 waves of 64 x 64, two blocks per CU
+  TILE2_C128x192 = 2,   // 4 waves of 64 x 96, two blocks per CU
+  TILE2_C64x128S3 = 3,  // 4 waves of 32 x 64, three LDS stages, two blocks per CU
+  TILE2_CONV_LAST = 3,
+  TILE2_W320x128 = 20,  // 8 waves of 80 x 64, one block per CU
+  TILE2_W128x128 = 21,  // 4 waves of 64 x 64
   TILE2_WGRAD_FIRST = 20,
-  TILE2_WGRAD_LAST = 23
+  TILE2_WGRAD_LAST = 21
 };
 TileInfo tile2_info(int tile);
 hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);
-// conv mode with halo reuse (igemm2.hip): 256-pixel tiles of whole image rows
-// x 160 output channels; every 64-channel input chunk's halo is loaded once
-// for all taps.  Applies when N % 160 == 0, W % 16 == 0, 256 % W == 0,
-// H*W % 256 == 0 and the halo fits 52 KB; no K split.
-bool halo_conv_fits(const Geo& g, int N);
-hipError_t launch_conv_halo(const GemmArgs& a, hipStream_t st);
 hipError_t launch_wgrad2(const GemmArgs& a, int tile, int splits, const void* zero16,
                          hipStream_t st);
-// Largest number of partial slots a tile needs when nb blocks share the
-// K-steps of an M x N weight gradient over P pixels (bm x bn tiles, bk
-// pixels per K-step).
-int sk_max_slots(int M, int N, int bm, int bn, long P, int bk, int nb);
 
 // ---- GroupNorm / reductions (norm.hip) -----------------------------------
 

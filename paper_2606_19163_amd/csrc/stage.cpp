@@ -105,15 +105,6 @@ struct pulse_stage {
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
   int conv_ksplit_cap = 16;  // largest conv K split (env PULSE_CONV_KSPLIT_MAX)
-  int wgrad_balance = 0;     // balanced weight-gradient split: 0 never (default: it
-                             // measured slower, its blocks share no pixel rows in L2),
-                             // 1 when the uniform split idles slots, 2 always
-                             // (env PULSE_WGRAD_BALANCE)
-  // halo-reuse conv: 0 never (default: it measured slower in the full step,
-  // where its 147 KB of LDS keeps the side stream's GEMMs off its CUs), 1
-  // when its grid fills the GPU, 2 whenever it fits
-  int halo = 0;
-  bool v2 = false;      // LDS-DMA GEMM kernels (bf16, 64-channel K-steps)
   Geo geo{};
   long P = 0;
   int G = 1;
@@ -247,11 +238,7 @@ int conv_tile(const pulse_stage* s, int N) {
   if (s->dtype == DT_F32) return TILE_64x64_F32;
   if (!s->k64) return TILE_128x128_K32;
   if (s->conv_tile_force >= 0) return s->conv_tile_force;
-  if (s->v2) {
-    return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128;
-  }
-  if (N % 320 == 0) return TILE_128x320;
-  return N % 160 == 0 ? TILE_256x160 : TILE_128x128;
+  return N % 160 == 0 ? TILE2_C128x160 : TILE2_C128x128;
 }
 
 // Tile shape of a weight-gradient GEMM (M output channels, N columns).
@@ -260,12 +247,11 @@ int wgrad_tile(const pulse_stage* s, int M, int N) {
   if (!s->k64) return TILE_128x128_K32;
   if (s->wgrad_tile_force >= 0) return s->wgrad_tile_force;
   (void)N;
-  if (s->v2) return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128;
-  if (M % 320 == 0) return TILE_320x160;
-  return M % 160 == 0 ? TILE_160x160 : TILE_128x128;
+  return M % 320 == 0 ? TILE2_W320x128 : TILE2_W128x128;
 }
 
-bool uses_v2(const pulse_stage* s) { return s->v2 && s->dtype == DT_BF16 && s->k64; }
+// bf16 with every channel count a multiple of 64: the LDS-DMA kernels
+bool uses_v2(const pulse_stage* s) { return s->dtype == DT_BF16 && s->k64; }
 
 TileInfo info_of(const pulse_stage* s, int tile) {
   return uses_v2(s) ? tile2_info(tile) : tile_info(tile);
@@ -315,36 +301,16 @@ int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
   return (int)((s->P + kc - 1) / kc);
 }
 
-// Weight-gradient work split: uniform pixel splits (pick_splits); with the
-// balanced split switched on (PULSE_WGRAD_BALANCE=1, when the uniform split
-// leaves more than a tenth of the resident-block slots idle, or 2, always)
-// the tiles' K-steps are dealt out evenly to one block per slot, at least 8
-// K-steps each.  It keeps every CU busy, but the blocks running together no
-// longer share pixel rows in L2, and it measured slower on every stage, so
-// it is off by default.  slots = partial slots the split writes per element.
+// Weight-gradient work split: uniform pixel splits of kchunk pixels
+// (pick_splits); every split writes one fp32 partial of M x N.
 struct WgradPlan {
-  int splits = 1, kchunk = 0, sk_blocks = 0, slots = 1;
+  int splits = 1, kchunk = 0, slots = 1;
 };
 
 WgradPlan wgrad_plan(const pulse_stage* s, int tile, int M, int N) {
   WgradPlan w;
   w.splits = pick_splits(s, tile, M, N, w.kchunk);
   w.slots = w.splits;
-  if (!uses_v2(s) || s->wgrad_balance == 0) return w;
-  const TileInfo ti = info_of(s, tile);
-  const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
-  const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : 1;
-  const long nslots = 256L * per_cu;
-  const long blocks = tiles * w.splits;
-  const long rounds = (blocks + nslots - 1) / nslots;
-  const double util = (double)blocks / (double)(rounds * nslots);
-  if (util >= 0.9 && s->wgrad_balance < 2) return w;
-  const long ktt = (s->P + ti.bk - 1) / ti.bk;
-  const long units = tiles * ktt;
-  const long nb = std::min(nslots, units / 8);
-  if (nb < 1) return w;
-  w.sk_blocks = (int)nb;
-  w.slots = sk_max_slots(M, N, ti.bm, ti.bn, s->P, ti.bk, (int)nb);
   return w;
 }
 
@@ -398,20 +364,12 @@ pulse_status build_layout(pulse_stage* s) {
     for (auto& b : s->eb) { chk(b.cin); chk(b.cout); chk(b.c0); }
     for (auto& b : s->db) { chk(b.cin); chk(b.cout); chk(b.c0); }
     s->k64 = k64;
-    // PULSE_GEMM_V1=1 selects the register-staged GEMM kernels; the tile
-    // overrides (tuning) index Tile2 on the LDS-DMA path, Tile otherwise
-    s->v2 = env_int("PULSE_GEMM_V1", 0) == 0;
+    // tile overrides (tuning) index Tile2; they apply on the LDS-DMA path
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
-    s->halo = env_int("PULSE_HALO", 0);
     s->conv_ksplit_cap = std::max(1, std::min(16, env_int("PULSE_CONV_KSPLIT_MAX", 16)));
-    s->wgrad_balance = std::max(0, std::min(2, env_int("PULSE_WGRAD_BALANCE", 0)));
-    if (s->v2) {
-      s->conv_tile_force = (ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
-      s->wgrad_tile_force = (wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
-    } else {
-      s->conv_tile_force = (ct >= 0 && ct <= TILE_160x160) ? ct : -1;
-      s->wgrad_tile_force = (wt >= 0 && wt <= TILE_160x160) ? wt : -1;
-    }
+    const bool v2 = s->dtype == DT_BF16 && k64;
+    s->conv_tile_force = (v2 && ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
+    s->wgrad_tile_force = (v2 && wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
   }
 
   // workspace: weight copies | rows | scratch
@@ -729,26 +687,19 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
     e1 = next_event(s);
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
-  // the halo-reuse kernel when it applies (one block per CU: only when the
-  // grid fills the GPU, unless forced) and no tile override is set
-  const bool halo = uses_v2(s) && s->conv_tile_force < 0 && ks == 1 && s->halo > 0 &&
-                    halo_conv_fits(s->geo, a.N) &&
-                    (s->halo == 2 || (s->P / 256) * (a.N / 160) >= 256);
   // output statistics from the epilogue: LDS-DMA tiles, no K split, whole
   // tiles per image, and room in the reduction buffer; else the caller's
   // GroupNorm computes them itself (stats_chunks stays 0)
   if (a.stats) {
     const int bm = info_of(s, tile).bm;
     const long rows = s->geo.hw() % bm == 0 ? (long)s->geo.B * (s->geo.hw() / bm) : 0;
-    if (stats_chunks && !halo && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
+    if (stats_chunks && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
         (size_t)rows * 2 * a.N <= s->red_cap)
       *stats_chunks = s->geo.hw() / bm;
     else
       a.stats = nullptr;
   }
-  if (halo)
-    HIPCHK(launch_conv_halo(a, st));
-  else if (uses_v2(s))
+  if (uses_v2(s))
     HIPCHK(launch_conv2(a, tile, st));
   else
     HIPCHK(launch_conv(a, tile, st));
@@ -838,7 +789,6 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
   if ((size_t)w.slots * M * n > s->part_cap)
     return fail(PULSE_E_SHAPE, "internal: wgrad partial buffer too small");
   a.kchunk = w.kchunk;
-  a.sk_blocks = w.sk_blocks;
   a.part = s->sf(s->s_part);
   if (uses_v2(s))
     HIPCHK(launch_wgrad2(a, tile, splits, s->scratch(s->s_zero), st));

@@ -118,21 +118,22 @@ def test_two_microbatch_accumulation():
     assert not bad, bad
 
 
-@pytest.mark.parametrize("tile", range(13))
+@pytest.mark.parametrize("tile", range(4))
 def test_every_conv_tile(tile, monkeypatch):
-    """Every implicit-GEMM conv tile shape of the LDS-DMA path (1-, 2- and
-    3/4-stage rings, 64- and 32-channel K-steps, with and without K splits)
-    against the oracle on the 64x64x320 stage's channels at a small image."""
+    """Every implicit-GEMM conv tile shape of the LDS-DMA path (128x160,
+    128x128, 128x192 with two stages, 64x128 with three; with and without K
+    splits) against the oracle on the 64x64x320 stage's channels at a small
+    image."""
     monkeypatch.setenv("PULSE_CONV_TILE", str(tile))
     _case(configs.shrink(configs.l64(), batch=2, hw=12, width=10), 2, f"l64s conv tile {tile}")
 
 
-@pytest.mark.parametrize("tile", [-1, 0, 2, 3, 4])
+@pytest.mark.parametrize("tile", [-1, 0, 1, 2, 3])
 def test_conv_epilogue_statistics(tile, monkeypatch):
     """Convs without a K split whose tiles lie inside one image compute the
     GroupNorm statistics of their output in the epilogue (GN2 after conv1,
     the next encoder block's GN1 after conv2): 16x16 images hold whole
-    128- and 256-pixel tiles; the K split is switched off so that the path
+    64- and 128-pixel tiles; the K split is switched off so that the path
     runs at a size the oracle finishes quickly."""
     monkeypatch.setenv("PULSE_CONV_KSPLIT_MAX", "1")
     if tile >= 0:
@@ -140,32 +141,8 @@ def test_conv_epilogue_statistics(tile, monkeypatch):
     _case(configs.shrink(configs.l64(), batch=2, hw=16), 2, f"l64s epilogue stats tile {tile}")
 
 
-@pytest.mark.parametrize("tile", [20, 21, 22, 23])
+@pytest.mark.parametrize("tile", [20, 21])
 def test_every_wgrad_tile(tile, monkeypatch):
     """Every weight-gradient tile shape of the LDS-DMA path."""
     monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
     _case(configs.shrink(configs.l32(), batch=2, hw=6, width=7), 3, f"l32s wgrad tile {tile}")
-
-
-@pytest.mark.parametrize("tile", [20, 21, 22, 23])
-@pytest.mark.parametrize("name,B,H,W", [("l64", 2, 12, 10), ("l32", 2, 6, 7)])
-def test_balanced_wgrad_split(tile, name, B, H, W, monkeypatch):
-    """The balanced weight-gradient split (the tiles' K-steps dealt out in
-    equal ranges, ranges crossing tile boundaries, per-tile partial slots
-    summed in order) forced on for every weight-gradient tile."""
-    monkeypatch.setenv("PULSE_WGRAD_BALANCE", "2")
-    monkeypatch.setenv("PULSE_WGRAD_TILE", str(tile))
-    d = configs.shrink(configs.get(name), batch=B, hw=H, width=W)
-    _case(d, configs.SEEDS[name], f"{name} balanced wgrad tile {tile}")
-
-
-@pytest.mark.parametrize("name,B,H,W", [("l64", 1, 16, 16), ("l64", 2, 32, 32),
-                                        ("l32", 1, 16, 16), ("l32", 1, 32, 32)])
-def test_halo_conv(name, B, H, W, monkeypatch):
-    """The halo-reuse conv kernel (whole-row 256-pixel tiles, one halo load
-    per 64-channel chunk for all taps), forced on at sizes the oracle runs
-    in seconds: single- and two-source inputs, the K-extended 1x1 shortcut,
-    tiles of 16, 8 and 4 image rows, zero halo at image borders."""
-    monkeypatch.setenv("PULSE_HALO", "2")
-    d = configs.shrink(configs.get(name), batch=B, hw=H, width=W)
-    _case(d, configs.SEEDS[name], f"{name} halo {B}x{H}x{W}")

@@ -157,10 +157,11 @@ def test_interleaved_microbatches_keep_their_skips():
         assert e < TOL, (k, e)
 
 
-@pytest.mark.parametrize("tile", range(13))
+@pytest.mark.parametrize("tile", range(4))
 def test_tstage_every_conv_tile(tile, monkeypatch):
-    """Every conv-mode tile shape on the token-major linear layers (ragged
-    rows and columns)."""
+    """Every conv-mode tile shape (128x160, 128x128, 128x192, 64x128 with
+    three stages) on the token-major linear layers (ragged rows and
+    columns)."""
     monkeypatch.setenv("PULSE_TCONV_TILE", str(tile))
     d = _mid()
     p, b = synth.make_tstage(d, 11)
@@ -169,7 +170,7 @@ def test_tstage_every_conv_tile(tile, monkeypatch):
     _compare(f"conv tile {tile}", got, ref)
 
 
-@pytest.mark.parametrize("tile", [20, 21, 22, 23])
+@pytest.mark.parametrize("tile", [20, 21])
 def test_tstage_every_wgrad_tile(tile, monkeypatch):
     monkeypatch.setenv("PULSE_TWGRAD_TILE", str(tile))
     d = _mid()
