@@ -72,6 +72,7 @@ def describe(name, descs):
 # each valid for the kernel and planning sources it was taken on
 TRAFFIC_WORKLOADS = {
     "l64": ["igemm2.hip", "kernels.hpp", "common.hpp", "stage.cpp"],
+    "l32": ["igemm2.hip", "kernels.hpp", "common.hpp", "stage.cpp"],
     "t768": ["igemm2.hip", "kernels.hpp", "common.hpp", "tstage.cpp"],
     "t1408": ["igemm2.hip", "kernels.hpp", "common.hpp", "tstage.cpp"],
 }
