@@ -515,8 +515,47 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // GroupNorm statistics of the output, one row per (image, M-tile).
   float* ct = reinterpret_cast<float*>(smem);
   constexpr int NV8 = C::BN / 8;
+  constexpr int NTK = (16 * NV8 + C::NT - 1) / C::NT;  // tasks per thread and slice
   static_assert(C::BN <= C::NT, "one thread per output column for the statistics");
   const bool stats = a.stats != nullptr;
+  const bool raw = a.ksplit > 1;  // raw partial; the finalize adds the epilogue terms
+  const bool has_res = a.resid.s0.ptr != nullptr;
+  // A thread's tasks keep their row within a slice and their 8 columns in
+  // every slice: the bias and, for a tile inside one image, its timestep
+  // row are loaded once; each slice's residual is loaded a slice ahead.
+  const long mlast = (m0 + C::BM < P ? m0 + C::BM : P) - 1;
+  const int img0 = (int)(m0 / HW);
+  const bool uni = mlast / HW == img0;
+  int trow[NTK], tnc[NTK];
+  bool tok[NTK];
+  float cb[NTK][8], cr[NTK][8], rres[NTK][8];
+#pragma unroll
+  for (int k = 0; k < NTK; ++k) {
+    const int e = tid + k * C::NT;
+    trow[k] = e / NV8;
+    tnc[k] = n0 + (e - trow[k] * NV8) * 8;
+    tok[k] = e < 16 * NV8 && tnc[k] < a.N;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) cb[k][q] = cr[k][q] = rres[k][q] = 0.f;
+    if (tok[k] && !raw) {
+      if (a.bias) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) cb[k][q] = a.bias[tnc[k] + q];
+      }
+      if (a.rowvec && uni) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) cr[k][q] = a.rowvec[(long)img0 * a.N + tnc[k] + q];
+      }
+    }
+  }
+  auto load_res = [&](int g, int i) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < NTK; ++k) {
+      const long m = m0 + g * C::WM + i * 16 + trow[k];
+      if (tok[k] && m < P) ld8(a.resid.s0, m, tnc[k], rres[k]);
+    }
+  };
+  if (has_res && !raw) load_res(0, 0);
   float csum = 0.f, csq = 0.f;
 #pragma unroll 1
   for (int g = 0; g < C::WAVES_M; ++g) {
@@ -524,15 +563,27 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     for (int i = 0; i < C::TM; ++i) {
       if (wm == g) acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct, wn, lane, i, acc);
       __syncthreads();
-      for (int e = tid; e < 16 * NV8; e += C::NT) {
-        const int row = e / NV8;
-        const int n = n0 + (e - row * NV8) * 8;
+      float rcur[NTK][8];
+#pragma unroll
+      for (int k = 0; k < NTK; ++k)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) rcur[k][q] = rres[k][q];
+      if (has_res && !raw) {
+        if (i + 1 < C::TM)
+          load_res(g, i + 1);
+        else if (g + 1 < C::WAVES_M)
+          load_res(g + 1, 0);
+      }
+#pragma unroll
+      for (int k = 0; k < NTK; ++k) {
+        const int row = trow[k];
+        const int n = tnc[k];
         const long m = m0 + g * C::WM + i * 16 + row;
-        if (m >= P || n >= a.N) continue;
+        if (!tok[k] || m >= P) continue;
         float* src = ct + row * C::LDC + (n - n0);
         const float4 s0 = reinterpret_cast<const float4*>(src)[0];
         const float4 s1 = reinterpret_cast<const float4*>(src)[1];
-        if (a.ksplit > 1) {  // raw partial; the finalize adds the epilogue terms
+        if (raw) {
           float4* dp = reinterpret_cast<float4*>(a.part + ((long)z * P + m) * a.N + n);
           dp[0] = s0;
           dp[1] = s1;
@@ -541,18 +592,21 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
         if (a.bias) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += a.bias[n + q];
+          for (int q = 0; q < 8; ++q) v[q] += cb[k][q];
         }
         if (a.rowvec) {
-          const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+          if (uni) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += rv[q];
+            for (int q = 0; q < 8; ++q) v[q] += cr[k][q];
+          } else {
+            const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += rv[q];
+          }
         }
-        if (a.resid.s0.ptr) {
-          float rr[8];
-          ld8(a.resid.s0, m, n, rr);
+        if (has_res) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] += rr[q];
+          for (int q = 0; q < 8; ++q) v[q] += rcur[k][q];
         }
         st8(a.out, a.out_dtype, a.ldo, m, n, v);
         if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
@@ -579,7 +633,6 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     }
   }
   if (stats && tid < C::BN && n0 + tid < a.N) {
-    // the launcher guarantees H*W % BM == 0: the tile lies in one image
     const int img = (int)(m0 / HW);
     const int chunk = (int)(m0 - (long)img * HW) / C::BM;
     float* dst = a.stats + ((long)img * (HW / C::BM) + chunk) * 2 * a.N + n0 + tid;
