@@ -16,7 +16,10 @@ import numpy as np
 
 from . import configs as _cfg
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpulse_stage.so")
+# PULSE_STAGE_LIB selects another build of the same library (the host
+# sanitizer build of the tests); it must exist like the default one
+LIB_PATH = os.environ.get("PULSE_STAGE_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libpulse_stage.so")
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                       "include", "pulse_stage.h")
 
