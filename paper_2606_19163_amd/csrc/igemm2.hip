@@ -846,26 +846,33 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   }
   __syncthreads();
 
-  // fp32 partials through LDS in 16-row slices, 16-byte stores
+  // fp32 partials through LDS, GPP wave rows (GPP * WM tile rows) at a
+  // time: those waves stage all their accumulators, then every thread
+  // stores 16-byte row pieces
   float* ct = reinterpret_cast<float*>(smem);
   float* part = a.part + (long)z * a.M * a.N;
   constexpr int NV4 = C::BN / 4;
+  constexpr int GPP = (2 * C::STAGE) / (C::WM * C::LDC * 4);  // wave rows per pass
+  static_assert(GPP >= 1, "one wave row of accumulators fits the LDS stages");
+  constexpr int ROWS = (GPP < C::WAVES_M ? GPP : C::WAVES_M) * C::WM;
 #pragma unroll 1
-  for (int g = 0; g < C::WAVES_M; ++g) {
+  for (int g0 = 0; g0 < C::WAVES_M; g0 += GPP) {
+    if (wm >= g0 && wm < g0 + GPP) {
 #pragma unroll
-    for (int i = 0; i < C::TM; ++i) {
-      if (wm == g) acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct, wn, lane, i, acc);
-      __syncthreads();
-      for (int e = tid; e < 16 * NV4; e += C::NT) {
-        const int row = e / NV4;
-        const int n = n0 + (e - row * NV4) * 4;
-        const int m = m0 + g * C::WM + i * 16 + row;
-        if (m >= a.M || n >= a.N) continue;
-        *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
-            *reinterpret_cast<const float4*>(ct + row * C::LDC + (n - n0));
-      }
-      __syncthreads();
+      for (int i = 0; i < C::TM; ++i)
+        acc16_to_lds<C::TM, C::TN, C::WN, C::LDC>(ct + ((wm - g0) * C::WM + i * 16) * C::LDC, wn,
+                                                  lane, i, acc);
     }
+    __syncthreads();
+    for (int e = tid; e < ROWS * NV4; e += C::NT) {
+      const int row = e / NV4;
+      const int n = n0 + (e - row * NV4) * 4;
+      const int m = m0 + g0 * C::WM + row;
+      if (row >= (C::WAVES_M - g0) * C::WM || m >= a.M || n >= a.N) continue;
+      *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
+          *reinterpret_cast<const float4*>(ct + row * C::LDC + (n - n0));
+    }
+    __syncthreads();
   }
 #else
   (void)a;
