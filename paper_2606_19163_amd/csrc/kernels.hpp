@@ -97,8 +97,9 @@ struct RedGrid {
 RedGrid red_grid(const Geo& g, int C);
 
 // partial[b][chunk][2][C]: per-channel sum and sum of squares of x.
+// copy (null: none): the channels below x.c0 of x as read, [P][x.c0]
 hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
-                                   hipStream_t st);
+                                   hipStream_t st, void* copy = nullptr);
 // mean/rstd [B][G] and the folded affine scale/shift [B][C].
 hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                     int G, float eps, const float* gamma, const float* beta,
@@ -154,6 +155,23 @@ hipError_t launch_chan_totals(const float* partial, const Geo& g, RedGrid rg, in
 hipError_t launch_temb_fwd(const void* temb, int dtype, int B, int D, int O, const float* Wl,
                            const float* bias_a, const float* bias_b, float* e,
                            hipStream_t st);
+// The projections of several stage blocks from one temb in one launch:
+// blk[k].e[b][o] (row stride ldE) for every block k < n; copy (null: none)
+// receives temb itself.
+constexpr int TEMB_MAX_BLOCKS = 16;
+struct TembFwdBlock {
+  const float* Wl;      // [O][D]
+  const float* bias_a;  // [O]
+  const float* bias_b;  // [O] or null
+  float* e;             // [B][ldE]
+  int O, ldE;
+};
+struct TembFwdSet {
+  TembFwdBlock blk[TEMB_MAX_BLOCKS];
+  int n;
+};
+hipError_t launch_temb_fwd_multi(const void* temb, int dtype, int B, int D,
+                                 const TembFwdSet& set, void* copy, hipStream_t st);
 // dWl += de^T SiLU(temb); dbl += sum_b de; db1 += sum_b de;
 // dtemb += (de Wl) * SiLU'(temb) (dtemb may be null).
 hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, int D, int O,

@@ -1,5 +1,7 @@
 // Timestep-embedding projection, weight re-layouts and conversions (gfx950).
 // All small or streaming; none is on the MFMA path.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -46,6 +48,144 @@ __global__ __launch_bounds__(64) void k_temb_fwd(const void* temb, int dtype, in
     float bias = bias_a[o];
     if (bias_b) bias += bias_b[o];
     e[(long)b * O + o] = s + bias;
+  }
+}
+
+// Every block's projection of one stage half in one launch.  Block
+// (row tile, stage block k, image group) of 4 waves, each wave 2 rows o of
+// Wl_k for 8 images.  Per slice of d every memory read is issued at once:
+// the wave's Wl rows (16-byte loads into registers) and SiLU(temb) of the 8
+// images (16-byte loads, activated into LDS); the lanes' 2 x 8 partial dot
+// products then meet in LDS in a fixed order.  The blocks of the first row
+// tile of stage block 0 also write the temb copy.
+constexpr int TP_ROWS = 2;                      // rows per wave
+constexpr int TP_IMG = 8;                       // images per block
+constexpr int TP_DS = 2048;                     // d slice
+constexpr int TP_J = TP_DS / 256;               // float4 loads per lane and row
+
+__global__ __launch_bounds__(256) void k_temb_fwd_multi(const void* temb, int dtype, int B,
+                                                        int D, TembFwdSet set, void* copy) {
+  __shared__ __attribute__((aligned(16))) float st[TP_IMG][TP_DS];
+  __shared__ float red[4][TP_ROWS * TP_IMG][65];
+  const int k = blockIdx.y;
+  const TembFwdBlock& blk = set.blk[k];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int b0 = blockIdx.z * TP_IMG;
+  const int o0 = (blockIdx.x * 4 + wave) * TP_ROWS;
+  const bool do_copy = copy && blockIdx.x == 0 && k == 0;
+  const bool vec = dtype == DT_BF16 && (D % 8) == 0;
+  float acc[TP_ROWS][TP_IMG];
+#pragma unroll
+  for (int r = 0; r < TP_ROWS; ++r)
+#pragma unroll
+    for (int i = 0; i < TP_IMG; ++i) acc[r][i] = 0.f;
+  for (int dc = 0; dc < D; dc += TP_DS) {
+    const int dn = min(TP_DS, D - dc);
+    // the wave's weight rows, all loads in flight together
+    float4 wv[TP_ROWS][TP_J];
+#pragma unroll
+    for (int r = 0; r < TP_ROWS; ++r) {
+      const int o = min(o0 + r, blk.O - 1);
+      const float* w = blk.Wl + (long)o * D + dc;
+#pragma unroll
+      for (int j = 0; j < TP_J; ++j) {
+        const int d = 4 * lane + 256 * j;
+        if ((D & 3) == 0 && d + 3 < dn) {
+          wv[r][j] = *reinterpret_cast<const float4*>(w + d);
+        } else {
+          wv[r][j].x = d < dn ? w[d] : 0.f;
+          wv[r][j].y = d + 1 < dn ? w[d + 1] : 0.f;
+          wv[r][j].z = d + 2 < dn ? w[d + 2] : 0.f;
+          wv[r][j].w = d + 3 < dn ? w[d + 3] : 0.f;
+        }
+      }
+    }
+    __syncthreads();  // the previous slice's LDS reads are done
+    if (vec) {
+      // 8-element pieces: TP_IMG * dn / 8 of them, at most 8 per thread
+      constexpr int NP = TP_IMG * TP_DS / 8 / 256;
+      uint4 q[NP];
+#pragma unroll
+      for (int j = 0; j < NP; ++j) {
+        const int e = threadIdx.x + 256 * j;
+        const int i = e / (TP_DS / 8), d = (e - i * (TP_DS / 8)) * 8;
+        q[j] = uint4{0u, 0u, 0u, 0u};
+        if (b0 + i < B && d < dn)
+          q[j] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(temb) +
+                                                 (long)(b0 + i) * D + dc + d);
+      }
+#pragma unroll
+      for (int j = 0; j < NP; ++j) {
+        const int e = threadIdx.x + 256 * j;
+        const int i = e / (TP_DS / 8), d = (e - i * (TP_DS / 8)) * 8;
+        if (do_copy && b0 + i < B && d < dn)
+          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(copy) + (long)(b0 + i) * D + dc + d) =
+              q[j];
+        const uint32_t w4[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
+        float v[8];
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          v[2 * h] = silu_f(__uint_as_float(w4[h] << 16));
+          v[2 * h + 1] = silu_f(__uint_as_float(w4[h] & 0xffff0000u));
+        }
+        if (!(b0 + i < B && d < dn)) {
+#pragma unroll
+          for (int h = 0; h < 8; ++h) v[h] = 0.f;
+        }
+        float4* dst = reinterpret_cast<float4*>(&st[i][d]);
+        dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+        dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+      }
+    } else {
+      for (int e = threadIdx.x; e < TP_IMG * TP_DS; e += 256) {
+        const int i = e / TP_DS, d = e - i * TP_DS;
+        float v = 0.f;
+        if (b0 + i < B && d < dn) {
+          const long at = (long)(b0 + i) * D + dc + d;
+          const float t = ld_any(temb, dtype, at);
+          if (do_copy) st_any(copy, dtype, at, t);
+          v = silu_f(t);
+        }
+        st[i][d] = v;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TP_J; ++j) {
+      const int d = 4 * lane + 256 * j;
+      if (d >= dn) break;
+#pragma unroll
+      for (int i = 0; i < TP_IMG; ++i) {
+        const float4 sv = *reinterpret_cast<const float4*>(&st[i][d]);
+#pragma unroll
+        for (int r = 0; r < TP_ROWS; ++r)
+          acc[r][i] += wv[r][j].x * sv.x + wv[r][j].y * sv.y + wv[r][j].z * sv.z +
+                       wv[r][j].w * sv.w;
+      }
+    }
+  }
+  // lane sums -> LDS; lane q < 16 of the wave then adds the 64 lanes of
+  // (row q / 8, image q % 8) in order
+#pragma unroll
+  for (int r = 0; r < TP_ROWS; ++r)
+#pragma unroll
+    for (int i = 0; i < TP_IMG; ++i) red[wave][r * TP_IMG + i][lane] = acc[r][i];
+  __syncthreads();
+  if (lane < TP_ROWS * TP_IMG) {
+    const int r = lane / TP_IMG, i = lane - r * TP_IMG;
+    const int o = o0 + r, b = b0 + i;
+    if (o < blk.O && b < B) {
+      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+      for (int l = 0; l < 64; l += 4) {
+        s0 += red[wave][lane][l];
+        s1 += red[wave][lane][l + 1];
+        s2 += red[wave][lane][l + 2];
+        s3 += red[wave][lane][l + 3];
+      }
+      float bias = blk.bias_a[o];
+      if (blk.bias_b) bias += blk.bias_b[o];
+      blk.e[(long)b * blk.ldE + o] = ((s0 + s1) + (s2 + s3)) + bias;
+    }
   }
 }
 
@@ -174,6 +314,19 @@ hipError_t launch_temb_fwd(const void* temb, int dtype, int B, int D, int O, con
                            hipStream_t st) {
   hipLaunchKernelGGL(k_temb_fwd, dim3(O, B), dim3(64), 0, st, temb, dtype, D, O, Wl, bias_a,
                      bias_b, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_temb_fwd_multi(const void* temb, int dtype, int B, int D,
+                                 const TembFwdSet& set, void* copy, hipStream_t st) {
+  if (set.n < 1 || set.n > TEMB_MAX_BLOCKS) return hipErrorInvalidValue;
+  int omax = 0;
+  for (int k = 0; k < set.n; ++k) omax = std::max(omax, set.blk[k].O);
+  const int rows_per_block = 4 * TP_ROWS;
+  hipLaunchKernelGGL(k_temb_fwd_multi,
+                     dim3((omax + rows_per_block - 1) / rows_per_block, set.n,
+                          (B + TP_IMG - 1) / TP_IMG),
+                     dim3(256), 0, st, temb, dtype, B, D, set, copy);
   return hipGetLastError();
 }
 

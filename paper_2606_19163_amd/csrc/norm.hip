@@ -137,12 +137,22 @@ __device__ __forceinline__ void step_pixels(int p, int py, int p1, long img0, lo
   }
 }
 
+// The backward pass runs the data-gradient chain beside the weight-gradient
+// GEMMs of a second stream, whose blocks hold 2 waves of 208 registers on
+// every SIMD: kernels of that chain that need at most 96 registers (5 waves
+// per SIMD) and 256-thread blocks still find room on those CUs instead of
+// waiting for the GEMM to drain.
+constexpr int GN_WAVES = 5;
 constexpr int U_STATS = 4;  // pixels per loop step of the reductions
-constexpr int U_BWD = 2;    // of the backward kernels (more live constants)
+constexpr int U_BWD = 1;    // of the backward reductions (within 96 registers)
+constexpr int U_APPLY = 1;  // of the backward apply (within 96 registers)
 
+// copy (null: none) receives the channels below x.c0 of every pixel, as
+// read ([P][x.c0], the element type of x): the stage keeps its input for the
+// backward without a pass of its own.
 template <int DT, bool ADD, int U = U_STATS>
 __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid rg,
-                                                          float* partial) {
+                                                          float* partial, void* copy) {
   __shared__ float sm[256 * 16];
   const Range r = block_range(g, rg, x.C);
   float acc[16];
@@ -151,12 +161,18 @@ __global__ __launch_bounds__(256) void k_gn_stats_partial(VIn x, Geo g, RedGrid 
   if (r.active) {
     const VCh8 h = resolve_v(x, r.c);
     const long img0 = (long)r.b * g.hw();
+    const bool cp = copy && r.c < x.c0;
     for (int p = r.p0 + threadIdx.y; p < r.p1; p += U * rg.py) {
       long pix[U];
       float w[U], f[U][8];
       step_pixels<U>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
       for (int u = 0; u < U; ++u) rdv8<DT, ADD>(h, pix[u], f[u]);
+      if (cp) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (p + u * rg.py < r.p1) st8(copy, DT, x.c0, pix[u], r.c, f[u]);
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -319,7 +335,7 @@ __device__ __forceinline__ void load_gn_const(GnConst& k, int b, int c, int C, i
 }
 
 template <int DT, bool ADD, int U = U_BWD>
-__global__ __launch_bounds__(256) void k_gn_bwd_partial(Src da, VIn x, Geo g,
+__global__ __launch_bounds__(256, GN_WAVES) void k_gn_bwd_partial(Src da, VIn x, Geo g,
                                                         RedGrid rg, const float* scale,
                                                         const float* shift, const float* mean,
                                                         const float* rstd, int G,
@@ -414,10 +430,12 @@ __global__ __launch_bounds__(256) void k_chan_per_image(const float* partial, in
 }
 
 // Channel totals over every image and chunk in one pass: slot 0 is added to
-// acc0 (and dup), slot 1 to acc1.  A 1024-thread block holds 16 channels x
-// 64 row lanes; lane y sums the (image, chunk) rows y, y+64, ... and the
-// lanes meet in a fixed LDS tree.
-constexpr int TX = 16, TY = 64;
+// acc0 (and dup), slot 1 to acc1.  A 256-thread block holds 8 channels x
+// 32 row lanes; lane y sums the (image, chunk) rows y, y+32, ... (8 loads
+// in flight, added in ascending row order) and the lanes meet in a fixed
+// LDS tree.  Small blocks and few registers: the kernel finds room beside
+// the GEMMs of the other stream.
+constexpr int TX = 8, TY = 32;
 
 __device__ __forceinline__ void chan_totals_block(const float* partial, int rows, int C,
                                                   int nslot, int cblock, float* acc0,
@@ -429,8 +447,7 @@ __device__ __forceinline__ void chan_totals_block(const float* partial, int rows
   if (c < C) {
     const long stride = 2L * C;
     const float* base = partial + c;
-    // NB rows in flight per lane, added in ascending row order
-    constexpr int NB = 16;
+    constexpr int NB = 8;
     for (int i0 = ty; i0 < rows; i0 += NB * TY) {
       float a[NB], e[NB];
 #pragma unroll
@@ -464,56 +481,40 @@ __device__ __forceinline__ void chan_totals_block(const float* partial, int rows
   }
 }
 
-__global__ __launch_bounds__(1024) void k_chan_totals(const float* partial, int rows, int C,
-                                                      int nslot, float* acc0, float* dup,
-                                                      float* acc1) {
+__global__ __launch_bounds__(256, GN_WAVES) void k_chan_totals(const float* partial, int rows, int C,
+                                                     int nslot, float* acc0, float* dup,
+                                                     float* acc1) {
   __shared__ float sm[2][TY][TX];
   chan_totals_block(partial, rows, C, nslot, blockIdx.x, acc0, dup, acc1, sm);
 }
 
-// Fixed-order sum of two fp64 values over a 1024-thread block.
-__device__ __forceinline__ void block_sum2_1k(double& a, double& b, double* sm) {
-  const int t = threadIdx.x;
-  sm[t] = a;
-  sm[1024 + t] = b;
-  __syncthreads();
-  for (int off = 512; off > 0; off >>= 1) {
-    if (t < off) {
-      sm[t] += sm[t + off];
-      sm[1024 + t] += sm[1024 + t + off];
-    }
-    __syncthreads();
-  }
-  a = sm[0];
-  b = sm[1024];
-}
-
-// GroupNorm backward finalize in one launch of 1024-thread blocks: blocks
-// [0, ceil(C/16)) add dbeta (sum dz) and dgamma (sum dz * xhat) over every
-// image and chunk; the remaining B*G blocks each reduce one (image, group)
-// to coef = (sum gamma*dz, sum gamma*dz*xhat) / count.
-__global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, Geo g,
-                                                          RedGrid rg, int C, int G,
-                                                          const float* gamma, float* coef,
-                                                          float* dgamma, float* dbeta) {
+// GroupNorm backward finalize in one launch of 256-thread blocks: blocks
+// [0, B*G) each reduce one (image, group) to coef = (sum gamma*dz,
+// sum gamma*dz*xhat) / count in fp64, with every load in flight before the
+// sums; blocks [B*G, B*G + ceil(C/8)) add dbeta (sum dz) and dgamma
+// (sum dz * xhat) over every image and chunk.
+__global__ __launch_bounds__(256, GN_WAVES) void k_gn_bwd_finalize(const float* partial, Geo g,
+                                                         RedGrid rg, int C, int G,
+                                                         const float* gamma, float* coef,
+                                                         float* dgamma, float* dbeta) {
   __shared__ float smc[2][TY][TX];
-  __shared__ double sm[2048];
-  const int nchb = (C + TX - 1) / TX;
-  if ((int)blockIdx.x < nchb) {
-    chan_totals_block(partial, g.B * rg.chunks, C, 2, blockIdx.x, dbeta, nullptr, dgamma, smc);
+  __shared__ double sm[512];
+  const int nbg = g.B * G;
+  if ((int)blockIdx.x >= nbg) {
+    chan_totals_block(partial, g.B * rg.chunks, C, 2, blockIdx.x - nbg, dbeta, nullptr, dgamma,
+                      smc);
     return;
   }
-  const int q = blockIdx.x - nchb;
-  const int b = q / G, gi = q - b * G;
+  const int b = blockIdx.x / G, gi = blockIdx.x - b * G;
   const int cg = C / G;
   double S1 = 0.0, S2 = 0.0;
-  constexpr int NB = 4;  // loads in flight per thread, added in ascending i
+  constexpr int NB = 8;  // loads in flight per thread, added in ascending i
   const int n = rg.chunks * cg;
-  for (int i0 = threadIdx.x; i0 < n; i0 += NB * 1024) {
+  for (int i0 = threadIdx.x; i0 < n; i0 += NB * 256) {
     float ga[NB], p1[NB], p2[NB];
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
-      const int i = i0 + k * 1024;
+      const int i = i0 + k * 256;
       ga[k] = p1[k] = p2[k] = 0.f;
       if (i < n) {
         const int ch = i / cg;
@@ -526,12 +527,12 @@ __global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, 
     }
 #pragma unroll
     for (int k = 0; k < NB; ++k)
-      if (i0 + k * 1024 < n) {
+      if (i0 + k * 256 < n) {
         S1 += (double)ga[k] * p1[k];
         S2 += (double)ga[k] * p2[k];
       }
   }
-  block_sum2_1k(S1, S2, sm);
+  block_sum2(S1, S2, sm);
   if (threadIdx.x == 0) {
     const double cnt = (double)g.hw() * cg;
     coef[(b * G + gi) * 2 + 0] = (float)(S1 / cnt);
@@ -543,8 +544,8 @@ __global__ __launch_bounds__(1024) void k_gn_bwd_finalize(const float* partial, 
 // embedding gradient); ADD0: the addend o.add0 (stage dtype) exists; NF: the
 // number of fp32 addends (o.add0's own and o.add1, in that order).  Each
 // instance keeps only the registers it needs.
-template <int DT, bool CHAN, bool ADD0, int NF>
-__global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
+template <int DT, bool CHAN, bool ADD0, int NF, int U = U_APPLY>
+__global__ __launch_bounds__(256, GN_WAVES) void k_gn_bwd_apply(Src da, VIn x, Geo g,
                                                       RedGrid rg, const float* scale,
                                                       const float* shift, const float* mean,
                                                       const float* rstd, const float* gamma,
@@ -605,12 +606,12 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
     const int dstride = first ? o.c_split : C - o.c_split;
     const int dc = first ? r.c : r.c - o.c_split;
     const long img0 = (long)r.b * g.hw();
-    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U_BWD * rg.py) {
-      long pix[U_BWD];
-      float w[U_BWD], f[U_BWD][8], d[U_BWD][8], e[U_BWD][8];
-      step_pixels<U_BWD>(p, rg.py, r.p1, img0, pix, w);
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U * rg.py) {
+      long pix[U];
+      float w[U], f[U][8], d[U][8], e[U][8];
+      step_pixels<U>(p, rg.py, r.p1, img0, pix, w);
 #pragma unroll
-      for (int u = 0; u < U_BWD; ++u) {
+      for (int u = 0; u < U; ++u) {
         rd8<DT>(hx, pix[u], f[u]);
         rd8<DT>(hd, pix[u], d[u]);
         if constexpr (ADD0) {
@@ -623,7 +624,7 @@ __global__ __launch_bounds__(256) void k_gn_bwd_apply(Src da, VIn x, Geo g,
         if constexpr (NF >= 2) add8(fa1, C, pix[u], e[u]);
       }
 #pragma unroll
-      for (int u = 0; u < U_BWD; ++u) {
+      for (int u = 0; u < U; ++u) {
         if (p + u * rg.py >= r.p1) break;
         float out[8];
 #pragma unroll
@@ -706,15 +707,16 @@ RedGrid red_grid(const Geo& g, int C) {
 }
 
 hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
-                                   hipStream_t st) {
+                                   hipStream_t st, void* copy) {
   const int dt = common_dt(x);
   if (dt < 0) return hipErrorInvalidValue;
   const bool add = x.add != nullptr;
+  if (copy && add) return hipErrorInvalidValue;  // the copy is of the tensor as stored
   auto kern = dt == DT_BF16 ? (add ? k_gn_stats_partial<DT_BF16, true>
                                    : k_gn_stats_partial<DT_BF16, false>)
                             : (add ? k_gn_stats_partial<DT_F32, true>
                                    : k_gn_stats_partial<DT_F32, false>);
-  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg, partial);
+  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg, partial, copy);
   return hipGetLastError();
 }
 
@@ -759,14 +761,14 @@ hipError_t launch_gn_bwd_finalize(const float* partial, const Geo& g, RedGrid rg
                                   int G, const float* gamma, float* coef, float* dgamma,
                                   float* dbeta, hipStream_t st) {
   const int nchb = (C + TX - 1) / TX;
-  hipLaunchKernelGGL(k_gn_bwd_finalize, dim3(nchb + g.B * G), dim3(1024), 0, st, partial, g, rg,
+  hipLaunchKernelGGL(k_gn_bwd_finalize, dim3(g.B * G + nchb), dim3(256), 0, st, partial, g, rg,
                      C, G, gamma, coef, dgamma, dbeta);
   return hipGetLastError();
 }
 
 hipError_t launch_chan_totals(const float* partial, const Geo& g, RedGrid rg, int C, int nslot,
                               float* acc0, float* dup, float* acc1, hipStream_t st) {
-  hipLaunchKernelGGL(k_chan_totals, dim3((C + TX - 1) / TX), dim3(1024), 0, st, partial,
+  hipLaunchKernelGGL(k_chan_totals, dim3((C + TX - 1) / TX), dim3(256), 0, st, partial,
                      g.B * rg.chunks, C, nslot, acc0, dup, acc1);
   return hipGetLastError();
 }

@@ -136,7 +136,6 @@ struct pulse_stage {
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_w2[2] = {nullptr, nullptr}, ev_w1[2] = {nullptr, nullptr};
-  hipEvent_t ev_temb = nullptr;  // the forward's timestep projections are ready
   // Every call shares the scratch buffers.  The stream of the last call that
   // enqueued work and an event recorded at its end let a call on another
   // stream wait for it first.
@@ -800,15 +799,20 @@ pulse_status wgrad(pulse_stage* s, int M, std::initializer_list<Seg> segs, const
 // GroupNorm+SiLU forward of x into dst0/dst1.  pre_chunks > 0: the
 // per-chunk channel sums of x are already in the reduction buffer, with that
 // many chunks per image (written by the producing conv's epilogue).
+// src (null: x) is what the statistics pass reads, and copy (null: none)
+// receives its first source as read: the stage's input arrives in the
+// caller's buffer and is kept, by the statistics pass, in the row that x
+// then points at.
 pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
                         const float* gamma, const float* beta, void* dst0, void* dst1,
-                        hipStream_t st, int pre_chunks = 0) {
+                        hipStream_t st, int pre_chunks = 0, const VIn* src = nullptr,
+                        void* copy = nullptr) {
   RedGrid rg = red_grid(s->geo, x.C);
   float* red = s->fwd(s->f_red);
   if (pre_chunks > 0)
     rg.chunks = pre_chunks;
   else
-    HIPCHK(launch_gn_stats_partial(x, s->geo, rg, red, st));
+    HIPCHK(launch_gn_stats_partial(src ? *src : x, s->geo, rg, red, st, copy));
   float* mean = reinterpret_cast<float*>(row + g.mean);
   float* rstd = reinterpret_cast<float*>(row + g.rstd);
   float* scale = reinterpret_cast<float*>(row + g.scale);
@@ -872,20 +876,20 @@ float* temb_slice(pulse_stage* s, int k) {
 // out_chunks non-null: ask conv2 for the statistics of `out` (receives their
 // chunks per image, 0 when not computed).
 pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin, void* out,
-                           void* out2, const float* e, bool wait_temb, int in_chunks,
-                           int* out_chunks, hipStream_t st) {
+                           void* out2, const float* e, int in_chunks, int* out_chunks,
+                           hipStream_t st, const VIn* xsrc = nullptr, void* xcopy = nullptr) {
   char* row = s->row_base(r);
   const int dt = s->dtype;
   void* a1_0 = row + b.a1_0;
   void* a1_1 = row + b.a1_1;
   pulse_status ps;
-  // a1 = SiLU(GN1(x)), one tensor per source
+  // a1 = SiLU(GN1(x)), one tensor per source (the first block's statistics
+  // pass reads the caller's input xsrc and keeps it in xin's row buffer)
   if ((ps = gn_forward(s, row, b.gn1, xin, s->pp(b.g1), s->pp(b.be1), a1_0, a1_1, st,
-                       in_chunks)) != PULSE_OK)
+                       in_chunks, xsrc, xcopy)) != PULSE_OK)
     return ps;
-  // e = b1 + bl + Wl SiLU(temb), computed for every block of the half on
-  // the side stream (temb_prefetch)
-  if (wait_temb && use_side(s)) HIPCHK(hipStreamWaitEvent(st, s->ev_temb, 0));
+  // e = b1 + bl + Wl SiLU(temb), computed for every block of the half
+  // beforehand (temb_project)
   const VIn a1 = (b.cin > b.c0) ? vin2(a1_0, dt, b.c0, a1_1, dt, b.cin - b.c0)
                                 : vin1(a1_0, dt, b.cin);
   void* h1 = row + b.h1;
@@ -966,30 +970,33 @@ pulse_status join_side(pulse_stage* s, hipStream_t st) {
 }
 
 // Timestep projections e_k = b1 + bl + Wl SiLU(temb) of every block of one
-// half, into consecutive [B][cmax] slices of the e buffer.  They run on the
-// side stream while the first block's GroupNorm runs here; the first conv1
-// waits for ev_temb.  The fork orders them after this stream's earlier
-// work, which includes every read of the previous call's projections.
-pulse_status temb_prefetch(pulse_stage* s, int r, const std::vector<Block>& blocks, int half,
-                           hipStream_t st) {
+// half, into consecutive [B][cmax] slices of the e buffer, in one launch per
+// 16 blocks on the caller's stream (a side stream would cost an event round
+// trip before the first conv); the first launch also keeps temb in the row.
+pulse_status temb_project(pulse_stage* s, int r, const std::vector<Block>& blocks, int half,
+                          const void* temb, hipStream_t st) {
   char* row = s->row_base(r);
-  hipStream_t sd = use_side(s) ? s->side : st;
-  pulse_status ps;
-  if ((ps = fork_side(s, st)) != PULSE_OK) return ps;
-  for (size_t k = 0; k < blocks.size(); ++k) {
-    const Block& b = blocks[k];
-    HIPCHK(launch_temb_fwd(row + s->row_temb[half], s->dtype, s->geo.B, s->D, b.cout,
-                           s->pp(b.Wl), s->pp(b.b1), s->pp(b.bl), temb_slice(s, (int)k), sd));
+  for (size_t k0 = 0; k0 < blocks.size(); k0 += TEMB_MAX_BLOCKS) {
+    TembFwdSet set{};
+    set.n = (int)std::min<size_t>(TEMB_MAX_BLOCKS, blocks.size() - k0);
+    for (int j = 0; j < set.n; ++j) {
+      const Block& b = blocks[k0 + j];
+      set.blk[j] = TembFwdBlock{s->pp(b.Wl), s->pp(b.b1), s->pp(b.bl),
+                                temb_slice(s, (int)(k0 + j)), b.cout, b.cout};
+    }
+    HIPCHK(launch_temb_fwd_multi(temb, s->dtype, s->geo.B, s->D, set,
+                                 k0 == 0 ? row + s->row_temb[half] : nullptr, st));
   }
-  if (use_side(s)) HIPCHK(hipEventRecord(s->ev_temb, s->side));
   return PULSE_OK;
 }
 
 // the gradient w.r.t. the block input goes (split/addends set by caller;
-// the residual / shortcut addend is filled in here).
+// the residual / shortcut addend is filled in here).  prev_dout: the
+// gradient buffer the block processed before this one read as its dout
+// (the side stream may still be reading it).
 pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xin,
                             const VIn& dout, GnBwdOut o, float* dtemb, hipStream_t st, int k,
-                            BwdSync& sy) {
+                            BwdSync& sy, const void* prev_dout) {
   const int par = k & 1;
   char* row = s->row_base(r);
   const int dt = s->dtype;
@@ -1073,9 +1080,11 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // GN1 backward + residual path -> gradient w.r.t. the block input
   o.add0 = b.conv_sc ? vin1(dxs, dt, b.cin) : dout;
   o.chan_partial = nullptr;
-  // the GN1 backward writes the gradient buffer that was the previous block's
-  // dout: wait until the side stream has read it
-  if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
+  // when the GN1 backward writes the gradient buffer that was the previous
+  // block's dout, the side stream must have read it (each wait costs this
+  // stream an event round trip)
+  if (prev_dout && o.dst0 == prev_dout)
+    if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
   return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
 }
 
@@ -1203,14 +1212,16 @@ pulse_status forward_impl(pulse_stage* s, pulse_half half, int32_t mb, const voi
       s->use_workspace_scratch();
     }
     if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
-    HIPCHK(hipMemcpyAsync(row + s->row_temb[half == PULSE_DEC ? 1 : 0], temb, (size_t)s->geo.B * s->D * s->esz,
-                          hipMemcpyDeviceToDevice, st));
+    // the timestep projections of every block of the half (temb kept in the row)
+    if ((ps = temb_project(s, r, half == PULSE_ENC ? s->eb : s->db, half == PULSE_DEC ? 1 : 0,
+                           temb, st)) != PULSE_OK)
+      return ps;
     if (half == PULSE_ENC) {
+      // the first statistics pass reads `in` and keeps it where the block
+      // input lives (its own row buffer, or the skip slot it also fills)
       void* xin_store = d.input_skip_slot >= 0 ? row + s->row_act[d.input_skip_slot]
                                                : row + s->row_xin;
-      HIPCHK(hipMemcpyAsync(xin_store, in, act_bytes(s, s->eb[0].cin), hipMemcpyDeviceToDevice,
-                            st));
-      if ((ps = temb_prefetch(s, r, s->eb, 0, st)) != PULSE_OK) return ps;
+      const VIn xsrc = vin1(in, dt, s->eb[0].cin);
       const int n = (int)s->eb.size();
       int chunks = 0;  // GN1 statistics of the next block's input, from conv2
       for (int k = 0; k < n; ++k) {
@@ -1226,22 +1237,23 @@ pulse_status forward_impl(pulse_stage* s, pulse_half half, int32_t mb, const voi
         }
         // the next encoder block normalises exactly this output
         const int in_chunks = chunks;
-        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), k == 0, in_chunks,
-                                k + 1 < n ? &chunks : nullptr, st)) != PULSE_OK)
+        if ((ps = block_forward(s, r, b, xin, o1, o2, temb_slice(s, k), in_chunks,
+                                k + 1 < n ? &chunks : nullptr, st, k == 0 ? &xsrc : nullptr,
+                                k == 0 ? xin_store : nullptr)) != PULSE_OK)
           return ps;
       }
-      (void)dt;
     } else {
-      HIPCHK(hipMemcpyAsync(row + s->row_u, in, act_bytes(s, s->db[0].c0),
-                            hipMemcpyDeviceToDevice, st));
-      if ((ps = temb_prefetch(s, r, s->db, 1, st)) != PULSE_OK) return ps;
       const int n = (int)s->db.size();
       for (int k = 0; k < n; ++k) {
         const Block& b = s->db[k];
         const VIn xin = block_input(s, r, b, k, nullptr);
+        // block 0 reads u from the caller and keeps it in the row
+        VIn xsrc = xin;
+        xsrc.s0.ptr = in;
         void* o1 = (k == n - 1) ? out : row + b.out_saved;
-        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), k == 0, 0, nullptr,
-                                st)) != PULSE_OK)
+        if ((ps = block_forward(s, r, b, xin, o1, nullptr, temb_slice(s, k), 0, nullptr, st,
+                                k == 0 ? &xsrc : nullptr,
+                                k == 0 ? row + s->row_u : nullptr)) != PULSE_OK)
           return ps;
       }
     }
@@ -1299,7 +1311,6 @@ void pulse_stage_destroy(pulse_stage* s) {
     if (s->ev_w2[i]) (void)hipEventDestroy(s->ev_w2[i]);
     if (s->ev_w1[i]) (void)hipEventDestroy(s->ev_w1[i]);
   }
-  if (s->ev_temb) (void)hipEventDestroy(s->ev_temb);
   if (s->ev_last) (void)hipEventDestroy(s->ev_last);
   if (s->side) (void)hipStreamDestroy(s->side);
   delete s;
@@ -1356,7 +1367,6 @@ pulse_status pulse_stage_bind(pulse_stage* s, const float* params, float* grads,
       HIPCHK(hipEventCreateWithFlags(&s->ev_w2[i], hipEventDisableTiming));
       HIPCHK(hipEventCreateWithFlags(&s->ev_w1[i], hipEventDisableTiming));
     }
-    HIPCHK(hipEventCreateWithFlags(&s->ev_temb, hipEventDisableTiming));
   }
   s->prm = params;
   s->grd = grads;
@@ -1451,6 +1461,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
     int cur = 0;
     BwdSync sy;
+    const void* prev_dy = nullptr;  // the dout of the block processed before
     if (half == PULSE_DEC) {
       const int n = (int)s->db.size();
       for (int k = n - 1; k >= 0; --k) {
@@ -1463,7 +1474,9 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
         o.dtype0 = dt;
         o.dst1 = row + s->row_grad[b.slot];
         o.dtype1 = DT_F32;
-        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy)) != PULSE_OK) return ps;
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy, prev_dy)) != PULSE_OK)
+          return ps;
+        prev_dy = dy.s0.ptr;
         cur ^= 1;
       }
     } else {
@@ -1492,7 +1505,9 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
         // the block input is the previous block's output (or the stage input):
         // its buffered skip gradient joins here, once
         o.add1 = dskip_of(k == 0 ? d.input_skip_slot : s->eb[k - 1].slot);
-        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy)) != PULSE_OK) return ps;
+        if ((ps = block_backward(s, r, b, xin, dy, o, dtemb, st, k, sy, prev_dy)) != PULSE_OK)
+          return ps;
+        prev_dy = dy.s0.ptr;
         cur ^= 1;
       }
     }
