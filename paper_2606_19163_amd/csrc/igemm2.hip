@@ -76,6 +76,8 @@ struct CfgC {
   static_assert(BK == 32 || BK == 64, "K-step");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert(16 * LDC * 4 <= STAGES * STAGE, "epilogue slice must fit the stages");
+  static_assert((2 * 16 * LDC + 4 * BN) * 4 <= STAGES * STAGE,
+                "GroupNorm-backward slices and constants must fit the stages");
   static_assert(STAGES * STAGE <= 160 * 1024, "LDS");
   static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "whole wave loads");
   static_assert(WLA % NW == 0, "A wave loads must split evenly over the waves");
@@ -285,7 +287,10 @@ __device__ __forceinline__ void acc16_to_lds(float* ct, int wn, int lane, int i,
 // CONV mode
 // ---------------------------------------------------------------------------
 
-template <class C>
+// GNB: the instance that writes the GroupNorm-backward sums (a.gnb) of a
+// plain output (no bias, timestep row, residual, copy, statistics or K
+// split); the others never do, so neither pays for the other's registers.
+template <class C, bool GNB = false>
 __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // the body exists for the device pass only (the host pass emits the launch stub)
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -517,9 +522,12 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   constexpr int NV8 = C::BN / 8;
   constexpr int NTK = (16 * NV8 + C::NT - 1) / C::NT;  // tasks per thread and slice
   static_assert(C::BN <= C::NT, "one thread per output column for the statistics");
-  const bool stats = a.stats != nullptr;
-  const bool raw = a.ksplit > 1;  // raw partial; the finalize adds the epilogue terms
-  const bool has_res = a.resid.s0.ptr != nullptr;
+  const bool stats = !GNB && a.stats != nullptr;
+  const bool raw = !GNB && a.ksplit > 1;  // raw partial; the finalize adds the epilogue terms
+  const bool has_res = !GNB && a.resid.s0.ptr != nullptr;
+  const float* const bias = GNB ? nullptr : a.bias;
+  const float* const rowvec = GNB ? nullptr : a.rowvec;
+  void* const out2 = GNB ? nullptr : a.out2;
   // A thread's tasks keep their row within a slice and their 8 columns in
   // every slice: the bias and, for a tile inside one image, its timestep
   // row are loaded once; each slice's residual is loaded a slice ahead.
@@ -538,13 +546,13 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) cb[k][q] = cr[k][q] = rres[k][q] = 0.f;
     if (tok[k] && !raw) {
-      if (a.bias) {
+      if (bias) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) cb[k][q] = a.bias[tnc[k] + q];
+        for (int q = 0; q < 8; ++q) cb[k][q] = bias[tnc[k] + q];
       }
-      if (a.rowvec && uni) {
+      if (rowvec && uni) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) cr[k][q] = a.rowvec[(long)img0 * a.N + tnc[k] + q];
+        for (int q = 0; q < 8; ++q) cr[k][q] = rowvec[(long)img0 * a.N + tnc[k] + q];
       }
     }
   }
@@ -557,6 +565,43 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   };
   if (has_res && !raw) load_res(0, 0);
   float csum = 0.f, csq = 0.f;
+  // GroupNorm-backward sums (a.gnb; whole tiles inside image img0, no K
+  // split).  The folded per-channel constants of the tile's columns sit in
+  // LDS after the staging slice (scale, shift, rstd, -mean * rstd); each
+  // slice's dz and dz * xhat go to LDS and thread t < BN adds column t over
+  // the slice's rows, as for the output statistics.  x of the next slice is
+  // in flight while the current one is processed.
+  constexpr bool gnb = GNB;
+  float* gk = ct + 2 * 16 * C::LDC;  // [4][BN]
+  uint4 gxr[NTK];
+#pragma unroll
+  for (int k = 0; k < NTK; ++k) gxr[k] = uint4{0u, 0u, 0u, 0u};
+  auto load_gx = [&](int g, int i) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < NTK; ++k) {
+      const long m = m0 + g * C::WM + i * 16 + trow[k];
+      if (tok[k] && m < P) {
+        const VIn& x = a.gnb_x;
+        const int c = tnc[k];
+        const Src& sx = c < x.c0 ? x.s0 : x.s1;
+        gxr[k] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(sx.ptr) + m * sx.C +
+                                                 (c < x.c0 ? c : c - x.c0));
+      }
+    }
+  };
+  float gsz = 0.f, gsx = 0.f;
+  if (gnb) {
+    load_gx(0, 0);
+    if (tid < C::BN && n0 + tid < a.N) {
+      const int c = n0 + tid;
+      const int gi = img0 * a.gnb_G + c / (a.N / a.gnb_G);
+      const float rs = a.gnb_rstd[gi];
+      gk[tid] = a.gnb_scale[(long)img0 * a.N + c];
+      gk[C::BN + tid] = a.gnb_shift[(long)img0 * a.N + c];
+      gk[2 * C::BN + tid] = rs;
+      gk[3 * C::BN + tid] = -a.gnb_mean[gi] * rs;
+    }
+  }
 #pragma unroll 1
   for (int g = 0; g < C::WAVES_M; ++g) {
 #pragma unroll
@@ -574,6 +619,15 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         else if (g + 1 < C::WAVES_M)
           load_res(g + 1, 0);
       }
+      uint4 xcur[NTK];
+#pragma unroll
+      for (int k = 0; k < NTK; ++k) xcur[k] = gxr[k];
+      if (gnb) {
+        if (i + 1 < C::TM)
+          load_gx(g, i + 1);
+        else if (g + 1 < C::WAVES_M)
+          load_gx(g + 1, 0);
+      }
 #pragma unroll
       for (int k = 0; k < NTK; ++k) {
         const int row = trow[k];
@@ -590,16 +644,16 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
           continue;
         }
         float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-        if (a.bias) {
+        if (bias) {
 #pragma unroll
           for (int q = 0; q < 8; ++q) v[q] += cb[k][q];
         }
-        if (a.rowvec) {
+        if (rowvec) {
           if (uni) {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] += cr[k][q];
           } else {
-            const float* rv = a.rowvec + (long)(m / HW) * a.N + n;
+            const float* rv = rowvec + (long)(m / HW) * a.N + n;
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] += rv[q];
           }
@@ -609,7 +663,28 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
           for (int q = 0; q < 8; ++q) v[q] += rcur[k][q];
         }
         st8(a.out, a.out_dtype, a.ldo, m, n, v);
-        if (a.out2) st8(a.out2, a.out_dtype, a.ldo, m, n, v);
+        if (out2) st8(out2, a.out_dtype, a.ldo, m, n, v);
+        if (gnb) {
+          // da as stored (the separate backward pass reads the bf16 tensor);
+          // dz to the staging slice, dz * xhat to the one after it
+          const uint32_t xw[4] = {xcur[k].x, xcur[k].y, xcur[k].z, xcur[k].w};
+          const float* kc = gk + (n - n0);
+          float dzv[8], dxv[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float x = __uint_as_float(q & 1 ? xw[q / 2] & 0xffff0000u : xw[q / 2] << 16);
+            const float d = a.out_dtype == DT_BF16 ? bf2f(f2bf(v[q])) : v[q];
+            const float dz = d * dsilu_f(x * kc[q] + kc[C::BN + q]);
+            dzv[q] = dz;
+            dxv[q] = dz * (x * kc[2 * C::BN + q] + kc[3 * C::BN + q]);
+          }
+          float4* w = reinterpret_cast<float4*>(src);
+          w[0] = make_float4(dzv[0], dzv[1], dzv[2], dzv[3]);
+          w[1] = make_float4(dzv[4], dzv[5], dzv[6], dzv[7]);
+          float4* w2 = reinterpret_cast<float4*>(src + 16 * C::LDC);
+          w2[0] = make_float4(dxv[0], dxv[1], dxv[2], dxv[3]);
+          w2[1] = make_float4(dxv[4], dxv[5], dxv[6], dxv[7]);
+        }
         if (stats) {
           float4* w = reinterpret_cast<float4*>(src);
           w[0] = make_float4(bf2f(f2bf(v[0])), bf2f(f2bf(v[1])), bf2f(f2bf(v[2])),
@@ -630,6 +705,17 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
         }
         __syncthreads();
       }
+      if (gnb) {
+        // rows past P hold no task's values: only whole tiles take this path
+        if (tid < C::BN) {
+#pragma unroll 4
+          for (int row = 0; row < 16; ++row) {
+            gsz += ct[row * C::LDC + tid];
+            gsx += ct[(16 + row) * C::LDC + tid];
+          }
+        }
+        __syncthreads();
+      }
     }
   }
   if (stats && tid < C::BN && n0 + tid < a.N) {
@@ -638,6 +724,12 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     float* dst = a.stats + ((long)img * (HW / C::BM) + chunk) * 2 * a.N + n0 + tid;
     dst[0] = csum;
     dst[a.N] = csq;
+  }
+  if (gnb && tid < C::BN && n0 + tid < a.N) {
+    const int chunk = (int)(m0 - (long)img0 * HW) / C::BM;
+    float* dst = a.gnb + ((long)img0 * (HW / C::BM) + chunk) * 2 * a.N + n0 + tid;
+    dst[0] = gsz;
+    dst[a.N] = gsx;
   }
 #else
   (void)a;
@@ -944,12 +1036,20 @@ using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
 template <class C>
 static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
   // output statistics need whole tiles inside one image and no K split
-  if (a.stats && (a.ksplit > 1 || a.g.hw() % C::BM != 0)) return hipErrorInvalidValue;
+  if ((a.stats || a.gnb) && (a.ksplit > 1 || a.g.hw() % C::BM != 0)) return hipErrorInvalidValue;
+  if (a.gnb && (a.gnb_G < 1 || a.N % a.gnb_G != 0 || a.resid.s0.ptr || a.bias || a.rowvec ||
+                a.out2 || a.stats || a.out_dtype != DT_BF16 || a.gnb_x.s0.dtype != DT_BF16 ||
+                (a.gnb_x.c0 < a.gnb_x.C && a.gnb_x.s1.dtype != DT_BF16) || a.gnb_x.add))
+    return hipErrorInvalidValue;
   const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
   const int ks = a.ksplit > 1 ? a.ksplit : 1;
-  hipLaunchKernelGGL(igemm2_conv<C>, dim3((unsigned)(tilesM * tilesN * ks)), dim3(C::NT), 0, st,
-                     a);
+  if (a.gnb)
+    hipLaunchKernelGGL((igemm2_conv<C, true>), dim3((unsigned)(tilesM * tilesN * ks)), dim3(C::NT),
+                       0, st, a);
+  else
+    hipLaunchKernelGGL((igemm2_conv<C, false>), dim3((unsigned)(tilesM * tilesN * ks)),
+                       dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || ks == 1) return e;
   const long vec = a.g.pixels() * (a.N / 8);

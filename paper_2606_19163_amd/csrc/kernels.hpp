@@ -49,6 +49,18 @@ struct GemmArgs {
   // per-channel sum and sum of squares of the output as stored (bf16), one
   // row per (image, M-tile): [B][H*W / BM][2][N]; null: not computed
   float* stats;
+  // Same conditions: the GroupNorm+SiLU backward sums of the output taken as
+  // the gradient da of a = SiLU(GN(x)): per channel, sum dz and sum dz*xhat
+  // with dz = da (as stored) * SiLU'(x*scale + shift) and xhat =
+  // (x - mean) * rstd, one row per (image, M-tile): [B][H*W / BM][2][N];
+  // null: not computed.  scale/shift [B][N], mean/rstd [B][gnb_G].
+  float* gnb;
+  VIn gnb_x;
+  const float* gnb_scale;
+  const float* gnb_shift;
+  const float* gnb_mean;
+  const float* gnb_rstd;
+  int gnb_G;
 };
 
 // implicit GEMM, register-staged (igemm.hip): the fp32 stage and bf16

@@ -104,6 +104,7 @@ struct pulse_stage {
   size_t esz = 4;
   bool k64 = false;     // every channel count is a multiple of 64
   int conv_tile_force = -1, wgrad_tile_force = -1;  // tuning overrides (env)
+  bool no_gnb = false;  // PULSE_NO_GNB: GroupNorm-backward sums by their own pass
   int conv_ksplit_cap = 16;  // largest conv K split (env PULSE_CONV_KSPLIT_MAX)
   Geo geo{};
   long P = 0;
@@ -366,6 +367,7 @@ pulse_status build_layout(pulse_stage* s) {
     // tile overrides (tuning) index Tile2; they apply on the LDS-DMA path
     const int ct = env_int("PULSE_CONV_TILE", -1), wt = env_int("PULSE_WGRAD_TILE", -1);
     s->conv_ksplit_cap = std::max(1, std::min(16, env_int("PULSE_CONV_KSPLIT_MAX", 16)));
+    s->no_gnb = env_int("PULSE_NO_GNB", 0) != 0;
     const bool v2 = s->dtype == DT_BF16 && k64;
     s->conv_tile_force = (v2 && ct >= 0 && ct <= TILE2_CONV_LAST) ? ct : -1;
     s->wgrad_tile_force = (v2 && wt >= TILE2_WGRAD_FIRST && wt <= TILE2_WGRAD_LAST) ? wt : -1;
@@ -698,6 +700,16 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
     else
       a.stats = nullptr;
   }
+  // GroupNorm-backward sums from the epilogue: the same conditions
+  if (a.gnb) {
+    const int bm = info_of(s, tile).bm;
+    const long rows = s->geo.hw() % bm == 0 ? (long)s->geo.B * (s->geo.hw() / bm) : 0;
+    if (stats_chunks && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
+        (size_t)rows * 2 * a.N <= s->red_cap && !s->no_gnb)
+      *stats_chunks = s->geo.hw() / bm;
+    else
+      a.gnb = nullptr;
+  }
   if (uses_v2(s))
     HIPCHK(launch_conv2(a, tile, st));
   else
@@ -744,10 +756,19 @@ Seg seg1(int begin, int C, const VIn& in, float* grad = nullptr) {
 // With `stats`, the output's GroupNorm partial sums come from the conv's
 // epilogue when the kernel can produce them: *stats_chunks receives their
 // chunks per image, or 0 when they were not computed.
+// The GroupNorm+SiLU backward sums a data-gradient conv can produce for the
+// GroupNorm whose output gradient it computes (see GemmArgs::gnb).
+struct GnbReq {
+  float* partial;
+  VIn x;
+  const float *scale, *shift, *mean, *rstd;
+};
+
 pulse_status conv_fwd(pulse_stage* s, int N, std::initializer_list<Seg> segs, const void* W,
                       int ldb, const float* bias, const float* rowvec, const VIn& resid,
                       void* out, void* out2, int out_dtype, hipStream_t st,
-                      float* stats = nullptr, int* stats_chunks = nullptr) {
+                      float* stats = nullptr, int* stats_chunks = nullptr,
+                      const GnbReq* gnb = nullptr) {
   GemmArgs a = gemm_base(s);
   a.M = (int)s->P;
   a.N = N;
@@ -767,6 +788,15 @@ pulse_status conv_fwd(pulse_stage* s, int N, std::initializer_list<Seg> segs, co
   a.out_dtype = out_dtype;
   a.ldo = N;
   a.stats = stats;
+  if (gnb) {
+    a.gnb = gnb->partial;
+    a.gnb_x = gnb->x;
+    a.gnb_scale = gnb->scale;
+    a.gnb_shift = gnb->shift;
+    a.gnb_mean = gnb->mean;
+    a.gnb_rstd = gnb->rstd;
+    a.gnb_G = s->G;
+  }
   return run_conv(s, a, st, stats_chunks);
 }
 
@@ -824,10 +854,12 @@ pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x
 }
 
 // GroupNorm+SiLU backward: da (fp32 [P][C]) -> o (split store + addends)
+// pre_chunks > 0: the per-chunk sums are already in the reduction buffer
+// (written by the data-gradient conv's epilogue, that many chunks per image).
 pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
                          const float* gamma, float* dgamma, float* dbeta, const void* da_ptr,
-                         const GnBwdOut& o, hipStream_t st) {
-  const RedGrid rg = red_grid(s->geo, x.C);
+                         const GnBwdOut& o, hipStream_t st, int pre_chunks = 0) {
+  RedGrid rg = red_grid(s->geo, x.C);
   float* red = s->sf(s->s_red);
   float* coef = s->sf(s->s_coef);
   const Src da = src_of(da_ptr, s->dtype, x.C);
@@ -835,9 +867,15 @@ pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& 
   const float* rstd = reinterpret_cast<const float*>(row + g.rstd);
   const float* scale = reinterpret_cast<const float*>(row + g.scale);
   const float* shift = reinterpret_cast<const float*>(row + g.shift);
-  HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
+  if (pre_chunks > 0) {
+    rg.chunks = pre_chunks;
+  } else {
+    HIPCHK(launch_gn_bwd_partial(da, x, s->geo, rg, scale, shift, mean, rstd, s->G, red, st));
+  }
   HIPCHK(launch_gn_bwd_finalize(red, s->geo, rg, x.C, s->G, gamma, coef, dgamma, dbeta, st));
-  HIPCHK(launch_gn_bwd_apply(da, x, s->geo, rg, scale, shift, mean, rstd, gamma, coef, s->G, o,
+  // the apply's block grid is its own
+  const RedGrid ra = red_grid(s->geo, x.C);
+  HIPCHK(launch_gn_bwd_apply(da, x, s->geo, ra, scale, shift, mean, rstd, gamma, coef, s->G, o,
                              st));
   return PULSE_OK;
 }
@@ -1030,8 +1068,18 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // data gradients are stored in the stage dtype (the MFMA operands they feed
   // are rounded to it anyway; the GroupNorm backward reads them once more)
   void* da = s->scratch(s->s_da);
+  // the GroupNorm-backward sums of GN2 (input h1) come from this conv's
+  // epilogue when it can produce them (gn2_chunks > 0)
+  float* red = s->sf(s->s_red);
+  const VIn h1v = vin1(row + b.h1, dt, b.cout);
+  const GnbReq gnb2{red, h1v, reinterpret_cast<const float*>(row + b.gn2.scale),
+                    reinterpret_cast<const float*>(row + b.gn2.shift),
+                    reinterpret_cast<const float*>(row + b.gn2.mean),
+                    reinterpret_cast<const float*>(row + b.gn2.rstd)};
+  int gn2_chunks = 0;
   if ((ps = conv_fwd(s, b.cout, {seg3(0, b.cout, dout)}, s->ws + b.wd2, 9 * b.cout, nullptr,
-                     nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
+                     nullptr, vnone(), da, nullptr, dt, st, nullptr, &gn2_chunks, &gnb2)) !=
+      PULSE_OK)
     return ps;
   void* dxs = s->scratch(s->s_dxs);
   if (b.conv_sc) {
@@ -1051,9 +1099,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     o2.c_split = b.cout;
     o2.add0 = vnone();
     o2.chan_partial = s->sf(s->s_chp[par]);
-    const VIn h1v = vin1(row + b.h1, dt, b.cout);
     if ((ps = gn_backward(s, row, b.gn2, h1v, s->pp(b.g2), s->gp(b.g2), s->gp(b.be2), da, o2,
-                          st)) != PULSE_OK)
+                          st, gn2_chunks)) != PULSE_OK)
       return ps;
   }
   // conv1 weight and data gradients
@@ -1074,8 +1121,14 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     return ps;
   if ((ps = mark_side(s, s->ev_w1[par])) != PULSE_OK) return ps;
   sy.w1[par] = true;
+  const GnbReq gnb1{red, xin, reinterpret_cast<const float*>(row + b.gn1.scale),
+                    reinterpret_cast<const float*>(row + b.gn1.shift),
+                    reinterpret_cast<const float*>(row + b.gn1.mean),
+                    reinterpret_cast<const float*>(row + b.gn1.rstd)};
+  int gn1_chunks = 0;
   if ((ps = conv_fwd(s, b.cin, {seg3(0, b.cout, dh1v)}, s->ws + b.wd1, 9 * b.cout, nullptr,
-                     nullptr, vnone(), da, nullptr, dt, st)) != PULSE_OK)
+                     nullptr, vnone(), da, nullptr, dt, st, nullptr, &gn1_chunks, &gnb1)) !=
+      PULSE_OK)
     return ps;
   // GN1 backward + residual path -> gradient w.r.t. the block input
   o.add0 = b.conv_sc ? vin1(dxs, dt, b.cin) : dout;
@@ -1085,7 +1138,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // stream an event round trip)
   if (prev_dout && o.dst0 == prev_dout)
     if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
-  return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st);
+  return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st,
+                     gn1_chunks);
 }
 
 pulse_status check_ptr(const void* p, const char* what) {
