@@ -1051,7 +1051,7 @@ static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((igemm2_conv<C, false>), dim3((unsigned)(tilesM * tilesN * ks)),
                        dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || ks == 1) return e;
+  if (e != hipSuccess || ks == 1 || a.skip_finalize) return e;
   const long vec = a.g.pixels() * (a.N / 8);
   const long blocks = std::min<long>((vec + 255) / 256, 2048);
   hipLaunchKernelGGL(conv_splitk_finalize, dim3((unsigned)blocks), dim3(256), 0, st, a);

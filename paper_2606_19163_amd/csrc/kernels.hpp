@@ -61,6 +61,9 @@ struct GemmArgs {
   const float* gnb_mean;
   const float* gnb_rstd;
   int gnb_G;
+  // host side, K split: launch only the GEMM (the caller runs
+  // launch_splitk_finalize_stats, which also reduces the statistics)
+  int skip_finalize;
 };
 
 // implicit GEMM, register-staged (igemm.hip): the fp32 stage and bf16
@@ -113,6 +116,11 @@ RedGrid red_grid(const Geo& g, int C);
 hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float* partial,
                                    hipStream_t st, void* copy = nullptr);
 // mean/rstd [B][G] and the folded affine scale/shift [B][C].
+// K-split conv finalize that also reduces the output: out = sum_z part[z]
+// (fixed order) + bias + rowvec + residual (bf16), and the per-channel sum
+// and sum of squares of the stored output per (image, chunk of the reduction
+// grid rg over N channels) row of a.stats.
+hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st);
 hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                     int G, float eps, const float* gamma, const float* beta,
                                     float* mean, float* rstd, float* scale, float* shift,

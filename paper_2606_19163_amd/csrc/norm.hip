@@ -673,6 +673,75 @@ __global__ __launch_bounds__(256) void k_chan_sum_partial(VIn v, Geo g, RedGrid 
   lane_reduce_store<8>(acc, sm, rg, v.C, base, nullptr);
 }
 
+// K-split conv finalize with the statistics of its output, on the grid of
+// the GroupNorm kernels: thread (channel vector, pixel lane) sums the fp32
+// partials of its 8 channels in split order (two pixels per step, their
+// loads in flight together), adds bias, the timestep row and the residual,
+// stores bf16 and accumulates the sum and sum of squares of the stored
+// values; the lanes meet in LDS (one row per chunk).  (The GroupNorm-
+// backward sums measured slower here than in their own pass.)
+__global__ __launch_bounds__(256) void k_splitk_finalize_stats(GemmArgs a, RedGrid rg) {
+  __shared__ float sm[256 * 16];
+  const Geo g = a.g;
+  const int N = a.N;
+  const Range r = block_range(g, rg, N);
+  float acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  if (r.active) {
+    const long zs = g.pixels() * (long)N;
+    float cb[8], cr[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) cb[q] = cr[q] = 0.f;
+    if (a.bias) load8f(a.bias + r.c, cb);
+    if (a.rowvec) load8f(a.rowvec + (long)r.b * N + r.c, cr);
+    const long img0 = (long)r.b * g.hw();
+    constexpr int U = 2;
+    for (int p = r.p0 + threadIdx.y; p < r.p1; p += U * rg.py) {
+      long px[U];
+      float w[U];
+      step_pixels<U>(p, rg.py, r.p1, img0, px, w);
+      float vv[U][8];
+#pragma unroll
+      for (int u = 0; u < U; ++u) load8f(a.part + px[u] * N + r.c, vv[u]);
+      for (int zz = 1; zz < a.ksplit; ++zz) {
+        float t[U][8];
+#pragma unroll
+        for (int u = 0; u < U; ++u) load8f(a.part + zz * zs + px[u] * N + r.c, t[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) vv[u][q] += t[u][q];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (p + u * rg.py >= r.p1) break;
+        float* v = vv[u];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] += cb[q];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] += cr[q];
+        if (a.resid.s0.ptr) {
+          float t[8];
+          ld8(a.resid.s0, px[u], r.c, t);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] += t[q];
+        }
+        st8(a.out, DT_BF16, a.ldo, px[u], r.c, v);
+        if (a.out2) st8(a.out2, DT_BF16, a.ldo, px[u], r.c, v);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float b = bf2f(f2bf(v[q]));  // as stored
+          acc[q] += b;
+          acc[8 + q] += b * b;
+        }
+      }
+    }
+  }
+  float* base = a.stats + ((long)r.b * rg.chunks + blockIdx.y) * 2 * N;
+  lane_reduce_store<16>(acc, sm, rg, N, base, base + N);
+}
+
 dim3 red_dims(const Geo& g, RedGrid rg, int C) {
   (void)C;
   return dim3(g.B, rg.chunks, rg.zb);
@@ -717,6 +786,15 @@ hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float
                             : (add ? k_gn_stats_partial<DT_F32, true>
                                    : k_gn_stats_partial<DT_F32, false>);
   hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, x, g, rg, partial, copy);
+  return hipGetLastError();
+}
+
+hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st) {
+  if (a.ksplit < 2 || !a.part || !a.stats || a.gnb || a.out_dtype != DT_BF16 || a.ldo != a.N ||
+      a.N % 8 != 0 || (a.resid.s0.ptr && (a.resid.s0.dtype != DT_BF16 || a.resid.add)))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_splitk_finalize_stats, red_dims(a.g, rg, a.N), red_block(rg), 0, st, a,
+                     rg);
   return hipGetLastError();
 }
 

@@ -688,32 +688,43 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
     e1 = next_event(s);
     if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
-  // output statistics from the epilogue: LDS-DMA tiles, no K split, whole
-  // tiles per image, and room in the reduction buffer; else the caller's
-  // GroupNorm computes them itself (stats_chunks stays 0)
-  if (a.stats) {
+  // Output statistics, or the GroupNorm-backward sums, from the conv: its
+  // epilogue without a K split (whole tiles per image); with a K split the
+  // statistics (not the backward sums, which measured slower there) from
+  // the finalize on the reduction grid; with room in the reduction buffer.
+  // Otherwise the caller's GroupNorm computes them itself (stats_chunks
+  // stays 0).
+  const bool want = (a.stats || a.gnb) && stats_chunks && uses_v2(s) &&
+                    !(a.gnb && s->no_gnb);
+  bool red_fin = false;
+  if (want && a.ksplit == 1) {
     const int bm = info_of(s, tile).bm;
     const long rows = s->geo.hw() % bm == 0 ? (long)s->geo.B * (s->geo.hw() / bm) : 0;
-    if (stats_chunks && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
-        (size_t)rows * 2 * a.N <= s->red_cap)
+    if (rows > 0 && (size_t)rows * 2 * a.N <= s->red_cap)
       *stats_chunks = s->geo.hw() / bm;
-    else
-      a.stats = nullptr;
+  } else if (want && a.stats && a.N % 8 == 0 && a.ldo == a.N && a.out_dtype == DT_BF16) {
+    const RedGrid rg = red_grid(s->geo, a.N);
+    if ((size_t)s->geo.B * rg.chunks * 2 * a.N <= s->red_cap) {
+      *stats_chunks = rg.chunks;
+      red_fin = true;
+    }
   }
-  // GroupNorm-backward sums from the epilogue: the same conditions
-  if (a.gnb) {
-    const int bm = info_of(s, tile).bm;
-    const long rows = s->geo.hw() % bm == 0 ? (long)s->geo.B * (s->geo.hw() / bm) : 0;
-    if (stats_chunks && uses_v2(s) && a.ksplit == 1 && rows > 0 &&
-        (size_t)rows * 2 * a.N <= s->red_cap && !s->no_gnb)
-      *stats_chunks = s->geo.hw() / bm;
-    else
-      a.gnb = nullptr;
+  if (!stats_chunks || *stats_chunks == 0) {
+    a.stats = nullptr;
+    a.gnb = nullptr;
   }
-  if (uses_v2(s))
+  if (red_fin) {
+    GemmArgs k = a;  // the GEMM alone; the finalize below reduces
+    k.stats = nullptr;
+    k.gnb = nullptr;
+    k.skip_finalize = 1;
+    HIPCHK(launch_conv2(k, tile, st));
+    HIPCHK(launch_splitk_finalize_stats(a, red_grid(s->geo, a.N), st));
+  } else if (uses_v2(s)) {
     HIPCHK(launch_conv2(a, tile, st));
-  else
+  } else {
     HIPCHK(launch_conv(a, tile, st));
+  }
   if (s->timing && e0 && e1) {
     HIPCHK(hipEventRecord(e1, st));
     s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K, conv_bytes(s, a)});
