@@ -658,13 +658,15 @@ double vin_bytes(const VIn& v, double pixels) {
 
 // Compulsory HBM bytes of one conv-mode launch: every input element once
 // (the 3x3 taps re-read the same pixels), the weights once, the residual,
-// and every output written.
+// the norm input that a launch reducing GroupNorm-backward sums reads, and
+// every output written.
 double conv_bytes(const pulse_stage* s, const GemmArgs& a) {
   const double P = (double)a.M;
   double b = 0.0;
   for (int i = 0; i < a.nseg; ++i) b += vin_bytes(a.seg[i].in, P);
   b += (double)a.N * a.K * elt_bytes(s->dtype);
   b += vin_bytes(a.resid, P);
+  if (a.gnb) b += vin_bytes(a.gnb_x, P);
   b += P * a.N * elt_bytes(a.out_dtype) * (a.out2 ? 2.0 : 1.0);
   return b;
 }
