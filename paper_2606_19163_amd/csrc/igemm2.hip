@@ -177,6 +177,12 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
   return x * q + (x < r ? x : r) + (bid >> 3);
 }
 
+// n / d with the launcher's reciprocal M of d (rcp_u32): a multiply-high,
+// or a divide where M is 0
+__device__ __forceinline__ uint32_t div_rcp(uint32_t n, uint32_t d, uint32_t M) {
+  return M ? __umulhi(n, M) : (d < 2 ? n : n / d);
+}
+
 __device__ __forceinline__ uint32_t lds_u32(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
@@ -307,7 +313,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   const int tilesN = (a.N + C::BN - 1) / C::BN;
   const int ntiles = (int)((P + C::BM - 1) / C::BM) * tilesN;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
-  const int z = lb / ntiles;
+  const int z = (int)div_rcp((uint32_t)lb, (uint32_t)ntiles, a.rcp_nt);
   const int bid = lb - z * ntiles;
   // Tile order within the XCD's range.  Up to 8 column tiles: row-major, a
   // row tile's A rows are reused across all of N and B is small.  Wider N:
@@ -316,8 +322,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // (row-major would stream the whole B through L2 once per row tile).
   int tn, tm;
   if (tilesN <= 8) {
-    tn = bid % tilesN;
-    tm = bid / tilesN;
+    tm = (int)div_rcp((uint32_t)bid, (uint32_t)tilesN, a.rcp_tn);
+    tn = bid - tm * tilesN;
   } else {
     constexpr int GM = 8;
     const int tilesM = ntiles / tilesN;
@@ -337,6 +343,12 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // this lane's wave loads: wl = wave + u * NW; A rows first, then B rows.
   // Lane (row rl = lane / 8 of the load, slot lane % 8) fetches logical chunk
   // (lane % 8) ^ swz(row).
+  // Image row and column of a tile pixel without divides: the tile's first
+  // pixel is at offset rem0 of its image, pixel m0 + r at rem0 + r < HW + BM,
+  // whose quotient by W (a row count that may run into the next images) and
+  // that row's remainder by H come from multiply-highs.
+  const uint32_t rem0 =
+      (uint32_t)m0 - div_rcp((uint32_t)m0, (uint32_t)HW, a.rcp_hw) * (uint32_t)HW;
   uint32_t ppix[C::NU], pmask[C::NU], coff[C::NU];
 #pragma unroll
   for (int u = 0; u < C::NU; ++u) {
@@ -347,25 +359,23 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     if (u < C::UA) {
       const int r = wl * C::RPL + lane / C::CPR;
       const long m = m0 + r;
-      uint32_t mask = 0;
-      if (m < P) {
-        const int img = (int)(m / HW);
-        const int rem = (int)(m - (long)img * HW);
-        const int h = rem / W;
-        const int w = rem - h * W;
-#pragma unroll
-        for (int t = 0; t < 9; ++t) {
-          const int hh = h + t / 3 - 1, ww = w + t % 3 - 1;
-          if (hh >= 0 && hh < H && ww >= 0 && ww < W) mask |= 1u << t;
-        }
-      }
+      const uint32_t t = rem0 + (uint32_t)r;
+      const uint32_t hr = div_rcp(t, (uint32_t)W, a.rcp_w);
+      const uint32_t w = t - hr * (uint32_t)W;
+      const uint32_t h = hr - div_rcp(hr, (uint32_t)H, a.rcp_h) * (uint32_t)H;
+      // taps t = 3 (dy + 1) + dx + 1: rows dy valid in rv, columns dx in cv
+      const uint32_t rv = (h > 0 ? 1u : 0u) | 2u | (h + 1 < (uint32_t)H ? 4u : 0u);
+      const uint32_t cv = (w > 0 ? 1u : 0u) | 2u | (w + 1 < (uint32_t)W ? 4u : 0u);
+      const uint32_t mask = ((rv & 1u) ? cv : 0u) | ((rv & 2u) ? cv << 3 : 0u) |
+                            ((rv & 4u) ? cv << 6 : 0u);
       ppix[u] = (uint32_t)(m < P ? m : 0);
-      pmask[u] = mask;
+      pmask[u] = m < P ? mask : 0u;
       coff[u] = (uint32_t)(((lane % C::CPR) ^ swz_row<C::RB>(r)) * 16);
     } else if (wl < C::WL) {
       const int r = (wl - C::WLA) * C::RPL + lane / C::CPR;
       const int n = n0 + r;
-      coff[u] = n < a.N ? (uint32_t)((long)n * a.ldb * 2 + ((lane % C::CPR) ^ swz_row<C::RB>(r)) * 16)
+      coff[u] = n < a.N ? (uint32_t)n * (uint32_t)(a.ldb * 2) +
+                              (uint32_t)(((lane % C::CPR) ^ swz_row<C::RB>(r)) * 16)
                         : OOB;
     }
   }
@@ -381,7 +391,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // divisions.  The weight column of (tap, channel c) is begin + tap*C + c.
   SegRt cur = seg_rt(a.seg[0], P);
   int iseg = 0, itap = 0, icb = 0, idy, idx;
-  {
+  if (kt0 > 0) {
     int q = kt0;  // first K-step of this split
     while (iseg < 2 && q >= cur.taps * (cur.C / C::BK)) {
       q -= cur.taps * (cur.C / C::BK);
@@ -392,6 +402,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     itap = q - (q / cur.taps) * cur.taps;
     idy = cur.taps == 9 ? itap / 3 - 1 : 0;
     idx = cur.taps == 9 ? itap % 3 - 1 : 0;
+  } else {
+    idy = idx = cur.taps == 9 ? -1 : 0;
   }
   auto advance = [&]() __attribute__((always_inline)) {
     ++itap;
@@ -532,8 +544,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
   // every slice: the bias and, for a tile inside one image, its timestep
   // row are loaded once; each slice's residual is loaded a slice ahead.
   const long mlast = (m0 + C::BM < P ? m0 + C::BM : P) - 1;
-  const int img0 = (int)(m0 / HW);
-  const bool uni = mlast / HW == img0;
+  const int img0 = (int)div_rcp((uint32_t)m0, (uint32_t)HW, a.rcp_hw);
+  const bool uni = (int)div_rcp((uint32_t)mlast, (uint32_t)HW, a.rcp_hw) == img0;
   int trow[NTK], tnc[NTK];
   bool tok[NTK];
   float cb[NTK][8], cr[NTK][8], rres[NTK][8];
@@ -719,7 +731,7 @@ __global__ __launch_bounds__(C::NT) void igemm2_conv(GemmArgs a) {
     }
   }
   if (stats && tid < C::BN && n0 + tid < a.N) {
-    const int img = (int)(m0 / HW);
+    const int img = img0;
     const int chunk = (int)(m0 - (long)img * HW) / C::BM;
     float* dst = a.stats + ((long)img * (HW / C::BM) + chunk) * 2 * a.N + n0 + tid;
     dst[0] = csum;
@@ -759,12 +771,13 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int H = a.g.H, W = a.g.W, HW = a.g.H * a.g.W;
   const long P = a.g.pixels();
-  const int z = lb / ntiles;
+  const int z = (int)div_rcp((uint32_t)lb, (uint32_t)ntiles, a.rcp_nt);
   const int tile = lb - z * ntiles;
   const long pbeg = (long)z * a.kchunk;
   const long pend = (pbeg + a.kchunk < P) ? pbeg + a.kchunk : P;
-  const int m0 = (tile / tilesN) * C::BM;
-  const int n0 = (tile % tilesN) * C::BN;
+  const int tmi = (int)div_rcp((uint32_t)tile, (uint32_t)tilesN, a.rcp_tn);
+  const int m0 = tmi * C::BM;
+  const int n0 = (tile - tmi * tilesN) * C::BN;
 
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gy.s0.ptr, P * a.gy.s0.C * 2);
   const uint32_t gpitch = (uint32_t)(a.gy.s0.C * 2);
@@ -803,7 +816,8 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
         const int s = seg_of(a.nseg, a.seg[1].begin, a.seg[2].begin, n);
         const Seg& sg = s == 0 ? a.seg[0] : (s == 1 ? a.seg[1] : a.seg[2]);
         const int rr = n - sg.begin;
-        const int tap = rr / sg.C;
+        const uint32_t rc = s == 0 ? a.rcp_segc[0] : (s == 1 ? a.rcp_segc[1] : a.rcp_segc[2]);
+        const int tap = (int)div_rcp((uint32_t)rr, (uint32_t)sg.C, rc);
         const int c = rr - tap * sg.C;
         const int t9 = sg.taps == 9 ? tap : 4;
         boy[u] = t9 / 3 - 1;
@@ -817,17 +831,19 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
       // image coordinates of pixel pbeg + r (advanced by 64 per K-step)
       const long p = pbeg + r;
       const long pp = p < P ? p : 0;
-      const int img = (int)(pp / HW);
-      const int rem = (int)(pp - (long)img * HW);
-      bh[u] = rem / W;
-      bw[u] = rem - bh[u] * W;
+      const uint32_t img = div_rcp((uint32_t)pp, (uint32_t)HW, a.rcp_hw);
+      const uint32_t rem = (uint32_t)pp - img * (uint32_t)HW;
+      const uint32_t hq = div_rcp(rem, (uint32_t)W, a.rcp_w);
+      bh[u] = (int)hq;
+      bw[u] = (int)(rem - hq * (uint32_t)W);
     }
   }
 
   // one K-step of BK pixels moves a pixel by kdw columns and kdh rows
   // (kdh < H; the carry of the columns adds at most one more row)
-  const int kdw = C::BK % W;
-  const int kdh = (C::BK / W) % H;
+  const int kq = (int)div_rcp((uint32_t)C::BK, (uint32_t)W, a.rcp_w);
+  const int kdw = C::BK - kq * W;
+  const int kdh = kq - (int)div_rcp((uint32_t)kq, (uint32_t)H, a.rcp_h) * H;
   auto issue = [&](int kt, char* base) __attribute__((always_inline)) {
     const long p0 = pbeg + (long)kt * C::BK;
 #pragma unroll
@@ -1034,7 +1050,21 @@ using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves, one block per CU
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
 
 template <class C>
-static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
+static hipError_t conv2_t(const GemmArgs& a_in, hipStream_t st) {
+  // 32-bit pixel indices and weight offsets
+  if (a_in.g.pixels() + C::BM >= (1L << 31) || (long)a_in.N * a_in.ldb * 2 >= (1L << 31))
+    return hipErrorInvalidValue;
+  GemmArgs a = a_in;
+  {
+    const long P = a.g.pixels(), HW = a.g.hw();
+    const long tN = (a.N + C::BN - 1) / C::BN, nt = ((P + C::BM - 1) / C::BM) * tN;
+    const long ks = a.ksplit > 1 ? a.ksplit : 1;
+    a.rcp_nt = rcp_u32(nt, nt * ks);
+    a.rcp_tn = rcp_u32(tN, nt);
+    a.rcp_hw = rcp_u32(HW, P + C::BM);
+    a.rcp_w = rcp_u32(a.g.W, HW + C::BM);
+    a.rcp_h = rcp_u32(a.g.H, (HW + C::BM) / a.g.W + 1);
+  }
   // output statistics need whole tiles inside one image and no K split
   if ((a.stats || a.gnb) && (a.ksplit > 1 || a.g.hw() % C::BM != 0)) return hipErrorInvalidValue;
   if (a.gnb && (a.gnb_G < 1 || a.N % a.gnb_G != 0 || a.resid.s0.ptr || a.bias || a.rowvec ||
@@ -1059,10 +1089,22 @@ static hipError_t conv2_t(const GemmArgs& a, hipStream_t st) {
 }
 
 template <class C>
-static hipError_t wgrad2_t(const GemmArgs& a, int splits, const void* zero16, hipStream_t st) {
+static hipError_t wgrad2_t(const GemmArgs& a_in, int splits, const void* zero16, hipStream_t st) {
+  if (a_in.g.pixels() >= (1L << 31)) return hipErrorInvalidValue;  // 32-bit pixel indices
+  GemmArgs a = a_in;
   const long tilesM = (a.M + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
   const long blocks = tilesM * tilesN * splits;
+  {
+    const long HW = a.g.hw();
+    a.rcp_nt = rcp_u32(tilesM * tilesN, blocks);
+    a.rcp_tn = rcp_u32(tilesN, tilesM * tilesN);
+    a.rcp_hw = rcp_u32(HW, a.g.pixels());
+    a.rcp_w = rcp_u32(a.g.W, std::max<long>(HW, C::BK));
+    a.rcp_h = rcp_u32(a.g.H, C::BK);
+    for (int i = 0; i < a.nseg && i < 3; ++i)
+      a.rcp_segc[i] = rcp_u32(a.seg[i].C, (long)a.seg[i].taps * a.seg[i].C);
+  }
   hipLaunchKernelGGL(igemm2_wgrad<C>, dim3((unsigned)blocks), dim3(C::NT), 0, st, a, zero16);
   return hipGetLastError();
 }

@@ -64,7 +64,21 @@ struct GemmArgs {
   // host side, K split: launch only the GEMM (the caller runs
   // launch_splitk_finalize_stats, which also reduces the statistics)
   int skip_finalize;
+  // set by the launchers of igemm2.hip (callers leave them 0): multiply-high
+  // reciprocals of the kernels' runtime divisors, each exact over the range
+  // it divides, or 0 where the kernel divides (see rcp_u32)
+  uint32_t rcp_w, rcp_h, rcp_hw, rcp_nt, rcp_tn;
+  uint32_t rcp_segc[3];
 };
+
+// Multiply-high reciprocal of d for quotients n / d with n <= nmax:
+// M = floor((2^32 - 1) / d) + 1 gives floor(n / d) = mulhi(n, M) whenever
+// n < 2^32 / d (the rounding error n (M - 2^32 / d) / 2^32 stays below
+// 1 / d).  0 where d < 2 or the range is too wide.
+inline uint32_t rcp_u32(uint64_t d, uint64_t nmax) {
+  if (d < 2 || nmax >= (1ull << 32) / d) return 0;
+  return (uint32_t)(0xffffffffull / d + 1);
+}
 
 // implicit GEMM, register-staged (igemm.hip): the fp32 stage and bf16
 // channel counts that are multiples of 32 but not of 64
