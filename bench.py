@@ -34,6 +34,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+# Overlapped decoder backward, measured per workload (same box, alternating
+# runs): 64x64x320 778 against 764 TFLOP/s; 32x32x640 697 against 705 (its
+# decoder's last weight GEMM then runs into the encoder's K-split convs); the
+# four-level wave 625 either way.
+OVERLAP_BWD_AUTO = ("l64",)
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the fp32 stage)
 METRIC = "stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s, 64x64x320 stage"
 
@@ -355,6 +360,10 @@ def main():
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
     ap.add_argument("--serial", action="store_true",
                     help="keep the whole backward on the stage stream (no side stream)")
+    ap.add_argument("--overlap-bwd", choices=("auto", "on", "off"), default="auto",
+                    help="start a microbatch's encoder backward beside the parameter-gradient "
+                         "tail of its decoder backward (auto: on for the workloads where "
+                         "that measured faster)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket the conv launches with HIP events")
     ap.add_argument("--library-gemm", action="store_true",
@@ -395,9 +404,15 @@ def main():
         p0, b0 = synth.make_all(descs[0], seed)
         params, bounds = [p0], [[b0]]
     stages, dev = [], []
+    overlap_on = args.overlap_bwd == "on" or (args.overlap_bwd == "auto" and
+                                              args.workload in OVERLAP_BWD_AUTO)
     for i, d in enumerate(descs):
         st = S.Stage(d)
         st.set_params(params[i])
+        # a microbatch's encoder backward starts beside the parameter-gradient
+        # tail of its decoder backward (bitwise the same results); it pays
+        # where the side stream is not the backward's bottleneck
+        st.overlap_bwd(overlap_on)
         stages.append(st)
         dev.append([{k: st.to_dev(v) for k, v in bb.items()} for bb in bounds[i]])
     dtembs = [torch.zeros((d["batch"], d["temb_dim"]), device="cuda") for d in descs]
@@ -487,6 +502,7 @@ def main():
         "microbatches_per_s": round(n_mb * args.steps / elapsed, 2),
         "gflop_per_step": round(flops_step / 1e9, 2),
         **step_stats(per),
+        "overlap_bwd": overlap_on,
     }
     if events and launches:
         achieved = kflops / (kms * 1e-3) / 1e12

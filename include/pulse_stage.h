@@ -187,6 +187,30 @@ pulse_status pulse_stage_backward(pulse_stage* st, pulse_half half, int32_t mb,
                                   const void* dout, void* din, float* dtemb_accum,
                                   void* stream);
 
+/* Overlapped decoder backward (default off).  The backward pass runs the
+ * parameter gradients (weight GEMMs, bias and timestep sums) on a second
+ * stream of the stage beside the data-gradient chain, and every backward
+ * call normally ends by making `stream` wait for that stream.  With this
+ * switch on, a DEC backward returns without that wait: the parameter-
+ * gradient work of its last block may still run, and an ENC backward of the
+ * same microbatch on the same stream starts beside it (it waits only where
+ * it writes a buffer that work still reads).  That work is ordered before
+ * everything enqueued on a stream after the next call on the stage (which
+ * joins it), or after pulse_stage_flush on that stream.  So with the switch
+ * on, the decoder half's parameter gradients and its dtemb_accum
+ * contributions are complete in `stream` order only after the next call or
+ * a flush (a device-wide synchronisation also covers them).  The results
+ * are bitwise those of the switch off.  It saves the wait where a
+ * microbatch's encoder backward follows its decoder backward on the device
+ * (a stage holding two adjacent pipeline stages, as the device with the
+ * two middle stages of a skip-collocated pipeline does). */
+pulse_status pulse_stage_overlap_bwd(pulse_stage* st, int32_t enable);
+
+/* Work enqueued on `stream` after this call is ordered after all work the
+ * stage has enqueued, on any stream, including parameter-gradient work an
+ * overlapped decoder backward left running.  Enqueues only stream waits. */
+pulse_status pulse_stage_flush(pulse_stage* st, void* stream);
+
 /* Copy `src` ([B,H,W,C_slot], stage dtype) into the activation entry of
  * (mb, slot) and mark it present: the hook by which a skip produced on
  * another device enters the cache (partial collocation, Sec. VIII-B).

@@ -94,6 +94,15 @@ pulse_status pulse::set_last_error(pulse_status s, const char* msg) {
   return s;
 }
 
+// Side-stream progress markers of one backward call: block k records w2
+// after its conv2 / shortcut parameter work (the last read of its dout) and
+// w1 after its conv1 weight gradient (the last read of its dh1); buffers
+// alternate between consecutive blocks, so block k waits for the marker of
+// the block that used the same buffer before it.
+struct BwdSync {
+  bool w2[2] = {false, false}, w1[2] = {false, false};
+};
+
 struct pulse_stage {
   // descriptor
   pulse_stage_desc d{};
@@ -136,6 +145,16 @@ struct pulse_stage {
   // concurrently with the data-gradient chain on the caller's stream
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // overlapped decoder backward (pulse_stage_overlap_bwd): a decoder
+  // backward may return with its last parameter-gradient work still on the
+  // side stream; the next call joins it, except an encoder backward of the
+  // same microbatch on the same stream, which continues beside it
+  bool overlap_bwd = false;
+  bool join_pending = false;
+  int32_t pending_mb = -1;
+  hipStream_t pending_st = nullptr;
+  BwdSync sy_pending;  // the decoder call's markers, carried into the encoder call
+  int par_pending = 0;  // parity of the decoder call's last block
   hipEvent_t ev_w2[2] = {nullptr, nullptr}, ev_w1[2] = {nullptr, nullptr};
   // Every call shares the scratch buffers.  The stream of the last call that
   // enqueued work and an event recorded at its end let a call on another
@@ -978,15 +997,6 @@ pulse_status fork_side(pulse_stage* s, hipStream_t st) {
   return PULSE_OK;
 }
 
-// Side-stream progress markers of one backward call: block k records w2
-// after its conv2 / shortcut parameter work (the last read of its dout) and
-// w1 after its conv1 weight gradient (the last read of its dh1); buffers
-// alternate between consecutive blocks, so block k waits for the marker of
-// the block that used the same buffer before it.
-struct BwdSync {
-  bool w2[2] = {false, false}, w1[2] = {false, false};
-};
-
 pulse_status mark_side(pulse_stage* s, hipEvent_t ev) {
   if (!use_side(s)) return PULSE_OK;
   HIPCHK(hipEventRecord(ev, s->side));
@@ -999,9 +1009,22 @@ pulse_status wait_mark(pulse_stage* s, hipEvent_t ev, bool recorded, hipStream_t
   return PULSE_OK;
 }
 
+// A decoder backward left running beside its stream: `st` waits for all of
+// the side stream's work so far.
+pulse_status settle_pending(pulse_stage* s, hipStream_t st) {
+  if (!s->join_pending) return PULSE_OK;
+  HIPCHK(hipEventRecord(s->ev_join, s->side));
+  HIPCHK(hipStreamWaitEvent(st, s->ev_join, 0));
+  s->join_pending = false;
+  return PULSE_OK;
+}
+
 // Calls may alternate streams: order this call's work after the previous
-// call's (a no-op on the same stream).
+// call's (a no-op on the same stream), including side-stream work that a
+// decoder backward left running.
 pulse_status order_after_last(pulse_stage* s, hipStream_t st) {
+  pulse_status ps;
+  if ((ps = settle_pending(s, st)) != PULSE_OK) return ps;
   if (s->have_last && s->last_st != st) HIPCHK(hipStreamWaitEvent(st, s->ev_last, 0));
   return PULSE_OK;
 }
@@ -1371,6 +1394,8 @@ pulse_status pulse_stage_create(const pulse_stage_desc* desc, pulse_stage** out)
 
 void pulse_stage_destroy(pulse_stage* s) {
   if (!s) return;
+  // work a decoder backward left on the side stream ends before its events go
+  if (s->side) (void)hipStreamSynchronize(s->side);
   for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
   if (s->ev_fork) (void)hipEventDestroy(s->ev_fork);
   if (s->ev_join) (void)hipEventDestroy(s->ev_join);
@@ -1525,9 +1550,21 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     char* row = s->row_base(r);
     const int dt = s->dtype;
     s->use_workspace_scratch();
-    if ((ps = order_after_last(s, st)) != PULSE_OK) return ps;
-    int cur = 0;
     BwdSync sy;
+    if (half == PULSE_ENC && s->join_pending && s->pending_mb == mb && s->pending_st == st &&
+        use_side(s)) {
+      // The decoder's last parameter-gradient work may still run on the side
+      // stream.  Its reads of the blocks' gradient buffers ended at its last
+      // conv2 marker, which this stream waits for before writing them; its
+      // dh1 and channel-sum buffers are guarded per parity by the carried
+      // markers; everything else it reads this call does not write.
+      sy = s->sy_pending;
+      HIPCHK(hipStreamWaitEvent(st, s->ev_w2[s->par_pending], 0));
+      s->join_pending = false;
+    } else if ((ps = order_after_last(s, st)) != PULSE_OK) {
+      return ps;
+    }
+    int cur = 0;
     const void* prev_dy = nullptr;  // the dout of the block processed before
     if (half == PULSE_DEC) {
       const int n = (int)s->db.size();
@@ -1578,8 +1615,16 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
         cur ^= 1;
       }
     }
-    // the caller's stream sees every side-stream result
-    if ((ps = join_side(s, st)) != PULSE_OK) return ps;
+    if (half == PULSE_DEC && s->overlap_bwd && use_side(s)) {
+      // the side stream's remaining work joins at the next call
+      s->join_pending = true;
+      s->pending_mb = mb;
+      s->pending_st = st;
+      s->sy_pending = sy;
+      s->par_pending = 0;  // the last block processed is block 0
+    } else if ((ps = join_side(s, st)) != PULSE_OK) {
+      return ps;  // the caller's stream sees every side-stream result
+    }
     if ((ps = mark_last(s, st)) != PULSE_OK) return ps;
   }
 
@@ -1696,6 +1741,18 @@ int32_t pulse_stage_inflight(const pulse_stage* s) {
   int n = 0;
   for (auto& r : s->rows) n += r.mb >= 0;
   return n;
+}
+
+pulse_status pulse_stage_overlap_bwd(pulse_stage* s, int32_t enable) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  s->overlap_bwd = enable != 0;
+  return PULSE_OK;
+}
+
+pulse_status pulse_stage_flush(pulse_stage* s, void* stream) {
+  if (!s) return fail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (s->dry) return PULSE_OK;
+  return order_after_last(s, static_cast<hipStream_t>(stream));
 }
 
 pulse_status pulse_stage_timing(pulse_stage* s, int32_t enable) {

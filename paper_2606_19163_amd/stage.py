@@ -117,6 +117,10 @@ def lib():
         L.pulse_stage_inflight.restype = _i32
         L.pulse_stage_timing.argtypes = [_vp, _i32]
         L.pulse_stage_timing.restype = st
+        L.pulse_stage_overlap_bwd.argtypes = [_vp, _i32]
+        L.pulse_stage_overlap_bwd.restype = st
+        L.pulse_stage_flush.argtypes = [_vp, _vp]
+        L.pulse_stage_flush.restype = st
         L.pulse_stage_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_int64),
                                               ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_double),
@@ -325,6 +329,12 @@ class Stage:
 
     def flops(self):
         return lib().pulse_stage_flops(self.h)
+
+    def overlap_bwd(self, enable):
+        _check(lib().pulse_stage_overlap_bwd(self.h, 1 if enable else 0))
+
+    def flush(self, stream=None):
+        _check(lib().pulse_stage_flush(self.h, None if self.dry else _stream_handle(stream)))
 
     def timing(self, enable):
         _check(lib().pulse_stage_timing(self.h, 1 if enable else 0))
