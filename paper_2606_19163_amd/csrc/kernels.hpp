@@ -167,10 +167,12 @@ struct GnBwdOut {
   float* chan_partial;  // optional per-(b, chunk, c) sums of the output
 };
 // dx = rstd * (gamma*dz - coef0 - xhat*coef1) + addends, split-stored.
+// done (may be null): an event recorded by the kernel's own completion.
 hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
-                               int G, const GnBwdOut& o, hipStream_t st);
+                               int G, const GnBwdOut& o, hipStream_t st,
+                               hipEvent_t done = nullptr);
 
 // partial[b][chunk][0][c] = sum over the chunk of v (v may carry an addend).
 hipError_t launch_chan_sum_partial(const VIn& v, const Geo& g, RedGrid rg, float* partial,

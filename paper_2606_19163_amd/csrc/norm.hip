@@ -5,6 +5,8 @@
 // block is one contiguous, coalesced read.  Reductions are deterministic:
 // fixed per-thread order, a fixed LDS tree, per-(image, chunk) partials and
 // a finalize that sums them in a fixed order (group sums in fp64).
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -871,7 +873,7 @@ auto bwd_apply_kernel(bool chan, bool add0, int nf) {
 hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGrid rg,
                                const float* scale, const float* shift, const float* mean,
                                const float* rstd, const float* gamma, const float* coef,
-                               int G, const GnBwdOut& o, hipStream_t st) {
+                               int G, const GnBwdOut& o, hipStream_t st, hipEvent_t done) {
   const int dt = common_dt(x);
   const bool add0 = o.add0.s0.ptr != nullptr;
   // x is a forward activation (no addend); add0 shares the stage dtype
@@ -881,8 +883,12 @@ hipError_t launch_gn_bwd_apply(const Src& da, const VIn& x, const Geo& g, RedGri
   const bool chan = o.chan_partial != nullptr;
   auto kern = dt == DT_BF16 ? bwd_apply_kernel<DT_BF16>(chan, add0, nf)
                             : bwd_apply_kernel<DT_F32>(chan, add0, nf);
-  hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg, scale, shift,
-                     mean, rstd, gamma, coef, G, o);
+  if (done)  // the event completes with the kernel (no marker packet of its own)
+    hipExtLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, nullptr, done, 0, da, x,
+                          g, rg, scale, shift, mean, rstd, gamma, coef, G, o);
+  else
+    hipLaunchKernelGGL(kern, red_dims(g, rg, x.C), red_block(rg), 0, st, da, x, g, rg, scale,
+                       shift, mean, rstd, gamma, coef, G, o);
   return hipGetLastError();
 }
 

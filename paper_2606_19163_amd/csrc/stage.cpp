@@ -145,6 +145,9 @@ struct pulse_stage {
   // concurrently with the data-gradient chain on the caller's stream
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // ev_fork was recorded by the completion of the last kernel enqueued on
+  // the caller's stream (the next fork needs no marker of its own)
+  bool fork_attached = false;
   // overlapped decoder backward (pulse_stage_overlap_bwd): a decoder
   // backward may return with its last parameter-gradient work still on the
   // side stream; the next call joins it, except an encoder backward of the
@@ -890,7 +893,8 @@ pulse_status gn_forward(pulse_stage* s, char* row, const GnSave& g, const VIn& x
 // (written by the data-gradient conv's epilogue, that many chunks per image).
 pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& x,
                          const float* gamma, float* dgamma, float* dbeta, const void* da_ptr,
-                         const GnBwdOut& o, hipStream_t st, int pre_chunks = 0) {
+                         const GnBwdOut& o, hipStream_t st, int pre_chunks = 0,
+                         hipEvent_t done = nullptr) {
   RedGrid rg = red_grid(s->geo, x.C);
   float* red = s->sf(s->s_red);
   float* coef = s->sf(s->s_coef);
@@ -908,7 +912,7 @@ pulse_status gn_backward(pulse_stage* s, char* row, const GnSave& g, const VIn& 
   // the apply's block grid is its own
   const RedGrid ra = red_grid(s->geo, x.C);
   HIPCHK(launch_gn_bwd_apply(da, x, s->geo, ra, scale, shift, mean, rstd, gamma, coef, s->G, o,
-                             st));
+                             st, done));
   return PULSE_OK;
 }
 
@@ -992,9 +996,19 @@ pulse_status block_forward(pulse_stage* s, int r, const Block& b, const VIn& xin
 // and the side work runs on `st`.
 pulse_status fork_side(pulse_stage* s, hipStream_t st) {
   if (!use_side(s)) return PULSE_OK;
-  HIPCHK(hipEventRecord(s->ev_fork, st));
+  // a marker between two kernels costs the stream a few microseconds; an
+  // event attached to the producing kernel's completion does not
+  if (!s->fork_attached) HIPCHK(hipEventRecord(s->ev_fork, st));
+  s->fork_attached = false;
   HIPCHK(hipStreamWaitEvent(s->side, s->ev_fork, 0));
   return PULSE_OK;
+}
+
+// The event the next fork may use when the kernel about to be enqueued on
+// the caller's stream is the last one before that fork.
+hipEvent_t attach_fork(pulse_stage* s, bool fork_follows) {
+  s->fork_attached = fork_follows && use_side(s);
+  return s->fork_attached ? s->ev_fork : nullptr;
 }
 
 pulse_status mark_side(pulse_stage* s, hipEvent_t ev) {
@@ -1136,7 +1150,7 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     o2.add0 = vnone();
     o2.chan_partial = s->sf(s->s_chp[par]);
     if ((ps = gn_backward(s, row, b.gn2, h1v, s->pp(b.g2), s->gp(b.g2), s->gp(b.be2), da, o2,
-                          st, gn2_chunks)) != PULSE_OK)
+                          st, gn2_chunks, attach_fork(s, true))) != PULSE_OK)
       return ps;
   }
   // conv1 weight and data gradients
@@ -1174,8 +1188,9 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // stream an event round trip)
   if (prev_dout && o.dst0 == prev_dout)
     if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
+  // the next block of this call forks right after this kernel
   return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st,
-                     gn1_chunks);
+                     gn1_chunks, attach_fork(s, k > 0));
 }
 
 pulse_status check_ptr(const void* p, const char* what) {
@@ -1550,6 +1565,7 @@ pulse_status pulse_stage_backward(pulse_stage* s, pulse_half half, int32_t mb, c
     char* row = s->row_base(r);
     const int dt = s->dtype;
     s->use_workspace_scratch();
+    s->fork_attached = false;
     BwdSync sy;
     if (half == PULSE_ENC && s->join_pending && s->pending_mb == mb && s->pending_st == st &&
         use_side(s)) {
