@@ -40,6 +40,11 @@
  *    so a call on a stream other than the previous call's first makes its
  *    stream wait for the previous call's work (an event recorded at the end
  *    of every call that enqueues work).
+ *  - Forward and backward calls may be captured into a HIP graph (stream
+ *    capture): replays do the captured work with bitwise the eager results.
+ *    A replay does not run the host-side bookkeeping, so capture a sequence
+ *    that leaves every microbatch where it found it (for example the
+ *    forward and backward of both halves of one microbatch).
  */
 #ifndef PULSE_STAGE_H
 #define PULSE_STAGE_H

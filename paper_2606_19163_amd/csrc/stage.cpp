@@ -1005,9 +1005,13 @@ pulse_status fork_side(pulse_stage* s, hipStream_t st) {
 }
 
 // The event the next fork may use when the kernel about to be enqueued on
-// the caller's stream is the last one before that fork.
-hipEvent_t attach_fork(pulse_stage* s, bool fork_follows) {
-  s->fork_attached = fork_follows && use_side(s);
+// the caller's stream is the last one before that fork.  Not under stream
+// capture: a graph takes its dependencies from recorded events.
+hipEvent_t attach_fork(pulse_stage* s, bool fork_follows, hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (fork_follows && use_side(s) && hipStreamIsCapturing(st, &cs) != hipSuccess)
+    cs = hipStreamCaptureStatusActive;  // unknown: take the marker
+  s->fork_attached = fork_follows && use_side(s) && cs == hipStreamCaptureStatusNone;
   return s->fork_attached ? s->ev_fork : nullptr;
 }
 
@@ -1150,7 +1154,7 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     o2.add0 = vnone();
     o2.chan_partial = s->sf(s->s_chp[par]);
     if ((ps = gn_backward(s, row, b.gn2, h1v, s->pp(b.g2), s->gp(b.g2), s->gp(b.be2), da, o2,
-                          st, gn2_chunks, attach_fork(s, true))) != PULSE_OK)
+                          st, gn2_chunks, attach_fork(s, true, st))) != PULSE_OK)
       return ps;
   }
   // conv1 weight and data gradients
@@ -1190,7 +1194,7 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
     if ((ps = wait_mark(s, s->ev_w2[par ^ 1], sy.w2[par ^ 1], st)) != PULSE_OK) return ps;
   // the next block of this call forks right after this kernel
   return gn_backward(s, row, b.gn1, xin, s->pp(b.g1), s->gp(b.g1), s->gp(b.be1), da, o, st,
-                     gn1_chunks, attach_fork(s, k > 0));
+                     gn1_chunks, attach_fork(s, k > 0, st));
 }
 
 pulse_status check_ptr(const void* p, const char* what) {

@@ -100,14 +100,18 @@ struct pulse_tstage {
   // workspace
   size_t ws_bytes = 0, off_rows = 0, row_size = 0;
   size_t row_slot[64] = {}, row_sgrad[64] = {};
-  size_t s_dy[2] = {0, 0}, s_dm = 0, s_da2 = 0, s_dh = 0, s_do = 0, s_dqkv = 0, s_da = 0,
-         s_dsx = 0, s_dv = 0, s_dsum = 0, s_kpart = 0, s_wpart = 0, s_red = 0, s_zero = 0;
+  // gradients that the side stream reads come in two copies, one per block
+  // parity, so that a block overwrites only what the block before the
+  // previous one left (the side stream rarely lags that far)
+  size_t s_dy[2] = {0, 0}, s_dm[2] = {0, 0}, s_da2 = 0, s_dh[2] = {0, 0}, s_do = 0,
+         s_dqkv[2] = {0, 0}, s_da = 0, s_dsx[2] = {0, 0}, s_dv = 0, s_dsum = 0, s_kpart = 0,
+         s_wpart = 0, s_red = 0, s_zero = 0;
   size_t kpart_cap = 0, wpart_cap = 0, red_cap = 0;
   size_t s_red2 = 0;  // reduction buffer of the side stream
   // column-sum partials of dh (LN2 backward) and of a decoder block's
   // skip-linear output gradient (LN1 backward): the bias gradients of proj
   // and skip without another pass over them
-  size_t s_cs_h = 0, s_cs_x = 0;
+  size_t s_cs_h[2] = {0, 0}, s_cs_x[2] = {0, 0};
   // side stream: the weight-gradient GEMMs and bias-gradient sums of the
   // backward pass run on it, concurrently with the data-gradient chain
   hipStream_t side = nullptr;
@@ -332,13 +336,15 @@ void build_layout(pulse_tstage* s) {
   const size_t lbytes = (size_t)s->B * s->H * s->L * 4;  // one fp32 per (image, head, token)
   s->s_dy[0] = take(act);
   s->s_dy[1] = take(act);
-  s->s_dm = take((size_t)T * R * 2);
+  for (int i = 0; i < 2; ++i) {
+    s->s_dm[i] = take((size_t)T * R * 2);
+    s->s_dh[i] = take(act);
+    s->s_dqkv[i] = take(3 * act);
+    s->s_dsx[i] = take(act);
+  }
   s->s_da2 = take(act);
-  s->s_dh = take(act);
   s->s_do = take(act);
-  s->s_dqkv = take(3 * act);
   s->s_da = take(act);
-  s->s_dsx = take(act);
   s->s_dv = take(act);
   s->s_dsum = take(lbytes);
   // partial buffers: the largest conv K split and weight-gradient split
@@ -365,8 +371,10 @@ void build_layout(pulse_tstage* s) {
   s->red_cap = red;
   s->s_red = take(red * 4);
   s->s_red2 = take(red * 4);
-  s->s_cs_h = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
-  s->s_cs_x = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
+  for (int i = 0; i < 2; ++i) {
+    s->s_cs_h[i] = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
+    s->s_cs_x[i] = take((size_t)ln_bwd_blocks(T) * 2 * C * 4);
+  }
   s->s_zero = take(256);
   // per-microbatch rows
   s->off_rows = off;
@@ -673,15 +681,15 @@ pulse_status param_grads(BwdSync& y, int M, const Seg& in, const void* gy, float
   return PULSE_OK;
 }
 
-// Scratch buffers that the side stream may still read, with the event that
-// frees each (null: free).
+// Scratch buffers of one parity that the side stream may still read, with
+// the event that frees each (null: free).
 struct SideReads {
   hipEvent_t dy = nullptr, dm = nullptr, dh = nullptr, dqkv = nullptr, dsx = nullptr;
 };
 
 // dx = d(block)/dx^T dy for the block input x; parameter gradients +=
-pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, const void* x,
-                       const void* dy, void* dx, float* dx_csum = nullptr) {
+pulse_status block_bwd(BwdSync& y, SideReads& rd, int par, char* row, const TBlock& b,
+                       const void* x, const void* dy, void* dx, float* dx_csum = nullptr) {
   pulse_tstage* s = y.s;
   hipStream_t st = y.st;
   const int C = s->C, R = s->R;
@@ -695,11 +703,11 @@ pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, co
   const float* st2 = reinterpret_cast<const float*>(row + b.r_st2);
   void* z = row + b.r_z;
   void* m = row + b.r_m;
-  void* dm = s->at(s->s_dm);
+  void* dm = s->at(s->s_dm[par]);
   void* da2 = s->at(s->s_da2);
-  void* dh = s->at(s->s_dh);
+  void* dh = s->at(s->s_dh[par]);
   void* dO = s->at(s->s_do);
-  void* dqkv = s->at(s->s_dqkv);
+  void* dqkv = s->at(s->s_dqkv[par]);
   void* da = s->at(s->s_da);
   // MLP: y = h + Fc2(GELU(Fc1(LN2(h))))
   TCHK(param_grads(y, C, tseg(R, tvin(m, R), s->gp(b.fc2W)), dy, s->gp(b.fc2b)));
@@ -713,7 +721,7 @@ pulse_status block_bwd(BwdSync& y, SideReads& rd, char* row, const TBlock& b, co
   TCHK(linear(s, C, tseg(R, tvin(dm, R)), s->at(b.t_fc1), R, nullptr, nullptr, da2, nullptr,
               DT_BF16, st));
   TCHK(wait_for(y, rd.dh));
-  float* cs_h = s->fat(s->s_cs_h);
+  float* cs_h = s->fat(s->s_cs_h[par]);
   TCHK(ln_backward(s, da2, h, st2, b.ln2g, b.ln2b, dy, dh, st, cs_h));
   // attention: h = x + Proj(MHA(LN1(x)))
   TCHK(param_grads(y, C, tseg(C, tvin(o, C), s->gp(b.projW)), dh, s->gp(b.projb), cs_h,
@@ -958,16 +966,17 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
     const int C = s->C, ne = s->d.n_enc, nd = s->d.n_dec;
     const long T = s->T;
     BwdSync y = bwd_sync(s, st);
-    SideReads rd;
+    SideReads rds[2];
     if (half == PULSE_DEC) {
       const void* dy = dout;
       hipEvent_t dy_read = nullptr;  // the side stream has read the previous block's dy
       for (int k = nd - 1; k >= 0; --k) {
         const TBlock& b = s->db[k];
-        void* dsx = s->at(s->s_dsx);
+        SideReads& rd = rds[k & 1];
+        void* dsx = s->at(s->s_dsx[k & 1]);
         TCHK(wait_for(y, rd.dsx));
-        float* cs_x = s->fat(s->s_cs_x);
-        TCHK(block_bwd(y, rd, row, b, row + b.r_x, dy, dsx, cs_x));
+        float* cs_x = s->fat(s->s_cs_x[k & 1]);
+        TCHK(block_bwd(y, rd, k & 1, row, b, row + b.r_x, dy, dsx, cs_x));
         // skip linear over [v || skip]
         const int slot = ne - 1 - k;
         const void* skip = row + s->row_slot[slot];
@@ -991,13 +1000,15 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
         const TBlock& b = s->eb[k];
         // the gradient reaching x_k: from its encoder consumer and from the
         // buffered skip gradient of its decoder consumer
+        SideReads& rd = rds[k & 1];
         void* dy = s->at(s->s_dy[0]);
-        TCHK(wait_for(y, rd.dy));
+        // the previous block's fc2 parameter gradient read this buffer
+        TCHK(wait_for(y, rds[(k + 1) & 1].dy));
         THIP(launch_add_cast(g, DT_BF16, reinterpret_cast<const float*>(row + s->row_sgrad[k]),
                              dy, DT_BF16, T * C, st));
         const void* x = k == 0 ? row + b.r_x : row + s->row_slot[k - 1];
         void* dx = k == 0 ? din : s->at(s->s_dy[1]);
-        TCHK(block_bwd(y, rd, row, b, x, dy, dx));
+        TCHK(block_bwd(y, rd, k & 1, row, b, x, dy, dx));
         g = dx;
       }
     }
