@@ -19,6 +19,8 @@
 //    lanes 4q + j/4, q = 0..3.  B columns may mix sources within one tile, so
 //    its DMA uses per-lane global addresses; invalid elements point at a
 //    zeroed 16-byte word.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <type_traits>
 
@@ -1050,7 +1052,7 @@ using W2_320x128 = CfgW<320, 128, 80, 64>;   // 8 waves, one block per CU
 using W2_128x128 = CfgW<128, 128, 64, 64>;   // 4 waves
 
 template <class C>
-static hipError_t conv2_t(const GemmArgs& a_in, hipStream_t st) {
+static hipError_t conv2_t(const GemmArgs& a_in, hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
   // 32-bit pixel indices and weight offsets
   if (a_in.g.pixels() + C::BM >= (1L << 31) || (long)a_in.N * a_in.ldb * 2 >= (1L << 31))
     return hipErrorInvalidValue;
@@ -1074,17 +1076,22 @@ static hipError_t conv2_t(const GemmArgs& a_in, hipStream_t st) {
   const long tilesM = (a.g.pixels() + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
   const int ks = a.ksplit > 1 ? a.ksplit : 1;
-  if (a.gnb)
-    hipLaunchKernelGGL((igemm2_conv<C, true>), dim3((unsigned)(tilesM * tilesN * ks)), dim3(C::NT),
-                       0, st, a);
+  const bool fin = ks > 1 && !a.skip_finalize;  // the K-split finalize follows here
+  const dim3 grid((unsigned)(tilesM * tilesN * ks)), block(C::NT);
+  auto kern = a.gnb ? igemm2_conv<C, true> : igemm2_conv<C, false>;
+  if (t0 || t1)
+    hipExtLaunchKernelGGL(kern, grid, block, 0, st, t0, fin ? nullptr : t1, 0, a);
   else
-    hipLaunchKernelGGL((igemm2_conv<C, false>), dim3((unsigned)(tilesM * tilesN * ks)),
-                       dim3(C::NT), 0, st, a);
+    hipLaunchKernelGGL(kern, grid, block, 0, st, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || ks == 1 || a.skip_finalize) return e;
+  if (e != hipSuccess || !fin) return e;
   const long vec = a.g.pixels() * (a.N / 8);
   const long blocks = std::min<long>((vec + 255) / 256, 2048);
-  hipLaunchKernelGGL(conv_splitk_finalize, dim3((unsigned)blocks), dim3(256), 0, st, a);
+  if (t1)
+    hipExtLaunchKernelGGL(conv_splitk_finalize, dim3((unsigned)blocks), dim3(256), 0, st, nullptr,
+                          t1, 0, a);
+  else
+    hipLaunchKernelGGL(conv_splitk_finalize, dim3((unsigned)blocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -1128,12 +1135,12 @@ TileInfo tile2_info(int t) {
   }
 }
 
-hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st) {
+hipError_t launch_conv2(const GemmArgs& a, int t, hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
   switch (t) {
-    case TILE2_C128x160: return conv2_t<C2_128x160>(a, st);
-    case TILE2_C128x192: return conv2_t<C2_128x192>(a, st);
-    case TILE2_C64x128S3: return conv2_t<C2_64x128S3>(a, st);
-    default: return conv2_t<C2_128x128>(a, st);
+    case TILE2_C128x160: return conv2_t<C2_128x160>(a, st, t0, t1);
+    case TILE2_C128x192: return conv2_t<C2_128x192>(a, st, t0, t1);
+    case TILE2_C64x128S3: return conv2_t<C2_64x128S3>(a, st, t0, t1);
+    default: return conv2_t<C2_128x128>(a, st, t0, t1);
   }
 }
 

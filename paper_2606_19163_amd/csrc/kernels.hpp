@@ -110,7 +110,11 @@ enum Tile2 : int {
   TILE2_WGRAD_LAST = 21
 };
 TileInfo tile2_info(int tile);
-hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st);
+// t0 / t1 (may be null): events recorded by the GEMM kernel's own start and
+// by the completion of the launch's last kernel (the GEMM or its K-split
+// finalize), which time the launch without marker packets around it.
+hipError_t launch_conv2(const GemmArgs& a, int tile, hipStream_t st, hipEvent_t t0 = nullptr,
+                        hipEvent_t t1 = nullptr);
 hipError_t launch_wgrad2(const GemmArgs& a, int tile, int splits, const void* zero16,
                          hipStream_t st);
 
@@ -134,7 +138,8 @@ hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float
 // (fixed order) + bias + rowvec + residual (bf16), and the per-channel sum
 // and sum of squares of the stored output per (image, chunk of the reduction
 // grid rg over N channels) row of a.stats.
-hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st);
+hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st,
+                                        hipEvent_t done = nullptr);
 hipError_t launch_gn_stats_finalize(const float* partial, const Geo& g, RedGrid rg, int C,
                                     int G, float eps, const float* gamma, const float* beta,
                                     float* mean, float* rstd, float* scale, float* shift,

@@ -791,12 +791,17 @@ hipError_t launch_gn_stats_partial(const VIn& x, const Geo& g, RedGrid rg, float
   return hipGetLastError();
 }
 
-hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st) {
+hipError_t launch_splitk_finalize_stats(const GemmArgs& a, RedGrid rg, hipStream_t st,
+                                        hipEvent_t done) {
   if (a.ksplit < 2 || !a.part || !a.stats || a.gnb || a.out_dtype != DT_BF16 || a.ldo != a.N ||
       a.N % 8 != 0 || (a.resid.s0.ptr && (a.resid.s0.dtype != DT_BF16 || a.resid.add)))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_splitk_finalize_stats, red_dims(a.g, rg, a.N), red_block(rg), 0, st, a,
-                     rg);
+  if (done)
+    hipExtLaunchKernelGGL(k_splitk_finalize_stats, red_dims(a.g, rg, a.N), red_block(rg), 0, st,
+                          nullptr, done, 0, a, rg);
+  else
+    hipLaunchKernelGGL(k_splitk_finalize_stats, red_dims(a.g, rg, a.N), red_block(rg), 0, st, a,
+                       rg);
   return hipGetLastError();
 }
 

@@ -706,12 +706,16 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
       return fail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
     a.part = s->fwd(s->f_kpart);
   }
+  // timed launches: the implicit-GEMM kernels record the events themselves
+  // at their start and completion; the register-staged path between markers
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
     e0 = next_event(s);
     e1 = next_event(s);
-    if (e0 && e1) HIPCHK(hipEventRecord(e0, st));
   }
+  const bool timed = e0 && e1;
+  const bool on_kernel = timed && uses_v2(s);
+  if (timed && !on_kernel) HIPCHK(hipEventRecord(e0, st));
   // Output statistics, or the GroupNorm-backward sums, from the conv: its
   // epilogue without a K split (whole tiles per image); with a K split the
   // statistics (not the backward sums, which measured slower there) from
@@ -742,15 +746,16 @@ pulse_status run_conv(pulse_stage* s, GemmArgs& a, hipStream_t st, int* stats_ch
     k.stats = nullptr;
     k.gnb = nullptr;
     k.skip_finalize = 1;
-    HIPCHK(launch_conv2(k, tile, st));
-    HIPCHK(launch_splitk_finalize_stats(a, red_grid(s->geo, a.N), st));
+    HIPCHK(launch_conv2(k, tile, st, on_kernel ? e0 : nullptr, nullptr));
+    HIPCHK(launch_splitk_finalize_stats(a, red_grid(s->geo, a.N), st,
+                                        on_kernel ? e1 : nullptr));
   } else if (uses_v2(s)) {
-    HIPCHK(launch_conv2(a, tile, st));
+    HIPCHK(launch_conv2(a, tile, st, on_kernel ? e0 : nullptr, on_kernel ? e1 : nullptr));
   } else {
     HIPCHK(launch_conv(a, tile, st));
   }
-  if (s->timing && e0 && e1) {
-    HIPCHK(hipEventRecord(e1, st));
+  if (timed) {
+    if (!on_kernel) HIPCHK(hipEventRecord(e1, st));
     s->timed.push_back(TimedLaunch{e0, e1, 2.0 * (double)a.M * a.N * a.K, conv_bytes(s, a)});
   }
   return PULSE_OK;

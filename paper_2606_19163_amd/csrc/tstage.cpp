@@ -499,15 +499,15 @@ pulse_status linear(pulse_tstage* s, int N, const Seg& in, const void* W, int ld
       return tfail(PULSE_E_SHAPE, "internal: conv partial buffer too small");
     a.part = s->fat(s->s_kpart);
   }
+  // timed launches: the kernels record the events at their start and completion
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (s->timing) {
     e0 = next_event(s);
     e1 = next_event(s);
-    if (e0 && e1) THIP(hipEventRecord(e0, st));
   }
-  THIP(launch_conv2(a, tile, st));
-  if (s->timing && e0 && e1) {
-    THIP(hipEventRecord(e1, st));
+  const bool timed = e0 && e1;
+  THIP(launch_conv2(a, tile, st, timed ? e0 : nullptr, timed ? e1 : nullptr));
+  if (timed) {
     const double P = (double)a.M;
     const double bytes = P * a.K * 2.0 + (double)N * a.K * 2.0 + (resid ? P * N * 2.0 : 0.0) +
                          P * N * (out_dtype == DT_BF16 ? 2.0 : 4.0) * (out2 ? 2.0 : 1.0);
