@@ -118,6 +118,25 @@ def test_microbatch_order_and_release():
     assert st.state(0, 0) == 0
 
 
+def test_overlapped_backward_bookkeeping_matches_joined():
+    """pulse_stage_overlap_bwd and pulse_stage_flush change no bookkeeping:
+    a dry-run stage walks the same states with the switch on, and a flush
+    is accepted at any point (it only orders work)."""
+    st = _dry(configs.l64())
+    st.overlap_bwd(True)
+    st.flush()
+    st.forward(S.ENC, 0, None, None)
+    st.forward(S.DEC, 0, None, None)
+    st.backward(S.DEC, 0, None)
+    st.flush()
+    assert st.state(0, 0) == S.ACT_PRESENT | S.GRAD_PRESENT
+    st.backward(S.ENC, 0, None)
+    assert st.inflight() == 0
+    st.overlap_bwd(False)
+    _expect_status(lambda: S._check(S.lib().pulse_stage_overlap_bwd(None, 1)), S.E_INVALID_ARG)
+    _expect_status(lambda: S._check(S.lib().pulse_stage_flush(None, None)), S.E_INVALID_ARG)
+
+
 def test_capacity_and_wave_order():
     d = configs.l64()
     d["max_inflight"] = 4
