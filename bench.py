@@ -37,8 +37,9 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 # Overlapped decoder backward, measured per workload (same box, alternating
 # runs): 64x64x320 778 against 764 TFLOP/s; 32x32x640 697 against 705 (its
 # decoder's last weight GEMM then runs into the encoder's K-split convs); the
-# four-level wave 625 either way.
-OVERLAP_BWD_AUTO = ("l64",)
+# four-level wave 625 either way; the transformer stages 372 against 371
+# (768 wide) and 665 against 657 (1408 wide).
+OVERLAP_BWD_AUTO = ("l64", "t768", "t1408")
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the fp32 stage)
 METRIC = "stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s, 64x64x320 stage"
 
@@ -286,6 +287,9 @@ def bench_tstage(args):
     params, b = synth.make_tstage(d, seed)
     st = TS.TStage(d)
     st.set_params(params)
+    overlap_on = args.overlap_bwd == "on" or (args.overlap_bwd == "auto" and
+                                              args.workload in OVERLAP_BWD_AUTO)
+    st.overlap_bwd(overlap_on)
     dev = {k: st.to_dev(v) for k, v in b.items()}
     outs = {k: st.act() for k in ("y_enc", "y_dec", "dx", "du")}
     if args.copy_calibration_mib > 0:
@@ -331,6 +335,7 @@ def bench_tstage(args):
         "microbatches_per_s": round(args.steps / elapsed, 2),
         "gflop_per_step": round(flops_step / 1e9, 2),
         **step_stats(per),
+        "overlap_bwd": overlap_on,
     }
     if launches:
         achieved = kflops / (kms * 1e-3) / 1e12

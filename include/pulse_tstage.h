@@ -107,6 +107,20 @@ pulse_status pulse_tstage_forward(pulse_tstage* st, pulse_half half, int32_t mb,
 pulse_status pulse_tstage_backward(pulse_tstage* st, pulse_half half, int32_t mb,
                                    const void* dout, void* din, void* stream);
 
+/* Overlapped decoder backward (default off), as pulse_stage_overlap_bwd: a
+ * DEC backward returns without waiting for its last parameter-gradient work
+ * on the stage's second stream; an ENC backward of the same microbatch on
+ * the same stream starts beside it, and any other call (or
+ * pulse_tstage_flush on a stream) orders that work before what follows it.
+ * The decoder half's parameter gradients are complete in `stream` order only
+ * after that.  Results are bitwise those of the switch off. */
+pulse_status pulse_tstage_overlap_bwd(pulse_tstage* st, int32_t enable);
+
+/* Work enqueued on `stream` after this call is ordered after the stage's
+ * side-stream work, including what an overlapped decoder backward left
+ * running.  Enqueues only stream waits. */
+pulse_status pulse_tstage_flush(pulse_tstage* st, void* stream);
+
 /* Copy the buffered gradient of (mb, slot) (fp32 [batch, tokens, width])
  * into dst without consuming it: an inspection hook for tests.
  * PULSE_E_CACHE_MISS when absent. */

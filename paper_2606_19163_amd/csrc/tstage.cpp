@@ -88,6 +88,12 @@ struct TTimed {
 
 }  // namespace
 
+// Scratch buffers of one parity that the side stream may still read, with
+// the event that frees each (null: free).
+struct SideReads {
+  hipEvent_t dy = nullptr, dm = nullptr, dh = nullptr, dqkv = nullptr, dsx = nullptr;
+};
+
 struct pulse_tstage {
   pulse_tstage_desc d{};
   bool dry = false;
@@ -117,6 +123,17 @@ struct pulse_tstage {
   hipStream_t side = nullptr;
   std::vector<hipEvent_t> sev;  // synchronisation events, reused per call
   size_t sev_used = 0;
+  // overlapped decoder backward (pulse_tstage_overlap_bwd): a decoder
+  // backward may return with its last parameter-gradient work still on the
+  // side stream; the next call joins it, except an encoder backward of the
+  // same microbatch on the same stream, which continues beside it with the
+  // decoder call's side-read events (their pool is not recycled until then)
+  bool overlap_bwd = false, join_pending = false;
+  int32_t pending_mb = -1;
+  hipStream_t pending_st = nullptr;
+  SideReads pending_rds[2];
+  hipEvent_t pending_dy = nullptr;  // the decoder's last read of a dy buffer
+  hipEvent_t ev_settle = nullptr;
   // GEMM tuning overrides (env, read at create; -1: the default choice)
   int conv_tile_force = -1, conv_ks_cap = 16, wgrad_tile_force = -1;
   // binding
@@ -627,15 +644,30 @@ hipEvent_t sync_event(pulse_tstage* s) {
   return s->sev[s->sev_used++];
 }
 
-BwdSync bwd_sync(pulse_tstage* s, hipStream_t st) {
+BwdSync bwd_sync(pulse_tstage* s, hipStream_t st, bool keep_events = false) {
   BwdSync y;
   y.s = s;
   y.st = st;
   y.on_side = s->side != nullptr && !s->timing;
   y.work = y.on_side ? s->side : st;
   y.red = s->fat(y.on_side ? s->s_red2 : s->s_red);
-  s->sev_used = 0;
+  if (!keep_events) s->sev_used = 0;
   return y;
+}
+
+// A decoder backward left running beside its stream: `st` waits for all of
+// the side stream's work so far (clear: the pending state is done with).
+pulse_status tsettle(const pulse_tstage* s, hipStream_t st) {
+  if (!s->join_pending) return PULSE_OK;
+  THIP(hipEventRecord(s->ev_settle, s->side));
+  THIP(hipStreamWaitEvent(st, s->ev_settle, 0));
+  return PULSE_OK;
+}
+
+pulse_status tsettle(pulse_tstage* s, hipStream_t st, bool clear) {
+  TCHK(tsettle(static_cast<const pulse_tstage*>(s), st));
+  if (clear) s->join_pending = false;
+  return PULSE_OK;
 }
 
 // make the side stream wait for everything enqueued on the caller's stream
@@ -680,12 +712,6 @@ pulse_status param_grads(BwdSync& y, int M, const Seg& in, const void* gy, float
   TCHK(linear_wgrad(y.s, M, in, gy, y.work));
   return PULSE_OK;
 }
-
-// Scratch buffers of one parity that the side stream may still read, with
-// the event that frees each (null: free).
-struct SideReads {
-  hipEvent_t dy = nullptr, dm = nullptr, dh = nullptr, dqkv = nullptr, dsx = nullptr;
-};
 
 // dx = d(block)/dx^T dy for the block input x; parameter gradients +=
 pulse_status block_bwd(BwdSync& y, SideReads& rd, int par, char* row, const TBlock& b,
@@ -807,6 +833,9 @@ pulse_status pulse_tstage_create(const pulse_tstage_desc* desc, pulse_tstage** o
 
 void pulse_tstage_destroy(pulse_tstage* s) {
   if (!s) return;
+  // work a decoder backward left on the side stream ends before its events go
+  if (s->side) (void)hipStreamSynchronize(s->side);
+  if (s->ev_settle) (void)hipEventDestroy(s->ev_settle);
   for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
   for (hipEvent_t e : s->sev) (void)hipEventDestroy(e);
   if (s->side) (void)hipStreamDestroy(s->side);
@@ -856,6 +885,7 @@ pulse_status pulse_tstage_bind(pulse_tstage* s, const float* params, float* grad
   if (!s->side && env_or("PULSE_SERIAL", 0) == 0) {
     // default priority, no implicit synchronisation with the null stream
     THIP(hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking));
+    THIP(hipEventCreateWithFlags(&s->ev_settle, hipEventDisableTiming));
   }
   s->prm = params;
   s->grd = grads;
@@ -873,6 +903,7 @@ pulse_status pulse_tstage_sync_params(pulse_tstage* s, void* stream) {
   }
   if (!s->bound) return tfail(PULSE_E_NOT_BOUND, "stage is not bound");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  TCHK(tsettle(s, st, true));
   const int C = s->C, R = s->R;
   for (auto* v : {&s->eb, &s->db})
     for (const TBlock& b : *v) {
@@ -918,6 +949,7 @@ pulse_status pulse_tstage_forward(pulse_tstage* s, pulse_half half, int32_t mb, 
   }
   if (!s->dry) {
     hipStream_t st = static_cast<hipStream_t>(stream);
+    TCHK(tsettle(s, st, true));
     char* row = s->row(r);
     const size_t act = (size_t)s->T * s->C * 2;
     const int ne = s->d.n_enc;
@@ -965,8 +997,23 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
     char* row = s->row(r);
     const int C = s->C, ne = s->d.n_enc, nd = s->d.n_dec;
     const long T = s->T;
-    BwdSync y = bwd_sync(s, st);
+    const bool carry = half == PULSE_ENC && s->join_pending && s->pending_mb == mb &&
+                       s->pending_st == st && s->side && !s->timing;
+    if (!carry) TCHK(tsettle(s, st, true));
+    BwdSync y = bwd_sync(s, st, carry);
     SideReads rds[2];
+    if (carry) {
+      // The decoder's last parameter-gradient work may still run on the side
+      // stream.  It read the dy buffers last in its final fc2 weight
+      // gradient, which this stream waits for before writing them; its dm,
+      // dh, dqkv and column-partial buffers are guarded per parity by the
+      // carried events; its skip-linear buffers this call does not write.
+      rds[0] = s->pending_rds[0];
+      rds[1] = s->pending_rds[1];
+      TCHK(wait_for(y, s->pending_dy));
+      s->join_pending = false;
+    }
+    hipEvent_t dec_dy_read = nullptr;
     if (half == PULSE_DEC) {
       const void* dy = dout;
       hipEvent_t dy_read = nullptr;  // the side stream has read the previous block's dy
@@ -994,6 +1041,7 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
                     row + s->row_sgrad[slot], nullptr, DT_F32, st));
         dy = dv;
       }
+      dec_dy_read = dy_read;
     } else {
       const void* g = dout;
       for (int k = ne - 1; k >= 0; --k) {
@@ -1012,7 +1060,17 @@ pulse_status pulse_tstage_backward(pulse_tstage* s, pulse_half half, int32_t mb,
         g = dx;
       }
     }
-    TCHK(join(y));
+    if (half == PULSE_DEC && s->overlap_bwd && y.on_side) {
+      // the side stream's remaining work joins at the next call
+      s->join_pending = true;
+      s->pending_mb = mb;
+      s->pending_st = st;
+      s->pending_rds[0] = rds[0];
+      s->pending_rds[1] = rds[1];
+      s->pending_dy = dec_dy_read;
+    } else {
+      TCHK(join(y));
+    }
   }
   if (half == PULSE_DEC) {
     s->rows[r].state = T_DEC_BWD;
@@ -1031,6 +1089,7 @@ pulse_status pulse_tstage_skip_grad(const pulse_tstage* s, int32_t mb, int32_t s
     return tfail(PULSE_E_CACHE_MISS, "no buffered skip gradient for microbatch %d", mb);
   if (s->dry) return PULSE_OK;
   TCHK(check_ptr(dst, "dst"));
+  TCHK(tsettle(s, static_cast<hipStream_t>(stream)));
   THIP(hipMemcpyAsync(dst, s->row(r) + s->row_sgrad[slot], (size_t)s->T * s->C * 4,
                       hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
   return PULSE_OK;
@@ -1056,8 +1115,24 @@ int32_t pulse_tstage_inflight(const pulse_tstage* s) {
   return n;
 }
 
+pulse_status pulse_tstage_overlap_bwd(pulse_tstage* s, int32_t enable) {
+  if (!s) return tfail(PULSE_E_INVALID_ARG, "stage is NULL");
+  s->overlap_bwd = enable != 0;
+  return PULSE_OK;
+}
+
+pulse_status pulse_tstage_flush(pulse_tstage* s, void* stream) {
+  if (!s) return tfail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (s->dry) return PULSE_OK;
+  return tsettle(s, static_cast<hipStream_t>(stream), true);
+}
+
 pulse_status pulse_tstage_timing(pulse_tstage* s, int32_t enable) {
   if (!s) return tfail(PULSE_E_INVALID_ARG, "stage is NULL");
+  if (s->join_pending) {  // timed calls keep everything on the caller's stream
+    THIP(hipStreamSynchronize(s->side));
+    s->join_pending = false;
+  }
   s->timing = enable != 0;
   s->timed.clear();
   s->ev_used = 0;

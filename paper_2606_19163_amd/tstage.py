@@ -59,6 +59,10 @@ def lib():
         L.pulse_tstage_reset.restype = st
         L.pulse_tstage_inflight.argtypes = [_vp]
         L.pulse_tstage_inflight.restype = _i32
+        L.pulse_tstage_overlap_bwd.argtypes = [_vp, _i32]
+        L.pulse_tstage_overlap_bwd.restype = st
+        L.pulse_tstage_flush.argtypes = [_vp, _vp]
+        L.pulse_tstage_flush.restype = st
         L.pulse_tstage_timing.argtypes = [_vp, _i32]
         L.pulse_tstage_timing.restype = st
         L.pulse_tstage_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_int64),
@@ -194,6 +198,12 @@ class TStage:
 
     def flops(self):
         return lib().pulse_tstage_flops(self.h)
+
+    def overlap_bwd(self, enable):
+        _check(lib().pulse_tstage_overlap_bwd(self.h, 1 if enable else 0))
+
+    def flush(self, stream=None):
+        _check(lib().pulse_tstage_flush(self.h, None if self.dry else _stream_handle(stream)))
 
     def timing(self, enable):
         _check(lib().pulse_tstage_timing(self.h, 1 if enable else 0))

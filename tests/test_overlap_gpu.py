@@ -100,3 +100,35 @@ def test_flush_orders_decoder_gradients_on_the_stream():
         torch.cuda.synchronize()
         st.release(0)
     assert torch.equal(grads[0], grads[1])
+
+
+def test_transformer_overlapped_decoder_backward_is_bitwise_the_joined_one():
+    """The same for the 768-wide transformer stage (two microbatches)."""
+    import torch
+    from paper_2606_19163_amd import tstage as TS
+    d = configs.get("t768")
+    params, b0 = synth.make_tstage(d, configs.SEEDS["t768"])
+    _, b1 = synth.make_tstage(d, configs.SEEDS["t768"] + 100)
+    res = []
+    for overlap in (False, True):
+        log(f"case overlap: t768, two microbatches, overlap={overlap}")
+        st = TS.TStage(d)
+        st.set_params(params)
+        st.zero_grads()
+        st.overlap_bwd(overlap)
+        outs = []
+        for mb, bb in enumerate((b0, b1)):
+            db = {k: st.to_dev(v) for k, v in bb.items()}
+            torch.cuda.synchronize()
+            y_enc = st.forward(TS.ENC, mb, db["x"])
+            y_dec = st.forward(TS.DEC, mb, db["u"])
+            du = st.backward(TS.DEC, mb, db["g_dec"])
+            dx = st.backward(TS.ENC, mb, db["g_enc"])
+            outs.append([y_enc, y_dec, du, dx])
+        torch.cuda.synchronize()
+        res.append(([[t.cpu() for t in o] for o in outs], st.grads.cpu()))
+    (oa, ga), (ob, gb) = res
+    for mb in range(2):
+        for i in range(4):
+            assert torch.equal(oa[mb][i], ob[mb][i]), f"t768 mb{mb} output {i} differs"
+    assert torch.equal(ga, gb), "t768 parameter gradients differ"
