@@ -1103,6 +1103,23 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
   // while the data-gradient chain continues here.  The side stream has its
   // own reduction buffer and weight-gradient partials.
   hipStream_t sd = use_side(s) ? s->side : st;
+  // The shortcut's data gradient (a 1x1 conv over dout: short K, its output
+  // twice dout's width) runs first and alone when this stage's convs fill
+  // the GPU without a K split: beside the weight GEMMs, whose blocks leave no
+  // room for its own on their CUs, it took three times as long.  Where the
+  // convs split K the weight GEMMs bound the backward, and it stays beside
+  // them, after the fork.
+  void* dxs = s->scratch(s->s_dxs);
+  auto shortcut_dgrad = [&]() -> pulse_status {
+    return conv_fwd(s, b.cin, {seg1(0, b.cout, dout)}, s->ws + b.wsd, b.cout, nullptr, nullptr,
+                    vnone(), dxs, nullptr, dt, st);
+  };
+  const bool sc_first =
+      b.conv_sc && conv_ksplit(s, conv_tile(s, b.cout), b.cout, 9 * b.cout) == 1;
+  if (sc_first) {
+    if ((ps = shortcut_dgrad()) != PULSE_OK) return ps;
+    s->fork_attached = false;  // the fork below orders the side stream after it
+  }
   if ((ps = fork_side(s, st)) != PULSE_OK) return ps;
   {
     const RedGrid rg = red_grid(s->geo, b.cout);
@@ -1140,12 +1157,8 @@ pulse_status block_backward(pulse_stage* s, int r, const Block& b, const VIn& xi
                      nullptr, vnone(), da, nullptr, dt, st, nullptr, &gn2_chunks, &gnb2)) !=
       PULSE_OK)
     return ps;
-  void* dxs = s->scratch(s->s_dxs);
-  if (b.conv_sc) {
-    if ((ps = conv_fwd(s, b.cin, {seg1(0, b.cout, dout)}, s->ws + b.wsd, b.cout, nullptr, nullptr,
-                       vnone(), dxs, nullptr, dt, st)) != PULSE_OK)
-      return ps;
-  }
+  if (b.conv_sc && !sc_first)
+    if ((ps = shortcut_dgrad()) != PULSE_OK) return ps;
   // GN2 backward -> dh1, with per-image channel sums (the temb gradient);
   // dh1 alternates between two buffers: the one written here was last read
   // by the conv1 weight gradient of the block before the previous one
