@@ -958,15 +958,40 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
 
   // fp32 partials through LDS, GPP wave rows (GPP * WM tile rows) at a
   // time: those waves stage all their accumulators, then every thread
-  // stores 16-byte row pieces
+  // stores 16-byte row pieces, into the split's partial or, with one pixel
+  // split, added into the gradient (one writer per element)
   float* ct = reinterpret_cast<float*>(smem);
   float* part = a.part + (long)z * a.M * a.N;
   constexpr int NV4 = C::BN / 4;
   constexpr int GPP = (2 * C::STAGE) / (C::WM * C::LDC * 4);  // wave rows per pass
   static_assert(GPP >= 1, "one wave row of accumulators fits the LDS stages");
   constexpr int ROWS = (GPP < C::WAVES_M ? GPP : C::WAVES_M) * C::WM;
+  constexpr int IT = (ROWS * NV4 + C::NT - 1) / C::NT;  // row pieces per thread and pass
 #pragma unroll 1
   for (int g0 = 0; g0 < C::WAVES_M; g0 += GPP) {
+    // one pixel split: fetch this pass's gradient pieces before staging the
+    // accumulators, so that their loads are in flight together (the host
+    // guarantees 16-byte aligned rows of a multiple of 4 columns)
+    float4 gv[IT];
+    float* gp[IT];
+    if (a.wdirect) {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int e = tid + it * C::NT;
+        const int row = e / NV4;
+        const int n = n0 + (e - row * NV4) * 4;
+        const int m = m0 + g0 * C::WM + row;
+        gp[it] = nullptr;
+        gv[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (e >= ROWS * NV4 || row >= (C::WAVES_M - g0) * C::WM || m >= a.M || n >= a.N)
+          continue;
+        // segment bounds are multiples of 8: the four columns share one
+        const int s = seg_of(a.nseg, a.seg[1].begin, a.seg[2].begin, n);
+        const Seg& sg = s == 0 ? a.seg[0] : (s == 1 ? a.seg[1] : a.seg[2]);
+        gp[it] = sg.grad + (long)m * (sg.end - sg.begin) + (n - sg.begin);
+        gv[it] = *reinterpret_cast<const float4*>(gp[it]);
+      }
+    }
     if (wm >= g0 && wm < g0 + GPP) {
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
@@ -974,13 +999,27 @@ __global__ __launch_bounds__(C::NT) void igemm2_wgrad(GemmArgs a, const void* ze
                                                   lane, i, acc);
     }
     __syncthreads();
-    for (int e = tid; e < ROWS * NV4; e += C::NT) {
-      const int row = e / NV4;
-      const int n = n0 + (e - row * NV4) * 4;
-      const int m = m0 + g0 * C::WM + row;
-      if (row >= (C::WAVES_M - g0) * C::WM || m >= a.M || n >= a.N) continue;
-      *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
-          *reinterpret_cast<const float4*>(ct + row * C::LDC + (n - n0));
+    if (a.wdirect) {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        if (!gp[it]) continue;
+        const int e = tid + it * C::NT;
+        const int row = e / NV4;
+        const int c = (e - row * NV4) * 4;
+        const float4 v = *reinterpret_cast<const float4*>(ct + row * C::LDC + c);
+        const float4 g = gv[it];
+        *reinterpret_cast<float4*>(gp[it]) =
+            make_float4(g.x + v.x, g.y + v.y, g.z + v.z, g.w + v.w);
+      }
+    } else {
+      for (int e = tid; e < ROWS * NV4; e += C::NT) {
+        const int row = e / NV4;
+        const int n = n0 + (e - row * NV4) * 4;
+        const int m = m0 + g0 * C::WM + row;
+        if (row >= (C::WAVES_M - g0) * C::WM || m >= a.M || n >= a.N) continue;
+        *reinterpret_cast<float4*>(part + (long)m * a.N + n) =
+            *reinterpret_cast<const float4*>(ct + row * C::LDC + (n - n0));
+      }
     }
     __syncthreads();
   }
@@ -1095,6 +1134,17 @@ static hipError_t conv2_t(const GemmArgs& a_in, hipStream_t st, hipEvent_t t0, h
   return hipGetLastError();
 }
 
+// One pixel split with 16-byte aligned gradient rows of a multiple of 4
+// columns: the GEMM epilogue adds into the gradients and no finalize runs.
+static bool wgrad_direct(const GemmArgs& a, int splits) {
+  if (splits != 1) return false;
+  for (int i = 0; i < a.nseg; ++i)
+    if (reinterpret_cast<uintptr_t>(a.seg[i].grad) % 16 != 0 ||
+        (a.seg[i].end - a.seg[i].begin) % 4 != 0)
+      return false;
+  return true;
+}
+
 template <class C>
 static hipError_t wgrad2_t(const GemmArgs& a_in, int splits, const void* zero16, hipStream_t st) {
   if (a_in.g.pixels() >= (1L << 31)) return hipErrorInvalidValue;  // 32-bit pixel indices
@@ -1102,6 +1152,7 @@ static hipError_t wgrad2_t(const GemmArgs& a_in, int splits, const void* zero16,
   const long tilesM = (a.M + C::BM - 1) / C::BM;
   const long tilesN = (a.N + C::BN - 1) / C::BN;
   const long blocks = tilesM * tilesN * splits;
+  a.wdirect = wgrad_direct(a, splits);
   {
     const long HW = a.g.hw();
     a.rcp_nt = rcp_u32(tilesM * tilesN, blocks);
@@ -1151,7 +1202,7 @@ hipError_t launch_wgrad2(const GemmArgs& a, int t, int splits, const void* zero1
     case TILE2_W320x128: e = wgrad2_t<W2_320x128>(a, splits, zero16, st); break;
     default: e = wgrad2_t<W2_128x128>(a, splits, zero16, st); break;
   }
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || wgrad_direct(a, splits)) return e;  // added in the epilogue
   return launch_wgrad_finalize(a, splits, st);
 }
 

@@ -45,6 +45,9 @@ struct GemmArgs {
   VIn gy;              // output gradient, M channels
   int kchunk;          // pixels per split
   float* part;         // [splits][M][N] fp32 partials (both modes)
+  int wdirect;         // set by the wgrad launcher: one pixel split, so the
+                       // epilogue adds its tile into the segment gradients
+                       // (one writer per element) and no finalize runs
   // CONV mode of the LDS-DMA kernels without a K split, when H*W % BM == 0:
   // per-channel sum and sum of squares of the output as stored (bf16), one
   // row per (image, M-tile): [B][H*W / BM][2][N]; null: not computed

@@ -295,22 +295,26 @@ int conv_ksplit(const pulse_stage* s, int tile, int N, int K) {
 // Pixel split of a weight-gradient GEMM.  With s splits the grid holds
 // tiles * s blocks of K / s pixels each; blocks run in ceil(tiles * s /
 // slots) rounds, and every split adds an fp32 partial of M x N that is
-// written once and read once by the finalize.  The split count minimises
-//   rounds(s) * T_tile / s + s * M * N * 8 / HBM
-// where T_tile is one tile's whole-K time at a nominal per-CU rate.
+// written once and read once by the finalize, which then reads and writes
+// the fp32 gradient.  The split count minimises
+//   rounds(s) * T_tile / s + bytes(s) * M * N / HBM
+// where T_tile is one tile's whole-K time at a nominal per-CU rate and
+// bytes(s) = 8 s + 8; on the LDS-DMA path one split adds its tile into the
+// gradient in the GEMM epilogue (no partial, no finalize): bytes(1) = 8.
 int pick_splits(const pulse_stage* s, int tile, int M, int N, int& kchunk) {
   const TileInfo ti = info_of(s, tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
   const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : (ti.bm * ti.bn <= 128 * 128 ? 2 : 1);
   const long slots = 256L * per_cu;  // resident blocks
   const double t_tile = 2.0 * ti.bm * ti.bn * (double)s->P / 3.0e12;  // s, per CU
-  const double t_part = (double)M * N * 8.0 / 4.0e12;                  // s, per split
+  const double t_elem = (double)M * N / 4.0e12;                       // s per byte per element
   const long maxs = std::max(1L, (long)(s->P / (4 * ti.bk)));          // >= 4 K-steps each
   long best = 1;
   double best_t = 1e30;
   for (long sp = 1; sp <= std::min(maxs, 256L); ++sp) {
     const long rounds = (tiles * sp + slots - 1) / slots;
-    const double t = rounds * t_tile / sp + sp * t_part;
+    const double bytes = sp == 1 && uses_v2(s) ? 8.0 : 8.0 * sp + 8.0;
+    const double t = rounds * t_tile / sp + bytes * t_elem;
     if (t < best_t * 0.999) {
       best_t = t;
       best = sp;

@@ -262,21 +262,24 @@ int twgrad_tile(int tile_force, int M, long P) {
 }
 
 // Token splits of a weight-gradient GEMM (M x N over P tokens): the count
-// that minimises rounds(s) * T_tile / s + s * M * N * 8 / HBM, as for the
-// ResBlock stage; kchunk receives the tokens per split
+// that minimises rounds(s) * T_tile / s + bytes(s) * M * N / HBM, as for
+// the ResBlock stage (bytes(s) = 8 s + 8 for s partials and the finalize,
+// 8 for one split added into the gradient in the GEMM epilogue); kchunk
+// receives the tokens per split
 int twgrad_splits(int tile, long P, int M, int N, int& kchunk) {
   const TileInfo ti = tile2_info(tile);
   const long tiles = (long)((M + ti.bm - 1) / ti.bm) * ((N + ti.bn - 1) / ti.bn);
   const long per_cu = ti.per_cu > 0 ? std::min(ti.per_cu, 2) : 1;
   const long slots = 256L * per_cu;
   const double t_tile = 2.0 * ti.bm * ti.bn * (double)P / 3.0e12;
-  const double t_part = (double)M * N * 8.0 / 4.0e12;
+  const double t_elem = (double)M * N / 4.0e12;
   const long maxs = std::max(1L, P / (4L * ti.bk));
   long best = 1;
   double best_t = 1e30;
   for (long sp = 1; sp <= std::min(maxs, 256L); ++sp) {
     const long rounds = (tiles * sp + slots - 1) / slots;
-    const double t = rounds * t_tile / sp + sp * t_part;
+    const double bytes = sp == 1 ? 8.0 : 8.0 * sp + 8.0;
+    const double t = rounds * t_tile / sp + bytes * t_elem;
     if (t < best_t * 0.999) {
       best_t = t;
       best = sp;

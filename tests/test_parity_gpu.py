@@ -69,7 +69,9 @@ def test_full_size(name, batch):
     the wave workload's shape, where the conv and weight-gradient plans pick
     other K splits.  The oracle runs on the whole microbatch, so every
     output, parameter gradient (the production weight-gradient split and its
-    finalize), cached skip and buffered skip gradient is compared."""
+    finalize, or at 16x16 and 8x8 the single split that adds into the
+    gradient in the GEMM epilogue), cached skip and buffered skip gradient
+    is compared."""
     desc = configs.get(name) if batch is None else configs.get(name, batch=batch)
     seed = configs.SEEDS[name]
     log(f"case {name} full B={desc['batch']}: GPU run")
