@@ -189,24 +189,57 @@ __global__ __launch_bounds__(256) void k_temb_fwd_multi(const void* temb, int dt
   }
 }
 
-// thread (o, d): dWl[o][d] += sum_b de[b][o] * SiLU(temb[b][d]); the extra
-// thread d == D of each row accumulates the bias gradients.
-__global__ void k_temb_bwd_w(const float* de, const void* temb, int dtype, int B, int D, int O,
-                             float* dWl, float* dbl, float* db1) {
-  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (long)O * (D + 1)) return;
-  const int o = (int)(i / (D + 1));
-  const int d = (int)(i - (long)o * (D + 1));
+// dWl[o][d] += sum_b de[b][o] * SiLU(temb[b][d]) over a 64 (d) x 16 (o)
+// tile per block: the tile's SiLU(temb) columns and de rows are staged in
+// LDS for up to 32 images at a time (each SiLU evaluated once per tile, not
+// once per output), and thread (d lane, row group g) owns rows 4 g .. 4 g + 3.
+// The blocks of the first d tile also sum de over the images for the bias
+// gradients.  Every sum runs over b in increasing order.
+constexpr int TB_D = 64, TB_O = 16, TB_B = 32;
+__global__ __launch_bounds__(256) void k_temb_bwd_w(const float* de, const void* temb, int dtype,
+                                                    int B, int D, int O, float* dWl, float* dbl,
+                                                    float* db1) {
+  __shared__ float sv[TB_B][TB_D];
+  __shared__ __attribute__((aligned(16))) float se[TB_B][TB_O];
+  const int tx = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int d0 = blockIdx.x * TB_D, o0 = blockIdx.y * TB_O;
+  const bool bias = blockIdx.x == 0 && threadIdx.x < TB_O;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  float sb = 0.f;
+  for (int b0 = 0; b0 < B; b0 += TB_B) {
+    const int nb = min(TB_B, B - b0);
+    __syncthreads();
+    for (int e = threadIdx.x; e < nb * TB_D; e += 256) {
+      const int bb = e / TB_D, c = e - bb * TB_D;
+      sv[bb][c] = d0 + c < D ? silu_f(ld_any(temb, dtype, (long)(b0 + bb) * D + d0 + c)) : 0.f;
+    }
+    for (int e = threadIdx.x; e < nb * TB_O; e += 256) {
+      const int bb = e / TB_O, c = e - bb * TB_O;
+      se[bb][c] = o0 + c < O ? de[(long)(b0 + bb) * O + o0 + c] : 0.f;
+    }
+    __syncthreads();
+    for (int bb = 0; bb < nb; ++bb) {
+      const float v = sv[bb][tx];
+      const float4 w = reinterpret_cast<const float4*>(&se[bb][0])[g];
+      acc[0] += w.x * v;
+      acc[1] += w.y * v;
+      acc[2] += w.z * v;
+      acc[3] += w.w * v;
+    }
+    if (bias)
+      for (int bb = 0; bb < nb; ++bb) sb += se[bb][threadIdx.x];
+  }
+  const int d = d0 + tx;
   if (d < D) {
-    float s = 0.f;
-    for (int b = 0; b < B; ++b)
-      s += de[(long)b * O + o] * silu_f(ld_any(temb, dtype, (long)b * D + d));
-    dWl[(long)o * D + d] += s;
-  } else {
-    float s = 0.f;
-    for (int b = 0; b < B; ++b) s += de[(long)b * O + o];
-    dbl[o] += s;
-    if (db1) db1[o] += s;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int o = o0 + 4 * g + j;
+      if (o < O) dWl[(long)o * D + d] += acc[j];
+    }
+  }
+  if (bias && o0 + threadIdx.x < O) {
+    dbl[o0 + threadIdx.x] += sb;
+    if (db1) db1[o0 + threadIdx.x] += sb;
   }
 }
 
@@ -333,7 +366,10 @@ hipError_t launch_temb_fwd_multi(const void* temb, int dtype, int B, int D,
 hipError_t launch_temb_bwd(const float* de, const void* temb, int dtype, int B, int D, int O,
                            const float* Wl, float* dWl, float* dbl, float* db1, float* dtemb,
                            hipStream_t st) {
-  hipLaunchKernelGGL(k_temb_bwd_w, dim3(nblk((long)O * (D + 1))), dim3(256), 0, st, de, temb,
+  if (O <= 0) return hipSuccess;
+  // at least one d tile: its blocks also produce the bias gradients
+  const int dt = std::max(1, (D + TB_D - 1) / TB_D);
+  hipLaunchKernelGGL(k_temb_bwd_w, dim3(dt, (O + TB_O - 1) / TB_O), dim3(256), 0, st, de, temb,
                      dtype, B, D, O, dWl, dbl, db1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !dtemb) return e;
