@@ -82,23 +82,33 @@ def test_full_size(name, batch):
     compare(desc, gpu, ref, label=f"{name} B={desc['batch']}", log_all=True)
 
 
-def test_two_microbatch_accumulation():
-    """Parameter gradients accumulate (+=) over microbatches: two l64
-    microbatches with different inputs, run through one stage in the bench's
-    launch configuration, against the sum of two oracle runs; each
-    microbatch's outputs against its own oracle run."""
+ACCUM = ["l64", "l16s"]
+
+
+@pytest.mark.parametrize("case", ACCUM)
+def test_two_microbatch_accumulation(case):
+    """Parameter gradients accumulate (+=) over microbatches: two
+    microbatches with different inputs, run through one stage, against the
+    sum of two oracle runs; each microbatch's outputs against its own oracle
+    run.  l64 in the bench's launch configuration (weight gradients through
+    pixel-split partials and the finalize); l16s, the 1280-channel level on
+    a few pixels, where every weight GEMM is one split whose epilogue adds
+    into gradients that the first microbatch left non-zero."""
     import torch
     from paper_2606_19163_amd import stage as S
-    desc = configs.l64()
-    params, b0 = synth.make_all(desc, configs.SEEDS["l64"])
-    _, b1 = synth.make_all(desc, configs.SEEDS["l64"] + 100)
+    if case == "l64":
+        desc, seed = configs.l64(), configs.SEEDS["l64"]
+    else:
+        desc, seed = configs.shrink(configs.l16(), batch=2, hw=6, width=5), configs.SEEDS["l16"]
+    params, b0 = synth.make_all(desc, seed)
+    _, b1 = synth.make_all(desc, seed + 100)
     st = S.Stage(desc)
     st.set_params(params)
     st.zero_grads()
     outs = []
     dtemb = torch.zeros((desc["batch"], desc["temb_dim"]), dtype=torch.float32, device="cuda")
     for mb, bb in enumerate((b0, b1)):
-        log(f"case l64 two microbatches: GPU microbatch {mb}")
+        log(f"case {case} two microbatches: GPU microbatch {mb}")
         db = {k: st.to_dev(v) for k, v in bb.items()}
         dt = torch.zeros_like(dtemb)
         o = S.run_microbatch(st, mb, db, dtemb=dt)
@@ -109,13 +119,13 @@ def test_two_microbatch_accumulation():
     grads = st.grads_dict()
     refs = []
     for mb, bb in enumerate((b0, b1)):
-        log(f"case l64 two microbatches: oracle microbatch {mb}")
+        log(f"case {case} two microbatches: oracle microbatch {mb}")
         refs.append(_oracle(desc, params, bb))
-        compare(desc, outs[mb], refs[mb], grads=False, label=f"l64 mb{mb}")
+        compare(desc, outs[mb], refs[mb], grads=False, label=f"{case} mb{mb}")
     total = {"grads": {k: refs[0]["grads"][k] + refs[1]["grads"][k] for k in refs[0]["grads"]}}
     errs = {k: rel_l2(grads[k], v) for k, v in total["grads"].items()}
     for k in sorted(errs):
-        log(f"  l64 two microbatches grad.{k} = {errs[k]:.3e}")
+        log(f"  {case} two microbatches grad.{k} = {errs[k]:.3e}")
     bad = {k: v for k, v in errs.items() if not (v <= 2e-2)}
     assert not bad, bad
 
