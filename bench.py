@@ -35,11 +35,12 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 # Overlapped decoder backward, measured per workload (same box, alternating
-# runs): 64x64x320 778 against 764 TFLOP/s; 32x32x640 697 against 705 (its
-# decoder's last weight GEMM then runs into the encoder's K-split convs); the
-# four-level wave 625 either way; the transformer stages 372 against 371
-# (768 wide) and 665 against 657 (1408 wide).
-OVERLAP_BWD_AUTO = ("l64", "t768", "t1408")
+# runs): 64x64x320 778 against 764 TFLOP/s; 32x32x640 725-728 against
+# 709-711 (since the timestep weight gradient takes less of the second
+# stream); 16x16x1280 840-841 against 844-847 and 8x8x1280 469 against
+# 471-474; the four-level wave 625 either way; the transformer stages 372
+# against 371 (768 wide) and 665 against 657 (1408 wide).
+OVERLAP_BWD_AUTO = ("l64", "l32", "t768", "t1408")
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the fp32 stage)
 METRIC = "stage fwd+bwd TFLOP/s (% bf16 MFMA peak) and microbatches/s, 64x64x320 stage"
 

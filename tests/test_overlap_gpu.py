@@ -1,8 +1,9 @@
 """Overlapped decoder backward (pulse_stage_overlap_bwd): a decoder backward
 that leaves its last parameter-gradient work on the stage's second stream,
 with the encoder backward starting beside it, gives bitwise the results of
-the joined backward, on the 64x64x320 stage in the bench's launch
-configuration; a flush orders that work before later work on a stream."""
+the joined backward, on the 64x64x320 and 32x32x640 stages in the bench's
+launch configuration; a flush orders that work before later work on a
+stream."""
 
 import pytest
 
@@ -47,15 +48,18 @@ def _same(a, b, label):
     assert torch.equal(ta, tb), f"{label}: dtemb differs"
 
 
-def test_overlapped_decoder_backward_is_bitwise_the_joined_one():
-    desc = configs.l64()
-    params, b0 = synth.make_all(desc, configs.SEEDS["l64"])
-    _, b1 = synth.make_all(desc, configs.SEEDS["l64"] + 100)
-    log("case overlap: l64, two microbatches, joined backward")
+@pytest.mark.parametrize("name", ["l64", "l32"])
+def test_overlapped_decoder_backward_is_bitwise_the_joined_one(name):
+    """Both stages the bench runs with it: 64x64x320, and 32x32x640 with its
+    shortcut convs and K-split convs."""
+    desc = configs.get(name)
+    params, b0 = synth.make_all(desc, configs.SEEDS[name])
+    _, b1 = synth.make_all(desc, configs.SEEDS[name] + 100)
+    log(f"case overlap: {name}, two microbatches, joined backward")
     ref = _run(desc, params, (b0, b1), overlap=False)
-    log("case overlap: l64, two microbatches, overlapped decoder backward")
+    log(f"case overlap: {name}, two microbatches, overlapped decoder backward")
     got = _run(desc, params, (b0, b1), overlap=True)
-    _same(ref, got, "overlapped")
+    _same(ref, got, f"{name} overlapped")
 
 
 def test_overlapped_decoder_backward_across_streams():
